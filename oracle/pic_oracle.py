@@ -1,0 +1,233 @@
+"""Plain CPU oracle of the position-independent cache-hit path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import or call this
+module; only the tests, the smoke check and the benchmark's CPU-baseline leg do.
+It shares no code with the GPU library: it is numpy only, written from the
+paper's definitions, and deliberately slow and literal.
+
+What it computes (SemPIC, "Learning Semantic Position-Independent KV Caches"):
+
+* Request layout: the canonical order prefix, D_1, S_1, ..., D_m, S_m, Q
+  (Sec. 2), with the link operator assigning each cached state its final
+  logical position (Sec. 2) through a token-level map from physical cache
+  slots to logical positions (App. C.1).  Here a physical slot index equals
+  its logical position and the inline spans S_i are empty.
+* RoPE relocation of a key compiled at position a to position b,
+  k_b = R(b) R(a)^{-1} k_a (Sec. 2, Eq. 3); values are reused unchanged (Sec. 2).
+* Causal attention of inline tokens over the linked cache with a frontier
+  mask: a token never sees a logically later position, whatever the physical
+  slot order (App. C.1); the completed cache then serves ordinary one-token
+  decoding (App. C.1, Sec. 5 "Cache-hit serving").
+
+Precision: inputs are float32 (bf16 inputs are exactly representable in it),
+angles, cos/sin, rotations, dot products and softmax sums are float64, and a
+stored result is rounded once to its storage type.
+
+Readings where the paper is silent (each one is also pinned by a test):
+  * rotate-half pairing of element i with element i + D/2 and inverse
+    frequencies theta_i = base^(-2i/D), no frequency scaling;
+  * one rotary transform shared by all layers;
+  * softmax scale 1/sqrt(D); GQA query head h reads kv head h // (Hq/Hkv);
+  * a token attends to every position <= its own (itself included).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+# --------------------------------------------------------------------------------------
+# Storage rounding
+# --------------------------------------------------------------------------------------
+
+
+def round_to_f32(x) -> np.ndarray:
+    """Round to float32 (nearest, ties to even)."""
+    return np.asarray(x, dtype=np.float64).astype(np.float32)
+
+
+def round_to_bf16(x) -> np.ndarray:
+    """Round a float64 value to the nearest bfloat16 (ties to even), returned as float32.
+
+    bfloat16 keeps 8 significant bits and float32's exponent range: split x into
+    mantissa m in [0.5, 1) and exponent e, round m * 2^8 to an integer with
+    ties to even (np.rint), and scale back.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)
+    return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8).astype(np.float32)
+
+
+def store(x, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return round_to_f32(x)
+    if dtype == "bf16":
+        return round_to_bf16(x)
+    raise ValueError(dtype)
+
+
+# --------------------------------------------------------------------------------------
+# Rotary transform R(p)  (Sec. 2, Eq. 3)
+# --------------------------------------------------------------------------------------
+
+
+def inv_freq(head_dim: int, theta: float) -> np.ndarray:
+    """theta_i = theta^(-2i/D) for i = 0 .. D/2-1, float64."""
+    i = np.arange(head_dim // 2, dtype=np.float64)
+    return np.power(float(theta), -2.0 * i / head_dim)
+
+
+def _cos_sin(pos, head_dim: int, theta: float):
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq(head_dim, theta)[None, :]
+    return np.cos(ang), np.sin(ang)
+
+
+def rope(x, pos, theta: float) -> np.ndarray:
+    """R(p) x for rows x[..., n, D] at positions pos[n]; float64 result.
+
+    Each pair (x_i, x_{i+D/2}) is turned by the angle p * theta_i:
+    (x_i cos - x_{i+D/2} sin, x_i sin + x_{i+D/2} cos).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    h = x.shape[-1] // 2
+    c, s = _cos_sin(pos, 2 * h, theta)
+    x1, x2 = x[..., :h], x[..., h:]
+    return np.concatenate([x1 * c - x2 * s, x1 * s + x2 * c], axis=-1)
+
+
+def rope_inverse(x, pos, theta: float) -> np.ndarray:
+    """R(p)^{-1} x = R(p)^T x (a rotation's inverse is its transpose); float64 result."""
+    x = np.asarray(x, dtype=np.float64)
+    h = x.shape[-1] // 2
+    c, s = _cos_sin(pos, 2 * h, theta)
+    x1, x2 = x[..., :h], x[..., h:]
+    return np.concatenate([x1 * c + x2 * s, -x1 * s + x2 * c], axis=-1)
+
+
+def rerotate_keys(k, a, b, theta: float) -> np.ndarray:
+    """Eq. 3 taken literally: k_b = R(b) (R(a)^{-1} k_a), two rotations in float64.
+
+    k: [..., n, D]; a, b: [n] compile-time and request-time positions.
+    """
+    return rope(rope_inverse(k, a, theta), b, theta)
+
+
+# --------------------------------------------------------------------------------------
+# Layout: token-level map from cache slots to logical positions (Sec. 2; App. C.1)
+# --------------------------------------------------------------------------------------
+
+
+@dataclass
+class RequestMap:
+    ctx_len: int
+    src_token: np.ndarray     # [ctx] pool token feeding each slot
+    compile_pos: np.ndarray   # [ctx] position a the slot's key was compiled at
+    logical_pos: np.ndarray   # [ctx] position b the slot holds in the request
+
+
+def plan_layout(requests, doc_offset, doc_len, doc_compile_pos) -> list[RequestMap]:
+    """Place each request's pool entries back to back in request order from position 0.
+
+    Entry e of a request occupies logical positions [b_e, b_e + len_e) with
+    b_e the running total of the entries before it; its token t was compiled at
+    doc_compile_pos[e] + t.  Slot index = logical position.
+    """
+    maps = []
+    for entries in requests:
+        src, a, b = [], [], []
+        pos = 0
+        for e in entries:
+            n = int(doc_len[e])
+            for t in range(n):
+                src.append(int(doc_offset[e]) + t)
+                a.append(int(doc_compile_pos[e]) + t)
+                b.append(pos + t)
+            pos += n
+        maps.append(RequestMap(pos, np.asarray(src, np.int64), np.asarray(a, np.int64),
+                               np.asarray(b, np.int64)))
+    return maps
+
+
+# --------------------------------------------------------------------------------------
+# Composition (link operator): re-rotated keys, unchanged values
+# --------------------------------------------------------------------------------------
+
+
+def compose_request(pool_k, pool_v, rmap: RequestMap, theta: float, dtype: str):
+    """One request, one layer.  pool_k/pool_v: [Hkv][pool_tokens][D] (float32 values).
+
+    Returns (K, V) of shape [Hkv][ctx][D], float32 values of the storage type.
+    """
+    k_src = np.asarray(pool_k, np.float64)[:, rmap.src_token, :]
+    k = store(rerotate_keys(k_src, rmap.compile_pos, rmap.logical_pos, theta), dtype)
+    v = np.asarray(pool_v, np.float32)[:, rmap.src_token, :].copy()
+    return k, v
+
+
+# --------------------------------------------------------------------------------------
+# Attention with the frontier causal mask (App. C.1)
+# --------------------------------------------------------------------------------------
+
+
+def attention(q, q_pos, k, v, k_pos, scale: float | None = None) -> np.ndarray:
+    """Masked softmax attention, float64.
+
+    q: [Hq][nq][D] at positions q_pos[nq]; k, v: [Hkv][nk][D] at positions k_pos[nk].
+    Query head h reads kv head h // (Hq // Hkv).  Key j is visible to query i
+    iff k_pos[j] <= q_pos[i] (the mask is by position, not by slot).
+    Returns o: [Hq][nq][D].
+    """
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    Hq, nq, D = q.shape
+    Hkv = k.shape[0]
+    n_rep = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    visible = np.asarray(k_pos)[None, :] <= np.asarray(q_pos)[:, None]          # [nq, nk]
+    out = np.empty((Hq, nq, D), np.float64)
+    for h in range(Hq):
+        g = h // n_rep
+        s = scale * (q[h] @ k[g].T)                                             # [nq, nk]
+        s = np.where(visible, s, -np.inf)
+        m = s.max(axis=1, keepdims=True)
+        w = np.exp(s - m)
+        out[h] = (w @ v[g]) / w.sum(axis=1, keepdims=True)
+    return out
+
+
+def suffix_prefill(k_ctx, v_ctx, q, k_suf, v_suf, scale: float | None = None):
+    """Prefill of Ls suffix tokens after a composed context (one request, one layer).
+
+    k_ctx, v_ctx: [Hkv][ctx][D] composed cache; q: [Ls][Hq][D]; k_suf, v_suf: [Ls][Hkv][D]
+    (suffix keys already carry their own positions).  The suffix K/V are appended at
+    positions [ctx, ctx + Ls) (App. C.1: inline KVs interleaved with the prepared
+    states); suffix token i sits at position ctx + i.
+    Returns (out [Ls][Hq][D] float64, K [Hkv][ctx+Ls][D], V [Hkv][ctx+Ls][D]).
+    """
+    ctx = k_ctx.shape[1]
+    Ls = q.shape[0]
+    K = np.concatenate([np.asarray(k_ctx, np.float32),
+                        np.transpose(np.asarray(k_suf, np.float32), (1, 0, 2))], axis=1)
+    V = np.concatenate([np.asarray(v_ctx, np.float32),
+                        np.transpose(np.asarray(v_suf, np.float32), (1, 0, 2))], axis=1)
+    pos = np.arange(ctx + Ls)
+    o = attention(np.transpose(q, (1, 0, 2)), ctx + np.arange(Ls), K, V, pos, scale)
+    return np.transpose(o, (1, 0, 2)), K, V
+
+
+def decode_step(K, V, length: int, q, k_new, v_new, scale: float | None = None):
+    """One decode step (one request, one layer): write k_new/v_new at position `length`,
+    then attend the single query at that position over positions [0, length].
+
+    K, V: [Hkv][>= length][D] valid up to `length`; q: [Hq][D]; k_new, v_new: [Hkv][D].
+    Returns (out [Hq][D] float64, K', V' of length + 1).
+    """
+    K2 = np.concatenate([np.asarray(K, np.float32)[:, :length],
+                         np.asarray(k_new, np.float32)[:, None, :]], axis=1)
+    V2 = np.concatenate([np.asarray(V, np.float32)[:, :length],
+                         np.asarray(v_new, np.float32)[:, None, :]], axis=1)
+    o = attention(np.asarray(q)[:, None, :], np.asarray([length]), K2, V2,
+                  np.arange(length + 1), scale)
+    return o[:, 0, :], K2, V2
