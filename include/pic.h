@@ -1,0 +1,188 @@
+/*
+ * pic.h - C ABI of the position-independent KV-cache hit path on MI355X (gfx950).
+ *
+ * The path serves a request from document KV caches compiled offline, each on its own,
+ * from position 0 (SemPIC, Sec. 2 and Sec. 5 "Cache-hit serving"):
+ *   1. plan:    give every cached token its logical position in the request's canonical
+ *               order (prefix, D_1, ..., D_m, then the query) - the link operator of Sec. 2,
+ *               realised as the token-level slot -> position map of App. C.1;
+ *   2. compose: gather each document's per-layer K/V into the request's cache, turning
+ *               every key from its compile position a to its logical position b,
+ *               k_b = R(b) R(a)^-1 k_a (Sec. 2, Eq. 3); values are copied unchanged;
+ *   3. prefill: append the suffix tokens' K/V after the composed context and run causal
+ *               attention of the suffix queries over it, with the frontier mask of App. C.1;
+ *   4. decode:  one-token attention steps over the completed cache (App. C.1, last sentence).
+ *
+ * Conventions shared by every call
+ *   - Pointers are DEVICE pointers unless marked [host].  The library never allocates or
+ *     frees memory and never synchronises: the caller owns every buffer, and every call
+ *     that takes a stream only enqueues work on it (stream is a hipStream_t; NULL is the
+ *     null stream).  Results are visible once that stream has reached the call.
+ *   - Element type of q/k/v/caches/outputs is model->dtype (PIC_F32: float, PIC_BF16:
+ *     bfloat16 bit patterns).  Arithmetic is fp32; stores round to nearest even.
+ *   - model->n_layers is the number of layers the buffers passed to the call hold (a
+ *     per-layer call passes 1 and pointers offset to that layer).
+ *   - Layouts (row-major, D = head_dim, L = model->n_layers):
+ *       pool   [L][Hkv][pool_tokens][D]    documents' compiled K or V, concatenated
+ *       cache  [L][batch][Hkv][cache_cap][D]  slot index = logical position
+ *       suffix q / out       [L][batch][n_suffix][Hq][D]
+ *       suffix k / v         [L][batch][n_suffix][Hkv][D]
+ *       decode q / out       [L][batch][Hq][D];  decode k_new / v_new [L][batch][Hkv][D]
+ *   - Device pointers must be 16-byte aligned.  Query head h reads kv head h / (Hq/Hkv).
+ *   - Every argument check runs on the host before anything is enqueued.  A failing call
+ *     returns a negative pic_status, enqueues nothing, and leaves a description for
+ *     pic_last_error() (thread-local).  A launch failure returns PIC_ERR_HIP.  Faults during
+ *     asynchronous execution surface at the caller's next synchronisation.
+ *   - Device-side tables (gather blocks, context lengths) are read as given; kernels clamp
+ *     every index they derive from them to the buffer sizes passed on the host, so a bad
+ *     table gives wrong values, never an out-of-bounds access.
+ */
+#ifndef PIC_H
+#define PIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PIC_OK = 0,
+  PIC_ERR_INVALID_ARG = -1,  /* null pointer, negative size, inconsistent shape */
+  PIC_ERR_UNSUPPORTED = -2,  /* valid but not built: head_dim, dtype, head ratio */
+  PIC_ERR_WORKSPACE = -3,    /* workspace missing or smaller than the query call says */
+  PIC_ERR_CAPACITY = -4,     /* output array or cache too small for the request */
+  PIC_ERR_MISALIGNED = -5,   /* a device pointer is not 16-byte aligned */
+  PIC_ERR_RANGE = -6,        /* a position shift or index beyond the table or pool */
+  PIC_ERR_HIP = -7           /* the HIP runtime refused a launch */
+} pic_status;
+
+typedef enum { PIC_F32 = 0, PIC_BF16 = 1 } pic_dtype;
+
+/* Attention shape of the decoder whose caches are served. head_dim must be 64 or 128;
+   n_q_heads must be a multiple of n_kv_heads.  rope_theta is the RoPE base: pair i of a
+   head (elements i and i + D/2) turns by p * rope_theta^(-2i/D) at position p, the same
+   transform in every layer. */
+typedef struct {
+  int32_t n_layers;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  pic_dtype dtype;
+  double rope_theta;
+} pic_model;
+
+/* Most tokens one gather block carries. */
+#define PIC_BLOCK_TOKENS 64
+
+/* One gather block of the composition map: n_tokens (1..PIC_BLOCK_TOKENS) consecutive pool
+   tokens starting at src_token go to consecutive cache slots of `request` starting at
+   dst_slot, their keys turned by `delta` = logical position - compile position (one value
+   per document, since both run contiguously inside it; Sec. 2, Eq. 3). */
+typedef struct {
+  int32_t request;
+  int32_t src_token;
+  int32_t dst_slot;
+  int32_t n_tokens;
+  int32_t delta;
+} pic_block;
+
+/* ---- 1. plan (host only; Sec. 2 canonical order and link operator; App. C.1 token map) ----
+   Lays each request's pool entries (documents, and a stored prefix if any) back to back from
+   logical position 0 in the order given, and splits them into gather blocks.
+     batch                      number of requests (>= 1)
+     n_entries [host, batch]    entries each request composes (>= 0)
+     entries   [host, sum n]    pool entry ids, request by request, in logical order
+     n_pool_entries             size of the three per-entry arrays below
+     entry_offset [host]        first pool token of each entry
+     entry_len    [host]        tokens in each entry (>= 1)
+     entry_compile_pos [host]   position the entry's first token was compiled at
+     pool_tokens                tokens in the pool; every entry must lie inside it
+     blocks [host out]          room for block_cap blocks
+     n_blocks [host out]        blocks written; on PIC_ERR_CAPACITY, blocks needed
+     ctx_len [host out, batch]  composed context length of each request
+   Fails with PIC_ERR_RANGE for an entry id or token range outside the pool or a context
+   longer than INT32_MAX, and PIC_ERR_CAPACITY when block_cap is too small. */
+pic_status pic_plan_layout(int32_t batch, const int32_t* n_entries, const int32_t* entries,
+                           int32_t n_pool_entries, const int32_t* entry_offset,
+                           const int32_t* entry_len, const int32_t* entry_compile_pos,
+                           int64_t pool_tokens, pic_block* blocks, int32_t block_cap,
+                           int32_t* n_blocks, int32_t* ctx_len);
+
+/* ---- 2a. delta-angle table (Sec. 2, Eq. 3: R(b) R(a)^-1 = R(b - a)) ----
+   Table of (cos, sin) of delta * theta_i for delta = 0..max_abs_delta and i = 0..D/2-1,
+   float32 pairs laid out [max_abs_delta + 1][D/2][2]; angles and cos/sin are evaluated in
+   float64 and rounded once.  Negative shifts use the same row with sin negated.
+   pic_rope_table_bytes returns the size (0 for an unsupported model or a negative or too
+   large max_abs_delta, at most 1 << 20).  pic_rope_table_init fills `table` on `stream`. */
+size_t pic_rope_table_bytes(const pic_model* model, int32_t max_abs_delta);
+pic_status pic_rope_table_init(const pic_model* model, int32_t max_abs_delta, void* table,
+                               size_t table_bytes, void* stream);
+
+/* ---- 2b. standalone key re-rotation (Sec. 2, Eq. 3) ----
+   k_out[t][h] = R(delta[t]) k_in[t][h] for t < n_tokens, h < n_heads; rows of head_dim.
+   k_in/k_out [n_tokens][n_heads][D] (may be the same buffer), delta [n_tokens] device int32
+   with |delta| <= max_abs_delta (a larger entry is clamped to the table), table from
+   pic_rope_table_init for this model and max_abs_delta.  model->n_layers is ignored
+   (fold layers into n_tokens). */
+pic_status pic_rerotate_keys(const pic_model* model, const void* k_in, void* k_out,
+                             int64_t n_tokens, int32_t n_heads, const int32_t* delta,
+                             const void* table, int32_t max_abs_delta, void* stream);
+
+/* ---- 2c. composition: fused re-rotate + gather (Sec. 2 link operator and Eq. 3; App. C.1) ----
+   For every layer, gather block and kv head: cache_k rows = R(delta) * pool_k rows and
+   cache_v rows = pool_v rows (bit-exact copy).  blocks [n_blocks] is a device copy of
+   pic_plan_layout's output; a block whose request, source range, destination range or delta
+   falls outside batch, pool_tokens, cache_cap or max_abs_delta is skipped.  Slots no block
+   covers are left untouched. */
+pic_status pic_compose(const pic_model* model, const void* pool_k, const void* pool_v,
+                       int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                       const void* table, int32_t max_abs_delta, void* cache_k, void* cache_v,
+                       int32_t batch, int32_t cache_cap, void* stream);
+
+/* ---- 3. suffix prefill (App. C.1: inline KVs interleaved, frontier causal mask) ----
+   Appends k_suf/v_suf of request b at cache slots [ctx_len[b], ctx_len[b] + n_suffix), then
+   for suffix token i (logical position ctx_len[b] + i) and query head h computes
+     out = sum_{j <= ctx_len[b] + i} softmax_j(scale * q . k_j) v_j
+   over kv head h / (Hq/Hkv).  Suffix q/k must already carry their own rotation.
+     ctx_len [device, batch]  composed lengths; entries are clamped to [0, max_ctx]
+     max_ctx [host]           bound on ctx_len; max_ctx + n_suffix <= cache_cap
+     scale                    softmax scale; 0 means 1/sqrt(head_dim)
+     workspace                pic_prefill_workspace_bytes(...) bytes (may be 0 bytes) */
+size_t pic_prefill_workspace_bytes(const pic_model* model, int32_t batch, int32_t n_suffix,
+                                   int32_t max_ctx);
+pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const void* k_suf,
+                                   const void* v_suf, void* cache_k, void* cache_v,
+                                   int32_t batch, int32_t cache_cap, const int32_t* ctx_len,
+                                   int32_t max_ctx, int32_t n_suffix, float scale, void* out,
+                                   void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- 4. decode (App. C.1: ordinary autoregressive decoding over the completed cache) ----
+   For request b the new token sits at slot p = base_len[b] + step: k_new/v_new are written
+   there, then its query attends over slots [0, p].  Split-K over the context: n_splits
+   chunks per (request, kv head) (0 picks a value), merged by log-sum-exp.
+     base_len [device, batch]  valid slots before the first decode step; clamped to
+                               [0, max_base_len]; max_base_len + step + 1 <= cache_cap
+     workspace                 pic_decode_workspace_bytes(...) bytes for the same batch,
+                               max_base_len + step + 1 and n_splits */
+size_t pic_decode_workspace_bytes(const pic_model* model, int32_t batch, int32_t max_len,
+                                  int32_t n_splits);
+pic_status pic_decode_attn(const pic_model* model, const void* q, const void* k_new,
+                           const void* v_new, void* cache_k, void* cache_v, int32_t batch,
+                           int32_t cache_cap, const int32_t* base_len, int32_t step,
+                           int32_t max_base_len, float scale, int32_t n_splits, void* out,
+                           void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- diagnostics ---- */
+const char* pic_status_string(pic_status status);
+/* Thread-local description of the last failure on this thread ("" if none). */
+const char* pic_last_error(void);
+/* Split count pic_decode_attn picks for n_splits = 0 (host only). */
+int32_t pic_decode_auto_splits(const pic_model* model, int32_t batch, int32_t max_len);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIC_H */

@@ -1,0 +1,402 @@
+// C ABI of libpic: argument validation, the layout planner and dispatch to the HIP kernels.
+// Every check runs before anything is enqueued; a failing call launches nothing.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "pic.h"
+#include "pic_internal.h"
+
+#define PIC_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local std::string g_last_error;
+
+pic_status fail(pic_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+pic_status ok() {
+  g_last_error.clear();
+  return PIC_OK;
+}
+
+pic_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(PIC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define PIC_CHECK(expr)              \
+  do {                               \
+    pic_status _s = (expr);          \
+    if (_s != PIC_OK) return _s;     \
+  } while (0)
+
+pic_status check_ptr(const void* p, const char* name) {
+  if (p == nullptr) return fail(PIC_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned16(p)) return fail(PIC_ERR_MISALIGNED, "%s is not 16-byte aligned", name);
+  return PIC_OK;
+}
+
+pic_status check_model(const pic_model* m) {
+  if (m == nullptr) return fail(PIC_ERR_INVALID_ARG, "model is NULL");
+  if (m->n_layers < 0) return fail(PIC_ERR_INVALID_ARG, "n_layers < 0");
+  if (m->n_q_heads <= 0 || m->n_kv_heads <= 0)
+    return fail(PIC_ERR_INVALID_ARG, "head counts must be positive");
+  if (m->n_q_heads % m->n_kv_heads != 0)
+    return fail(PIC_ERR_INVALID_ARG, "n_q_heads (%d) is not a multiple of n_kv_heads (%d)",
+                m->n_q_heads, m->n_kv_heads);
+  if (m->head_dim != 64 && m->head_dim != 128)
+    return fail(PIC_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", m->head_dim);
+  if (m->dtype != PIC_F32 && m->dtype != PIC_BF16)
+    return fail(PIC_ERR_UNSUPPORTED, "dtype %d", (int)m->dtype);
+  return PIC_OK;
+}
+
+constexpr int32_t kMaxAbsDelta = 1 << 20;
+
+size_t elem_bytes(const pic_model* m) { return m->dtype == PIC_F32 ? 4 : 2; }
+
+float scale_log2_of(const pic_model* m, float scale) {
+  const double s = scale == 0.f ? 1.0 / std::sqrt((double)m->head_dim) : (double)scale;
+  return (float)(s * 1.4426950408889634);  // log2(e)
+}
+
+pic::AttnShape shape_of(const pic_model* m, int32_t batch, int32_t cache_cap, float scale) {
+  pic::AttnShape s;
+  s.n_layers = m->n_layers;
+  s.n_q_heads = m->n_q_heads;
+  s.n_kv_heads = m->n_kv_heads;
+  s.head_dim = m->head_dim;
+  s.batch = batch;
+  s.cache_cap = cache_cap;
+  s.scale_log2 = scale_log2_of(m, scale);
+  return s;
+}
+
+pic_status check_attn_model(const pic_model* m) {
+  PIC_CHECK(check_model(m));
+  if (m->dtype == PIC_BF16 && m->head_dim != 128)
+    return fail(PIC_ERR_UNSUPPORTED, "bf16 attention is built for head_dim 128 only");
+  return PIC_OK;
+}
+
+}  // namespace
+
+PIC_API const char* pic_status_string(pic_status s) {
+  switch (s) {
+    case PIC_OK: return "PIC_OK";
+    case PIC_ERR_INVALID_ARG: return "PIC_ERR_INVALID_ARG";
+    case PIC_ERR_UNSUPPORTED: return "PIC_ERR_UNSUPPORTED";
+    case PIC_ERR_WORKSPACE: return "PIC_ERR_WORKSPACE";
+    case PIC_ERR_CAPACITY: return "PIC_ERR_CAPACITY";
+    case PIC_ERR_MISALIGNED: return "PIC_ERR_MISALIGNED";
+    case PIC_ERR_RANGE: return "PIC_ERR_RANGE";
+    case PIC_ERR_HIP: return "PIC_ERR_HIP";
+  }
+  return "PIC_ERR_UNKNOWN";
+}
+
+PIC_API const char* pic_last_error(void) { return g_last_error.c_str(); }
+
+// ---------------------------------------------------------------------------------------------
+// 1. plan
+// ---------------------------------------------------------------------------------------------
+
+PIC_API pic_status pic_plan_layout(int32_t batch, const int32_t* n_entries, const int32_t* entries,
+                                   int32_t n_pool_entries, const int32_t* entry_offset,
+                                   const int32_t* entry_len, const int32_t* entry_compile_pos,
+                                   int64_t pool_tokens, pic_block* blocks, int32_t block_cap,
+                                   int32_t* n_blocks, int32_t* ctx_len) {
+  if (batch <= 0) return fail(PIC_ERR_INVALID_ARG, "batch must be >= 1");
+  if (!n_entries || !entry_offset || !entry_len || !entry_compile_pos || !n_blocks || !ctx_len)
+    return fail(PIC_ERR_INVALID_ARG, "a required host array is NULL");
+  if (n_pool_entries < 0 || block_cap < 0 || pool_tokens < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  int64_t total_entries = 0;
+  for (int32_t b = 0; b < batch; ++b) {
+    if (n_entries[b] < 0) return fail(PIC_ERR_INVALID_ARG, "n_entries[%d] < 0", b);
+    total_entries += n_entries[b];
+  }
+  if (total_entries > 0 && !entries) return fail(PIC_ERR_INVALID_ARG, "entries is NULL");
+  for (int32_t e = 0; e < n_pool_entries; ++e) {
+    if (entry_len[e] <= 0) return fail(PIC_ERR_INVALID_ARG, "entry_len[%d] must be >= 1", e);
+    if (entry_offset[e] < 0 || (int64_t)entry_offset[e] + entry_len[e] > pool_tokens)
+      return fail(PIC_ERR_RANGE, "pool entry %d [%d, %lld) lies outside the %lld-token pool", e,
+                  entry_offset[e], (long long)entry_offset[e] + entry_len[e],
+                  (long long)pool_tokens);
+    if (entry_compile_pos[e] < 0 || (int64_t)entry_compile_pos[e] + entry_len[e] > INT32_MAX)
+      return fail(PIC_ERR_RANGE, "entry_compile_pos[%d] out of range", e);
+  }
+  // count blocks and check ranges first, so a failing call writes nothing
+  int64_t need = 0;
+  const int32_t* ent = entries;
+  for (int32_t b = 0; b < batch; ++b) {
+    int64_t pos = 0;
+    for (int32_t k = 0; k < n_entries[b]; ++k) {
+      const int32_t e = ent[k];
+      if (e < 0 || e >= n_pool_entries)
+        return fail(PIC_ERR_RANGE, "request %d entry %d: pool entry id %d out of [0, %d)", b, k, e,
+                    n_pool_entries);
+      need += (entry_len[e] + PIC_BLOCK_TOKENS - 1) / PIC_BLOCK_TOKENS;
+      pos += entry_len[e];
+      if (pos > INT32_MAX) return fail(PIC_ERR_RANGE, "request %d context exceeds INT32_MAX", b);
+    }
+    ent += n_entries[b];
+  }
+  if (need > INT32_MAX) return fail(PIC_ERR_CAPACITY, "too many blocks");
+  *n_blocks = (int32_t)need;
+  if (need > block_cap)
+    return fail(PIC_ERR_CAPACITY, "%lld blocks needed, room for %d", (long long)need, block_cap);
+  if (need > 0 && !blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
+
+  int32_t nb = 0;
+  ent = entries;
+  for (int32_t b = 0; b < batch; ++b) {
+    int32_t pos = 0;   // logical position = cache slot
+    for (int32_t k = 0; k < n_entries[b]; ++k) {
+      const int32_t e = ent[k];
+      const int32_t len = entry_len[e];
+      const int32_t delta = pos - entry_compile_pos[e];  // b_i - a_i, Eq. 3
+      for (int32_t t = 0; t < len; t += PIC_BLOCK_TOKENS) {
+        pic_block& blk = blocks[nb++];
+        blk.request = b;
+        blk.src_token = entry_offset[e] + t;
+        blk.dst_slot = pos + t;
+        blk.n_tokens = len - t < PIC_BLOCK_TOKENS ? len - t : PIC_BLOCK_TOKENS;
+        blk.delta = delta;
+      }
+      pos += len;
+    }
+    ctx_len[b] = pos;
+    ent += n_entries[b];
+  }
+  return ok();
+}
+
+// ---------------------------------------------------------------------------------------------
+// 2. re-rotation and composition
+// ---------------------------------------------------------------------------------------------
+
+PIC_API size_t pic_rope_table_bytes(const pic_model* model, int32_t max_abs_delta) {
+  if (check_model(model) != PIC_OK) return 0;
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta) return 0;
+  return (size_t)(max_abs_delta + 1) * (model->head_dim / 2) * sizeof(float) * 2;
+}
+
+PIC_API pic_status pic_rope_table_init(const pic_model* model, int32_t max_abs_delta, void* table,
+                                       size_t table_bytes, void* stream) {
+  PIC_CHECK(check_model(model));
+  if (!(model->rope_theta > 1.0) || !std::isfinite(model->rope_theta))
+    return fail(PIC_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
+    return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
+  PIC_CHECK(check_ptr(table, "table"));
+  const size_t need = pic_rope_table_bytes(model, max_abs_delta);
+  if (table_bytes < need)
+    return fail(PIC_ERR_CAPACITY, "table needs %zu bytes, got %zu", need, table_bytes);
+  const int half = model->head_dim / 2;
+  double inv_freq[64];
+  for (int i = 0; i < half; ++i)
+    inv_freq[i] = std::pow(model->rope_theta, -2.0 * i / model->head_dim);
+  return hip_status(pic::launch_rope_table(inv_freq, half, max_abs_delta,
+                                           static_cast<float2*>(table), (hipStream_t)stream),
+                    "rope table launch");
+}
+
+PIC_API pic_status pic_rerotate_keys(const pic_model* model, const void* k_in, void* k_out,
+                                     int64_t n_tokens, int32_t n_heads, const int32_t* delta,
+                                     const void* table, int32_t max_abs_delta, void* stream) {
+  PIC_CHECK(check_model(model));
+  if (n_tokens < 0 || n_heads <= 0) return fail(PIC_ERR_INVALID_ARG, "n_tokens < 0 or n_heads < 1");
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
+    return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
+  if (n_tokens == 0) return ok();
+  PIC_CHECK(check_ptr(k_in, "k_in"));
+  PIC_CHECK(check_ptr(k_out, "k_out"));
+  PIC_CHECK(check_ptr(table, "table"));
+  if (!delta) return fail(PIC_ERR_INVALID_ARG, "delta is NULL");
+  return hip_status(pic::launch_rerotate(model->dtype, model->head_dim, k_in, k_out,
+                                         n_tokens * n_heads, n_heads, delta,
+                                         static_cast<const float2*>(table), max_abs_delta,
+                                         (hipStream_t)stream),
+                    "rerotate launch");
+}
+
+PIC_API pic_status pic_compose(const pic_model* model, const void* pool_k, const void* pool_v,
+                               int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                               const void* table, int32_t max_abs_delta, void* cache_k,
+                               void* cache_v, int32_t batch, int32_t cache_cap, void* stream) {
+  PIC_CHECK(check_model(model));
+  if (pool_tokens < 0 || n_blocks < 0 || batch < 0 || cache_cap < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
+    return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
+  if (model->n_kv_heads > 65535 || model->n_layers > 65535)
+    return fail(PIC_ERR_UNSUPPORTED, "more than 65535 kv heads or layers in one call");
+  if (n_blocks == 0 || model->n_layers == 0) return ok();
+  PIC_CHECK(check_ptr(pool_k, "pool_k"));
+  PIC_CHECK(check_ptr(pool_v, "pool_v"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  PIC_CHECK(check_ptr(table, "table"));
+  if (!blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
+  return hip_status(pic::launch_compose(model->dtype, model->head_dim, model->n_layers,
+                                        model->n_kv_heads, pool_k, pool_v, pool_tokens, blocks,
+                                        n_blocks, static_cast<const float2*>(table),
+                                        max_abs_delta, cache_k, cache_v, batch, cache_cap,
+                                        (hipStream_t)stream),
+                    "compose launch");
+}
+
+// ---------------------------------------------------------------------------------------------
+// 3. suffix prefill
+// ---------------------------------------------------------------------------------------------
+
+PIC_API size_t pic_prefill_workspace_bytes(const pic_model* model, int32_t batch, int32_t n_suffix,
+                                           int32_t max_ctx) {
+  if (check_attn_model(model) != PIC_OK || batch < 0 || n_suffix < 0 || max_ctx < 0) return 0;
+  if (model->dtype == PIC_F32) return 0;
+  return pic::prefill_bf16_workspace(shape_of(model, batch, max_ctx + n_suffix, 0.f), n_suffix,
+                                     max_ctx);
+}
+
+PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const void* k_suf,
+                                           const void* v_suf, void* cache_k, void* cache_v,
+                                           int32_t batch, int32_t cache_cap, const int32_t* ctx_len,
+                                           int32_t max_ctx, int32_t n_suffix, float scale,
+                                           void* out, void* workspace, size_t ws_bytes,
+                                           void* stream) {
+  PIC_CHECK(check_attn_model(model));
+  if (batch < 0 || cache_cap < 0 || max_ctx < 0 || n_suffix < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (!(scale >= 0.f) || !std::isfinite(scale))
+    return fail(PIC_ERR_INVALID_ARG, "scale must be finite and >= 0");
+  if ((int64_t)max_ctx + n_suffix > cache_cap)
+    return fail(PIC_ERR_CAPACITY, "max_ctx + n_suffix = %lld exceeds cache_cap %d",
+                (long long)max_ctx + n_suffix, cache_cap);
+  if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX)
+    return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
+  if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
+  PIC_CHECK(check_ptr(q, "q"));
+  PIC_CHECK(check_ptr(k_suf, "k_suf"));
+  PIC_CHECK(check_ptr(v_suf, "v_suf"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  PIC_CHECK(check_ptr(out, "out"));
+  if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
+  const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
+  if (need > 0 && (workspace == nullptr || ws_bytes < need))
+    return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  const hipStream_t st = (hipStream_t)stream;
+  const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
+  // a4: suffix K/V into slots [ctx, ctx + n_suffix) (App. C.1: inline KVs interleaved)
+  PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
+                                          model->n_kv_heads, k_suf, v_suf, cache_k, cache_v,
+                                          batch, cache_cap, ctx_len, max_ctx, 0, n_suffix, st),
+                       "suffix append launch"));
+  if (model->dtype == PIC_F32)
+    return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
+                                                static_cast<const float*>(cache_k),
+                                                static_cast<const float*>(cache_v), ctx_len,
+                                                max_ctx, 0, n_suffix, static_cast<float*>(out), st),
+                      "prefill attention launch");
+  return hip_status(pic::launch_prefill_bf16(s, static_cast<const pic::bf16_t*>(q),
+                                             static_cast<const pic::bf16_t*>(cache_k),
+                                             static_cast<const pic::bf16_t*>(cache_v), ctx_len,
+                                             max_ctx, n_suffix, static_cast<pic::bf16_t*>(out),
+                                             workspace, ws_bytes, st),
+                    "prefill attention launch");
+}
+
+// ---------------------------------------------------------------------------------------------
+// 4. decode
+// ---------------------------------------------------------------------------------------------
+
+PIC_API int32_t pic_decode_auto_splits(const pic_model* model, int32_t batch, int32_t max_len) {
+  if (check_attn_model(model) != PIC_OK || batch <= 0 || max_len <= 0) return 1;
+  if (model->dtype == PIC_F32) return 1;
+  return pic::decode_bf16_auto_splits(shape_of(model, batch, max_len, 0.f), max_len);
+}
+
+PIC_API size_t pic_decode_workspace_bytes(const pic_model* model, int32_t batch, int32_t max_len,
+                                          int32_t n_splits) {
+  if (check_attn_model(model) != PIC_OK || batch < 0 || max_len < 0 || n_splits < 0) return 0;
+  if (model->dtype == PIC_F32) return 0;
+  if (n_splits == 0) n_splits = pic_decode_auto_splits(model, batch, max_len);
+  return pic::decode_bf16_workspace(shape_of(model, batch, max_len, 0.f), max_len, n_splits);
+}
+
+PIC_API pic_status pic_decode_attn(const pic_model* model, const void* q, const void* k_new,
+                                   const void* v_new, void* cache_k, void* cache_v, int32_t batch,
+                                   int32_t cache_cap, const int32_t* base_len, int32_t step,
+                                   int32_t max_base_len, float scale, int32_t n_splits, void* out,
+                                   void* workspace, size_t ws_bytes, void* stream) {
+  PIC_CHECK(check_attn_model(model));
+  if (batch < 0 || cache_cap < 0 || step < 0 || max_base_len < 0 || n_splits < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (!(scale >= 0.f) || !std::isfinite(scale))
+    return fail(PIC_ERR_INVALID_ARG, "scale must be finite and >= 0");
+  const int64_t max_len = (int64_t)max_base_len + step + 1;
+  if (max_len > cache_cap)
+    return fail(PIC_ERR_CAPACITY, "max_base_len + step + 1 = %lld exceeds cache_cap %d",
+                (long long)max_len, cache_cap);
+  const int n_rep = model->n_q_heads / model->n_kv_heads;
+  if (model->dtype == PIC_BF16 && n_rep > 16)
+    return fail(PIC_ERR_UNSUPPORTED, "bf16 decode supports up to 16 query heads per kv head");
+  if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  if ((int64_t)batch * model->n_q_heads > INT32_MAX)
+    return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
+  if (batch == 0 || model->n_layers == 0) return ok();
+  PIC_CHECK(check_ptr(q, "q"));
+  PIC_CHECK(check_ptr(k_new, "k_new"));
+  PIC_CHECK(check_ptr(v_new, "v_new"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  PIC_CHECK(check_ptr(out, "out"));
+  if (!base_len) return fail(PIC_ERR_INVALID_ARG, "base_len is NULL");
+  const hipStream_t st = (hipStream_t)stream;
+  const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
+  if (model->dtype == PIC_F32) {
+    PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
+                                            model->n_kv_heads, k_new, v_new, cache_k, cache_v,
+                                            batch, cache_cap, base_len, max_base_len, step, 1, st),
+                         "decode append launch"));
+    return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
+                                                static_cast<const float*>(cache_k),
+                                                static_cast<const float*>(cache_v), base_len,
+                                                max_base_len, step, 1, static_cast<float*>(out), st),
+                      "decode attention launch");
+  }
+  if (n_splits == 0) n_splits = pic::decode_bf16_auto_splits(s, (int32_t)max_len);
+  if ((int64_t)n_splits * batch * model->n_kv_heads > INT32_MAX)
+    return fail(PIC_ERR_UNSUPPORTED, "too many splits");
+  if (n_splits > max_len) n_splits = (int32_t)max_len;
+  const size_t need = pic::decode_bf16_workspace(s, (int32_t)max_len, n_splits);
+  if (workspace == nullptr || ws_bytes < need)
+    return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  PIC_CHECK(check_ptr(workspace, "workspace"));
+  PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
+                                          model->n_kv_heads, k_new, v_new, cache_k, cache_v, batch,
+                                          cache_cap, base_len, max_base_len, step, 1, st),
+                       "decode append launch"));
+  return hip_status(pic::launch_decode_bf16(s, static_cast<const pic::bf16_t*>(q),
+                                            static_cast<const pic::bf16_t*>(cache_k),
+                                            static_cast<const pic::bf16_t*>(cache_v), base_len,
+                                            max_base_len, step, n_splits,
+                                            static_cast<pic::bf16_t*>(out), workspace, ws_bytes, st),
+                    "decode attention launch");
+}

@@ -1,0 +1,76 @@
+// Internal declarations of libpic: device helpers and the kernel launchers the C ABI calls.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pic.h"
+
+namespace pic {
+
+typedef uint16_t bf16_t;  // bfloat16 bit pattern
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// float -> bfloat16, round to nearest even (inputs here are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
+// ---- launchers (each returns hipSuccess or the launch error) ----
+
+hipError_t launch_rope_table(const double* inv_freq_host, int half, int32_t max_abs_delta,
+                             float2* table, hipStream_t stream);
+
+hipError_t launch_rerotate(pic_dtype dt, int head_dim, const void* k_in, void* k_out,
+                           int64_t n_rows, int32_t n_heads, const int32_t* delta,
+                           const float2* table, int32_t max_abs_delta, hipStream_t stream);
+
+hipError_t launch_compose(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                          const void* pool_k, const void* pool_v, int64_t pool_tokens,
+                          const pic_block* blocks, int32_t n_blocks, const float2* table,
+                          int32_t max_abs_delta, void* cache_k, void* cache_v, int32_t batch,
+                          int32_t cache_cap, hipStream_t stream);
+
+// Writes suffix (n_new tokens per request) K/V rows [L][B][n_new][Hkv][D] into cache slots
+// [base[b] + offset, base[b] + offset + n_new) with base clamped to [0, max_base].
+hipError_t launch_append(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                         const void* k_new, const void* v_new, void* cache_k, void* cache_v,
+                         int32_t batch, int32_t cache_cap, const int32_t* base, int32_t max_base,
+                         int32_t offset, int32_t n_new, hipStream_t stream);
+
+struct AttnShape {
+  int n_layers, n_q_heads, n_kv_heads, head_dim, batch, cache_cap;
+  float scale_log2;  // softmax scale * log2(e)
+};
+
+// fp32 attention, one query row per workgroup.  Prefill: rows [L][B][n_q][Hq], query token i
+// of request b sits at position base[b] + offset + i and sees slots [0, that position].
+hipError_t launch_attn_rows_f32(const AttnShape& s, const float* q, const float* cache_k,
+                                const float* cache_v, const int32_t* base, int32_t max_base,
+                                int32_t offset, int32_t n_q, float* out, hipStream_t stream);
+
+size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx);
+hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
+                               const bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
+                               int32_t n_suffix, bf16_t* out, void* workspace, size_t ws_bytes,
+                               hipStream_t stream);
+
+int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len);
+size_t decode_bf16_workspace(const AttnShape& s, int32_t max_len, int32_t n_splits);
+hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
+                              const bf16_t* cache_v, const int32_t* base_len, int32_t max_base,
+                              int32_t step, int32_t n_splits, bf16_t* out, void* workspace,
+                              size_t ws_bytes, hipStream_t stream);
+
+}  // namespace pic

@@ -1,0 +1,279 @@
+// RoPE relocation of cached keys and composition of document caches (Sec. 2, Eq. 3; App. C.1).
+//
+// A key compiled at position a moves to position b by R(b) R(a)^-1 = R(b - a): each pair
+// (x_i, x_{i+D/2}) turns by delta * theta_i.  Both positions run contiguously through a
+// document, so one delta serves a whole gather block and its cos/sin row is loaded once per
+// workgroup from a table built in float64.  Values are copied unchanged.
+//
+// Memory traffic is the whole cost (6 flops per 2 elements), so every access is a 16-byte
+// vector and a row of D elements is split across lanes such that one lane owns element
+// chunk [c, c + VEC) of both halves: the two members of every rotated pair sit in the
+// same lane.
+#include "pic_internal.h"
+
+namespace pic {
+namespace {
+
+struct InvFreq {
+  double v[64];
+};
+
+__global__ void rope_table_kernel(InvFreq invf, int half, int32_t max_abs_delta, float2* table) {
+  const int64_t n = (int64_t)(max_abs_delta + 1) * half;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t d = idx / half;
+    const int i = (int)(idx - d * half);
+    const double ang = (double)d * invf.v[i];
+    table[idx] = make_float2((float)cos(ang), (float)sin(ang));
+  }
+}
+
+template <typename T>
+struct Vec16;  // 16 bytes of T as float lanes
+
+template <>
+struct Vec16<float> {
+  static constexpr int N = 4;
+  __device__ static void load(const float* p, float (&x)[4]) {
+    const float4 v = *reinterpret_cast<const float4*>(p);
+    x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+  }
+  __device__ static void store(float* p, const float (&x)[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+  }
+};
+
+template <>
+struct Vec16<bf16_t> {
+  static constexpr int N = 8;
+  __device__ static void load(const bf16_t* p, float (&x)[8]) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ static void store(bf16_t* p, const float (&x)[8]) {
+    uint4 v;
+    v.x = pack_bf16x2(x[0], x[1]);
+    v.y = pack_bf16x2(x[2], x[3]);
+    v.z = pack_bf16x2(x[4], x[5]);
+    v.w = pack_bf16x2(x[6], x[7]);
+    *reinterpret_cast<uint4*>(p) = v;
+  }
+};
+
+// cos/sin of the lane's VEC frequencies for shift delta (|delta| already within the table).
+template <int VEC, int HALF>
+__device__ __forceinline__ void load_cs(const float2* table, int32_t delta, int c0, float (&cs)[VEC],
+                                        float (&sn)[VEC]) {
+  const int32_t ad = delta < 0 ? -delta : delta;
+  const float2* row = table + (int64_t)ad * HALF + c0;
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) {
+    const float2 t = row[i];
+    cs[i] = t.x;
+    sn[i] = delta < 0 ? -t.y : t.y;
+  }
+}
+
+template <int VEC>
+__device__ __forceinline__ void rotate(float (&x1)[VEC], float (&x2)[VEC], const float (&cs)[VEC],
+                                       const float (&sn)[VEC]) {
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) {
+    const float a = x1[i], b = x2[i];
+    x1[i] = fmaf(a, cs[i], -(b * sn[i]));
+    x2[i] = fmaf(a, sn[i], b * cs[i]);
+  }
+}
+
+// grid (n_blocks, Hkv, L), 256 threads.  One workgroup moves one gather block of one kv head.
+template <typename T, int HD>
+__global__ void __launch_bounds__(256) compose_kernel(
+    const T* __restrict__ pool_k, const T* __restrict__ pool_v, int64_t pool_tokens,
+    const pic_block* __restrict__ blocks, const float2* __restrict__ table, int32_t max_abs_delta,
+    T* __restrict__ cache_k, T* __restrict__ cache_v, int32_t batch, int32_t cache_cap) {
+  using V = Vec16<T>;
+  constexpr int VEC = V::N;
+  constexpr int HALF = HD / 2;
+  constexpr int LPR = HALF / VEC;          // lanes per row
+  constexpr int RPP = 256 / LPR;           // rows per pass
+  constexpr int PASSES = (PIC_BLOCK_TOKENS + RPP - 1) / RPP;
+
+  const pic_block blk = blocks[blockIdx.x];
+  if (blk.request < 0 || blk.request >= batch || blk.n_tokens <= 0 ||
+      blk.n_tokens > PIC_BLOCK_TOKENS || blk.src_token < 0 ||
+      (int64_t)blk.src_token + blk.n_tokens > pool_tokens || blk.dst_slot < 0 ||
+      (int64_t)blk.dst_slot + blk.n_tokens > cache_cap || blk.delta > max_abs_delta ||
+      blk.delta < -max_abs_delta)
+    return;
+
+  const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
+  const int j = threadIdx.x % LPR, r0 = threadIdx.x / LPR;
+  const int c0 = j * VEC;
+
+  float cs[VEC], sn[VEC];
+  load_cs<VEC, HALF>(table, blk.delta, c0, cs, sn);
+
+  const int64_t src_row0 = ((int64_t)l * Hkv + h) * pool_tokens + blk.src_token;
+  const int64_t dst_row0 = (((int64_t)l * batch + blk.request) * Hkv + h) * cache_cap + blk.dst_slot;
+
+  float k1[PASSES][VEC], k2[PASSES][VEC], v1[PASSES][VEC], v2[PASSES][VEC];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const int t = r0 + p * RPP;
+    if (t < blk.n_tokens) {
+      const int64_t s = (src_row0 + t) * HD;
+      V::load(pool_k + s + c0, k1[p]);
+      V::load(pool_k + s + HALF + c0, k2[p]);
+      V::load(pool_v + s + c0, v1[p]);
+      V::load(pool_v + s + HALF + c0, v2[p]);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const int t = r0 + p * RPP;
+    if (t < blk.n_tokens) {
+      rotate<VEC>(k1[p], k2[p], cs, sn);
+      const int64_t d = (dst_row0 + t) * HD;
+      V::store(cache_k + d + c0, k1[p]);
+      V::store(cache_k + d + HALF + c0, k2[p]);
+      V::store(cache_v + d + c0, v1[p]);
+      V::store(cache_v + d + HALF + c0, v2[p]);
+    }
+  }
+}
+
+// rows [n_tokens][n_heads][HD]; one (row, chunk) per thread, grid-stride.
+template <typename T, int HD>
+__global__ void __launch_bounds__(256) rerotate_kernel(const T* k_in, T* k_out, int64_t n_rows,
+                                                       int32_t n_heads, const int32_t* __restrict__ delta,
+                                                       const float2* __restrict__ table,
+                                                       int32_t max_abs_delta) {
+  using V = Vec16<T>;
+  constexpr int VEC = V::N;
+  constexpr int HALF = HD / 2;
+  constexpr int LPR = HALF / VEC;
+  const int64_t n_items = n_rows * LPR;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n_items;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = idx / LPR;
+    const int c0 = (int)(idx - row * LPR) * VEC;
+    int32_t d = delta[row / n_heads];
+    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
+    float cs[VEC], sn[VEC], x1[VEC], x2[VEC];
+    load_cs<VEC, HALF>(table, d, c0, cs, sn);
+    V::load(k_in + row * HD + c0, x1);
+    V::load(k_in + row * HD + HALF + c0, x2);
+    rotate<VEC>(x1, x2, cs, sn);
+    V::store(k_out + row * HD + c0, x1);
+    V::store(k_out + row * HD + HALF + c0, x2);
+  }
+}
+
+// New rows [L][B][n_new][Hkv][HD] -> cache slots base[b] + offset + i.  16 bytes per thread.
+template <typename T, int HD>
+__global__ void __launch_bounds__(256) append_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
+                                                     T* __restrict__ cache_k, T* __restrict__ cache_v,
+                                                     int n_kv_heads, int32_t batch, int32_t cache_cap,
+                                                     const int32_t* __restrict__ base, int32_t max_base,
+                                                     int32_t offset, int32_t n_new, int64_t n_rows) {
+  constexpr int CPR = HD * sizeof(T) / 16;  // 16-byte chunks per row
+  const int64_t n_items = n_rows * CPR;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n_items;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = idx / CPR;
+    const int c = (int)(idx - row * CPR);
+    // row = ((l * B + b) * n_new + i) * Hkv + h
+    const int h = (int)(row % n_kv_heads);
+    const int64_t r1 = row / n_kv_heads;
+    const int i = (int)(r1 % n_new);
+    const int64_t lb = r1 / n_new;  // l * B + b
+    const int b = (int)(lb % batch);
+    int32_t bl = base[b];
+    bl = bl < 0 ? 0 : (bl > max_base ? max_base : bl);
+    const int64_t slot = (int64_t)bl + offset + i;
+    if (slot >= cache_cap) continue;
+    const int64_t dst = ((lb * n_kv_heads + h) * cache_cap + slot) * HD;
+    const uint4* sk = reinterpret_cast<const uint4*>(k_new + row * HD) + c;
+    const uint4* sv = reinterpret_cast<const uint4*>(v_new + row * HD) + c;
+    reinterpret_cast<uint4*>(cache_k + dst)[c] = *sk;
+    reinterpret_cast<uint4*>(cache_v + dst)[c] = *sv;
+  }
+}
+
+int grid_for(int64_t items, int threads) {
+  int64_t g = (items + threads - 1) / threads;
+  if (g < 1) g = 1;
+  if (g > 65536) g = 65536;
+  return (int)g;
+}
+
+}  // namespace
+
+hipError_t launch_rope_table(const double* inv_freq_host, int half, int32_t max_abs_delta,
+                             float2* table, hipStream_t stream) {
+  InvFreq f;
+  for (int i = 0; i < 64; ++i) f.v[i] = i < half ? inv_freq_host[i] : 0.0;
+  const int64_t n = (int64_t)(max_abs_delta + 1) * half;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(grid_for(n, 256)), dim3(256), 0, stream, f, half,
+                     max_abs_delta, table);
+  return hipGetLastError();
+}
+
+#define PIC_DISPATCH_TD(dt, hd, KERNEL_CALL)                                      \
+  do {                                                                            \
+    if ((dt) == PIC_F32 && (hd) == 64) { using T = float; constexpr int HD = 64; KERNEL_CALL; } \
+    else if ((dt) == PIC_F32) { using T = float; constexpr int HD = 128; KERNEL_CALL; }         \
+    else if ((hd) == 64) { using T = bf16_t; constexpr int HD = 64; KERNEL_CALL; }               \
+    else { using T = bf16_t; constexpr int HD = 128; KERNEL_CALL; }                              \
+  } while (0)
+
+hipError_t launch_rerotate(pic_dtype dt, int head_dim, const void* k_in, void* k_out,
+                           int64_t n_rows, int32_t n_heads, const int32_t* delta,
+                           const float2* table, int32_t max_abs_delta, hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  PIC_DISPATCH_TD(dt, head_dim, {
+    constexpr int LPR = HD / 2 / (16 / (int)sizeof(T));
+    hipLaunchKernelGGL((rerotate_kernel<T, HD>), dim3(grid_for(n_rows * LPR, 256)), dim3(256), 0,
+                       stream, (const T*)k_in, (T*)k_out, n_rows, n_heads, delta, table,
+                       max_abs_delta);
+  });
+  return hipGetLastError();
+}
+
+hipError_t launch_compose(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                          const void* pool_k, const void* pool_v, int64_t pool_tokens,
+                          const pic_block* blocks, int32_t n_blocks, const float2* table,
+                          int32_t max_abs_delta, void* cache_k, void* cache_v, int32_t batch,
+                          int32_t cache_cap, hipStream_t stream) {
+  if (n_blocks == 0 || n_layers == 0) return hipSuccess;
+  const dim3 grid(n_blocks, n_kv_heads, n_layers);
+  PIC_DISPATCH_TD(dt, head_dim, {
+    hipLaunchKernelGGL((compose_kernel<T, HD>), grid, dim3(256), 0, stream, (const T*)pool_k,
+                       (const T*)pool_v, pool_tokens, blocks, table, max_abs_delta, (T*)cache_k,
+                       (T*)cache_v, batch, cache_cap);
+  });
+  return hipGetLastError();
+}
+
+hipError_t launch_append(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
+                         const void* k_new, const void* v_new, void* cache_k, void* cache_v,
+                         int32_t batch, int32_t cache_cap, const int32_t* base, int32_t max_base,
+                         int32_t offset, int32_t n_new, hipStream_t stream) {
+  const int64_t n_rows = (int64_t)n_layers * batch * n_new * n_kv_heads;
+  if (n_rows == 0) return hipSuccess;
+  PIC_DISPATCH_TD(dt, head_dim, {
+    constexpr int CPR = HD * (int)sizeof(T) / 16;
+    hipLaunchKernelGGL((append_kernel<T, HD>), dim3(grid_for(n_rows * CPR, 256)), dim3(256), 0,
+                       stream, (const T*)k_new, (const T*)v_new, (T*)cache_k, (T*)cache_v,
+                       n_kv_heads, batch, cache_cap, base, max_base, offset, n_new, n_rows);
+  });
+  return hipGetLastError();
+}
+
+}  // namespace pic

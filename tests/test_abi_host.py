@@ -1,0 +1,177 @@
+"""Host-side checks of the C ABI: the library loads and exports every declared symbol, the
+layout planner matches the oracle's slot map bit for bit, and every argument check fails
+with its status code before anything is enqueued (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings
+from hypothesis import strategies as st
+
+import paper_2607_28069_amd as pic
+from oracle import pic_oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pic.LIB_PATH):
+        from paper_2607_28069_amd.build import build
+        build()
+    return pic.load()
+
+
+def test_library_exports_every_declared_symbol(lib):
+    header = open(os.path.join(ROOT, "include", "pic.h")).read()
+    declared = set(re.findall(r"\b(pic_[a-z0-9_]+)\s*\(", header))
+    assert declared == set(pic.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert pic.pic_status_string(-6) == "PIC_ERR_RANGE"
+
+
+def _expand(blocks, batch):
+    """Per request: slot -> (src token, delta) from the planner's gather blocks."""
+    out = [dict() for _ in range(batch)]
+    for b in blocks:
+        assert 1 <= b["n_tokens"] <= pic.PIC_BLOCK_TOKENS
+        for t in range(b["n_tokens"]):
+            slot = int(b["dst_slot"]) + t
+            assert slot not in out[b["request"]]
+            out[b["request"]][slot] = (int(b["src_token"]) + t, int(b["delta"]))
+    return out
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.data())
+def test_planner_matches_oracle_layout(lib, data):
+    n_pool = data.draw(st.integers(1, 10))
+    lens = np.array(data.draw(st.lists(st.integers(1, 200), min_size=n_pool, max_size=n_pool)))
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+    cpos = np.array(data.draw(st.lists(st.integers(0, 3000), min_size=n_pool, max_size=n_pool)))
+    batch = data.draw(st.integers(1, 4))
+    reqs = [list(data.draw(st.permutations(range(n_pool)))[: data.draw(st.integers(0, n_pool))])
+            for _ in range(batch)]
+    blocks, ctx = pic.pic_plan_layout(reqs, offs, lens, cpos, int(lens.sum()))
+    maps = O.plan_layout(reqs, offs, lens, cpos)
+    got = _expand(blocks, batch)
+    for b, m in enumerate(maps):
+        assert ctx[b] == m.ctx_len
+        assert sorted(got[b]) == list(range(m.ctx_len))
+        src = np.array([got[b][s][0] for s in range(m.ctx_len)], dtype=np.int64)
+        delta = np.array([got[b][s][1] for s in range(m.ctx_len)], dtype=np.int64)
+        assert np.array_equal(src, m.src_token)
+        assert np.array_equal(delta, m.logical_pos - m.compile_pos)
+
+
+def test_planner_tiny_workload(lib):
+    blocks, ctx = pic.pic_plan_layout([[2, 0, 1]], [0, 128, 256], [128, 128, 16], [0, 0, 0], 272)
+    assert list(ctx) == [272]
+    rows = [tuple(int(x) for x in b) for b in blocks]
+    assert rows == [(0, 256, 0, 16, 0), (0, 0, 16, 64, 16), (0, 64, 80, 64, 16),
+                    (0, 128, 144, 64, 144), (0, 192, 208, 64, 144)]
+
+
+def test_planner_errors(lib):
+    with pytest.raises(pic.PicError) as e:
+        pic.pic_plan_layout([[0, 3]], [0, 10], [10, 10], [0, 0], 20)
+    assert e.value.status == -6                          # entry id out of range
+    with pytest.raises(pic.PicError) as e:
+        pic.pic_plan_layout([[0]], [0, 15], [10, 10], [0, 0], 20)
+    assert e.value.status == -6                          # entry outside the pool
+    with pytest.raises(pic.PicError) as e:
+        pic.pic_plan_layout([[0]], [0], [0], [0], 20)
+    assert e.value.status == -1                          # empty entry
+    n = ctypes.c_int32(0)
+    ctx = np.zeros(1, np.int32)
+    one = np.array([1], np.int32)
+    z = np.array([0], np.int32)
+    ln = np.array([200], np.int32)
+    P = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    blk = np.zeros(2, pic.BLOCK_DTYPE)
+    st_ = lib.pic_plan_layout(1, P(one), P(z), 1, P(z), P(ln), P(z), 200, P(blk), 2, ctypes.byref(n), P(ctx))
+    assert st_ == -4 and n.value == 4                    # capacity: 4 blocks needed
+    assert "4 blocks needed" in pic.pic_last_error()
+
+
+FAKE = 0x10000          # an aligned, never-dereferenced device address
+MIS = 0x10008           # misaligned
+
+
+def _model(**kw):
+    base = dict(n_layers=1, n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16", rope_theta=5e5)
+    base.update(kw)
+    return pic.Model.of(**base)
+
+
+def _compose(lib, m, **kw):
+    a = dict(pool_k=FAKE, pool_v=FAKE, pool_tokens=1000, blocks=FAKE, n_blocks=4, table=FAKE,
+             max_abs_delta=100, cache_k=FAKE, cache_v=FAKE, batch=2, cache_cap=1000)
+    a.update(kw)
+    return lib.pic_compose(ctypes.byref(m), a["pool_k"], a["pool_v"], a["pool_tokens"], a["blocks"],
+                           a["n_blocks"], a["table"], a["max_abs_delta"], a["cache_k"], a["cache_v"],
+                           a["batch"], a["cache_cap"], None)
+
+
+def _prefill(lib, m, ws_bytes=0, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, ck=FAKE, cv=FAKE, batch=2, cap=600, ctx=FAKE, max_ctx=500,
+             ns=64, scale=0.0, out=FAKE)
+    a.update(kw)
+    return lib.pic_suffix_prefill_attn(ctypes.byref(m), a["q"], a["k"], a["v"], a["ck"], a["cv"],
+                                       a["batch"], a["cap"], a["ctx"], a["max_ctx"], a["ns"],
+                                       a["scale"], a["out"], None, ws_bytes, None)
+
+
+def _decode(lib, m, ws=FAKE, ws_bytes=1 << 30, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, ck=FAKE, cv=FAKE, batch=2, cap=600, base=FAKE, step=0,
+             max_base=500, scale=0.0, splits=0, out=FAKE)
+    a.update(kw)
+    return lib.pic_decode_attn(ctypes.byref(m), a["q"], a["k"], a["v"], a["ck"], a["cv"], a["batch"],
+                               a["cap"], a["base"], a["step"], a["max_base"], a["scale"], a["splits"],
+                               a["out"], ws, ws_bytes, None)
+
+
+def test_argument_checks_fail_before_any_launch(lib):
+    m = _model()
+    assert _compose(lib, _model(head_dim=96)) == -2
+    assert _compose(lib, _model(n_q_heads=30)) == -1
+    assert _compose(lib, _model(dtype=7)) == -2
+    assert _compose(lib, m, pool_k=None) == -1
+    assert _compose(lib, m, cache_v=MIS) == -5
+    assert _compose(lib, m, max_abs_delta=-1) == -6
+    assert _compose(lib, m, batch=-1) == -1
+    assert _compose(lib, m, n_blocks=0) == 0            # nothing to do, nothing launched
+
+    assert _prefill(lib, m, max_ctx=580) == -4           # 580 + 64 > cache_cap 600
+    assert _prefill(lib, m, q=MIS) == -5
+    assert _prefill(lib, m, ctx=None) == -1
+    assert _prefill(lib, m, scale=-1.0) == -1
+    assert _prefill(lib, _model(head_dim=64)) == -2      # bf16 attention: head_dim 128 only
+    assert _prefill(lib, m, ns=0) == 0
+
+    assert _decode(lib, m, step=100) == -4               # 500 + 100 + 1 > 600
+    assert _decode(lib, m, ws=None) == -3
+    assert _decode(lib, m, ws_bytes=16) == -3
+    assert _decode(lib, _model(n_q_heads=136, n_kv_heads=8)) == -2   # 17 heads per kv head
+    assert _decode(lib, m, base=None) == -1
+    assert "base_len" in pic.pic_last_error()
+
+    assert lib.pic_rerotate_keys(ctypes.byref(m), FAKE, FAKE, 10, 8, None, FAKE, 10, None) == -1
+    assert lib.pic_rerotate_keys(ctypes.byref(m), MIS, FAKE, 10, 8, FAKE, FAKE, 10, None) == -5
+    assert lib.pic_rope_table_init(ctypes.byref(m), 10, FAKE, 16, None) == -4
+    assert lib.pic_rope_table_init(ctypes.byref(_model(rope_theta=0.5)), 10, FAKE, 1 << 20, None) == -1
+
+
+def test_sizes(lib):
+    m = _model()
+    assert pic.pic_rope_table_bytes(m, 65535) == 65536 * 64 * 8
+    assert pic.pic_rope_table_bytes(m, -1) == 0
+    assert pic.pic_rope_table_bytes(m, (1 << 20) + 1) == 0
+    s = pic.pic_decode_auto_splits(m, 64, 16640)
+    assert s >= 1
+    assert pic.pic_decode_workspace_bytes(m, 64, 16640, 0) == 64 * 32 * s * 130 * 4
+    assert pic.pic_decode_workspace_bytes(m, 64, 16640, 3) == 64 * 32 * 3 * 130 * 4
+    assert pic.pic_prefill_workspace_bytes(_model(dtype="f32", head_dim=64), 1, 16, 272) == 0
