@@ -149,20 +149,19 @@ __global__ void __launch_bounds__(64) decode_bf16_kernel(DecodeArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int key = k0 + 16 * mb + 4 * g4 + e;
-        const float s = key < c1 ? sacc[mb][e] * a.scale_log2 : -INFINITY;
-        sacc[mb][e] = s;
-        mx = fmaxf(mx, s);
+        if (key >= c1) sacc[mb][e] = -INFINITY;
+        mx = fmaxf(mx, sacc[mb][e]);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
+    const float m_new = fmaxf(m_run, mx * a.scale_log2);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     m_run = m_new;
     float p[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      p[e] = exp2f(sacc[0][e] - m_new);
-      p[4 + e] = exp2f(sacc[1][e] - m_new);
+      p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[0][e], a.scale_log2, -m_new));
+      p[4 + e] = __builtin_amdgcn_exp2f(fmaf(sacc[1][e], a.scale_log2, -m_new));
     }
     float psum = 0.f;
 #pragma unroll
@@ -206,7 +205,7 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
   for (int s = 0; s < n_splits; ++s) {
     const float ms = ml[2 * s];
     if (ms == -INFINITY) continue;
-    const float w = exp2f(ms - M);
+    const float w = __builtin_amdgcn_exp2f(ms - M);
     den += w * ml[2 * s + 1];
     const float2 o = *reinterpret_cast<const float2*>(ws_o + (row * n_splits + s) * kHD + d);
     o0 += w * o.x;
@@ -220,7 +219,7 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
 
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len) {
   const int64_t pairs = (int64_t)s.batch * s.n_kv_heads;
-  const int64_t target_waves = 4096;
+  const int64_t target_waves = 2048;   // about one resident round of waves
   int64_t splits = (target_waves + pairs - 1) / pairs;
   const int64_t max_splits = (max_len + 255) / 256;   // keep chunks >= 256 keys
   if (splits > max_splits) splits = max_splits;

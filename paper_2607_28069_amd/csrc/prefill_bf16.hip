@@ -119,16 +119,16 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int kq = tid >> 4;          // K: keys kq + 16 u;  V: keys 4 kq + u   (u = 0..3)
   u32x4 kreg[4], vreg[4];
 
+  // Rows past the last key are clamped to it: their scores are masked, so they enter the
+  // PV product with probability 0 (finite values, no branch around the loads).
   auto load_tile = [&](int t) {
     const int k0 = t * kKeys;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int kk = k0 + kq + 16 * u;
-      kreg[u] = kk < n_keys ? *reinterpret_cast<const u32x4*>(Kg + (int64_t)kk * kHD + 8 * dc)
-                            : u32x4{0, 0, 0, 0};
-      const int kv = k0 + 4 * kq + u;
-      vreg[u] = kv < n_keys ? *reinterpret_cast<const u32x4*>(Vg + (int64_t)kv * kHD + 8 * dc)
-                            : u32x4{0, 0, 0, 0};
+      const int kk = min(k0 + kq + 16 * u, n_keys - 1);
+      kreg[u] = *reinterpret_cast<const u32x4*>(Kg + (int64_t)kk * kHD + 8 * dc);
+      const int kv = min(k0 + 4 * kq + u, n_keys - 1);
+      vreg[u] = *reinterpret_cast<const u32x4*>(Vg + (int64_t)kv * kHD + 8 * dc);
     }
   };
 
@@ -171,73 +171,73 @@ prefill_bf16_kernel(PrefillArgs a) {
 
     // ---- S^T = K Q^T for keys [64 t, 64 t + 64): two 32-key blocks
     const uint32_t* kb = k_lds + buf * kKBuf;
-    f32x16_t sacc[2];
+    // two independent accumulation chains, interleaved
+    f32x16_t sacc[2] = {f32x16_t{}, f32x16_t{}};
+    const uint32_t* krow = kb + n * kKStride + 4 * hh;
 #pragma unroll
-    for (int kb2 = 0; kb2 < 2; ++kb2) {
-      sacc[kb2] = f32x16_t{};
-      const uint32_t* krow = kb + (32 * kb2 + n) * kKStride + 4 * hh;
+    for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(krow + 8 * ks);
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(krow + 32 * kb2 * kKStride + 8 * ks);
         sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qop[ks], sacc[kb2], 0, 0, 0);
       }
-    }
 
-    // ---- online softmax over this lane's query column
+    // ---- online softmax over this lane's query column.  Scores stay unscaled until the
+    // exponent: p = exp2(s * scale * log2(e) - m), one FMA and one v_exp_f32 per score.
     const int k0 = t * kKeys;
-    const bool need_mask = k0 + kKeys - 1 > ctx;   // tile reaches into the suffix (or past it)
+    if (k0 + kKeys - 1 > ctx) {   // tile reaches into the suffix (or past the last key)
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = k0 + 32 * kb2 + 8 * (e >> 2) + 4 * hh + (e & 3);
+          if (key > qpos) sacc[kb2][e] = -INFINITY;
+        }
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float s = sacc[kb2][e] * a.scale_log2;
-        if (need_mask) {
-          const int key = k0 + 32 * kb2 + 8 * (e >> 2) + 4 * hh + (e & 3);
-          if (key > qpos) s = -INFINITY;
-        }
-        sacc[kb2][e] = s;
-        mx = fmaxf(mx, s);
-      }
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[kb2][e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
+    const float m_tile = mx * a.scale_log2;
+    // The reference max only moves when a score exceeds it by more than 2^8 (then the
+    // accumulators are rescaled, for the whole wave at once); otherwise p <= 256, which
+    // float32 sums and bf16 probabilities hold without loss of relative precision.
+    if (__any(m_tile > m_run + 8.f)) {
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int db = 0; db < 4; ++db) oacc[db] *= alpha;
+    }
 
-    bf16x8_t pop[4];
+    // ---- P^T (bf16) slice by slice, each followed by its four O^T += V^T P^T products
+    // (four independent accumulators), so the exponentials of the next slice can overlap the
+    // matrix products of the current one.
+    const uint32_t* vb = v_lds + buf * kVBuf;
     float psum = 0.f;
 #pragma unroll
-    for (int kb2 = 0; kb2 < 2; ++kb2)
+    for (int s4 = 0; s4 < 4; ++s4) {
+      const int kb2 = s4 >> 1, u = s4 & 1;
+      uint32_t pw[4];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        uint32_t pw[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float p0 = exp2f(sacc[kb2][8 * u + 2 * j] - m_new);
-          const float p1 = exp2f(sacc[kb2][8 * u + 2 * j + 1] - m_new);
-          psum += p0 + p1;
-          pw[j] = pack_bf16x2(p0, p1);
-        }
-        pop[2 * kb2 + u] = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
+      for (int j = 0; j < 4; ++j) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[kb2][8 * u + 2 * j], a.scale_log2, -m_run));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[kb2][8 * u + 2 * j + 1], a.scale_log2, -m_run));
+        psum += p0 + p1;
+        pw[j] = pack_bf16x2(p0, p1);
       }
-    l_part = l_part * alpha + psum;
-
+      const bf16x8_t pop = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
 #pragma unroll
-    for (int db = 0; db < 4; ++db) oacc[db] *= alpha;
-
-    // ---- O^T += V^T P^T
-    const uint32_t* vb = v_lds + buf * kVBuf;
-#pragma unroll
-    for (int db = 0; db < 4; ++db) {
-      const int d = 32 * db + n;
-      const uint32_t* vrow = vb + d * kVStride;
-      const int sw = v_swz(d);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const u32x4 vv = *reinterpret_cast<const u32x4*>(vrow + ((8 * s + 4 * hh) ^ sw));
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pop[s], oacc[db], 0, 0, 0);
+      for (int db = 0; db < 4; ++db) {
+        const int d = 32 * db + n;
+        const u32x4 vv = *reinterpret_cast<const u32x4*>(vb + d * kVStride + ((8 * s4 + 4 * hh) ^ v_swz(d)));
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pop, oacc[db], 0, 0, 0);
       }
     }
+    l_part += psum;
 
     if (t + 1 < n_tiles) store_tile(buf ^ 1);
     __syncthreads();
