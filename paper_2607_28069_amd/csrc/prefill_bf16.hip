@@ -14,12 +14,18 @@
 //    single cross-lane exchange (lane l <-> l ^ 32) and the row sum none until the end.
 //  * O^T = V^T P^T with the same instruction: the probabilities, rounded to bf16, are already
 //    in the B-operand layout (keys along k) once the tile's keys are numbered in the order
-//    the accumulator holds them; V is written transposed into LDS in that key order, so each
-//    A operand is one 16-byte LDS read.
-//  * K and V tiles are double-buffered in LDS: the next tile's global loads are in flight
-//    while the current tile is multiplied; one barrier per tile.
+//    the accumulator holds them.  V stays row-major in LDS; its A operand (8 keys at one head
+//    dim per lane) comes from two transposing reads (ds_read_b64_tr_b16), which also apply
+//    that key order.
+//  * Tiles move global -> LDS with global_load_lds_dwordx4 (no register staging).  The 16-byte
+//    chunks of a row are XOR-swizzled so that every LDS read is free of bank conflicts.
+//  * Software pipeline, one barrier per tile: K runs one tile ahead of V.  While the matrix
+//    core computes the scores of tile t+1, the vector unit turns the scores of tile t into
+//    probabilities, which then feed the PV products of tile t.
 //  * Workgroups sharing a (request, kv head) key stream are mapped onto the same XCD (blocks
 //    are dealt round-robin over the 8 XCDs), so that stream is fetched into one L2.
+#include <type_traits>
+
 #include "pic_internal.h"
 
 namespace pic {
@@ -28,26 +34,34 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kRowsPerWave = 32;
 constexpr int kRowsPerWG = kWaves * kRowsPerWave;
-constexpr int kKeys = 64;                 // keys per tile
+constexpr int kKeys = 64;                      // keys per tile
 constexpr int kHD = 128;
-constexpr int kKStride = kHD / 2 + 4;     // dwords per K row in LDS (bank spread, 16-B aligned)
-constexpr int kVStride = kKeys / 2 + 4;   // dwords per transposed V row (one head dim) in LDS
-constexpr int kKBuf = kKeys * kKStride;   // dwords
-constexpr int kVBuf = kHD * kVStride;     // dwords
+constexpr int kRowBytes = kHD * 2;             // 256
+constexpr int kTileBytes = kKeys * kRowBytes;  // 16 KB
 constexpr int kNumXcd = 8;
 
+#define LDS_AS __attribute__((address_space(3)))
+#define GLOBAL_AS __attribute__((address_space(1)))
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// Position of key `key` (0..63) of a tile inside a transposed-V row: swap bits 2 and 3, the
-// order in which the S^T accumulator hands probabilities to the B operand.
+// Key order inside a tile as the S^T accumulator hands probabilities to the B operand of the
+// PV product: k index kappa <-> key with bits 2 and 3 swapped (an involution).
 __device__ __forceinline__ int key_perm(int key) {
   return (key & ~12) | ((key & 4) << 1) | ((key & 8) >> 1);
 }
 
-// Dword column swizzle of transposed-V rows: rows 8 apart start in different bank groups.
-__device__ __forceinline__ int v_swz(int d) { return ((d >> 3) & 3) * 8; }
+// Byte offset of 16-byte chunk c of tile row `key`.  K is read 16 bytes per lane across 32
+// rows, V 8 bytes per lane across 4 rows by the transposing read; each has its own XOR
+// swizzle of the chunk index that keeps those reads free of bank conflicts (for 32 or 64
+// four-byte banks).
+__device__ __forceinline__ int k_swz(int key) { return key & 15; }
+__device__ __forceinline__ int v_swz(int key) { return ((key & 3) * 5) & 15; }
+__device__ __forceinline__ int k_off(int key, int c) { return key * kRowBytes + ((c ^ k_swz(key)) << 4); }
+__device__ __forceinline__ int v_off(int key, int c) { return key * kRowBytes + ((c ^ v_swz(key)) << 4); }
 
 struct PrefillArgs {
   const bf16_t* q;
@@ -63,8 +77,12 @@ struct PrefillArgs {
 
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_bf16_kernel(PrefillArgs a) {
-  __shared__ __attribute__((aligned(16))) uint32_t k_lds[2 * kKBuf];
-  __shared__ __attribute__((aligned(16))) uint32_t v_lds[2 * kVBuf];
+  // Four distinct buffers (not one array indexed by parity) so the compiler can see that
+  // loads in flight into one buffer do not alias reads from another.
+  __shared__ __attribute__((aligned(16))) uint8_t k_lds0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t k_lds1[kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds1[kTileBytes];
 
   // XCD-aware block order: hardware block w runs on XCD w % 8; give each XCD a contiguous
   // range of logical blocks so the m-tiles of one (request, kv head) share an L2.
@@ -86,7 +104,6 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, hh = lane >> 5;   // query column, lane half
 
-  // ---- rows of this wave and workgroup
   const int row0_wg = mt * kRowsPerWG;
   const int last_row_wg = min(row0_wg + kRowsPerWG, M) - 1;
   const int pos_max_wg = ctx + last_row_wg / n_rep;   // furthest key any row here sees
@@ -108,82 +125,77 @@ prefill_bf16_kernel(PrefillArgs a) {
   {
     const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + qrow * kHD);
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-      u32x4 v = row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0};
-      qop[ks] = as_bf16x8(v);
-    }
+    for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0});
   }
 
-  // ---- tile staging: thread -> (16-byte chunk dc, key group) for K and V
-  const int dc = tid & 15;          // 8 head dims [8 dc, 8 dc + 8)
-  const int kq = tid >> 4;          // K: keys kq + 16 u;  V: keys 4 kq + u   (u = 0..3)
-  u32x4 kreg[4], vreg[4];
-
-  // Rows past the last key are clamped to it: their scores are masked, so they enter the
-  // PV product with probability 0 (finite values, no branch around the loads).
-  auto load_tile = [&](int t) {
-    const int k0 = t * kKeys;
+  // ---- global -> LDS tile loads.  Wave w fills rows 16 w .. 16 w + 15 of a tile, 4 rows per
+  // instruction: the instruction writes 1 KB of LDS, lane `lane` landing at byte 16 * lane, so
+  // lane -> (row 16 w + 4 i + lane / 16, chunk slot lane % 16) and it fetches the global chunk
+  // the swizzle puts in that slot.  Rows past the last key are clamped to it: their scores
+  // are masked, so they enter the PV product with probability 0.
+  const int ld_row = 16 * wave + (lane >> 4), ld_slot = lane & 15;
+  auto load_tile = [&](const bf16_t* src, uint8_t* dst_tile, int t, bool is_v) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int kk = min(k0 + kq + 16 * u, n_keys - 1);
-      kreg[u] = *reinterpret_cast<const u32x4*>(Kg + (int64_t)kk * kHD + 8 * dc);
-      const int kv = min(k0 + 4 * kq + u, n_keys - 1);
-      vreg[u] = *reinterpret_cast<const u32x4*>(Vg + (int64_t)kv * kHD + 8 * dc);
+    for (int i = 0; i < 4; ++i) {
+      const int key = ld_row + 4 * i;
+      const int c = ld_slot ^ (is_v ? v_swz(key) : k_swz(key));
+      const int kk = min(t * kKeys + key, n_keys - 1);
+      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(src + (int64_t)kk * kHD + 8 * c),
+                                       (LDS_AS void*)(dst_tile + (16 * wave + 4 * i) * kRowBytes),
+                                       16, 0, 0);
     }
   };
+  auto wait_loads = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };   // vmcnt(0)
 
-  auto store_tile = [&](int buf) {
-    uint32_t* kb = k_lds + buf * kKBuf;
+  // ---- S^T = K Q^T for one tile: two independent 32-key accumulation chains
+  auto scores = [&](const uint8_t* kt, f32x16_t (&s)[2]) {
+    s[0] = f32x16_t{};
+    s[1] = f32x16_t{};
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      *reinterpret_cast<u32x4*>(kb + (kq + 16 * u) * kKStride + 4 * dc) = kreg[u];
-    // V transposed: row = head dim, 4 consecutive keys 4kq..4kq+3 packed into 8 bytes.
-    uint32_t* vb = v_lds + buf * kVBuf;
-    const int col = key_perm(4 * kq) >> 1;   // dword column of key 4kq (even)
+    for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int word = e >> 1;
-      uint32_t lo, hi;
-      if (e & 1) {
-        lo = (vreg[0][word] >> 16) | (vreg[1][word] & 0xFFFF0000u);
-        hi = (vreg[2][word] >> 16) | (vreg[3][word] & 0xFFFF0000u);
-      } else {
-        lo = (vreg[0][word] & 0xFFFFu) | (vreg[1][word] << 16);
-        hi = (vreg[2][word] & 0xFFFFu) | (vreg[3][word] << 16);
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + k_off(32 * kb2 + n, 2 * ks + hh));
+        s[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qop[ks], s[kb2], 0, 0, 0);
       }
-      const int d = 8 * dc + e;
-      *reinterpret_cast<uint2*>(vb + d * kVStride + (col ^ v_swz(d))) = make_uint2(lo, hi);
-    }
   };
+
+  // Transposing reads of V^T: 16-lane group G = lane / 16, lane j = lane % 16 = 4 rr + qq
+  // points at row key_perm(16 s4 + 8 hh + 4 half + rr), head dims 32 db + 16 (G & 1) + 4 qq
+  // .. +3; lane i of the group then receives head dim 32 db + (lane & 31) of those 4 rows.
+  const int tr_rr = (lane & 15) >> 2, tr_qq = lane & 3, tr_g1 = (lane >> 4) & 1;
 
   f32x16_t oacc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) oacc[i] = f32x16_t{};
   float m_run = -INFINITY, l_part = 0.f;
 
-  load_tile(0);
-  store_tile(0);
+  // ---- prologue: K0, V0, K1 resident; scores of tile 0
+  load_tile(Kg, k_lds0, 0, false);
+  load_tile(Vg, v_lds0, 0, true);
+  if (n_tiles > 1) load_tile(Kg, k_lds1, 1, false);
+  wait_loads();
   __syncthreads();
+  f32x16_t scur[2];
+  scores(k_lds0, scur);
+  __syncthreads();   // every wave is done with K buffer 0 before tile 2 lands there
 
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1);
+  // One tile.  Resident on entry: K(t+1) in K slot (t+1)&1, V(t) in V slot t&1 (P = t & 1,
+  // a compile-time constant so every buffer below is a distinct, known array).
+  auto tile = [&](int t, auto parity) {
+    constexpr int P = decltype(parity)::value;
+    uint8_t* const k_next = P ? k_lds0 : k_lds1;   // holds K(t+1)
+    uint8_t* const k_free = P ? k_lds1 : k_lds0;   // receives K(t+2)
+    uint8_t* const v_cur = P ? v_lds1 : v_lds0;    // holds V(t)
+    uint8_t* const v_free = P ? v_lds0 : v_lds1;   // receives V(t+1)
+    if (t + 2 < n_tiles) load_tile(Kg, k_free, t + 2, false);
+    if (t + 1 < n_tiles) load_tile(Vg, v_free, t + 1, true);
 
-    // ---- S^T = K Q^T for keys [64 t, 64 t + 64): two 32-key blocks
-    const uint32_t* kb = k_lds + buf * kKBuf;
-    // two independent accumulation chains, interleaved
-    f32x16_t sacc[2] = {f32x16_t{}, f32x16_t{}};
-    const uint32_t* krow = kb + n * kKStride + 4 * hh;
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(krow + 32 * kb2 * kKStride + 8 * ks);
-        sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qop[ks], sacc[kb2], 0, 0, 0);
-      }
+    f32x16_t snext[2];
+    if (t + 1 < n_tiles) scores(k_next, snext);
 
-    // ---- online softmax over this lane's query column.  Scores stay unscaled until the
-    // exponent: p = exp2(s * scale * log2(e) - m), one FMA and one v_exp_f32 per score.
+    // ---- online softmax of tile t over this lane's query column.  Scores stay unscaled
+    // until the exponent: p = exp2(s * scale * log2(e) - m), one FMA and one v_exp_f32 each.
     const int k0 = t * kKeys;
     if (k0 + kKeys - 1 > ctx) {   // tile reaches into the suffix (or past the last key)
 #pragma unroll
@@ -191,14 +203,14 @@ prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = k0 + 32 * kb2 + 8 * (e >> 2) + 4 * hh + (e & 3);
-          if (key > qpos) sacc[kb2][e] = -INFINITY;
+          if (key > qpos) scur[kb2][e] = -INFINITY;
         }
     }
     float mx = -INFINITY;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[kb2][e]);
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, scur[kb2][e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_tile = mx * a.scale_log2;
     // The reference max only moves when a score exceeds it by more than 2^8 (then the
@@ -213,10 +225,8 @@ prefill_bf16_kernel(PrefillArgs a) {
       for (int db = 0; db < 4; ++db) oacc[db] *= alpha;
     }
 
-    // ---- P^T (bf16) slice by slice, each followed by its four O^T += V^T P^T products
-    // (four independent accumulators), so the exponentials of the next slice can overlap the
-    // matrix products of the current one.
-    const uint32_t* vb = v_lds + buf * kVBuf;
+    // ---- P^T slice by slice, each followed by its four O^T += V^T P^T products
+    const uint8_t* vt = v_cur;
     float psum = 0.f;
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
@@ -224,23 +234,37 @@ prefill_bf16_kernel(PrefillArgs a) {
       uint32_t pw[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[kb2][8 * u + 2 * j], a.scale_log2, -m_run));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[kb2][8 * u + 2 * j + 1], a.scale_log2, -m_run));
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j], a.scale_log2, -m_run));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j + 1], a.scale_log2, -m_run));
         psum += p0 + p1;
         pw[j] = pack_bf16x2(p0, p1);
       }
       const bf16x8_t pop = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
+      const int key0 = key_perm(16 * s4 + 8 * hh + tr_rr);
+      const int key1 = key_perm(16 * s4 + 8 * hh + 4 + tr_rr);
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
-        const int d = 32 * db + n;
-        const u32x4 vv = *reinterpret_cast<const u32x4*>(vb + d * kVStride + ((8 * s4 + 4 * hh) ^ v_swz(d)));
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), pop, oacc[db], 0, 0, 0);
+        const int c = 4 * db + 2 * tr_g1 + (tr_qq >> 1);
+        const int bofs = 8 * (tr_qq & 1);
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vt + v_off(key0, c) + bofs));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vt + v_off(key1, c) + bofs));
+        const bf16x8_t vv = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pop, oacc[db], 0, 0, 0);
       }
     }
     l_part += psum;
 
-    if (t + 1 < n_tiles) store_tile(buf ^ 1);
+    if (t + 1 < n_tiles) {
+      scur[0] = snext[0];
+      scur[1] = snext[1];
+    }
+    wait_loads();
     __syncthreads();
+  };
+
+  for (int t = 0; t < n_tiles; t += 2) {
+    tile(t, std::integral_constant<int, 0>{});
+    if (t + 1 < n_tiles) tile(t + 1, std::integral_constant<int, 1>{});
   }
 
   // ---- normalise and store: lane holds head dims 32 db + 8 q + 4 hh + (0..3) of its row
