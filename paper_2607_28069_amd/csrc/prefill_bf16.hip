@@ -101,7 +101,8 @@ prefill_bf16_kernel(PrefillArgs a) {
   ctx = ctx < 0 ? 0 : (ctx > a.max_ctx ? a.max_ctx : ctx);
   const int n_keys = ctx + a.n_suffix;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases in SGPRs
   const int n = lane & 31, hh = lane >> 5;   // query column, lane half
 
   const int row0_wg = mt * kRowsPerWG;
@@ -128,24 +129,55 @@ prefill_bf16_kernel(PrefillArgs a) {
     for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0});
   }
 
-  // ---- global -> LDS tile loads.  Wave w fills rows 16 w .. 16 w + 15 of a tile, 4 rows per
-  // instruction: the instruction writes 1 KB of LDS, lane `lane` landing at byte 16 * lane, so
-  // lane -> (row 16 w + 4 i + lane / 16, chunk slot lane % 16) and it fetches the global chunk
-  // the swizzle puts in that slot.  Rows past the last key are clamped to it: their scores
-  // are masked, so they enter the PV product with probability 0.
-  const int ld_row = 16 * wave + (lane >> 4), ld_slot = lane & 15;
+  // ---- global -> LDS tile loads.  Instruction i of wave w writes 1 KB of LDS = tile rows
+  // 16 i + 4 w .. +3, lane `lane` landing at byte 16 * lane: row 16 i + 4 w + lane / 16, chunk
+  // slot lane % 16, filled from the global chunk the swizzle puts in that slot.  The swizzles
+  // use key bits 0..3 (K) and 0..1 (V), which do not change with i, so each lane's source
+  // offset within a 16-row step is one constant.  Rows past the last key (only in the last
+  // tile) are clamped to it: their scores are masked, so they enter PV with probability 0.
+  const int ld_row = 4 * wave + (lane >> 4), ld_slot = lane & 15;
+  const int k_goff = ld_row * kHD + 8 * (ld_slot ^ k_swz(ld_row));   // elements
+  const int v_goff = ld_row * kHD + 8 * (ld_slot ^ v_swz(ld_row));
+  const int v_gc = ld_slot ^ v_swz(ld_row), k_gc = ld_slot ^ k_swz(ld_row);
   auto load_tile = [&](const bf16_t* src, uint8_t* dst_tile, int t, bool is_v) {
+    const int goff = is_v ? v_goff : k_goff;
+    if ((t + 1) * kKeys <= n_keys) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int key = ld_row + 4 * i;
-      const int c = ld_slot ^ (is_v ? v_swz(key) : k_swz(key));
-      const int kk = min(t * kKeys + key, n_keys - 1);
-      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(src + (int64_t)kk * kHD + 8 * c),
-                                       (LDS_AS void*)(dst_tile + (16 * wave + 4 * i) * kRowBytes),
-                                       16, 0, 0);
+      for (int i = 0; i < 4; ++i) {
+        const bf16_t* base = src + (int64_t)(t * kKeys + 16 * i) * kHD;   // uniform
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(base + goff),
+                                         (LDS_AS void*)(dst_tile + (16 * i + 4 * wave) * kRowBytes),
+                                         16, 0, 0);
+      }
+    } else {
+      const int c = is_v ? v_gc : k_gc;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kk = min(t * kKeys + 16 * i + ld_row, n_keys - 1);
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(src + (int64_t)kk * kHD + 8 * c),
+                                         (LDS_AS void*)(dst_tile + (16 * i + 4 * wave) * kRowBytes),
+                                         16, 0, 0);
+      }
     }
   };
   auto wait_loads = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };   // vmcnt(0)
+
+  // ---- per-lane LDS read offsets, fixed for the whole loop (buffer, 32-row block and
+  // 16-row slice steps are immediate offsets)
+  int k_rd[8];   // S^T A operand: row n, chunk 2 ks + hh
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) k_rd[ks] = k_off(n, 2 * ks + hh);
+  // Transposing reads of V^T: 16-lane group G = lane / 16, lane j = lane % 16 = 4 rr + qq
+  // points at row key_perm(16 s4 + 8 hh + 4 half + rr) = 16 s4 + 8 half + 4 hh + rr, head dims
+  // 32 db + 16 (G & 1) + 4 qq .. +3; lane i of the group then receives head dim
+  // 32 db + (lane & 31) of those 4 rows.
+  const int tr_rr = (lane & 15) >> 2, tr_qq = lane & 3, tr_g1 = (lane >> 4) & 1;
+  int v_rd[4][2];
+#pragma unroll
+  for (int db = 0; db < 4; ++db)
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+      v_rd[db][half] = v_off(8 * half + 4 * hh + tr_rr, 4 * db + 2 * tr_g1 + (tr_qq >> 1)) + 8 * (tr_qq & 1);
 
   // ---- S^T = K Q^T for one tile: two independent 32-key accumulation chains
   auto scores = [&](const uint8_t* kt, f32x16_t (&s)[2]) {
@@ -155,67 +187,48 @@ prefill_bf16_kernel(PrefillArgs a) {
     for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + k_off(32 * kb2 + n, 2 * ks + hh));
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + k_rd[ks] + 32 * kb2 * kRowBytes);
         s[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qop[ks], s[kb2], 0, 0, 0);
       }
   };
-
-  // Transposing reads of V^T: 16-lane group G = lane / 16, lane j = lane % 16 = 4 rr + qq
-  // points at row key_perm(16 s4 + 8 hh + 4 half + rr), head dims 32 db + 16 (G & 1) + 4 qq
-  // .. +3; lane i of the group then receives head dim 32 db + (lane & 31) of those 4 rows.
-  const int tr_rr = (lane & 15) >> 2, tr_qq = lane & 3, tr_g1 = (lane >> 4) & 1;
 
   f32x16_t oacc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) oacc[i] = f32x16_t{};
   float m_run = -INFINITY, l_part = 0.f;
 
-  // ---- prologue: K0, V0, K1 resident; scores of tile 0
-  load_tile(Kg, k_lds0, 0, false);
-  load_tile(Vg, v_lds0, 0, true);
-  if (n_tiles > 1) load_tile(Kg, k_lds1, 1, false);
-  wait_loads();
-  __syncthreads();
-  f32x16_t scur[2];
-  scores(k_lds0, scur);
-  __syncthreads();   // every wave is done with K buffer 0 before tile 2 lands there
+  // Both lane halves hold keys of the same query column: (x[l], x[l ^ 32]) as a pair, for
+  // all lanes, from one v_permlane32_swap.
+  auto pair_max = [](float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  };
+  auto pair_sum = [](float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  };
 
-  // One tile.  Resident on entry: K(t+1) in K slot (t+1)&1, V(t) in V slot t&1 (P = t & 1,
-  // a compile-time constant so every buffer below is a distinct, known array).
-  auto tile = [&](int t, auto parity) {
-    constexpr int P = decltype(parity)::value;
-    uint8_t* const k_next = P ? k_lds0 : k_lds1;   // holds K(t+1)
-    uint8_t* const k_free = P ? k_lds1 : k_lds0;   // receives K(t+2)
-    uint8_t* const v_cur = P ? v_lds1 : v_lds0;    // holds V(t)
-    uint8_t* const v_free = P ? v_lds0 : v_lds1;   // receives V(t+1)
-    if (t + 2 < n_tiles) load_tile(Kg, k_free, t + 2, false);
-    if (t + 1 < n_tiles) load_tile(Vg, v_free, t + 1, true);
-
-    f32x16_t snext[2];
-    if (t + 1 < n_tiles) scores(k_next, snext);
-
-    // ---- online softmax of tile t over this lane's query column.  Scores stay unscaled
-    // until the exponent: p = exp2(s * scale * log2(e) - m), one FMA and one v_exp_f32 each.
+  // Scores of tile t are complete: apply the frontier mask where the tile reaches past a
+  // query's position, and move the reference max if a score exceeds it by more than 2^8
+  // (rescaling what has been accumulated, for the whole wave at once).  Otherwise p <= 256,
+  // which float32 sums and bf16 probabilities hold without loss of relative precision.
+  auto finish_scores = [&](int t, f32x16_t (&s)[2]) {
     const int k0 = t * kKeys;
-    if (k0 + kKeys - 1 > ctx) {   // tile reaches into the suffix (or past the last key)
+    if (k0 + kKeys - 1 > ctx) {
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = k0 + 32 * kb2 + 8 * (e >> 2) + 4 * hh + (e & 3);
-          if (key > qpos) scur[kb2][e] = -INFINITY;
+          if (key > qpos) s[kb2][e] = -INFINITY;
         }
     }
     float mx = -INFINITY;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, scur[kb2][e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_tile = mx * a.scale_log2;
-    // The reference max only moves when a score exceeds it by more than 2^8 (then the
-    // accumulators are rescaled, for the whole wave at once); otherwise p <= 256, which
-    // float32 sums and bf16 probabilities hold without loss of relative precision.
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kb2][e]);
+    const float m_tile = pair_max(mx) * a.scale_log2;
     if (__any(m_tile > m_run + 8.f)) {
       const float m_new = fmaxf(m_run, m_tile);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -224,51 +237,85 @@ prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
       for (int db = 0; db < 4; ++db) oacc[db] *= alpha;
     }
+  };
 
-    // ---- P^T slice by slice, each followed by its four O^T += V^T P^T products
-    const uint8_t* vt = v_cur;
+  // ---- prologue: K0, V0, K1 resident; scores of tile 0
+  load_tile(Kg, k_lds0, 0, false);
+  load_tile(Vg, v_lds0, 0, true);
+  if (n_tiles > 1) load_tile(Kg, k_lds1, 1, false);
+  wait_loads();
+  __syncthreads();
+  f32x16_t s_a[2], s_b[2];   // scores of the current / next tile, swapped every tile
+  scores(k_lds0, s_a);
+  finish_scores(0, s_a);
+  __syncthreads();   // every wave is done with K buffer 0 before tile 2 lands there
+
+  // One tile.  Resident on entry: K(t+1) in K slot (t+1)&1, V(t) in V slot t&1 (P = t & 1,
+  // a compile-time constant so every buffer below is a distinct, known array); the scores of
+  // tile t are finished.  The body between the loads and the next-tile bookkeeping has no
+  // branches, so the scheduler can interleave the matrix products of the next tile's scores
+  // and of this tile's PV with the exponentials of this tile.
+  auto tile = [&](int t, auto parity, f32x16_t (&scur)[2], f32x16_t (&snext)[2]) {
+    constexpr int P = decltype(parity)::value;
+    uint8_t* const k_next = P ? k_lds0 : k_lds1;   // holds K(t+1)
+    uint8_t* const k_free = P ? k_lds1 : k_lds0;   // receives K(t+2)
+    const uint8_t* const v_cur = P ? v_lds1 : v_lds0;   // holds V(t)
+    uint8_t* const v_free = P ? v_lds0 : v_lds1;   // receives V(t+1)
+    if (t + 2 < n_tiles) load_tile(Kg, k_free, t + 2, false);
+    if (t + 1 < n_tiles) load_tile(Vg, v_free, t + 1, true);
+
+    // (scores of a tile past the last one are computed on stale LDS and dropped)
+    snext[0] = f32x16_t{};
+    snext[1] = f32x16_t{};
     float psum = 0.f;
+    const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
+      // a quarter of the next tile's S^T products
+#pragma unroll
+      for (int ks = 2 * s4; ks < 2 * s4 + 2; ++ks)
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2) {
+          const u32x4 kv = *reinterpret_cast<const u32x4*>(k_next + k_rd[ks] + 32 * kb2 * kRowBytes);
+          snext[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qop[ks], snext[kb2], 0, 0, 0);
+        }
+      // probabilities of slice s4 of this tile (keys 16 s4 .. 16 s4 + 15 in accumulator order)
       const int kb2 = s4 >> 1, u = s4 & 1;
       uint32_t pw[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j], a.scale_log2, -m_run));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j + 1], a.scale_log2, -m_run));
-        psum += p0 + p1;
         pw[j] = pack_bf16x2(p0, p1);
+        // row sum of the bf16 probabilities the PV product uses (one v_dot2 per pair)
+        psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[j]), ones, psum, false);
       }
       const bf16x8_t pop = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
-      const int key0 = key_perm(16 * s4 + 8 * hh + tr_rr);
-      const int key1 = key_perm(16 * s4 + 8 * hh + 4 + tr_rr);
+      // O^T += V^T P^T for this slice
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
-        const int c = 4 * db + 2 * tr_g1 + (tr_qq >> 1);
-        const int bofs = 8 * (tr_qq & 1);
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vt + v_off(key0, c) + bofs));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vt + v_off(key1, c) + bofs));
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (LDS_AS i16x4*)(v_cur + v_rd[db][0] + 16 * s4 * kRowBytes));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (LDS_AS i16x4*)(v_cur + v_rd[db][1] + 16 * s4 * kRowBytes));
         const bf16x8_t vv = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pop, oacc[db], 0, 0, 0);
       }
     }
     l_part += psum;
 
-    if (t + 1 < n_tiles) {
-      scur[0] = snext[0];
-      scur[1] = snext[1];
-    }
+    if (t + 1 < n_tiles) finish_scores(t + 1, snext);
     wait_loads();
     __syncthreads();
   };
 
   for (int t = 0; t < n_tiles; t += 2) {
-    tile(t, std::integral_constant<int, 0>{});
-    if (t + 1 < n_tiles) tile(t + 1, std::integral_constant<int, 1>{});
+    tile(t, std::integral_constant<int, 0>{}, s_a, s_b);
+    if (t + 1 < n_tiles) tile(t + 1, std::integral_constant<int, 1>{}, s_b, s_a);
   }
 
   // ---- normalise and store: lane holds head dims 32 db + 8 q + 4 hh + (0..3) of its row
-  const float l_tot = l_part + __shfl_xor(l_part, 32, 64);
+  const float l_tot = pair_sum(l_part);
   const float inv = 1.f / l_tot;
   if (row_ok) {
     bf16_t* orow = a.out + qrow * kHD;
