@@ -7,7 +7,8 @@
 // position ctx + i and sees keys [0, ctx + i]; only the last key tiles need a mask.
 //
 // Kernel shape (gfx950, wave64):
-//  * 4 waves per workgroup, 32 query rows per wave (128 rows per workgroup), key tiles of 64.
+//  * 8 waves per workgroup, 32 query rows per wave (256 rows per workgroup), key tiles of 64:
+//    every K/V tile brought into LDS serves 256 query rows.
 //  * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: A = K rows
 //    from LDS, B = Q^T held in registers for the whole key loop.  In the accumulator layout
 //    each lane then owns ONE query column and 32 of the tile's keys, so the row max needs a
@@ -31,7 +32,8 @@
 namespace pic {
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
 constexpr int kRowsPerWG = kWaves * kRowsPerWave;
 constexpr int kKeys = 64;                      // keys per tile
@@ -39,6 +41,7 @@ constexpr int kHD = 128;
 constexpr int kRowBytes = kHD * 2;             // 256
 constexpr int kTileBytes = kKeys * kRowBytes;  // 16 KB
 constexpr int kNumXcd = 8;
+constexpr int kLoadSteps = kKeys / (4 * kWaves);   // 1 KB load instructions per wave per tile
 
 #define LDS_AS __attribute__((address_space(3)))
 #define GLOBAL_AS __attribute__((address_space(1)))
@@ -75,7 +78,7 @@ struct PrefillArgs {
   float scale_log2;
 };
 
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_bf16_kernel(PrefillArgs a) {
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
   // loads in flight into one buffer do not alias reads from another.
@@ -130,12 +133,12 @@ prefill_bf16_kernel(PrefillArgs a) {
   }
 
   // ---- global -> LDS tile loads.  Instruction i of wave w writes 1 KB of LDS = tile rows
-  // 16 i + 4 w .. +3, lane `lane` landing at byte 16 * lane: row 16 i + 4 w + lane / 16, chunk
-  // slot lane % 16, filled from the global chunk the swizzle puts in that slot.  The swizzles
-  // use key bits 0..3 (K) and 0..1 (V), which do not change with i, so each lane's source
-  // offset within a 16-row step is one constant.  Rows past the last key (only in the last
+  // 4 (kWaves i + w) .. +3, lane `lane` landing at byte 16 * lane: row 4 kWaves i + 4 w +
+  // lane / 16, chunk slot lane % 16, filled from the global chunk the swizzle puts in that
+  // slot.  The swizzles use key bits 0..3 (K) and 0..1 (V), which do not change with i, so
+  // each lane's source offset within one step is a constant.  Rows past the last key (only in the last
   // tile) are clamped to it: their scores are masked, so they enter PV with probability 0.
-  const int ld_row = 4 * wave + (lane >> 4), ld_slot = lane & 15;
+  const int ld_row = 4 * wave + (lane >> 4), ld_slot = lane & 15;   // row within a step
   const int k_goff = ld_row * kHD + 8 * (ld_slot ^ k_swz(ld_row));   // elements
   const int v_goff = ld_row * kHD + 8 * (ld_slot ^ v_swz(ld_row));
   const int v_gc = ld_slot ^ v_swz(ld_row), k_gc = ld_slot ^ k_swz(ld_row);
@@ -143,19 +146,19 @@ prefill_bf16_kernel(PrefillArgs a) {
     const int goff = is_v ? v_goff : k_goff;
     if ((t + 1) * kKeys <= n_keys) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bf16_t* base = src + (int64_t)(t * kKeys + 16 * i) * kHD;   // uniform
+      for (int i = 0; i < kLoadSteps; ++i) {
+        const bf16_t* base = src + (int64_t)(t * kKeys + 4 * kWaves * i) * kHD;   // uniform
         __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(base + goff),
-                                         (LDS_AS void*)(dst_tile + (16 * i + 4 * wave) * kRowBytes),
+                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
                                          16, 0, 0);
       }
     } else {
       const int c = is_v ? v_gc : k_gc;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int kk = min(t * kKeys + 16 * i + ld_row, n_keys - 1);
+      for (int i = 0; i < kLoadSteps; ++i) {
+        const int kk = min(t * kKeys + 4 * kWaves * i + ld_row, n_keys - 1);
         __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(src + (int64_t)kk * kHD + 8 * c),
-                                         (LDS_AS void*)(dst_tile + (16 * i + 4 * wave) * kRowBytes),
+                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
                                          16, 0, 0);
       }
     }
@@ -359,7 +362,7 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
   a.scale_log2 = s.scale_log2;
   const int per_xcd = (a.n_wg + kNumXcd - 1) / kNumXcd;
   const dim3 grid(per_xcd * kNumXcd, s.n_layers);
-  hipLaunchKernelGGL(prefill_bf16_kernel, grid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(prefill_bf16_kernel, grid, dim3(kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
