@@ -73,8 +73,13 @@ struct PrefillArgs {
   const int32_t* ctx_len;
   bf16_t* out;
   int32_t max_ctx, n_suffix, batch, cache_cap, n_q_heads, n_kv_heads;
-  int32_t m_tiles;   // ceil(n_suffix * n_rep / kRowsPerWG)
-  int32_t n_wg;      // m_tiles * batch * n_kv_heads
+  int32_t m_tiles;          // ceil(n_suffix * n_rep / kRowsPerWG)
+  int32_t n_splits;         // key-range splits per (m-tile, request, kv head)
+  int32_t tiles_per_split;  // key tiles per split
+  int32_t n_wg;             // m_tiles * n_splits * batch * n_kv_heads
+  int64_t rows_total;       // L * batch * n_suffix * Hq (query rows of one split's partials)
+  float* ws_o;              // [n_splits][rows_total][D] unnormalised partial outputs
+  float2* ws_ml;            // [n_splits][rows_total] (reference max, row sum)
   float scale_log2;
 };
 
@@ -94,7 +99,8 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int logical = (w % kNumXcd) * per_xcd + w / kNumXcd;
   if (logical >= a.n_wg) return;
   const int mt = logical % a.m_tiles;
-  const int bg = logical / a.m_tiles;
+  const int split = (logical / a.m_tiles) % a.n_splits;
+  const int bg = logical / (a.m_tiles * a.n_splits);
   const int b = bg / a.n_kv_heads, g = bg % a.n_kv_heads;
   const int l = blockIdx.y;
 
@@ -111,7 +117,9 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int row0_wg = mt * kRowsPerWG;
   const int last_row_wg = min(row0_wg + kRowsPerWG, M) - 1;
   const int pos_max_wg = ctx + last_row_wg / n_rep;   // furthest key any row here sees
-  const int n_tiles = (pos_max_wg + kKeys) / kKeys;
+  // this workgroup's key tiles: [t0, t0 + n_tiles) of the (pos_max_wg + 1) visible keys
+  const int t0 = split * a.tiles_per_split;
+  const int n_tiles = min((pos_max_wg + kKeys) / kKeys - t0, a.tiles_per_split);
 
   const int r = row0_wg + wave * kRowsPerWave + n;    // this lane's query row
   const bool row_ok = r < M;
@@ -123,6 +131,12 @@ prefill_bf16_kernel(PrefillArgs a) {
   const bf16_t* Kg = a.cache_k + bh_kv * kHD;
   const bf16_t* Vg = a.cache_v + bh_kv * kHD;
   const int64_t qrow = (((int64_t)l * a.batch + b) * a.n_suffix + tok) * a.n_q_heads + hq;
+
+  const int64_t orow = (((int64_t)l * a.batch + b) * a.n_suffix + tok) * a.n_q_heads + hq;
+  if (n_tiles <= 0) {   // (uniform) a split past this workgroup's last visible key
+    if (a.n_splits > 1 && row_ok && hh == 0) a.ws_ml[split * a.rows_total + orow] = make_float2(-INFINITY, 0.f);
+    return;
+  }
 
   // ---- Q^T operand: lane (n, hh) holds q[row n][16 ks + 8 hh .. +8) for ks = 0..7
   bf16x8_t qop[8];
@@ -215,7 +229,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   // query's position, and move the reference max if a score exceeds it by more than 2^8
   // (rescaling what has been accumulated, for the whole wave at once).  Otherwise p <= 256,
   // which float32 sums and bf16 probabilities hold without loss of relative precision.
-  auto finish_scores = [&](int t, f32x16_t (&s)[2]) {
+  auto finish_scores = [&](int t, f32x16_t (&s)[2]) {   // t: global tile index
     const int k0 = t * kKeys;
     if (k0 + kKeys - 1 > ctx) {
 #pragma unroll
@@ -243,14 +257,14 @@ prefill_bf16_kernel(PrefillArgs a) {
   };
 
   // ---- prologue: K0, V0, K1 resident; scores of tile 0
-  load_tile(Kg, k_lds0, 0, false);
-  load_tile(Vg, v_lds0, 0, true);
-  if (n_tiles > 1) load_tile(Kg, k_lds1, 1, false);
+  load_tile(Kg, k_lds0, t0, false);
+  load_tile(Vg, v_lds0, t0, true);
+  if (n_tiles > 1) load_tile(Kg, k_lds1, t0 + 1, false);
   wait_loads();
   __syncthreads();
   f32x16_t s_a[2], s_b[2];   // scores of the current / next tile, swapped every tile
   scores(k_lds0, s_a);
-  finish_scores(0, s_a);
+  finish_scores(t0, s_a);
   __syncthreads();   // every wave is done with K buffer 0 before tile 2 lands there
 
   // One tile.  Resident on entry: K(t+1) in K slot (t+1)&1, V(t) in V slot t&1 (P = t & 1,
@@ -258,14 +272,14 @@ prefill_bf16_kernel(PrefillArgs a) {
   // tile t are finished.  The body between the loads and the next-tile bookkeeping has no
   // branches, so the scheduler can interleave the matrix products of the next tile's scores
   // and of this tile's PV with the exponentials of this tile.
-  auto tile = [&](int t, auto parity, f32x16_t (&scur)[2], f32x16_t (&snext)[2]) {
+  auto tile = [&](int t, auto parity, f32x16_t (&scur)[2], f32x16_t (&snext)[2]) {   // t: local
     constexpr int P = decltype(parity)::value;
     uint8_t* const k_next = P ? k_lds0 : k_lds1;   // holds K(t+1)
     uint8_t* const k_free = P ? k_lds1 : k_lds0;   // receives K(t+2)
     const uint8_t* const v_cur = P ? v_lds1 : v_lds0;   // holds V(t)
     uint8_t* const v_free = P ? v_lds0 : v_lds1;   // receives V(t+1)
-    if (t + 2 < n_tiles) load_tile(Kg, k_free, t + 2, false);
-    if (t + 1 < n_tiles) load_tile(Vg, v_free, t + 1, true);
+    if (t + 2 < n_tiles) load_tile(Kg, k_free, t0 + t + 2, false);
+    if (t + 1 < n_tiles) load_tile(Vg, v_free, t0 + t + 1, true);
 
     // (scores of a tile past the last one are computed on stale LDS and dropped)
     snext[0] = f32x16_t{};
@@ -307,7 +321,7 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
     l_part += psum;
 
-    if (t + 1 < n_tiles) finish_scores(t + 1, snext);
+    if (t + 1 < n_tiles) finish_scores(t0 + t + 1, snext);
     wait_loads();
     __syncthreads();
   };
@@ -317,11 +331,12 @@ prefill_bf16_kernel(PrefillArgs a) {
     if (t + 1 < n_tiles) tile(t + 1, std::integral_constant<int, 1>{}, s_b, s_a);
   }
 
-  // ---- normalise and store: lane holds head dims 32 db + 8 q + 4 hh + (0..3) of its row
+  // ---- lane holds head dims 32 db + 8 qd + 4 hh + (0..3) of its row
   const float l_tot = pair_sum(l_part);
-  const float inv = 1.f / l_tot;
-  if (row_ok) {
-    bf16_t* orow = a.out + qrow * kHD;
+  if (!row_ok) return;
+  if (a.n_splits == 1) {   // normalise and store bf16
+    const float inv = 1.f / l_tot;
+    bf16_t* op = a.out + orow * kHD;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
 #pragma unroll
@@ -330,21 +345,96 @@ prefill_bf16_kernel(PrefillArgs a) {
         uint2 v;
         v.x = pack_bf16x2(oacc[db][4 * qd] * inv, oacc[db][4 * qd + 1] * inv);
         v.y = pack_bf16x2(oacc[db][4 * qd + 2] * inv, oacc[db][4 * qd + 3] * inv);
-        *reinterpret_cast<uint2*>(orow + d) = v;
+        *reinterpret_cast<uint2*>(op + d) = v;
       }
+  } else {                 // unnormalised partial for the split combine
+    float* op = a.ws_o + (split * a.rows_total + orow) * kHD;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd)
+        *reinterpret_cast<float4*>(op + 32 * db + 8 * qd + 4 * hh) =
+            make_float4(oacc[db][4 * qd], oacc[db][4 * qd + 1], oacc[db][4 * qd + 2], oacc[db][4 * qd + 3]);
+    if (hh == 0) a.ws_ml[split * a.rows_total + orow] = make_float2(m_run, l_tot);
   }
+}
+
+// Merge the key-range splits of each query row by log-sum-exp.  grid (rows_total / 4), 256
+// threads: one wave per row, two head dims per lane.
+__global__ void __launch_bounds__(256) prefill_combine_kernel(const float* __restrict__ ws_o,
+                                                              const float2* __restrict__ ws_ml,
+                                                              int32_t n_splits, int64_t rows_total,
+                                                              bf16_t* __restrict__ out) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows_total) return;
+  const int d = 2 * (threadIdx.x & 63);
+  float M = -INFINITY;
+  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ws_ml[s * rows_total + row].x);
+  float den = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int s = 0; s < n_splits; ++s) {
+    const float2 ml = ws_ml[s * rows_total + row];
+    if (ml.x == -INFINITY) continue;
+    const float w = __builtin_amdgcn_exp2f(ml.x - M);
+    den += w * ml.y;
+    const float2 o = *reinterpret_cast<const float2*>(ws_o + (s * rows_total + row) * kHD + d);
+    o0 += w * o.x;
+    o1 += w * o.y;
+  }
+  const float inv = 1.f / den;
+  reinterpret_cast<uint32_t*>(out + row * kHD)[threadIdx.x & 63] = pack_bf16x2(o0 * inv, o1 * inv);
+}
+
+struct SplitPlan {
+  int m_tiles, n_splits, tiles_per_split;
+};
+
+// Key-range splits: enough workgroups to cover the 256 compute units in whole rounds, each
+// split keeping at least 8 key tiles.  Cost in units of one workgroup-tile (~2 us):
+// rounds * tiles per split, plus, for split runs, the fp32 partials each split writes and the
+// combine reads back (520 bytes per query row, twice, at ~4 TB/s) and one tile per split.
+// Ties (within 3%) go to fewer splits.
+SplitPlan plan_splits(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
+  SplitPlan p;
+  const int64_t M = (int64_t)n_suffix * (s.n_q_heads / s.n_kv_heads);
+  p.m_tiles = (int)((M + kRowsPerWG - 1) / kRowsPerWG);
+  const int64_t base = (int64_t)p.m_tiles * s.batch * s.n_kv_heads * s.n_layers;
+  const double rows = (double)s.n_layers * s.batch * n_suffix * s.n_q_heads;
+  const int tiles = (max_ctx + n_suffix + kKeys - 1) / kKeys;
+  int best = 1;
+  double best_cost = 1e30;
+  for (int sp = 1; sp <= 8; ++sp) {
+    const int tps = (tiles + sp - 1) / sp;
+    if (sp > 1 && tps < 8) break;
+    const int64_t rounds = (base * sp + 255) / 256;
+    const double partials = sp > 1 ? sp * (1.0 + rows * 2.0 * (kHD + 2) * 4 / 4e12 / 2e-6) : 0.0;
+    const double cost = (double)rounds * tps + partials;
+    if (cost < best_cost * 0.97) {
+      best_cost = cost;
+      best = sp;
+    }
+  }
+  p.n_splits = best;
+  p.tiles_per_split = (tiles + best - 1) / best;
+  return p;
 }
 
 }  // namespace
 
-size_t prefill_bf16_workspace(const AttnShape&, int32_t, int32_t) { return 0; }
+size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
+  const SplitPlan p = plan_splits(s, n_suffix, max_ctx);
+  if (p.n_splits == 1) return 0;
+  const size_t rows = (size_t)s.n_layers * s.batch * n_suffix * s.n_q_heads;
+  return (size_t)p.n_splits * rows * (kHD + 2) * sizeof(float);
+}
 
 hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
                                const bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
-                               int32_t n_suffix, bf16_t* out, void*, size_t, hipStream_t stream) {
+                               int32_t n_suffix, bf16_t* out, void* workspace, size_t ws_bytes,
+                               hipStream_t stream) {
   const int n_rep = s.n_q_heads / s.n_kv_heads;
   const int64_t M = (int64_t)n_suffix * n_rep;
   if (M == 0 || s.batch == 0 || s.n_layers == 0) return hipSuccess;
+  const SplitPlan p = plan_splits(s, n_suffix, max_ctx);
   PrefillArgs a;
   a.q = q;
   a.cache_k = cache_k;
@@ -357,12 +447,23 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
   a.cache_cap = s.cache_cap;
   a.n_q_heads = s.n_q_heads;
   a.n_kv_heads = s.n_kv_heads;
-  a.m_tiles = (int32_t)((M + kRowsPerWG - 1) / kRowsPerWG);
-  a.n_wg = a.m_tiles * s.batch * s.n_kv_heads;
+  a.m_tiles = p.m_tiles;
+  a.n_splits = p.n_splits;
+  a.tiles_per_split = p.tiles_per_split;
+  a.n_wg = p.m_tiles * p.n_splits * s.batch * s.n_kv_heads;
+  a.rows_total = (int64_t)s.n_layers * s.batch * n_suffix * s.n_q_heads;
+  a.ws_o = static_cast<float*>(workspace);
+  a.ws_ml = reinterpret_cast<float2*>(a.ws_o + (size_t)p.n_splits * a.rows_total * kHD);
   a.scale_log2 = s.scale_log2;
+  if (p.n_splits > 1 && (workspace == nullptr || ws_bytes < prefill_bf16_workspace(s, n_suffix, max_ctx)))
+    return hipErrorInvalidValue;
   const int per_xcd = (a.n_wg + kNumXcd - 1) / kNumXcd;
   const dim3 grid(per_xcd * kNumXcd, s.n_layers);
   hipLaunchKernelGGL(prefill_bf16_kernel, grid, dim3(kThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.n_splits == 1) return e;
+  hipLaunchKernelGGL(prefill_combine_kernel, dim3((unsigned)((a.rows_total + 3) / 4)), dim3(256), 0,
+                     stream, a.ws_o, a.ws_ml, p.n_splits, a.rows_total, out);
   return hipGetLastError();
 }
 
