@@ -3,7 +3,7 @@
 
 One step = one pass of the whole path over one batch of requests:
   plan (host) -> copy of the gather blocks to the device -> compose all layers (re-rotate +
-  gather) -> suffix prefill attention layer by layer -> one decode token layer by layer.
+  gather) -> suffix prefill attention layer by layer -> decode tokens layer by layer.
 The first four are the cache-hit TTFT region, timed like the paper's TTFT boundary (App. C.2):
 device-synchronised at both ends, starting right before layout construction; projections,
 MLP and LM head have no weights here, so the region holds only the attention path.
@@ -15,6 +15,7 @@ the stream the kernels run on.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -26,20 +27,25 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_MFMA_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA
 METRIC = "composed-cache TTFT (ms/request); prefill attn TFLOP/s; rerotate+decode HBM GB/s"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = {"suffix_prefill_attn": "paper_2607_28069_amd/csrc/prefill_bf16.hip",
+                  "compose": "paper_2607_28069_amd/csrc/rope_compose.hip",
+                  "decode_attn": "paper_2607_28069_amd/csrc/decode_bf16.hip"}
 
 
-def parse():
+def parse(argv=None):
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--warmup", type=int, default=40)
     p.add_argument("--workload", default="c3", help="c1..c5 or a workload name")
-    p.add_argument("--decode-tokens", type=int, default=1, help="decode tokens per step")
+    p.add_argument("--decode-tokens", type=int, default=None,
+                   help="decode tokens per step (default: the workload's decode steps, else 1)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-budget-s", type=float, default=12.0)
+    p.add_argument("--cpu-budget-s", type=float, default=15.0)
     p.add_argument("--copy-calib-gib", type=float, default=0.0,
                    help="also run a plain device copy of this size per step (counter calibration)")
-    return p.parse_args()
+    return p.parse_args(argv)
 
 
 # ------------------------------------------------------------------------------------------
@@ -47,20 +53,144 @@ def parse():
 # ------------------------------------------------------------------------------------------
 
 def compose_bytes(w, ctx, n_layers):
-    # K and V rows: read from the pool and written to the cache, D elements each
+    """K and V rows read from the pool and written to the cache, D elements each."""
     return int(sum(ctx)) * w.n_kv_heads * n_layers * 4 * w.head_dim * w.elem_bytes
 
 
 def prefill_flops(w, ctx):
-    # 4 * Hq * D per visible (query, key) pair: QK^T and PV, 2 flops per multiply-add
+    """4 * Hq * D per visible (query, key) pair (QK^T and PV, 2 flops per multiply-add)."""
     Ls = w.n_suffix
     pairs = sum(Ls * c + Ls * (Ls + 1) // 2 for c in ctx)
     return 4 * w.n_q_heads * w.head_dim * pairs
 
 
 def decode_bytes(w, n_vis):
-    # every visible K and V row is read once per layer
+    """Every visible K and V row is read once per layer."""
     return int(sum(n_vis)) * w.n_kv_heads * 2 * w.head_dim * w.elem_bytes
+
+
+def source_hash(rel):
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+# ------------------------------------------------------------------------------------------
+# device workload
+# ------------------------------------------------------------------------------------------
+
+class DeviceWorkload:
+    """Every tensor of one workload, resident on the device, plus the per-step driver.
+
+    `layers` < w.n_layers builds a workload with fewer layers of the same per-layer shape.
+    """
+
+    def __init__(self, w, dev, n_dec: int, layers: int | None = None):
+        import numpy as np
+        import torch
+
+        import paper_2607_28069_amd as pic
+        from synth import inputs as S
+
+        self.w, self.dev, self.n_dec = w, dev, n_dec
+        self.L = L = w.n_layers if layers is None else layers
+        self.dt = dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+        B, Hq, Hkv, D, Ls = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_suffix
+        self.lay = lay = S.pool_layout(w)
+        self.ctx_host = S.context_lengths(lay)
+        self.max_ctx = int(self.ctx_host.max())
+        self.cap = self.max_ctx + Ls + n_dec
+        self.model = pic.Model.of(L, Hq, Hkv, D, w.dtype, w.rope_theta)
+        self.m1 = self.model.with_layers(1)
+
+        def per_layer(tensor, shape):
+            t = torch.empty((L,) + tuple(shape), dtype=dt, device=dev)
+            for l in range(L):
+                t[l] = S.device_normal(w, tensor, shape, l, dev, dt)
+            return t
+
+        self.pool_k = per_layer("pool_k", (Hkv, lay.pool_tokens, D))
+        self.pool_v = per_layer("pool_v", (Hkv, lay.pool_tokens, D))
+        self.q = per_layer("q", (B, Ls, Hq, D))
+        self.k_suf = per_layer("k_suf", (B, Ls, Hkv, D))
+        self.v_suf = per_layer("v_suf", (B, Ls, Hkv, D))
+        self.dq = per_layer("dq", (B, Hq, D))
+        self.dk = per_layer("dk", (B, Hkv, D))
+        self.dv = per_layer("dv", (B, Hkv, D))
+        self.cache_k = torch.zeros((L, B, Hkv, self.cap, D), dtype=dt, device=dev)
+        self.cache_v = torch.zeros_like(self.cache_k)
+        self.out = torch.empty((L, B, Ls, Hq, D), dtype=dt, device=dev)
+        self.dout = torch.empty((max(n_dec, 1), L, B, Hq, D), dtype=dt, device=dev)
+        self.mad = self.cap
+        self.table = torch.empty(pic.pic_rope_table_bytes(self.model, self.mad) // 4, dtype=torch.float32,
+                                 device=dev)
+        pic.pic_rope_table_init(self.model, self.mad, self.table)
+        self.ctx_dev = torch.from_numpy(self.ctx_host.astype(np.int32)).to(dev)
+        self.base_dev = torch.from_numpy((self.ctx_host + Ls).astype(np.int32)).to(dev)
+        self.max_base = self.max_ctx + Ls
+        self.ws_pre = torch.empty(max(pic.pic_prefill_workspace_bytes(self.m1, B, Ls, self.max_ctx), 16),
+                                  dtype=torch.uint8, device=dev)
+        self.ws_dec = torch.empty(max(pic.pic_decode_workspace_bytes(self.m1, B, self.max_base + n_dec, 0), 16),
+                                  dtype=torch.uint8, device=dev)
+        n_blocks_max = sum((int(n) + 63) // 64 for r in lay.requests for n in lay.doc_len[r])
+        self.blocks_pinned = torch.empty(n_blocks_max * 5, dtype=torch.int32, pin_memory=True)
+        self.blocks_dev = torch.empty(n_blocks_max * 5, dtype=torch.int32, device=dev)
+
+    def step(self, rec: dict | None = None, calib=None):
+        """One pass of the path; with `rec`, appends timings (ms) to its lists."""
+        import numpy as np
+        import torch
+
+        import paper_2607_28069_amd as pic
+
+        w, L, B, Ls = self.w, self.L, self.w.batch, self.w.n_suffix
+        stream = torch.cuda.current_stream()
+        ev = lambda: torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        # -- TTFT region
+        lay = self.lay
+        blocks, ctx = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len,
+                                          lay.doc_compile_pos, lay.pool_tokens)
+        nb = len(blocks)
+        self.blocks_pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32)))
+        self.blocks_dev[: nb * 5].copy_(self.blocks_pinned[: nb * 5], non_blocking=True)
+        e0, e1 = ev(), ev()
+        e0.record(stream)
+        pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
+                        self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
+        e1.record(stream)
+        pre = []
+        for l in range(L if Ls else 0):
+            a, b = ev(), ev()
+            a.record(stream)
+            pic.pic_suffix_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l], self.cache_k[l],
+                                        self.cache_v[l], B, self.cap, self.ctx_dev, self.max_ctx, Ls,
+                                        self.out[l], self.ws_pre)
+            b.record(stream)
+            pre.append((a, b))
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        # -- decode
+        dec = []
+        for t in range(self.n_dec):
+            for l in range(L):
+                a, b = ev(), ev()
+                a.record(stream)
+                pic.pic_decode_attn(self.m1, self.dq[l], self.dk[l], self.dv[l], self.cache_k[l],
+                                    self.cache_v[l], B, self.cap, self.base_dev, t, self.max_base,
+                                    self.dout[t, l], self.ws_dec)
+                b.record(stream)
+                dec.append((a, b))
+        if calib is not None:
+            calib[1].copy_(calib[0])
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        if rec is not None:
+            rec["ttft"].append((t1 - t0) * 1e3)
+            rec["step"].append((t2 - t0) * 1e3)
+            rec["compose"].append(e0.elapsed_time(e1))
+            rec["prefill"] += [a.elapsed_time(b) for a, b in pre]
+            rec["decode"] += [a.elapsed_time(b) for a, b in dec]
 
 
 # ------------------------------------------------------------------------------------------
@@ -68,7 +198,8 @@ def decode_bytes(w, n_vis):
 # ------------------------------------------------------------------------------------------
 
 def cpu_baseline(w, budget_s):
-    import numpy as np
+    """The oracle on the host cores: plan + compose + suffix prefill for request-layers of the
+    same workload, cycling over requests until `budget_s` of CPU work, scaled to ms/request."""
     from threadpoolctl import threadpool_info
 
     from oracle import pic_oracle as O
@@ -76,30 +207,27 @@ def cpu_baseline(w, budget_s):
 
     lay = S.pool_layout(w)
     inp = S.host_layer(w, lay, 0)
-    maps = O.plan_layout(lay.requests[:1], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)
     samples = []
     t_end = time.perf_counter() + budget_s
     b = 0
     while True:
         t0 = time.perf_counter()
-        m = O.plan_layout([lay.requests[b % w.batch]], lay.doc_offset, lay.doc_len,
-                          lay.doc_compile_pos)[0]
+        r = b % w.batch
+        m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
         K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], m, w.rope_theta, w.dtype)
         if w.n_suffix:
-            O.suffix_prefill(K, V, inp["q"][b % w.batch], inp["k_suf"][b % w.batch],
-                             inp["v_suf"][b % w.batch])
+            O.suffix_prefill(K, V, inp["q"][r], inp["k_suf"][r], inp["v_suf"][r])
         samples.append(time.perf_counter() - t0)
         b += 1
-        if time.perf_counter() > t_end or b >= w.batch:
+        if time.perf_counter() > t_end:
             break
     per_req_layer = sum(samples) / len(samples)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    del maps
     return {
         "value": per_req_layer * w.n_layers * 1e3, "unit": "ms/request", "cores": int(threads),
         "kind": "oracle",
-        "sample": f"{len(samples)} request(s) x 1 layer of {w.name} (plan + compose + suffix prefill, "
-                  f"fp64 numpy), scaled x{w.n_layers} layers; {sum(samples):.1f} s of CPU work",
+        "sample": f"{len(samples)} request-layers of {w.name} (plan + compose + suffix prefill in fp64 "
+                  f"numpy, BLAS threads = cores), mean x {w.n_layers} layers; {sum(samples):.1f} s of CPU work",
     }
 
 
@@ -113,130 +241,42 @@ def main():
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     import paper_2607_28069_amd as pic
     import synth
-    from synth import inputs as S
 
     pic.load()   # raises if libpic.so is missing: there is no fallback
     w = synth.get(args.workload)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
-    L, B, Hq, Hkv, D, Ls = w.n_layers, w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_suffix
-    n_dec = max(args.decode_tokens, 0)
-
-    # ---- setup, outside any timed region ("model loading" and cache store)
-    lay = S.pool_layout(w)
-    ctx_host = S.context_lengths(lay)
-    max_ctx = int(ctx_host.max())
-    cap = max_ctx + Ls + n_dec
-    model = pic.Model.of(L, Hq, Hkv, D, w.dtype, w.rope_theta)
-    m1 = model.with_layers(1)
-
-    def per_layer(tensor, shape):
-        t = torch.empty((L,) + tuple(shape), dtype=dt, device=dev)
-        for l in range(L):
-            t[l] = S.device_normal(w, tensor, shape, l, dev, dt)
-        return t
-
-    pool_k = per_layer("pool_k", (Hkv, lay.pool_tokens, D))
-    pool_v = per_layer("pool_v", (Hkv, lay.pool_tokens, D))
-    q = per_layer("q", (B, Ls, Hq, D))
-    k_suf = per_layer("k_suf", (B, Ls, Hkv, D))
-    v_suf = per_layer("v_suf", (B, Ls, Hkv, D))
-    dq = per_layer("dq", (B, Hq, D))
-    dk = per_layer("dk", (B, Hkv, D))
-    dv = per_layer("dv", (B, Hkv, D))
-    cache_k = torch.zeros((L, B, Hkv, cap, D), dtype=dt, device=dev)
-    cache_v = torch.zeros_like(cache_k)
-    out = torch.empty((L, B, Ls, Hq, D), dtype=dt, device=dev)
-    dout = torch.empty((L, B, Hq, D), dtype=dt, device=dev)
-    mad = cap
-    table = torch.empty(pic.pic_rope_table_bytes(model, mad) // 4, dtype=torch.float32, device=dev)
-    pic.pic_rope_table_init(model, mad, table)
-    ctx_dev = torch.from_numpy(ctx_host.astype(np.int32)).to(dev)
-    base_dev = torch.from_numpy((ctx_host + Ls).astype(np.int32)).to(dev)
-    max_base = max_ctx + Ls
-    ws_pre = torch.empty(max(pic.pic_prefill_workspace_bytes(m1, B, Ls, max_ctx), 16), dtype=torch.uint8, device=dev)
-    ws_dec = torch.empty(max(pic.pic_decode_workspace_bytes(m1, B, max_base + n_dec, 0), 16),
-                         dtype=torch.uint8, device=dev)
-    n_blocks_max = sum((int(n) + 63) // 64 for r in lay.requests for n in lay.doc_len[r])
-    blocks_pinned = torch.empty(n_blocks_max * 5, dtype=torch.int32, pin_memory=True)
-    blocks_dev = torch.empty(n_blocks_max * 5, dtype=torch.int32, device=dev)
+    n_dec = args.decode_tokens if args.decode_tokens is not None else (w.decode_steps or 1)
+    wl = DeviceWorkload(w, dev, n_dec)
     calib = None
     if args.copy_calib_gib > 0:
         n = int(args.copy_calib_gib * (1 << 30)) // 2
-        calib = (torch.empty(n, dtype=torch.bfloat16, device=dev).normal_(), torch.empty(n, dtype=torch.bfloat16, device=dev))
-    stream = torch.cuda.current_stream()
+        calib = (torch.empty(n, dtype=torch.bfloat16, device=dev).normal_(),
+                 torch.empty(n, dtype=torch.bfloat16, device=dev))
 
-    ev = lambda: torch.cuda.Event(enable_timing=True)
     rec = {"compose": [], "prefill": [], "decode": [], "ttft": [], "step": []}
-
-    def step(timing: bool):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        # -- TTFT region
-        blocks, ctx = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len,
-                                          lay.doc_compile_pos, lay.pool_tokens)
-        nb = len(blocks)
-        blocks_pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32)))
-        blocks_dev[: nb * 5].copy_(blocks_pinned[: nb * 5], non_blocking=True)
-        e0, e1 = ev(), ev()
-        e0.record(stream)
-        pic.pic_compose(model, pool_k, pool_v, lay.pool_tokens, blocks_dev, nb, table, mad,
-                        cache_k, cache_v, B, cap)
-        e1.record(stream)
-        pre = []
-        for l in range(L):
-            a, b = ev(), ev()
-            a.record(stream)
-            pic.pic_suffix_prefill_attn(m1, q[l], k_suf[l], v_suf[l], cache_k[l], cache_v[l], B, cap,
-                                        ctx_dev, max_ctx, Ls, out[l], ws_pre)
-            b.record(stream)
-            pre.append((a, b))
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        # -- decode
-        dec = []
-        for t in range(n_dec):
-            for l in range(L):
-                a, b = ev(), ev()
-                a.record(stream)
-                pic.pic_decode_attn(m1, dq[l], dk[l], dv[l], cache_k[l], cache_v[l], B, cap, base_dev, t,
-                                    max_base, dout[l], ws_dec)
-                b.record(stream)
-                dec.append((a, b))
-        if calib is not None:
-            calib[1].copy_(calib[0])
-        torch.cuda.synchronize()
-        t2 = time.perf_counter()
-        if timing:
-            rec["ttft"].append((t1 - t0) * 1e3)
-            rec["step"].append((t2 - t0) * 1e3)
-            rec["compose"].append(e0.elapsed_time(e1))
-            rec["prefill"] += [a.elapsed_time(b) for a, b in pre]
-            rec["decode"] += [a.elapsed_time(b) for a, b in dec]
-        return ctx
-
     for _ in range(args.warmup):
-        step(False)
+        wl.step(None, calib)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
-        step(True)
+        wl.step(rec, calib)
     torch.cuda.synchronize()
     total_ms = (time.perf_counter() - t_start) * 1e3
 
     mean = lambda x: float(sum(x) / len(x)) if x else 0.0
-    ctx = [int(c) for c in ctx_host]
+    L, B, Ls = wl.L, w.batch, w.n_suffix
+    ctx = [int(c) for c in wl.ctx_host]
     ttft_ms = mean(rec["ttft"])
     comp_ms, pre_ms, dec_ms = mean(rec["compose"]), mean(rec["prefill"]), mean(rec["decode"])
     comp_b = compose_bytes(w, ctx, L)
     pre_f_layer = prefill_flops(w, ctx)
-    dec_b_layer = decode_bytes(w, [c + Ls + 1 for c in ctx])   # step 0 sees ctx + Ls + 1 slots
+    # decode step t sees ctx + Ls + t + 1 slots; average over the steps of one bench step
+    dec_b_layer = sum(decode_bytes(w, [c + Ls + t + 1 for c in ctx]) for t in range(n_dec)) / max(n_dec, 1)
     kernels = {
         "compose": {"bound": "hbm", "achieved": comp_b / (comp_ms * 1e-3) / 1e9 if comp_ms else None,
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "ms_per_launch": comp_ms,
@@ -244,7 +284,7 @@ def main():
         "suffix_prefill_attn": {"bound": "mfma",
                                 "achieved": pre_f_layer / (pre_ms * 1e-3) / 1e12 if pre_ms else None,
                                 "peak": BF16_MFMA_PEAK_TFS, "unit": "TFLOP/s", "ms_per_launch": pre_ms,
-                                "per_launch": pre_f_layer, "launches_per_step": L},
+                                "per_launch": pre_f_layer, "launches_per_step": L if Ls else 0},
         "decode_attn": {"bound": "hbm", "achieved": dec_b_layer / (dec_ms * 1e-3) / 1e9 if dec_ms else None,
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "ms_per_launch": dec_ms,
                         "per_launch": dec_b_layer, "launches_per_step": L * n_dec},
@@ -254,8 +294,14 @@ def main():
         k["ms_per_step"] = k["ms_per_launch"] * k["launches_per_step"]
     dom_name = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dom = kernels[dom_name]
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):   # counter-measured HBM bytes, valid for the profiled source only
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f).get(w.name, {}).get(dom_name)
+        if t and t.get("source_sha256_16") == source_hash(KERNEL_SOURCES[dom_name]):
+            traffic = t["bytes_per_launch"]
     roofline = {"kernel": dom_name, "bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
-                "unit": dom["unit"], "frac": dom["frac"], "traffic": None}
+                "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
 
     res = {
         "metric": METRIC,
@@ -268,8 +314,9 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "layers": L, "q_heads": Hq, "kv_heads": Hkv, "head_dim": D,
-                   "rope_theta": w.rope_theta, "batch": B, "context_tokens": ctx[0] if len(set(ctx)) == 1 else ctx,
+        "config": {"workload": w.name, "layers": L, "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads,
+                   "head_dim": w.head_dim, "rope_theta": w.rope_theta, "batch": B,
+                   "context_tokens": ctx[0] if len(set(ctx)) == 1 else ctx,
                    "suffix_tokens": Ls, "decode_tokens_per_step": n_dec, "pool_docs": w.pool_docs,
                    "docs_per_request": w.docs_per_request},
         "ttft_ms_batch": ttft_ms,
