@@ -165,7 +165,8 @@ pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const 
      base_len [device, batch]  valid slots before the first decode step; clamped to
                                [0, max_base_len]; max_base_len + step + 1 <= cache_cap
      workspace                 pic_decode_workspace_bytes(...) bytes for the same batch,
-                               max_base_len + step + 1 and n_splits */
+                               max_base_len + step + 1 and n_splits; 0 bytes (NULL allowed)
+                               when the split count is 1 */
 size_t pic_decode_workspace_bytes(const pic_model* model, int32_t batch, int32_t max_len,
                                   int32_t n_splits);
 pic_status pic_decode_attn(const pic_model* model, const void* q, const void* k_new,

@@ -1,54 +1,69 @@
 // Single-token decode attention over the completed cache (App. C.1: the linked cache then serves
-// ordinary autoregressive decoding), bf16 storage, split over the context.
+// ordinary autoregressive decoding), bf16 storage.
 //
 // Per (layer, request b, kv head g) the n_rep query heads of g (one token) attend over slots
-// [0, p] with p = base_len[b] + step.  The step reads every cached K/V row once, so it is bound
-// by HBM bandwidth; arithmetic goes to MFMA only so that it costs no VALU time:
-//  * one wave per workgroup, one context chunk per workgroup; the chunk is streamed in 32-key
-//    tiles with 16-byte loads that cover 4 whole rows per instruction, the next tile's loads
-//    in flight while the current one is used;
-//  * S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_16x16x32_bf16 with the query heads along
-//    N (n_rep <= 16; unused columns are zero), K and transposed V staged in the wave's LDS;
-//  * each chunk leaves (m, l, unnormalised O) in fp32 workspace and a second kernel merges the
-//    chunks by log-sum-exp and writes bf16.
+// [0, p] with p = base_len[b] + step, the new token's slot.  A step reads every cached K/V row
+// once, so it is bound by HBM bandwidth; arithmetic goes to MFMA only so that it costs no VALU
+// time:
+//  * a workgroup of 4 waves covers one context range of one (request, kv head); each wave
+//    streams its own quarter in 32-key tiles, with the next tile's loads in flight while the
+//    current one is used and no barrier inside the loop;
+//  * S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with the query heads along N (n_rep <= 16, unused
+//    columns zero): K goes straight from global memory into the A-operand layout (16 bytes per
+//    lane, 64 contiguous bytes per row per instruction);
+//  * O^T = V^T P^T with the same instruction: V moves global -> LDS with global_load_lds_dwordx4
+//    (row-major, chunk-swizzled) and its A operand comes from two transposing reads
+//    (ds_read_b64_tr_b16); the swizzle keeps those reads free of bank conflicts;
+//  * the new token's K/V are read straight from k_new/v_new by the wave whose range holds slot p,
+//    and written into the cache by that workgroup (no separate append launch);
+//  * the 4 waves merge by log-sum-exp in LDS; a context split over several workgroups (only when
+//    (request, kv head) pairs alone do not fill the GPU) leaves fp32 partials for a combine pass.
+#include <type_traits>
+
 #include "pic_internal.h"
 
 namespace pic {
 namespace {
 
 constexpr int kHD = 128;
-constexpr int kTile = 32;                    // keys per tile
-constexpr int kKStride = kHD / 2 + 4;        // dwords per K row in LDS
-constexpr int kVStride = kTile / 2 + 4;      // dwords per transposed-V row in LDS
-constexpr int kMaxRep = 16;
+constexpr int kWaves = 4;
+constexpr int kTile = 32;                          // keys per wave tile
+constexpr int kRowBytes = kHD * 2;                 // 256
+constexpr int kVTileBytes = kTile * kRowBytes;     // 8 KB per wave per buffer
+constexpr int kMinWaveKeys = 64;
+
+#define LDS_AS __attribute__((address_space(3)))
+#define GLOBAL_AS __attribute__((address_space(1)))
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// Order of a tile's keys along the k axis of the P^T operand.  The S^T accumulator gives lane
-// group g4 = lane / 16 keys {4 g4 + e} and {16 + 4 g4 + e}; the B operand wants lane group g4
-// to hold k = 8 g4 .. 8 g4 + 7.  kappa(key) is the k index a key takes.
-__device__ __forceinline__ int kappa(int key) {
-  return (((key >> 2) & 3) << 3) | (((key >> 4) & 1) << 2) | (key & 3);
-}
+// V tile rows are 256 bytes; 16-byte chunk c of row `key` sits at slot c ^ v_swz(key).
+__device__ __forceinline__ int v_swz(int key) { return ((key & 3) << 1) | (((key >> 2) & 1) << 3); }
 
 struct DecodeArgs {
   const bf16_t* q;        // [L][B][Hq][D]
-  const bf16_t* cache_k;  // [L][B][Hkv][cap][D]
-  const bf16_t* cache_v;
+  const bf16_t* k_new;    // [L][B][Hkv][D]
+  const bf16_t* v_new;
+  bf16_t* cache_k;        // [L][B][Hkv][cap][D]
+  bf16_t* cache_v;
   const int32_t* base_len;
-  float* ws_o;            // [L][B][Hq][S][D]
+  bf16_t* out;            // [L][B][Hq][D]
+  float* ws_o;            // [L][B][Hq][S][D]   (n_splits > 1)
   float* ws_ml;           // [L][B][Hq][S][2]
   int32_t batch, cache_cap, n_q_heads, n_kv_heads, max_base, step, n_splits, chunk;
   float scale_log2;
 };
 
-// grid (S * B * Hkv, L), 64 threads
-__global__ void __launch_bounds__(64) decode_bf16_kernel(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) uint32_t k_lds[kTile * kKStride];
-  __shared__ __attribute__((aligned(16))) uint32_t v_lds[kHD * kVStride];
+// grid (S * B * Hkv, L), 256 threads
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+decode_bf16_kernel(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds0[kWaves * kVTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds1[kWaves * kVTileBytes];
 
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int split = blockIdx.x % a.n_splits;
   const int bg = blockIdx.x / a.n_splits;
   const int b = bg / a.n_kv_heads, g = bg % a.n_kv_heads;
@@ -57,16 +72,30 @@ __global__ void __launch_bounds__(64) decode_bf16_kernel(DecodeArgs a) {
 
   int32_t base = a.base_len[b];
   base = base < 0 ? 0 : (base > a.max_base ? a.max_base : base);
-  int n_vis = base + a.step + 1;
+  const int p = base + a.step;                       // the new token's slot
+  int n_vis = p + 1;
   if (n_vis > a.cache_cap) n_vis = a.cache_cap;
-  const int c0 = split * a.chunk;
-  const int c1 = min(c0 + a.chunk, n_vis);
+  const int wc0 = min(split * a.chunk, n_vis);
+  const int wc1 = min(wc0 + a.chunk, n_vis);
+  const int sub = a.chunk / kWaves;                  // multiple of kTile
+  const int c0 = min(wc0 + wave * sub, wc1);
+  const int c1 = min(c0 + sub, wc1);
+
+  const int64_t bh_kv = (((int64_t)l * a.batch + b) * a.n_kv_heads + g);
+  const bf16_t* Kg = a.cache_k + bh_kv * a.cache_cap * kHD;
+  const bf16_t* Vg = a.cache_v + bh_kv * a.cache_cap * kHD;
+  const bf16_t* Kn = a.k_new + bh_kv * kHD;
+  const bf16_t* Vn = a.v_new + bh_kv * kHD;
+
+  // The workgroup holding slot p writes the new token into the cache.  Nobody reads that row
+  // from the cache during this launch: the wave whose range holds it reads k_new / v_new.
+  if (p < a.cache_cap && p >= wc0 && p < wc1 && wave == 0 && lane < 32) {
+    const int c = lane & 15;
+    u32x4* dst = reinterpret_cast<u32x4*>((lane < 16 ? a.cache_k : a.cache_v) + (bh_kv * a.cache_cap + p) * kHD);
+    dst[c] = reinterpret_cast<const u32x4*>(lane < 16 ? Kn : Vn)[c];
+  }
 
   const int n = lane & 15, g4 = lane >> 4;
-  const int64_t bh_kv = (((int64_t)l * a.batch + b) * a.n_kv_heads + g) * a.cache_cap;
-  const bf16_t* Kg = a.cache_k + bh_kv * kHD;
-  const bf16_t* Vg = a.cache_v + bh_kv * kHD;
-
   // Q^T operand: lane (n, g4) holds q[head g*n_rep + n][32 ks + 8 g4 .. +8)
   bf16x8_t qop[4];
   {
@@ -77,121 +106,179 @@ __global__ void __launch_bounds__(64) decode_bf16_kernel(DecodeArgs a) {
     for (int ks = 0; ks < 4; ++ks) qop[ks] = as_bf16x8(ok ? qp[4 * ks + g4] : u32x4{0, 0, 0, 0});
   }
 
-  const int dc = lane & 15;   // 16-byte chunk of a row: head dims [8 dc, 8 dc + 8)
-  const int kr = lane >> 4;   // K: keys kr + 4 u (u = 0..7); V: keys 4 (kr + 4 i) + u
-  u32x4 kreg[8], vreg[8];
-  auto load_tile = [&](int k0) {
+  // K of one tile, straight into the A-operand layout: [mb][ks] = row k0 + 16 mb + n, head
+  // dims 32 ks + 8 g4 .. +8.  Rows past the range are clamped (their scores are masked).
+  auto load_k = [&](int k0, u32x4 (&kr)[2][4]) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int kk = k0 + kr + 4 * u;
-      kreg[u] = kk < c1 ? *reinterpret_cast<const u32x4*>(Kg + (int64_t)kk * kHD + 8 * dc)
-                        : u32x4{0, 0, 0, 0};
-    }
+    for (int mb = 0; mb < 2; ++mb) {
+      const int row = min(k0 + 16 * mb + n, c1 - 1);
+      const bf16_t* src = row == p ? Kn : Kg + (int64_t)row * kHD;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int kv = k0 + 4 * (kr + 4 * i) + u;
-        vreg[4 * i + u] = kv < c1 ? *reinterpret_cast<const u32x4*>(Vg + (int64_t)kv * kHD + 8 * dc)
-                                  : u32x4{0, 0, 0, 0};
-      }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      *reinterpret_cast<u32x4*>(k_lds + (kr + 4 * u) * kKStride + 4 * dc) = kreg[u];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int col = kappa(4 * (kr + 4 * i)) >> 1;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int word = e >> 1;
-        uint32_t lo, hi;
-        if (e & 1) {
-          lo = (vreg[4 * i + 0][word] >> 16) | (vreg[4 * i + 1][word] & 0xFFFF0000u);
-          hi = (vreg[4 * i + 2][word] >> 16) | (vreg[4 * i + 3][word] & 0xFFFF0000u);
-        } else {
-          lo = (vreg[4 * i + 0][word] & 0xFFFFu) | (vreg[4 * i + 1][word] << 16);
-          hi = (vreg[4 * i + 2][word] & 0xFFFFu) | (vreg[4 * i + 3][word] << 16);
-        }
-        *reinterpret_cast<uint2*>(v_lds + (8 * dc + e) * kVStride + col) = make_uint2(lo, hi);
-      }
+      for (int ks = 0; ks < 4; ++ks)
+        kr[mb][ks] = *reinterpret_cast<const u32x4*>(src + 32 * ks + 8 * g4);
     }
   };
+  // V of one tile into this wave's LDS buffer: instruction i fills rows 4 i .. 4 i + 3, lane
+  // -> row 4 i + lane / 16, chunk slot lane % 16 (holding chunk slot ^ v_swz(row)).
+  const int ld_r = lane >> 4, ld_slot = lane & 15;
+  auto load_v = [&](int k0, uint8_t* buf) {
+#pragma unroll
+    for (int i = 0; i < kTile / 4; ++i) {
+      const int rl = 4 * i + ld_r;
+      const int row = min(k0 + rl, c1 - 1);
+      const int c = ld_slot ^ v_swz(rl);
+      const bf16_t* src = (row == p ? Vn : Vg + (int64_t)row * kHD) + 8 * c;
+      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)src,
+                                       (LDS_AS void*)(buf + wave * kVTileBytes + 4 * i * kRowBytes), 16, 0, 0);
+    }
+  };
+
+  // Transposing-read offsets: 16-lane group G = g4, lane j = 4 rr + qq points at row
+  // 16 half + 4 G + rr, head dims 16 db + 4 qq .. +3; lane i then receives head dim 16 db + i.
+  // Kept in registers: computed inline, the compiler makes these reads wait for the V loads in
+  // flight into the other buffer.
+  const int rr = (lane & 15) >> 2, qq = lane & 3;
+  int v_rd_off[8][2];
+#pragma unroll
+  for (int db = 0; db < 8; ++db)
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int row = 16 * half + 4 * g4 + rr;
+      v_rd_off[db][half] = row * kRowBytes + (((2 * db + (qq >> 1)) ^ v_swz(row)) << 4) + 8 * (qq & 1);
+    }
+  auto v_rd = [&](int db, int half) { return v_rd_off[db][half]; };
 
   f32x4_t oacc[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) oacc[i] = f32x4_t{};
   float m_run = -INFINITY, l_part = 0.f;
+  const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
 
-  if (c0 < c1) load_tile(c0);
-  for (int k0 = c0; k0 < c1; k0 += kTile) {
-    __syncthreads();            // previous tile's LDS reads are done
-    store_tile();
-    __syncthreads();
-    if (k0 + kTile < c1) load_tile(k0 + kTile);
-
-    // S^T: keys [k0 + 16 mb, +16) x 16 query columns
-    f32x4_t sacc[2];
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      sacc[mb] = f32x4_t{};
-      const uint32_t* krow = k_lds + (16 * mb + n) * kKStride + 4 * g4;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(krow + 16 * ks);
-        sacc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kv), qop[ks], sacc[mb], 0, 0, 0);
-      }
+  // One tile at k0; P = tile parity selects the (static) LDS buffers, so the compiler sees
+  // that the loads in flight into one buffer do not alias reads from the other.
+  auto tile = [&](int k0, auto parity, u32x4 (&kcur)[2][4], u32x4 (&knext)[2][4]) {
+    constexpr int P = decltype(parity)::value;
+    const uint8_t* vcur = P ? v_lds1 : v_lds0;
+    uint8_t* vnext = P ? v_lds0 : v_lds1;
+    if (k0 + kTile < c1) {
+      load_k(k0 + kTile, knext);
+      load_v(k0 + kTile, vnext);
     }
+    f32x4_t sacc[2] = {f32x4_t{}, f32x4_t{}};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+        sacc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kcur[mb][ks]), qop[ks], sacc[mb], 0, 0, 0);
     float mx = -INFINITY;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int key = k0 + 16 * mb + 4 * g4 + e;
-        if (key >= c1) sacc[mb][e] = -INFINITY;
+        if (k0 + 16 * mb + 4 * g4 + e >= c1) sacc[mb][e] = -INFINITY;
         mx = fmaxf(mx, sacc[mb][e]);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx * a.scale_log2);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float p[8];
+    const float m_tile = mx * a.scale_log2;
+    if (__any(m_tile > m_run + 8.f)) {   // lazy reference max, as in the prefill kernel
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[0][e], a.scale_log2, -m_new));
-      p[4 + e] = __builtin_amdgcn_exp2f(fmaf(sacc[1][e], a.scale_log2, -m_new));
+      for (int db = 0; db < 8; ++db) oacc[db] *= alpha;
     }
-    float psum = 0.f;
+    uint32_t pw[4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) psum += p[j];
-    l_part = l_part * alpha + psum;
-    const bf16x8_t pop = as_bf16x8(u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                                         pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])});
+    for (int j = 0; j < 2; ++j) {
+      pw[j] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(sacc[0][2 * j], a.scale_log2, -m_run)),
+                          __builtin_amdgcn_exp2f(fmaf(sacc[0][2 * j + 1], a.scale_log2, -m_run)));
+      pw[2 + j] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(sacc[1][2 * j], a.scale_log2, -m_run)),
+                              __builtin_amdgcn_exp2f(fmaf(sacc[1][2 * j + 1], a.scale_log2, -m_run)));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      l_part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[j]), ones, l_part, false);
+    // P^T operand: k index 8 g4 + j <-> key 16 (j / 4) + 4 g4 + j % 4 (accumulator order)
+    const bf16x8_t pop = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
+    const uint8_t* vw = vcur + wave * kVTileBytes;
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
-      oacc[db] *= alpha;
-      const u32x4 vv = *reinterpret_cast<const u32x4*>(v_lds + (16 * db + n) * kVStride + 4 * g4);
-      oacc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), pop, oacc[db], 0, 0, 0);
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vw + v_rd(db, 0)));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vw + v_rd(db, 1)));
+      const bf16x8_t vv = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      oacc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, pop, oacc[db], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the next tile is resident
+  };
+
+  u32x4 k_a[2][4], k_b[2][4];
+  if (c0 < c1) {
+    load_k(c0, k_a);
+    load_v(c0, v_lds0);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    for (int k0 = c0; k0 < c1; k0 += 2 * kTile) {
+      tile(k0, std::integral_constant<int, 0>{}, k_a, k_b);
+      if (k0 + kTile < c1) tile(k0 + kTile, std::integral_constant<int, 1>{}, k_b, k_a);
     }
   }
 
+  // ---- merge the 4 waves (log-sum-exp) through LDS, reusing the V buffers
   float l_tot = l_part + __shfl_xor(l_part, 16, 64);
   l_tot += __shfl_xor(l_tot, 32, 64);
+  __syncthreads();
+  float* o_lds = reinterpret_cast<float*>(v_lds0);    // [4][16][128] fp32 = 32 KB
+  float* ml_lds = reinterpret_cast<float*>(v_lds1);   // [4][16][2]
   if (n < n_rep) {
-    const int hq = g * n_rep + n;
-    const int64_t slot = (((int64_t)l * a.batch + b) * a.n_q_heads + hq) * a.n_splits + split;
-    float* wo = a.ws_o + slot * kHD;
 #pragma unroll
     for (int db = 0; db < 8; ++db)
-      *reinterpret_cast<float4*>(wo + 16 * db + 4 * g4) =
+      *reinterpret_cast<float4*>(o_lds + (wave * 16 + n) * kHD + 16 * db + 4 * g4) =
           make_float4(oacc[db][0], oacc[db][1], oacc[db][2], oacc[db][3]);
-    if (g4 == 0) *reinterpret_cast<float2*>(a.ws_ml + 2 * slot) = make_float2(m_run, l_tot);
+    if (g4 == 0) {
+      ml_lds[(wave * 16 + n) * 2] = m_run;
+      ml_lds[(wave * 16 + n) * 2 + 1] = l_tot;
+    }
+  }
+  __syncthreads();
+  // thread -> (query n = tid / 16, head dims 8 (tid % 16) .. +8)
+  const int mn = tid >> 4, md = 8 * (tid & 15);
+  if (mn < n_rep) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, ml_lds[(w * 16 + mn) * 2]);
+    float den = 0.f, o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float mw = ml_lds[(w * 16 + mn) * 2];
+      if (mw == -INFINITY) continue;   // an empty wave range
+      const float wt = __builtin_amdgcn_exp2f(mw - M);
+      den += wt * ml_lds[(w * 16 + mn) * 2 + 1];
+      const float4 x0 = *reinterpret_cast<const float4*>(o_lds + (w * 16 + mn) * kHD + md);
+      const float4 x1 = *reinterpret_cast<const float4*>(o_lds + (w * 16 + mn) * kHD + md + 4);
+      o[0] += wt * x0.x; o[1] += wt * x0.y; o[2] += wt * x0.z; o[3] += wt * x0.w;
+      o[4] += wt * x1.x; o[5] += wt * x1.y; o[6] += wt * x1.z; o[7] += wt * x1.w;
+    }
+    const int64_t row = ((int64_t)l * a.batch + b) * a.n_q_heads + g * n_rep + mn;
+    if (a.n_splits == 1) {
+      const float inv = 1.f / den;
+      uint4 v;
+      v.x = pack_bf16x2(o[0] * inv, o[1] * inv);
+      v.y = pack_bf16x2(o[2] * inv, o[3] * inv);
+      v.z = pack_bf16x2(o[4] * inv, o[5] * inv);
+      v.w = pack_bf16x2(o[6] * inv, o[7] * inv);
+      *reinterpret_cast<uint4*>(a.out + row * kHD + md) = v;
+    } else {
+      const int64_t slot = row * a.n_splits + split;
+      float* wo = a.ws_o + slot * kHD + md;
+      *reinterpret_cast<float4*>(wo) = make_float4(o[0], o[1], o[2], o[3]);
+      *reinterpret_cast<float4*>(wo + 4) = make_float4(o[4], o[5], o[6], o[7]);
+      if (md == 0) *reinterpret_cast<float2*>(a.ws_ml + 2 * slot) = make_float2(M, den);
+    }
   }
 }
 
-// grid (B * Hq, L), 64 threads: merge the chunks of one query head by log-sum-exp.
+// grid (B * Hq, L), 64 threads: merge the splits of one query head by log-sum-exp.
 __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restrict__ ws_o,
                                                             const float* __restrict__ ws_ml,
                                                             int32_t n_splits, int64_t rows_per_layer,
@@ -217,35 +304,41 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
 
 }  // namespace
 
+// Workgroups per (request, kv head): enough 4-wave workgroups for about two resident rounds
+// (512 per launch), each wave keeping at least kMinWaveKeys keys.
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len) {
-  const int64_t pairs = (int64_t)s.batch * s.n_kv_heads;
-  const int64_t target_waves = 2048;   // about one resident round of waves
-  int64_t splits = (target_waves + pairs - 1) / pairs;
-  const int64_t max_splits = (max_len + 255) / 256;   // keep chunks >= 256 keys
+  const int64_t pairs = (int64_t)s.batch * s.n_kv_heads * s.n_layers;
+  int64_t splits = (512 + pairs - 1) / pairs;
+  const int64_t max_splits = (max_len + kWaves * kMinWaveKeys - 1) / (kWaves * kMinWaveKeys);
   if (splits > max_splits) splits = max_splits;
   if (splits < 1) splits = 1;
   return (int32_t)splits;
 }
 
 size_t decode_bf16_workspace(const AttnShape& s, int32_t, int32_t n_splits) {
+  if (n_splits <= 1) return 0;
   const size_t rows = (size_t)s.n_layers * s.batch * s.n_q_heads * n_splits;
   return rows * (kHD + 2) * sizeof(float);
 }
 
-hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
-                              const bf16_t* cache_v, const int32_t* base_len, int32_t max_base,
-                              int32_t step, int32_t n_splits, bf16_t* out, void* workspace,
-                              size_t, hipStream_t stream) {
+hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_new,
+                              const bf16_t* v_new, bf16_t* cache_k, bf16_t* cache_v,
+                              const int32_t* base_len, int32_t max_base, int32_t step,
+                              int32_t n_splits, bf16_t* out, void* workspace, size_t,
+                              hipStream_t stream) {
   if (s.batch == 0 || s.n_layers == 0) return hipSuccess;
   const int32_t max_len = max_base + step + 1;
   DecodeArgs a;
   a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
   a.cache_k = cache_k;
   a.cache_v = cache_v;
   a.base_len = base_len;
+  a.out = out;
   const size_t rows = (size_t)s.n_layers * s.batch * s.n_q_heads * n_splits;
   a.ws_o = static_cast<float*>(workspace);
-  a.ws_ml = a.ws_o + rows * kHD;
+  a.ws_ml = a.ws_o ? a.ws_o + rows * kHD : nullptr;
   a.batch = s.batch;
   a.cache_cap = s.cache_cap;
   a.n_q_heads = s.n_q_heads;
@@ -253,13 +346,13 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   a.max_base = max_base;
   a.step = step;
   a.n_splits = n_splits;
-  int32_t chunk = (max_len + n_splits - 1) / n_splits;
-  a.chunk = (chunk + kTile - 1) / kTile * kTile;
+  const int32_t chunk = (max_len + n_splits - 1) / n_splits;
+  a.chunk = (chunk + kWaves * kTile - 1) / (kWaves * kTile) * (kWaves * kTile);
   a.scale_log2 = s.scale_log2;
   hipLaunchKernelGGL(decode_bf16_kernel, dim3(n_splits * s.batch * s.n_kv_heads, s.n_layers),
-                     dim3(64), 0, stream, a);
+                     dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || n_splits == 1) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(s.batch * s.n_q_heads, s.n_layers), dim3(64), 0,
                      stream, a.ws_o, a.ws_ml, n_splits, (int64_t)s.batch * s.n_q_heads, out);
   return hipGetLastError();

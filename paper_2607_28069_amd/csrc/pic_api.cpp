@@ -386,16 +386,14 @@ PIC_API pic_status pic_decode_attn(const pic_model* model, const void* q, const 
     return fail(PIC_ERR_UNSUPPORTED, "too many splits");
   if (n_splits > max_len) n_splits = (int32_t)max_len;
   const size_t need = pic::decode_bf16_workspace(s, (int32_t)max_len, n_splits);
-  if (workspace == nullptr || ws_bytes < need)
+  if (need > 0 && (workspace == nullptr || ws_bytes < need))
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
-  PIC_CHECK(check_ptr(workspace, "workspace"));
-  PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
-                                          model->n_kv_heads, k_new, v_new, cache_k, cache_v, batch,
-                                          cache_cap, base_len, max_base_len, step, 1, st),
-                       "decode append launch"));
+  if (need > 0) PIC_CHECK(check_ptr(workspace, "workspace"));
   return hip_status(pic::launch_decode_bf16(s, static_cast<const pic::bf16_t*>(q),
-                                            static_cast<const pic::bf16_t*>(cache_k),
-                                            static_cast<const pic::bf16_t*>(cache_v), base_len,
+                                            static_cast<const pic::bf16_t*>(k_new),
+                                            static_cast<const pic::bf16_t*>(v_new),
+                                            static_cast<pic::bf16_t*>(cache_k),
+                                            static_cast<pic::bf16_t*>(cache_v), base_len,
                                             max_base_len, step, n_splits,
                                             static_cast<pic::bf16_t*>(out), workspace, ws_bytes, st),
                     "decode attention launch");

@@ -66,9 +66,11 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
 
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len);
 size_t decode_bf16_workspace(const AttnShape& s, int32_t max_len, int32_t n_splits);
-hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
-                              const bf16_t* cache_v, const int32_t* base_len, int32_t max_base,
-                              int32_t step, int32_t n_splits, bf16_t* out, void* workspace,
-                              size_t ws_bytes, hipStream_t stream);
+// Also writes k_new / v_new into slot base_len[b] + step of the cache.
+hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_new,
+                              const bf16_t* v_new, bf16_t* cache_k, bf16_t* cache_v,
+                              const int32_t* base_len, int32_t max_base, int32_t step,
+                              int32_t n_splits, bf16_t* out, void* workspace, size_t ws_bytes,
+                              hipStream_t stream);
 
 }  // namespace pic

@@ -172,6 +172,9 @@ def test_sizes(lib):
     assert pic.pic_rope_table_bytes(m, (1 << 20) + 1) == 0
     s = pic.pic_decode_auto_splits(m, 64, 16640)
     assert s >= 1
-    assert pic.pic_decode_workspace_bytes(m, 64, 16640, 0) == 64 * 32 * s * 130 * 4
+    # fp32 partials (head_dim outputs + max + denominator) per split; none without a split
+    assert pic.pic_decode_workspace_bytes(m, 64, 16640, 0) == (0 if s == 1 else 64 * 32 * s * 130 * 4)
+    assert pic.pic_decode_workspace_bytes(m, 64, 16640, 1) == 0
     assert pic.pic_decode_workspace_bytes(m, 64, 16640, 3) == 64 * 32 * 3 * 130 * 4
+    assert pic.pic_decode_auto_splits(m, 1, 16640) > 1
     assert pic.pic_prefill_workspace_bytes(_model(dtype="f32", head_dim=64), 1, 16, 272) == 0
