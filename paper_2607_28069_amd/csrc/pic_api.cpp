@@ -303,20 +303,24 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   const hipStream_t st = (hipStream_t)stream;
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
-  // a4: suffix K/V into slots [ctx, ctx + n_suffix) (App. C.1: inline KVs interleaved)
-  PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
-                                          model->n_kv_heads, k_suf, v_suf, cache_k, cache_v,
-                                          batch, cache_cap, ctx_len, max_ctx, 0, n_suffix, st),
-                       "suffix append launch"));
-  if (model->dtype == PIC_F32)
+  // a4: suffix K/V into slots [ctx, ctx + n_suffix) (App. C.1: inline KVs interleaved); the
+  // bf16 kernel does this itself
+  if (model->dtype == PIC_F32) {
+    PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
+                                            model->n_kv_heads, k_suf, v_suf, cache_k, cache_v,
+                                            batch, cache_cap, ctx_len, max_ctx, 0, n_suffix, st),
+                         "suffix append launch"));
     return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
                                                 static_cast<const float*>(cache_k),
                                                 static_cast<const float*>(cache_v), ctx_len,
                                                 max_ctx, 0, n_suffix, static_cast<float*>(out), st),
                       "prefill attention launch");
+  }
   return hip_status(pic::launch_prefill_bf16(s, static_cast<const pic::bf16_t*>(q),
-                                             static_cast<const pic::bf16_t*>(cache_k),
-                                             static_cast<const pic::bf16_t*>(cache_v), ctx_len,
+                                             static_cast<const pic::bf16_t*>(k_suf),
+                                             static_cast<const pic::bf16_t*>(v_suf),
+                                             static_cast<pic::bf16_t*>(cache_k),
+                                             static_cast<pic::bf16_t*>(cache_v), ctx_len,
                                              max_ctx, n_suffix, static_cast<pic::bf16_t*>(out),
                                              workspace, ws_bytes, st),
                     "prefill attention launch");

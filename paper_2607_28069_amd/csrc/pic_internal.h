@@ -59,8 +59,10 @@ hipError_t launch_attn_rows_f32(const AttnShape& s, const float* q, const float*
                                 int32_t offset, int32_t n_q, float* out, hipStream_t stream);
 
 size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx);
-hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
-                               const bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
+// Also writes k_suf / v_suf into cache slots [ctx_len[b], ctx_len[b] + n_suffix).
+hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_suf,
+                               const bf16_t* v_suf, bf16_t* cache_k, bf16_t* cache_v,
+                               const int32_t* ctx_len, int32_t max_ctx,
                                int32_t n_suffix, bf16_t* out, void* workspace, size_t ws_bytes,
                                hipStream_t stream);
 

@@ -25,6 +25,9 @@
 //    probabilities, which then feed the PV products of tile t.
 //  * Workgroups sharing a (request, kv head) key stream are mapped onto the same XCD (blocks
 //    are dealt round-robin over the 8 XCDs), so that stream is fetched into one L2.
+//  * The suffix's own keys/values are read straight from k_suf / v_suf; one workgroup per
+//    (request, kv head) also stores them into cache slots [ctx, ctx + n_suffix) (no separate
+//    append launch, and no workgroup reads those slots from the cache).
 #include <type_traits>
 
 #include "pic_internal.h"
@@ -68,8 +71,10 @@ __device__ __forceinline__ int v_off(int key, int c) { return key * kRowBytes + 
 
 struct PrefillArgs {
   const bf16_t* q;
-  const bf16_t* cache_k;
-  const bf16_t* cache_v;
+  const bf16_t* k_suf;      // [L][B][n_suffix][Hkv][D]
+  const bf16_t* v_suf;
+  bf16_t* cache_k;
+  bf16_t* cache_v;
   const int32_t* ctx_len;
   bf16_t* out;
   int32_t max_ctx, n_suffix, batch, cache_cap, n_q_heads, n_kv_heads;
@@ -130,6 +135,19 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int64_t bh_kv = (((int64_t)l * a.batch + b) * a.n_kv_heads + g) * a.cache_cap;
   const bf16_t* Kg = a.cache_k + bh_kv * kHD;
   const bf16_t* Vg = a.cache_v + bh_kv * kHD;
+  // suffix token i of this (request, kv head): row i with a stride of Hkv rows
+  const int64_t suf0 = (((int64_t)l * a.batch + b) * a.n_suffix * a.n_kv_heads + g) * kHD;
+  const int64_t suf_stride = (int64_t)a.n_kv_heads * kHD;
+  const bf16_t* Ks = a.k_suf + suf0;
+  const bf16_t* Vs = a.v_suf + suf0;
+  if (mt == 0 && split == 0) {   // cache assembly: suffix rows into slots [ctx, ctx + n_suffix)
+    for (int c = tid; c < a.n_suffix * 32; c += kThreads) {
+      const int i = c >> 5, part = c & 31;           // row i, 16-byte chunk part % 16 of K or V
+      const int64_t src = i * suf_stride + 8 * (part & 15);
+      bf16_t* dst = (part < 16 ? a.cache_k : a.cache_v) + (bh_kv + ctx + i) * kHD + 8 * (part & 15);
+      *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>((part < 16 ? Ks : Vs) + src);
+    }
+  }
   const int64_t qrow = (((int64_t)l * a.batch + b) * a.n_suffix + tok) * a.n_q_heads + hq;
 
   const int64_t orow = (((int64_t)l * a.batch + b) * a.n_suffix + tok) * a.n_q_heads + hq;
@@ -158,7 +176,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int v_gc = ld_slot ^ v_swz(ld_row), k_gc = ld_slot ^ k_swz(ld_row);
   auto load_tile = [&](const bf16_t* src, uint8_t* dst_tile, int t, bool is_v) {
     const int goff = is_v ? v_goff : k_goff;
-    if ((t + 1) * kKeys <= n_keys) {
+    if ((t + 1) * kKeys <= ctx) {
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
         const bf16_t* base = src + (int64_t)(t * kKeys + 4 * kWaves * i) * kHD;   // uniform
@@ -167,11 +185,14 @@ prefill_bf16_kernel(PrefillArgs a) {
                                          16, 0, 0);
       }
     } else {
+      // a tile reaching the suffix: its keys come from k_suf / v_suf
       const int c = is_v ? v_gc : k_gc;
+      const bf16_t* suf = is_v ? Vs : Ks;
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
         const int kk = min(t * kKeys + 4 * kWaves * i + ld_row, n_keys - 1);
-        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(src + (int64_t)kk * kHD + 8 * c),
+        const bf16_t* row = kk < ctx ? src + (int64_t)kk * kHD : suf + (kk - ctx) * suf_stride;
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + 8 * c),
                                          (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
                                          16, 0, 0);
       }
@@ -427,8 +448,9 @@ size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_
   return (size_t)p.n_splits * rows * (kHD + 2) * sizeof(float);
 }
 
-hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
-                               const bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
+hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_suf,
+                               const bf16_t* v_suf, bf16_t* cache_k, bf16_t* cache_v,
+                               const int32_t* ctx_len, int32_t max_ctx,
                                int32_t n_suffix, bf16_t* out, void* workspace, size_t ws_bytes,
                                hipStream_t stream) {
   const int n_rep = s.n_q_heads / s.n_kv_heads;
@@ -437,6 +459,8 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
   const SplitPlan p = plan_splits(s, n_suffix, max_ctx);
   PrefillArgs a;
   a.q = q;
+  a.k_suf = k_suf;
+  a.v_suf = v_suf;
   a.cache_k = cache_k;
   a.cache_v = cache_v;
   a.ctx_len = ctx_len;
