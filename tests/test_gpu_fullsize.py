@@ -94,3 +94,40 @@ def test_qwen7b_32k_full_per_layer_shape():
     for r in (0, 5):
         _check_request(wl, 0, r, tokens=[0, 1, 63, 64, 100, 255], decode_steps=1)
         print(f"[c5] request {r} ok", flush=True)
+
+
+def test_llama8b_decode_256_steps_all_layers():
+    # The whole decode workload: 64 requests x 16K composed context x 32 layers, 256 decode
+    # steps.  The appended region of every request's cache is bit-exact on the first and the
+    # last layer; attention at steps 0, 1, 127 and 255 is checked against the oracle for
+    # requests {0, 63} on layers {0, 31} plus one more request on the last layer.
+    torch.cuda.empty_cache()
+    w = synth.get("c4")
+    n_dec = w.decode_steps
+    wl = DeviceWorkload(w, DEV, n_dec=n_dec)
+    wl.step()
+    torch.cuda.synchronize()
+    L, Ls = wl.L, w.n_suffix
+    assert Ls == 0   # the decode workload has no suffix: decoding starts right after the context
+    print(f"[c4] ctx={wl.max_ctx} cap={wl.cap} layers={L} steps={n_dec}", flush=True)
+    for l in (0, L - 1):
+        for r in range(w.batch):
+            c = int(wl.ctx_host[r]) + Ls
+            for cache, new in ((wl.cache_k, wl.dk), (wl.cache_v, wl.dv)):
+                app = cache[l, r, :, c:c + n_dec]
+                assert torch.equal(app, new[l, r][:, None, :].expand_as(app)), (l, r)
+    print("[c4] appended regions bit-exact", flush=True)
+    lay = wl.lay
+    for l, reqs in ((0, (0, 63)), (L - 1, (0, 63, 17))):
+        pool_k, pool_v = _host(wl.pool_k[l]), _host(wl.pool_v[l])
+        for r in reqs:
+            m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+            K, V = O.compose_request(pool_k, pool_v, m, w.rope_theta, w.dtype)
+            n = m.ctx_len + Ls
+            q, dk, dv = _host(wl.dq[l, r]), _host(wl.dk[l, r]), _host(wl.dv[l, r])
+            for t in (0, 1, 127, n_dec - 1):
+                Kt = np.concatenate([K, np.repeat(dk[:, None, :], t + 1, axis=1)], axis=1)
+                Vt = np.concatenate([V, np.repeat(dv[:, None, :], t + 1, axis=1)], axis=1)
+                ref = O.attention(q[:, None, :], np.asarray([n + t]), Kt, Vt, np.arange(n + t + 1))[:, 0]
+                assert_attn_close(_host(wl.dout[t, l, r]), ref, w.dtype)
+            print(f"[c4] layer {l} request {r} steps 0/1/127/{n_dec - 1} ok", flush=True)
