@@ -1,8 +1,8 @@
-"""Full-size GPU parity: the workloads at their real per-layer shapes, run through the same
-driver and launch configuration the benchmark times (one compose launch over all layers,
-per-layer prefill and decode calls), checked against the CPU oracle on sampled
-(layer, request) pairs.  Sampled keys/values are compared in full; attention outputs are
-compared for every head of every sampled token.
+"""Full-size GPU parity: the workloads at their real shapes, run through the same driver and
+launch configuration the benchmark times (one compose launch over all layers, per-layer prefill
+and decode calls), checked against the CPU oracle: every request's composed cache on one layer,
+and attention (every head of the sampled tokens) plus decode steps on sampled (layer, request)
+pairs spanning the first, middle and last layers.
 
 Tolerances as in test_gpu_parity: values bit-exact, bf16 keys within 1 bf16 ulp (+1e-5),
 bf16 attention within 2e-2 + 1e-2 |ref| and relative Frobenius error <= 1e-2.
@@ -83,17 +83,46 @@ def test_llama8b_decode_full_per_layer_shape():
         print(f"[c4] layer {l} request {r} ok", flush=True)
 
 
-def test_qwen7b_32k_full_per_layer_shape():
-    # 8 requests x ~32K context (32 jittered documents in per-request order), 256 suffix
-    # tokens; 1 of the 28 identical layers.
-    w = synth.get("c5")
-    wl = DeviceWorkload(w, DEV, n_dec=1, layers=1)
+def _check_compose_all_requests(wl, l):
+    """Every request's composed K/V on layer l, all elements: V bit-exact, K within 1 bf16 ulp."""
+    w, lay = wl.w, wl.lay
+    pool_k, pool_v = _host(wl.pool_k[l]), _host(wl.pool_v[l])
+    for r in range(w.batch):
+        m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+        K, V = O.compose_request(pool_k, pool_v, m, w.rope_theta, w.dtype)
+        n = m.ctx_len
+        assert np.array_equal(_host(wl.cache_v[l, r])[:, :n].view(np.uint32), V.view(np.uint32)), r
+        assert assert_keys_close(_host(wl.cache_k[l, r])[:, :n], K, w.dtype) > 0.999, r
+
+
+def test_llama8b_32layer_compose_all_requests():
+    # The bench configuration again: every request's composed cache on the last layer, and
+    # attention (all suffix tokens and heads) of one request on the middle layer.
+    w = synth.get("c3")
+    wl = DeviceWorkload(w, DEV, n_dec=1)
     wl.step()
     torch.cuda.synchronize()
-    print(f"[c5] ctx={list(wl.ctx_host)} cap={wl.cap}", flush=True)
-    for r in (0, 5):
-        _check_request(wl, 0, r, tokens=[0, 1, 63, 64, 100, 255], decode_steps=1)
-        print(f"[c5] request {r} ok", flush=True)
+    _check_compose_all_requests(wl, wl.L - 1)
+    print(f"[c3] layer {wl.L - 1}: all {w.batch} requests composed correctly", flush=True)
+    _check_request(wl, wl.L // 2, 3, decode_steps=1)
+    print(f"[c3] layer {wl.L // 2} request 3 ok", flush=True)
+
+
+def test_qwen7b_32k_all_layers():
+    # 8 requests x ~32K context (32 jittered documents in per-request order), 256 suffix
+    # tokens, all 28 layers: every request's composed cache on the last layer; attention of
+    # sampled suffix tokens (first and last, tile edges) and one decode step on the first,
+    # middle and last layers.
+    w = synth.get("c5")
+    wl = DeviceWorkload(w, DEV, n_dec=1)
+    wl.step()
+    torch.cuda.synchronize()
+    print(f"[c5] ctx={[int(c) for c in wl.ctx_host]} cap={wl.cap} layers={wl.L}", flush=True)
+    _check_compose_all_requests(wl, wl.L - 1)
+    print(f"[c5] layer {wl.L - 1}: all {w.batch} requests composed correctly", flush=True)
+    for l, r in ((0, 0), (wl.L // 2, 5), (wl.L - 1, 7)):
+        _check_request(wl, l, r, tokens=[0, 1, 63, 64, 100, 255], decode_steps=1)
+        print(f"[c5] layer {l} request {r} ok", flush=True)
 
 
 def test_llama8b_decode_256_steps_all_layers():
