@@ -11,7 +11,10 @@ What it computes (SemPIC, "Learning Semantic Position-Independent KV Caches"):
   (Sec. 2), with the link operator assigning each cached state its final
   logical position (Sec. 2) through a token-level map from physical cache
   slots to logical positions (App. C.1).  Here a physical slot index equals
-  its logical position and the inline spans S_i are empty.
+  its logical position.  The plain layout has a stored prefix and empty S_i;
+  the general (frontier) layout interleaves inline spans - tokens computed at
+  request time, whose keys/values sit at their own logical slots and whose
+  queries are prefilled - with the cached documents.
 * RoPE relocation of a key compiled at position a to position b,
   k_b = R(b) R(a)^{-1} k_a (Sec. 2, Eq. 3); values are reused unchanged (Sec. 2).
 * Causal attention of inline tokens over the linked cache with a frontier
@@ -148,6 +151,42 @@ def plan_layout(requests, doc_offset, doc_len, doc_compile_pos) -> list[RequestM
     return maps
 
 
+@dataclass
+class FrontierMap:
+    total_len: int            # positions the request occupies (cached + inline)
+    cached: RequestMap        # cached slots; cached.ctx_len = number of cached tokens
+    inline_pos: np.ndarray    # [n_inline] positions of the inline tokens, increasing
+
+
+def plan_frontier(items_per_request, doc_offset, doc_len, doc_compile_pos) -> list[FrontierMap]:
+    """General canonical order P, D_1, S_1, ..., D_m, S_m, Q (Sec. 2) with inline spans.
+
+    Each request is a list of items in logical order: a pool entry id (>= 0), whose
+    tokens keep their compiled keys up to the relocation of Eq. 3, or -n for a span of n
+    inline tokens (computed at request time).  Items occupy consecutive logical
+    positions from 0; slot index = logical position (App. C.1).
+    """
+    maps = []
+    for items in items_per_request:
+        src, a, b, inl = [], [], [], []
+        pos = 0
+        for it in items:
+            if it < 0:
+                inl.extend(range(pos, pos - it))
+                pos -= it
+                continue
+            n = int(doc_len[it])
+            for t in range(n):
+                src.append(int(doc_offset[it]) + t)
+                a.append(int(doc_compile_pos[it]) + t)
+                b.append(pos + t)
+            pos += n
+        cached = RequestMap(len(src), np.asarray(src, np.int64), np.asarray(a, np.int64),
+                            np.asarray(b, np.int64))
+        maps.append(FrontierMap(pos, cached, np.asarray(inl, np.int64)))
+    return maps
+
+
 # --------------------------------------------------------------------------------------
 # Composition (link operator): re-rotated keys, unchanged values
 # --------------------------------------------------------------------------------------
@@ -214,6 +253,30 @@ def suffix_prefill(k_ctx, v_ctx, q, k_suf, v_suf, scale: float | None = None):
                         np.transpose(np.asarray(v_suf, np.float32), (1, 0, 2))], axis=1)
     pos = np.arange(ctx + Ls)
     o = attention(np.transpose(q, (1, 0, 2)), ctx + np.arange(Ls), K, V, pos, scale)
+    return np.transpose(o, (1, 0, 2)), K, V
+
+
+def frontier_prefill(k_cached, v_cached, fmap: FrontierMap, q, k_inl, v_inl,
+                     scale: float | None = None):
+    """Prefill of a request's inline tokens in the general layout (one layer).
+
+    k_cached, v_cached: [Hkv][n_cached][D] composed cache rows in the order of
+    fmap.cached (logical positions fmap.cached.logical_pos); q: [n_inline][Hq][D];
+    k_inl, v_inl: [n_inline][Hkv][D] (inline keys already carry their positions).
+    The inline K/V are placed at their own logical slots, interleaved with the
+    cached states (App. C.1), and inline token i attends over every position
+    <= fmap.inline_pos[i].
+    Returns (out [n_inline][Hq][D] float64, K, V [Hkv][total_len][D] by position).
+    """
+    Hkv, _, D = np.shape(k_cached)
+    T = fmap.total_len
+    K = np.full((Hkv, T, D), np.nan, np.float32)
+    V = np.full((Hkv, T, D), np.nan, np.float32)
+    K[:, fmap.cached.logical_pos] = np.asarray(k_cached, np.float32)
+    V[:, fmap.cached.logical_pos] = np.asarray(v_cached, np.float32)
+    K[:, fmap.inline_pos] = np.transpose(np.asarray(k_inl, np.float32), (1, 0, 2))
+    V[:, fmap.inline_pos] = np.transpose(np.asarray(v_inl, np.float32), (1, 0, 2))
+    o = attention(np.transpose(q, (1, 0, 2)), fmap.inline_pos, K, V, np.arange(T), scale)
     return np.transpose(o, (1, 0, 2)), K, V
 
 

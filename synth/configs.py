@@ -32,6 +32,11 @@ class Workload:
     doc_len_jitter: tuple[int, int] | None = None   # inclusive range for jittered lengths
     fixed_order: tuple[int, ...] | None = None      # fixed document order (tiny case)
     all_docs_permuted: bool = False                 # each request is a permutation of the whole pool
+    # General frontier layout (P, D_1, S_1, ..., D_m, S_m, Q with inline P and S_i): tokens of
+    # an inline prefix and of the inline span after every document.  0/0 = the plain layout
+    # (stored prefix entry, documents back to back, then the n_suffix query tokens).
+    inline_prefix: int = 0
+    inline_span: int = 0
     seed: int = 0
     notes: str = ""
 
@@ -42,6 +47,15 @@ class Workload:
     @property
     def elem_bytes(self) -> int:
         return 4 if self.dtype == "f32" else 2
+
+    @property
+    def frontier(self) -> bool:
+        return self.inline_prefix > 0 or self.inline_span > 0
+
+    @property
+    def n_inline(self) -> int:
+        """Inline tokens per request (prefilled as queries): P, every S_i and Q."""
+        return self.inline_prefix + self.docs_per_request * self.inline_span + self.n_suffix
 
 
 WORKLOADS: dict[str, Workload] = {
@@ -71,6 +85,24 @@ WORKLOADS: dict[str, Workload] = {
         prefix_len=0, n_suffix=256, batch=8, doc_len_jitter=(768, 1280),
         all_docs_permuted=True,
         notes="32 docs with lengths ~U{768..1280}, each request a permutation of all 32 (~32K)"),
+    # General frontier layout: the prefix and a span after every document are inline tokens
+    # whose queries are prefilled together with the final query span.
+    "tiny_frontier_f32": Workload(
+        name="tiny_frontier_f32", dtype="f32", n_layers=1, n_q_heads=4, n_kv_heads=2,
+        head_dim=64, rope_theta=1e4, pool_docs=3, doc_len=96, docs_per_request=3, prefix_len=0,
+        n_suffix=16, batch=2, inline_prefix=16, inline_span=8,
+        notes="inline prefix 16, 3 docs x 96 each followed by an 8-token inline span, 16 query tokens"),
+    "llama8b_frontier_1layer": Workload(
+        name="llama8b_frontier_1layer", dtype="bf16", n_layers=1, n_q_heads=32, n_kv_heads=8,
+        head_dim=128, rope_theta=5e5, pool_docs=16, doc_len=512, docs_per_request=8,
+        prefix_len=0, n_suffix=64, batch=4, inline_prefix=48, inline_span=24,
+        notes="inline prefix 48, 8 docs x 512 each followed by a 24-token inline span, 64 query tokens"),
+    "llama8b_frontier": Workload(
+        name="llama8b_frontier", dtype="bf16", n_layers=32, n_q_heads=32, n_kv_heads=8,
+        head_dim=128, rope_theta=5e5, pool_docs=64, doc_len=1024, docs_per_request=10,
+        prefix_len=0, n_suffix=128, batch=16, inline_prefix=128, inline_span=32,
+        notes="the 32-layer Llama shape with an inline 128-token prefix and a 32-token inline span "
+              "after each of the 10 documents (576 inline tokens per request)"),
 }
 
 # Short aliases in the order the workloads are listed above.

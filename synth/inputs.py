@@ -59,6 +59,7 @@ class PoolLayout:
     pool_tokens: int
     prefix_entry: int             # index of the instruction-prefix entry, or -1
     requests: list[list[int]]     # per request: pool entries in logical order
+    items: list[list[int]] | None = None   # frontier layouts: entries (>= 0) and inline spans (-n)
 
 
 def pool_layout(w: Workload) -> PoolLayout:
@@ -93,7 +94,19 @@ def pool_layout(w: Workload) -> PoolLayout:
         else:
             docs = [int(x) for x in g.choice(w.pool_docs, size=w.docs_per_request, replace=False)]
         requests.append(([prefix_entry] if prefix_entry >= 0 else []) + docs)
-    return PoolLayout(offs, lens_a, compile_pos, int(lens_a.sum()), prefix_entry, requests)
+    items = None
+    if w.frontier:
+        items = []
+        for entries in requests:
+            it = [-w.inline_prefix] if w.inline_prefix > 0 else []
+            for e in entries:
+                it.append(e)
+                if w.inline_span > 0 and e != prefix_entry:
+                    it.append(-w.inline_span)
+            if w.n_suffix > 0:
+                it.append(-w.n_suffix)
+            items.append(it)
+    return PoolLayout(offs, lens_a, compile_pos, int(lens_a.sum()), prefix_entry, requests, items)
 
 
 def context_lengths(layout: PoolLayout) -> np.ndarray:
@@ -117,9 +130,12 @@ def host_layer(w: Workload, layout: PoolLayout, layer: int) -> dict[str, np.ndar
     pool_v:     [Hkv][pool_tokens][D];
     q, k_suf, v_suf: [B][Ls][H][D] suffix tokens (already at their positions);
     dq, dk, dv: [steps][B][H][D] decode-step tokens.
+    Frontier workloads: q, k_suf, v_suf hold all n_inline inline tokens of a request in
+    position order (prefix, each span, the query span), already at their positions.
     For bf16 workloads the values are already bf16-representable.
     """
-    Hq, Hkv, D, B, Ls = w.n_q_heads, w.n_kv_heads, w.head_dim, w.batch, w.n_suffix
+    Hq, Hkv, D, B = w.n_q_heads, w.n_kv_heads, w.head_dim, w.batch
+    Ls = w.n_inline if w.frontier else w.n_suffix
     out = {
         "pool_k_raw": normal_f32(w, "pool_k", (Hkv, layout.pool_tokens, D), layer),
         "pool_v": normal_f32(w, "pool_v", (Hkv, layout.pool_tokens, D), layer),

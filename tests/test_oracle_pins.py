@@ -278,6 +278,118 @@ def test_composed_cache_equals_full_recompute_single_layer():
     np.testing.assert_allclose(np.transpose(out, (1, 0, 2)), ref, atol=2e-5)
 
 
+# ------------------------------------------------------------------------------------
+# general frontier layout (inline prefix and inline spans between documents)
+# ------------------------------------------------------------------------------------
+
+def test_frontier_layout_hand_computed():
+    # P (4 inline), D_0 (8 cached), S_1 (2 inline), D_1 (5 cached), Q (3 inline)
+    (m,) = O.plan_frontier([[-4, 0, -2, 1, -3]], [0, 8], [8, 5], [0, 0])
+    assert m.total_len == 22
+    assert m.inline_pos.tolist() == [0, 1, 2, 3, 12, 13, 19, 20, 21]
+    assert m.cached.logical_pos.tolist() == list(range(4, 12)) + list(range(14, 19))
+    assert m.cached.src_token.tolist() == list(range(0, 8)) + list(range(8, 13))
+    assert m.cached.compile_pos.tolist() == list(range(8)) + list(range(5))
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.data())
+def test_frontier_layout_is_a_bijection(data):
+    n_docs = data.draw(st.integers(1, 5))
+    lens = np.asarray(data.draw(st.lists(st.integers(1, 40), min_size=n_docs, max_size=n_docs)))
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    items = data.draw(st.lists(st.one_of(st.integers(0, n_docs - 1), st.integers(-9, -1)),
+                               min_size=1, max_size=8))
+    (m,) = O.plan_frontier([items], offs, lens, np.zeros(n_docs, int))
+    both = np.concatenate([m.cached.logical_pos, m.inline_pos])
+    assert sorted(both.tolist()) == list(range(m.total_len))
+    assert np.all(np.diff(m.inline_pos) > 0)
+    assert m.inline_pos.size == -sum(i for i in items if i < 0)
+
+
+def test_frontier_without_inner_spans_reduces_to_suffix_prefill():
+    Hq, Hkv, D, theta, Ls = 4, 2, 32, 1e4, 6
+    lens, offs = np.array([20, 13]), np.array([0, 20])
+    pool_k = rng.standard_normal((Hkv, 33, D)).astype(np.float32)
+    pool_v = rng.standard_normal((Hkv, 33, D)).astype(np.float32)
+    (m,) = O.plan_layout([[1, 0]], offs, lens, np.zeros(2, int))
+    (f,) = O.plan_frontier([[1, 0, -Ls]], offs, lens, np.zeros(2, int))
+    K, V = O.compose_request(pool_k, pool_v, m, theta, "f32")
+    Kc, Vc = O.compose_request(pool_k, pool_v, f.cached, theta, "f32")
+    assert np.array_equal(K, Kc) and np.array_equal(V, Vc)
+    q = rng.standard_normal((Ls, Hq, D))
+    ks = rng.standard_normal((Ls, Hkv, D)).astype(np.float32)
+    vs = rng.standard_normal((Ls, Hkv, D)).astype(np.float32)
+    a, Ka, Va = O.suffix_prefill(K, V, q, ks, vs)
+    b, Kb, Vb = O.frontier_prefill(Kc, Vc, f, q, ks, vs)
+    assert np.array_equal(a, b) and np.array_equal(Ka, Kb) and np.array_equal(Va, Vb)
+
+
+def test_frontier_prefill_equals_full_causal_recompute():
+    # Inline prefix, a span between the documents and a query span: composing the cached
+    # documents and prefilling every inline token must equal plain causal attention over the
+    # whole prompt with every key and query rotated directly at its logical position
+    # (torch SDPA with a causal mask as the outside computation).
+    Hq, Hkv, D, theta = 4, 2, 64, 1e4
+    lens, offs = np.array([30, 21]), np.array([0, 30])
+    items = [-5, 1, -4, 0, -6]
+    (f,) = O.plan_frontier([items], offs, lens, np.zeros(2, int))
+    T, n_inl = f.total_len, f.inline_pos.size
+    raw_k = rng.standard_normal((Hkv, T, D))           # by logical position
+    raw_v = rng.standard_normal((Hkv, T, D)).astype(np.float32)
+    raw_q = rng.standard_normal((Hq, T, D))
+    # the offline compiler's output: each document's keys rotated from position 0
+    pool_k = np.zeros((Hkv, 51, D), np.float32)
+    pool_v = np.zeros((Hkv, 51, D), np.float32)
+    pool_k[:, f.cached.src_token] = O.round_to_f32(
+        O.rope(raw_k[:, f.cached.logical_pos], f.cached.compile_pos, theta))
+    pool_v[:, f.cached.src_token] = raw_v[:, f.cached.logical_pos]
+    Kc, Vc = O.compose_request(pool_k, pool_v, f.cached, theta, "f32")
+    ip = f.inline_pos
+    q = np.transpose(O.rope(raw_q[:, ip], ip, theta), (1, 0, 2))
+    k_inl = np.transpose(O.round_to_f32(O.rope(raw_k[:, ip], ip, theta)), (1, 0, 2))
+    v_inl = np.transpose(raw_v[:, ip], (1, 0, 2))
+    out, K, V = O.frontier_prefill(Kc, Vc, f, q, k_inl, v_inl)
+    assert not np.isnan(K).any() and not np.isnan(V).any()
+
+    def rot_half(x, pos):   # textbook rotate-half RoPE in torch, float64
+        x = torch.from_numpy(np.asarray(x, np.float64))
+        inv = 1.0 / theta ** (torch.arange(0, D, 2, dtype=torch.float64) / D)
+        ang = torch.from_numpy(np.asarray(pos, np.float64))[:, None] * inv[None, :]
+        cos, sin = torch.cat([ang.cos(), ang.cos()], -1), torch.cat([ang.sin(), ang.sin()], -1)
+        x1, x2 = x[..., : D // 2], x[..., D // 2:]
+        return x * cos + torch.cat([-x2, x1], -1) * sin
+
+    allpos = np.arange(T)
+    qf = rot_half(raw_q, allpos)
+    kf = rot_half(raw_k, allpos).repeat_interleave(Hq // Hkv, 0)
+    vf = torch.from_numpy(raw_v.astype(np.float64)).repeat_interleave(Hq // Hkv, 0)
+    ref = torch.nn.functional.scaled_dot_product_attention(qf[None], kf[None], vf[None],
+                                                           is_causal=True)[0].numpy()
+    np.testing.assert_allclose(np.transpose(out, (1, 0, 2)), ref[:, ip], atol=2e-5)
+    assert n_inl == 15
+
+
+def test_frontier_mask_hides_later_documents():
+    # The span after the first document must not see the second document: making the
+    # second document's values huge changes only queries at or after its positions.
+    Hq, Hkv, D = 2, 1, 16
+    lens, offs = np.array([10, 10]), np.array([0, 10])
+    (f,) = O.plan_frontier([[0, -3, 1, -2]], offs, lens, np.zeros(2, int))
+    Kc = rng.standard_normal((Hkv, 20, D)).astype(np.float32)
+    Vc = rng.standard_normal((Hkv, 20, D)).astype(np.float32)
+    q = rng.standard_normal((5, Hq, D))
+    ks = rng.standard_normal((5, Hkv, D)).astype(np.float32)
+    vs = rng.standard_normal((5, Hkv, D)).astype(np.float32)
+    a, _, _ = O.frontier_prefill(Kc, Vc, f, q, ks, vs)
+    Vc2 = Vc.copy()
+    Vc2[:, 10:] = 1e6                                  # second document (positions 13..22)
+    b, _, _ = O.frontier_prefill(Kc, Vc2, f, q, ks, vs)
+    assert f.inline_pos.tolist() == [10, 11, 12, 23, 24]
+    assert np.array_equal(a[:3], b[:3])
+    assert np.abs(b[3:]).max() > 1e3
+
+
 def test_decode_step_equals_prefill_row():
     Hq, Hkv, D = 4, 2, 32
     K = rng.standard_normal((Hkv, 40, D)).astype(np.float32)
