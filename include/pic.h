@@ -110,6 +110,27 @@ pic_status pic_plan_layout(int32_t batch, const int32_t* n_entries, const int32_
                            int64_t pool_tokens, pic_block* blocks, int32_t block_cap,
                            int32_t* n_blocks, int32_t* ctx_len);
 
+/* ---- 1b. plan with inline spans (Sec. 2 canonical order P, D_1, S_1, ..., D_m, S_m, Q;
+   App. C.1 token map) ----
+   Like pic_plan_layout, but a request's items mix pool entries (id >= 0) with inline spans,
+   written -n for n >= 1 inline tokens: tokens computed at request time (an inline prefix P,
+   the spans S_i, the query Q) whose K/V the caller supplies already rotated at their
+   positions and whose queries pic_frontier_prefill_attn computes.  Items are laid back to
+   back from position 0.
+     n_items [host, batch], items [host, sum n_items]   per request, in logical order
+     total_len [host out, batch]        positions the request occupies (cached + inline)
+     inline_pos [host out, batch x inline_cap]  each request's inline positions, increasing;
+                                        entries past n_inline[b] are set to -1
+     n_inline [host out, batch]         inline tokens of each request
+   The other arguments and failures are those of pic_plan_layout; in addition
+   PIC_ERR_CAPACITY when a request has more than inline_cap inline tokens. */
+pic_status pic_plan_frontier(int32_t batch, const int32_t* n_items, const int32_t* items,
+                             int32_t n_pool_entries, const int32_t* entry_offset,
+                             const int32_t* entry_len, const int32_t* entry_compile_pos,
+                             int64_t pool_tokens, pic_block* blocks, int32_t block_cap,
+                             int32_t* n_blocks, int32_t* total_len, int32_t* inline_pos,
+                             int32_t inline_cap, int32_t* n_inline);
+
 /* ---- 2a. delta-angle table (Sec. 2, Eq. 3: R(b) R(a)^-1 = R(b - a)) ----
    Table of (cos, sin) of delta * theta_i for delta = 0..max_abs_delta and i = 0..D/2-1,
    float32 pairs laid out [max_abs_delta + 1][D/2][2]; angles and cos/sin are evaluated in
@@ -157,6 +178,31 @@ pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const 
                                    int32_t batch, int32_t cache_cap, const int32_t* ctx_len,
                                    int32_t max_ctx, int32_t n_suffix, float scale, void* out,
                                    void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- 3b. frontier prefill (App. C.1: inline KVs interleaved with the prepared states at
+   their logical slots; a query never sees a logically later position) ----
+   Stores k_inl/v_inl of inline token i of request b at cache slot pos[b][i], then for that
+   token and query head h computes
+     out = sum_{j <= pos[b][i]} softmax_j(scale * q . k_j) v_j
+   over kv head h / (Hq/Hkv).  Every slot up to a request's largest position must hold its
+   K/V once the call's own tokens are stored (pic_compose for the documents).
+     q / out        [L][batch][n_inline][Hq][D];  k_inl / v_inl [L][batch][n_inline][Hkv][D]
+     pos            [device, batch x n_inline] positions (pic_plan_frontier's inline_pos);
+                    entries are clamped to [0, max_len - 1]
+     n_valid        [device, batch] inline tokens used per request; rows i >= n_valid[b]
+                    are neither stored nor computed (their out rows are left untouched)
+     max_len [host] bound on every request's length; max_len <= cache_cap
+     scale          softmax scale; 0 means 1/sqrt(head_dim)
+     workspace      pic_frontier_workspace_bytes(...) bytes (may be 0 bytes)
+   Results assume each request's positions increase with i (as the planner gives them). */
+size_t pic_frontier_workspace_bytes(const pic_model* model, int32_t batch, int32_t n_inline,
+                                    int32_t max_len);
+pic_status pic_frontier_prefill_attn(const pic_model* model, const void* q, const void* k_inl,
+                                     const void* v_inl, void* cache_k, void* cache_v,
+                                     int32_t batch, int32_t cache_cap, const int32_t* pos,
+                                     const int32_t* n_valid, int32_t n_inline, int32_t max_len,
+                                     float scale, void* out, void* workspace, size_t ws_bytes,
+                                     void* stream);
 
 /* ---- 4. decode (App. C.1: ordinary autoregressive decoding over the completed cache) ----
    For request b the new token sits at slot p = base_len[b] + step: k_new/v_new are written

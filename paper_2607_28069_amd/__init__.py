@@ -22,8 +22,9 @@ STATUS = {0: "PIC_OK", -1: "PIC_ERR_INVALID_ARG", -2: "PIC_ERR_UNSUPPORTED", -3:
           -4: "PIC_ERR_CAPACITY", -5: "PIC_ERR_MISALIGNED", -6: "PIC_ERR_RANGE", -7: "PIC_ERR_HIP"}
 
 # Every symbol include/pic.h declares.
-EXPORTS = ("pic_plan_layout", "pic_rope_table_bytes", "pic_rope_table_init", "pic_rerotate_keys",
-           "pic_compose", "pic_prefill_workspace_bytes", "pic_suffix_prefill_attn",
+EXPORTS = ("pic_plan_layout", "pic_plan_frontier", "pic_rope_table_bytes", "pic_rope_table_init",
+           "pic_rerotate_keys", "pic_compose", "pic_prefill_workspace_bytes",
+           "pic_suffix_prefill_attn", "pic_frontier_workspace_bytes", "pic_frontier_prefill_attn",
            "pic_decode_workspace_bytes", "pic_decode_attn", "pic_status_string", "pic_last_error",
            "pic_decode_auto_splits")
 
@@ -67,12 +68,15 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     MP = ctypes.POINTER(Model)
     sig = {
         "pic_plan_layout": (ctypes.c_int, [I32, P, P, I32, P, P, P, I64, P, I32, P, P]),
+        "pic_plan_frontier": (ctypes.c_int, [I32, P, P, I32, P, P, P, I64, P, I32, P, P, P, I32, P]),
         "pic_rope_table_bytes": (SZ, [MP, I32]),
         "pic_rope_table_init": (ctypes.c_int, [MP, I32, P, SZ, P]),
         "pic_rerotate_keys": (ctypes.c_int, [MP, P, P, I64, I32, P, P, I32, P]),
         "pic_compose": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, P, I32, I32, P]),
         "pic_prefill_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_suffix_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, P, P, SZ, P]),
+        "pic_frontier_workspace_bytes": (SZ, [MP, I32, I32, I32]),
+        "pic_frontier_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, P, I32, I32, F, P, P, SZ, P]),
         "pic_decode_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_decode_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, I32, P, P, SZ, P]),
         "pic_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -136,6 +140,34 @@ def pic_plan_layout(requests, entry_offset, entry_len, entry_compile_pos, pool_t
     return blocks[: n_blocks.value], ctx
 
 
+def pic_plan_frontier(items, entry_offset, entry_len, entry_compile_pos, pool_tokens):
+    """items: per request, a list of pool entry ids (>= 0) and inline spans (-n).
+
+    Returns (blocks structured array, total_len [B], inline_pos [B][max inline] with -1
+    padding, n_inline [B])."""
+    lib = load()
+    n_items, p_n = _host_i32([len(r) for r in items])
+    flat, p_flat = _host_i32([e for r in items for e in r] or [0])
+    off, p_off = _host_i32(entry_offset)
+    ln, p_len = _host_i32(entry_len)
+    cp, p_cp = _host_i32(entry_compile_pos)
+    cap = max([sum(-e for e in r if e < 0) for r in items] + [1])
+    n_blocks = ctypes.c_int32(0)
+    total = np.zeros(len(items), np.int32)
+    inl = np.zeros((len(items), cap), np.int32)
+    n_inl = np.zeros(len(items), np.int32)
+    args = lambda blocks, n: (len(items), p_n, p_flat, len(off), p_off, p_len, p_cp, int(pool_tokens),
+                              blocks, n, ctypes.byref(n_blocks), total.ctypes.data_as(ctypes.c_void_p),
+                              inl.ctypes.data_as(ctypes.c_void_p), cap,
+                              n_inl.ctypes.data_as(ctypes.c_void_p))
+    st = lib.pic_plan_frontier(*args(None, 0))
+    if st not in (0, -4):
+        _check(st)
+    blocks = np.zeros(max(n_blocks.value, 1), BLOCK_DTYPE)
+    _check(lib.pic_plan_frontier(*args(blocks.ctypes.data_as(ctypes.c_void_p), len(blocks))))
+    return blocks[: n_blocks.value], total, inl, n_inl
+
+
 def pic_rope_table_bytes(model: Model, max_abs_delta: int) -> int:
     return load().pic_rope_table_bytes(ctypes.byref(model), max_abs_delta)
 
@@ -170,6 +202,20 @@ def pic_suffix_prefill_attn(model: Model, q, k_suf, v_suf, cache_k, cache_v, bat
                                           _ptr(cache_k), _ptr(cache_v), int(batch), int(cache_cap),
                                           _ptr(ctx_len), int(max_ctx), int(n_suffix), float(scale),
                                           _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pic_frontier_workspace_bytes(model: Model, batch, n_inline, max_len) -> int:
+    return load().pic_frontier_workspace_bytes(ctypes.byref(model), batch, n_inline, max_len)
+
+
+def pic_frontier_prefill_attn(model: Model, q, k_inl, v_inl, cache_k, cache_v, batch, cache_cap, pos,
+                              n_valid, n_inline, max_len, out, workspace=None, scale=0.0, stream=None):
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().pic_frontier_prefill_attn(ctypes.byref(model), _ptr(q), _ptr(k_inl), _ptr(v_inl),
+                                            _ptr(cache_k), _ptr(cache_v), int(batch), int(cache_cap),
+                                            _ptr(pos), _ptr(n_valid), int(n_inline), int(max_len),
+                                            float(scale), _ptr(out), _ptr(workspace), ws_bytes,
+                                            _stream(stream)))
 
 
 def pic_decode_workspace_bytes(model: Model, batch, max_len, n_splits=0) -> int:

@@ -1,5 +1,6 @@
 // float32 attention of query rows over the composed cache with the frontier mask of App. C.1:
-// the query at logical position p sees slots [0, p] (slot index = logical position).
+// the query at logical position p sees slots [0, p] (slot index = logical position).  The
+// position of each query token comes from a RowPos (contiguous after a base, or a table).
 //
 // This path serves float32 caches (small models and exact checks); it is plain VALU code,
 // one workgroup per query row: keys are scored 256 at a time into LDS, then the weighted
@@ -39,8 +40,7 @@ __device__ float block_reduce(float x, float* red) {
 template <int HD>
 __global__ void __launch_bounds__(kThreads) attn_rows_f32_kernel(
     AttnShape s, const float* __restrict__ q, const float* __restrict__ cache_k,
-    const float* __restrict__ cache_v, const int32_t* __restrict__ base, int32_t max_base,
-    int32_t offset, int32_t n_q, float* __restrict__ out) {
+    const float* __restrict__ cache_v, RowPos pos, int32_t n_q, float* __restrict__ out) {
   constexpr int G = kThreads / HD;  // key groups in the value pass
   __shared__ float q_s[HD];
   __shared__ float p_s[kThreads];
@@ -55,9 +55,9 @@ __global__ void __launch_bounds__(kThreads) attn_rows_f32_kernel(
   const int b = (int)(row / ((int64_t)Hq * n_q));
   const int g = h / (Hq / Hkv);
 
-  int32_t bl = base[b];
-  bl = bl < 0 ? 0 : (bl > max_base ? max_base : bl);
-  int64_t n_vis = (int64_t)bl + offset + i + 1;
+  const int64_t qpos = pos(b, i);
+  if (qpos < 0) return;   // (uniform) an unused row
+  int64_t n_vis = qpos + 1;
   if (n_vis > s.cache_cap) n_vis = s.cache_cap;
 
   const int64_t qrow = ((int64_t)l * s.batch * n_q * Hq + row) * HD;
@@ -111,17 +111,17 @@ __global__ void __launch_bounds__(kThreads) attn_rows_f32_kernel(
 }  // namespace
 
 hipError_t launch_attn_rows_f32(const AttnShape& s, const float* q, const float* cache_k,
-                                const float* cache_v, const int32_t* base, int32_t max_base,
-                                int32_t offset, int32_t n_q, float* out, hipStream_t stream) {
+                                const float* cache_v, const RowPos& pos, int32_t n_q, float* out,
+                                hipStream_t stream) {
   const int64_t rows = (int64_t)s.batch * n_q * s.n_q_heads;
   if (rows == 0 || s.n_layers == 0) return hipSuccess;
   const dim3 grid((unsigned)rows, s.n_layers);
   if (s.head_dim == 64)
     hipLaunchKernelGGL(attn_rows_f32_kernel<64>, grid, dim3(kThreads), 0, stream, s, q, cache_k,
-                       cache_v, base, max_base, offset, n_q, out);
+                       cache_v, pos, n_q, out);
   else
     hipLaunchKernelGGL(attn_rows_f32_kernel<128>, grid, dim3(kThreads), 0, stream, s, q, cache_k,
-                       cache_v, base, max_base, offset, n_q, out);
+                       cache_v, pos, n_q, out);
   return hipGetLastError();
 }
 

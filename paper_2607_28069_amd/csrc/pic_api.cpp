@@ -115,22 +115,27 @@ PIC_API const char* pic_last_error(void) { return g_last_error.c_str(); }
 // 1. plan
 // ---------------------------------------------------------------------------------------------
 
-PIC_API pic_status pic_plan_layout(int32_t batch, const int32_t* n_entries, const int32_t* entries,
-                                   int32_t n_pool_entries, const int32_t* entry_offset,
-                                   const int32_t* entry_len, const int32_t* entry_compile_pos,
-                                   int64_t pool_tokens, pic_block* blocks, int32_t block_cap,
-                                   int32_t* n_blocks, int32_t* ctx_len) {
+namespace {
+
+// Shared by both planners: items are pool entry ids (>= 0) or, when inline spans are allowed,
+// -n for n inline tokens.  Items are laid back to back from position 0.
+pic_status plan_items(int32_t batch, const int32_t* n_items, const int32_t* items, bool allow_inline,
+                      int32_t n_pool_entries, const int32_t* entry_offset, const int32_t* entry_len,
+                      const int32_t* entry_compile_pos, int64_t pool_tokens, pic_block* blocks,
+                      int32_t block_cap, int32_t* n_blocks, int32_t* total_len, int32_t* inline_pos,
+                      int32_t inline_cap, int32_t* n_inline) {
   if (batch <= 0) return fail(PIC_ERR_INVALID_ARG, "batch must be >= 1");
-  if (!n_entries || !entry_offset || !entry_len || !entry_compile_pos || !n_blocks || !ctx_len)
+  if (!n_items || !entry_offset || !entry_len || !entry_compile_pos || !n_blocks || !total_len)
     return fail(PIC_ERR_INVALID_ARG, "a required host array is NULL");
-  if (n_pool_entries < 0 || block_cap < 0 || pool_tokens < 0)
+  if (allow_inline && !n_inline) return fail(PIC_ERR_INVALID_ARG, "n_inline is NULL");
+  if (n_pool_entries < 0 || block_cap < 0 || pool_tokens < 0 || inline_cap < 0)
     return fail(PIC_ERR_INVALID_ARG, "negative size");
-  int64_t total_entries = 0;
+  int64_t total_items = 0;
   for (int32_t b = 0; b < batch; ++b) {
-    if (n_entries[b] < 0) return fail(PIC_ERR_INVALID_ARG, "n_entries[%d] < 0", b);
-    total_entries += n_entries[b];
+    if (n_items[b] < 0) return fail(PIC_ERR_INVALID_ARG, "item count of request %d < 0", b);
+    total_items += n_items[b];
   }
-  if (total_entries > 0 && !entries) return fail(PIC_ERR_INVALID_ARG, "entries is NULL");
+  if (total_items > 0 && !items) return fail(PIC_ERR_INVALID_ARG, "the item list is NULL");
   for (int32_t e = 0; e < n_pool_entries; ++e) {
     if (entry_len[e] <= 0) return fail(PIC_ERR_INVALID_ARG, "entry_len[%d] must be >= 1", e);
     if (entry_offset[e] < 0 || (int64_t)entry_offset[e] + entry_len[e] > pool_tokens)
@@ -140,34 +145,51 @@ PIC_API pic_status pic_plan_layout(int32_t batch, const int32_t* n_entries, cons
     if (entry_compile_pos[e] < 0 || (int64_t)entry_compile_pos[e] + entry_len[e] > INT32_MAX)
       return fail(PIC_ERR_RANGE, "entry_compile_pos[%d] out of range", e);
   }
-  // count blocks and check ranges first, so a failing call writes nothing
+  // count blocks and inline tokens and check ranges first, so a failing call writes nothing
   int64_t need = 0;
-  const int32_t* ent = entries;
+  const int32_t* it = items;
   for (int32_t b = 0; b < batch; ++b) {
-    int64_t pos = 0;
-    for (int32_t k = 0; k < n_entries[b]; ++k) {
-      const int32_t e = ent[k];
-      if (e < 0 || e >= n_pool_entries)
-        return fail(PIC_ERR_RANGE, "request %d entry %d: pool entry id %d out of [0, %d)", b, k, e,
-                    n_pool_entries);
-      need += (entry_len[e] + PIC_BLOCK_TOKENS - 1) / PIC_BLOCK_TOKENS;
-      pos += entry_len[e];
-      if (pos > INT32_MAX) return fail(PIC_ERR_RANGE, "request %d context exceeds INT32_MAX", b);
+    int64_t pos = 0, inl = 0;
+    for (int32_t k = 0; k < n_items[b]; ++k) {
+      const int32_t e = it[k];
+      if (e < 0 && allow_inline) {
+        if (e == INT32_MIN) return fail(PIC_ERR_RANGE, "request %d item %d: span too long", b, k);
+        pos += -(int64_t)e;
+        inl += -(int64_t)e;
+      } else {
+        if (e < 0 || e >= n_pool_entries)
+          return fail(PIC_ERR_RANGE, "request %d item %d: pool entry id %d out of [0, %d)", b, k,
+                      e, n_pool_entries);
+        need += (entry_len[e] + PIC_BLOCK_TOKENS - 1) / PIC_BLOCK_TOKENS;
+        pos += entry_len[e];
+      }
+      if (pos > INT32_MAX) return fail(PIC_ERR_RANGE, "request %d exceeds INT32_MAX positions", b);
     }
-    ent += n_entries[b];
+    if (allow_inline && inl > inline_cap)
+      return fail(PIC_ERR_CAPACITY, "request %d has %lld inline tokens, room for %d", b,
+                  (long long)inl, inline_cap);
+    it += n_items[b];
   }
   if (need > INT32_MAX) return fail(PIC_ERR_CAPACITY, "too many blocks");
   *n_blocks = (int32_t)need;
   if (need > block_cap)
     return fail(PIC_ERR_CAPACITY, "%lld blocks needed, room for %d", (long long)need, block_cap);
   if (need > 0 && !blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
+  if (allow_inline && inline_cap > 0 && !inline_pos)
+    return fail(PIC_ERR_INVALID_ARG, "inline_pos is NULL");
 
   int32_t nb = 0;
-  ent = entries;
+  it = items;
   for (int32_t b = 0; b < batch; ++b) {
     int32_t pos = 0;   // logical position = cache slot
-    for (int32_t k = 0; k < n_entries[b]; ++k) {
-      const int32_t e = ent[k];
+    int32_t inl = 0;
+    for (int32_t k = 0; k < n_items[b]; ++k) {
+      const int32_t e = it[k];
+      if (e < 0) {   // inline span (Sec. 2: P and the S_i are computed at request time)
+        for (int32_t t = 0; t < -e; ++t) inline_pos[(int64_t)b * inline_cap + inl++] = pos + t;
+        pos += -e;
+        continue;
+      }
       const int32_t len = entry_len[e];
       const int32_t delta = pos - entry_compile_pos[e];  // b_i - a_i, Eq. 3
       for (int32_t t = 0; t < len; t += PIC_BLOCK_TOKENS) {
@@ -180,10 +202,37 @@ PIC_API pic_status pic_plan_layout(int32_t batch, const int32_t* n_entries, cons
       }
       pos += len;
     }
-    ctx_len[b] = pos;
-    ent += n_entries[b];
+    total_len[b] = pos;
+    if (allow_inline) {
+      n_inline[b] = inl;
+      for (int32_t i = inl; i < inline_cap; ++i) inline_pos[(int64_t)b * inline_cap + i] = -1;
+    }
+    it += n_items[b];
   }
   return ok();
+}
+
+}  // namespace
+
+PIC_API pic_status pic_plan_layout(int32_t batch, const int32_t* n_entries, const int32_t* entries,
+                                   int32_t n_pool_entries, const int32_t* entry_offset,
+                                   const int32_t* entry_len, const int32_t* entry_compile_pos,
+                                   int64_t pool_tokens, pic_block* blocks, int32_t block_cap,
+                                   int32_t* n_blocks, int32_t* ctx_len) {
+  return plan_items(batch, n_entries, entries, false, n_pool_entries, entry_offset, entry_len,
+                    entry_compile_pos, pool_tokens, blocks, block_cap, n_blocks, ctx_len, nullptr,
+                    0, nullptr);
+}
+
+PIC_API pic_status pic_plan_frontier(int32_t batch, const int32_t* n_items, const int32_t* items,
+                                     int32_t n_pool_entries, const int32_t* entry_offset,
+                                     const int32_t* entry_len, const int32_t* entry_compile_pos,
+                                     int64_t pool_tokens, pic_block* blocks, int32_t block_cap,
+                                     int32_t* n_blocks, int32_t* total_len, int32_t* inline_pos,
+                                     int32_t inline_cap, int32_t* n_inline) {
+  return plan_items(batch, n_items, items, true, n_pool_entries, entry_offset, entry_len,
+                    entry_compile_pos, pool_tokens, blocks, block_cap, n_blocks, total_len,
+                    inline_pos, inline_cap, n_inline);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -306,14 +355,17 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
   // a4: suffix K/V into slots [ctx, ctx + n_suffix) (App. C.1: inline KVs interleaved); the
   // bf16 kernel does this itself
   if (model->dtype == PIC_F32) {
+    pic::RowPos pos;
+    pos.base = ctx_len;
+    pos.max_base = max_ctx;
     PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
                                             model->n_kv_heads, k_suf, v_suf, cache_k, cache_v,
-                                            batch, cache_cap, ctx_len, max_ctx, 0, n_suffix, st),
+                                            batch, cache_cap, pos, n_suffix, st),
                          "suffix append launch"));
     return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
                                                 static_cast<const float*>(cache_k),
-                                                static_cast<const float*>(cache_v), ctx_len,
-                                                max_ctx, 0, n_suffix, static_cast<float*>(out), st),
+                                                static_cast<const float*>(cache_v), pos, n_suffix,
+                                                static_cast<float*>(out), st),
                       "prefill attention launch");
   }
   return hip_status(pic::launch_prefill_bf16(s, static_cast<const pic::bf16_t*>(q),
@@ -324,6 +376,70 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
                                              max_ctx, n_suffix, static_cast<pic::bf16_t*>(out),
                                              workspace, ws_bytes, st),
                     "prefill attention launch");
+}
+
+PIC_API size_t pic_frontier_workspace_bytes(const pic_model* model, int32_t batch,
+                                            int32_t n_inline, int32_t max_len) {
+  if (check_attn_model(model) != PIC_OK || batch < 0 || n_inline < 0 || max_len < 0) return 0;
+  if (model->dtype == PIC_F32) return 0;
+  const int32_t max_ctx = max_len > n_inline ? max_len - n_inline : 0;
+  return pic::prefill_bf16_workspace(shape_of(model, batch, max_len, 0.f), n_inline, max_ctx);
+}
+
+PIC_API pic_status pic_frontier_prefill_attn(const pic_model* model, const void* q,
+                                             const void* k_inl, const void* v_inl, void* cache_k,
+                                             void* cache_v, int32_t batch, int32_t cache_cap,
+                                             const int32_t* pos, const int32_t* n_valid,
+                                             int32_t n_inline, int32_t max_len, float scale,
+                                             void* out, void* workspace, size_t ws_bytes,
+                                             void* stream) {
+  PIC_CHECK(check_attn_model(model));
+  if (batch < 0 || cache_cap < 0 || n_inline < 0 || max_len < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (!(scale >= 0.f) || !std::isfinite(scale))
+    return fail(PIC_ERR_INVALID_ARG, "scale must be finite and >= 0");
+  if (max_len > cache_cap)
+    return fail(PIC_ERR_CAPACITY, "max_len %d exceeds cache_cap %d", max_len, cache_cap);
+  if ((int64_t)batch * model->n_q_heads * n_inline > INT32_MAX)
+    return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
+  if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  if (batch == 0 || n_inline == 0 || model->n_layers == 0 || max_len == 0) return ok();
+  PIC_CHECK(check_ptr(q, "q"));
+  PIC_CHECK(check_ptr(k_inl, "k_inl"));
+  PIC_CHECK(check_ptr(v_inl, "v_inl"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  PIC_CHECK(check_ptr(out, "out"));
+  if (!pos) return fail(PIC_ERR_INVALID_ARG, "pos is NULL");
+  if (!n_valid) return fail(PIC_ERR_INVALID_ARG, "n_valid is NULL");
+  const size_t need = pic_frontier_workspace_bytes(model, batch, n_inline, max_len);
+  if (need > 0 && (workspace == nullptr || ws_bytes < need))
+    return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  const hipStream_t st = (hipStream_t)stream;
+  const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
+  pic::RowPos rp;
+  rp.table = pos;
+  rp.n_valid = n_valid;
+  rp.n = n_inline;
+  rp.max_pos = max_len - 1;
+  // inline K/V at their logical slots, interleaved with the composed documents (App. C.1)
+  PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
+                                          model->n_kv_heads, k_inl, v_inl, cache_k, cache_v,
+                                          batch, cache_cap, rp, n_inline, st),
+                       "inline append launch"));
+  if (model->dtype == PIC_F32)
+    return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
+                                                static_cast<const float*>(cache_k),
+                                                static_cast<const float*>(cache_v), rp, n_inline,
+                                                static_cast<float*>(out), st),
+                      "frontier attention launch");
+  return hip_status(pic::launch_prefill_bf16_table(s, static_cast<const pic::bf16_t*>(q),
+                                                   static_cast<const pic::bf16_t*>(cache_k),
+                                                   static_cast<const pic::bf16_t*>(cache_v), rp,
+                                                   n_inline, max_len,
+                                                   static_cast<pic::bf16_t*>(out), workspace,
+                                                   ws_bytes, st),
+                    "frontier attention launch");
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -375,14 +491,18 @@ PIC_API pic_status pic_decode_attn(const pic_model* model, const void* q, const 
   const hipStream_t st = (hipStream_t)stream;
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   if (model->dtype == PIC_F32) {
+    pic::RowPos pos;
+    pos.base = base_len;
+    pos.max_base = max_base_len;
+    pos.offset = step;
     PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
                                             model->n_kv_heads, k_new, v_new, cache_k, cache_v,
-                                            batch, cache_cap, base_len, max_base_len, step, 1, st),
+                                            batch, cache_cap, pos, 1, st),
                          "decode append launch"));
     return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
                                                 static_cast<const float*>(cache_k),
-                                                static_cast<const float*>(cache_v), base_len,
-                                                max_base_len, step, 1, static_cast<float*>(out), st),
+                                                static_cast<const float*>(cache_v), pos, 1,
+                                                static_cast<float*>(out), st),
                       "decode attention launch");
   }
   if (n_splits == 0) n_splits = pic::decode_bf16_auto_splits(s, (int32_t)max_len);

@@ -40,23 +40,47 @@ hipError_t launch_compose(pic_dtype dt, int head_dim, int n_layers, int n_kv_hea
                           int32_t max_abs_delta, void* cache_k, void* cache_v, int32_t batch,
                           int32_t cache_cap, hipStream_t stream);
 
-// Writes suffix (n_new tokens per request) K/V rows [L][B][n_new][Hkv][D] into cache slots
-// [base[b] + offset, base[b] + offset + n_new) with base clamped to [0, max_base].
+// Logical position (= cache slot) of row i of request b among n per-request rows (suffix
+// tokens, inline tokens, a decode token): either base[b] clamped to [0, max_base], plus
+// offset + i; or, with a table, table[b * n + i] clamped to [0, max_pos] for i < n_valid[b]
+// and -1 (row unused) otherwise.
+struct RowPos {
+  const int32_t* base = nullptr;
+  int32_t max_base = 0, offset = 0;
+  const int32_t* table = nullptr;
+  const int32_t* n_valid = nullptr;
+  int32_t n = 0, max_pos = 0;
+
+  __device__ __forceinline__ int64_t operator()(int b, int i) const {
+    if (table) {
+      if (i >= n_valid[b]) return -1;
+      const int32_t p = table[(int64_t)b * n + i];
+      return p < 0 ? 0 : (p > max_pos ? max_pos : p);
+    }
+    int32_t bl = base[b];
+    bl = bl < 0 ? 0 : (bl > max_base ? max_base : bl);
+    return (int64_t)bl + offset + i;
+  }
+};
+
+// Writes the K/V rows [L][B][n_new][Hkv][D] of per-request tokens into the cache slots `pos`
+// gives them (rows with no position or a slot past cache_cap are skipped).
 hipError_t launch_append(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                          const void* k_new, const void* v_new, void* cache_k, void* cache_v,
-                         int32_t batch, int32_t cache_cap, const int32_t* base, int32_t max_base,
-                         int32_t offset, int32_t n_new, hipStream_t stream);
+                         int32_t batch, int32_t cache_cap, const RowPos& pos, int32_t n_new,
+                         hipStream_t stream);
 
 struct AttnShape {
   int n_layers, n_q_heads, n_kv_heads, head_dim, batch, cache_cap;
   float scale_log2;  // softmax scale * log2(e)
 };
 
-// fp32 attention, one query row per workgroup.  Prefill: rows [L][B][n_q][Hq], query token i
-// of request b sits at position base[b] + offset + i and sees slots [0, that position].
+// fp32 attention, one query row per workgroup.  Rows [L][B][n_q][Hq]: query token i of
+// request b sits at position pos(b, i) and sees slots [0, that position]; rows without a
+// position are left untouched.
 hipError_t launch_attn_rows_f32(const AttnShape& s, const float* q, const float* cache_k,
-                                const float* cache_v, const int32_t* base, int32_t max_base,
-                                int32_t offset, int32_t n_q, float* out, hipStream_t stream);
+                                const float* cache_v, const RowPos& pos, int32_t n_q, float* out,
+                                hipStream_t stream);
 
 size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx);
 // Also writes k_suf / v_suf into cache slots [ctx_len[b], ctx_len[b] + n_suffix).
@@ -65,6 +89,13 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
                                const int32_t* ctx_len, int32_t max_ctx,
                                int32_t n_suffix, bf16_t* out, void* workspace, size_t ws_bytes,
                                hipStream_t stream);
+// General layout: n_q query tokens per request at the positions of `pos` (a table); every
+// slot up to the largest position must already hold its K/V.  Workspace as for a suffix
+// prefill of n_q tokens after max_len - n_q context tokens.
+hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
+                                     const bf16_t* cache_v, const RowPos& pos, int32_t n_q,
+                                     int32_t max_len, bf16_t* out, void* workspace,
+                                     size_t ws_bytes, hipStream_t stream);
 
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len);
 size_t decode_bf16_workspace(const AttnShape& s, int32_t max_len, int32_t n_splits);

@@ -1,10 +1,13 @@
 // Suffix prefill attention on bf16 MFMA (App. C.1: inline tokens attend over the linked cache
 // under the frontier causal mask; Sec. 5 "Cache-hit serving").
 //
-// Problem per (layer, request b, kv head g): M = n_suffix * n_rep query rows (the n_rep query
+// Problem per (layer, request b, kv head g): M = n_q * n_rep query rows (the n_rep query
 // heads of kv head g are packed into the row dimension, row r = token r / n_rep, head
-// g * n_rep + r % n_rep) against n_keys = ctx + n_suffix keys.  Query token i sits at
-// position ctx + i and sees keys [0, ctx + i]; only the last key tiles need a mask.
+// g * n_rep + r % n_rep).  A query token at position p sees keys [0, p].  Suffix mode: token
+// i sits at ctx + i after the composed context (n_keys = ctx + n_q).  Table mode (general
+// frontier layout, inline tokens interleaved with documents): token i sits at a position
+// from a table, and a workgroup's key range ends at its furthest row's position.  Only tiles
+// past a workgroup's nearest row position need a mask.
 //
 // Kernel shape (gfx950, wave64):
 //  * 8 waves per workgroup, 32 query rows per wave (256 rows per workgroup), key tiles of 64:
@@ -28,6 +31,7 @@
 //  * The suffix's own keys/values are read straight from k_suf / v_suf; one workgroup per
 //    (request, kv head) also stores them into cache slots [ctx, ctx + n_suffix) (no separate
 //    append launch, and no workgroup reads those slots from the cache).
+#include <climits>
 #include <type_traits>
 
 #include "pic_internal.h"
@@ -69,6 +73,11 @@ __device__ __forceinline__ int v_swz(int key) { return ((key & 3) * 5) & 15; }
 __device__ __forceinline__ int k_off(int key, int c) { return key * kRowBytes + ((c ^ k_swz(key)) << 4); }
 __device__ __forceinline__ int v_off(int key, int c) { return key * kRowBytes + ((c ^ v_swz(key)) << 4); }
 
+// Two ways to place the query tokens (n_suffix per request):
+//  * suffix: token i of request b at position ctx_len[b] + i, after the composed context;
+//    its K/V come from k_suf / v_suf and are stored into the cache by this kernel;
+//  * table (general frontier layout): token i at q_pos[b * n_suffix + i] for i < n_valid[b];
+//    every visible slot, the tokens' own included, is already in the cache.
 struct PrefillArgs {
   const bf16_t* q;
   const bf16_t* k_suf;      // [L][B][n_suffix][Hkv][D]
@@ -76,6 +85,9 @@ struct PrefillArgs {
   bf16_t* cache_k;
   bf16_t* cache_v;
   const int32_t* ctx_len;
+  const int32_t* q_pos;     // table mode: [B][n_suffix]
+  const int32_t* n_valid;   // table mode: [B]
+  int32_t max_pos;          // table mode: positions are clamped to [0, max_pos]
   bf16_t* out;
   int32_t max_ctx, n_suffix, batch, cache_cap, n_q_heads, n_kv_heads;
   int32_t m_tiles;          // ceil(n_suffix * n_rep / kRowsPerWG)
@@ -88,6 +100,7 @@ struct PrefillArgs {
   float scale_log2;
 };
 
+template <bool kTable>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_bf16_kernel(PrefillArgs a) {
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
@@ -111,26 +124,57 @@ prefill_bf16_kernel(PrefillArgs a) {
 
   const int n_rep = a.n_q_heads / a.n_kv_heads;
   const int M = a.n_suffix * n_rep;
-  int32_t ctx = a.ctx_len[b];
-  ctx = ctx < 0 ? 0 : (ctx > a.max_ctx ? a.max_ctx : ctx);
-  const int n_keys = ctx + a.n_suffix;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: LDS bases in SGPRs
   const int n = lane & 31, hh = lane >> 5;   // query column, lane half
 
   const int row0_wg = mt * kRowsPerWG;
-  const int last_row_wg = min(row0_wg + kRowsPerWG, M) - 1;
-  const int pos_max_wg = ctx + last_row_wg / n_rep;   // furthest key any row here sees
+  const int r = row0_wg + wave * kRowsPerWave + n;    // this lane's query row
+  bool row_ok = r < M;
+  const int tok = row_ok ? r / n_rep : a.n_suffix - 1;
+  const int hq = g * n_rep + (row_ok ? r % n_rep : 0);
+  // ctx: keys below it come from the cache (suffix mode: the composed context);
+  // pos_min_wg / pos_max_wg: nearest / furthest position of this workgroup's query rows
+  int ctx, qpos, pos_min_wg, pos_max_wg;
+  if constexpr (!kTable) {
+    ctx = a.ctx_len[b];
+    ctx = ctx < 0 ? 0 : (ctx > a.max_ctx ? a.max_ctx : ctx);
+    pos_min_wg = ctx + row0_wg / n_rep;
+    pos_max_wg = ctx + (min(row0_wg + kRowsPerWG, M) - 1) / n_rep;
+    qpos = ctx + tok;
+  } else {
+    __shared__ int red_lo[kWaves], red_hi[kWaves];
+    int nv = a.n_valid[b];
+    nv = nv < 0 ? 0 : (nv > a.n_suffix ? a.n_suffix : nv);
+    row_ok = row_ok && tok < nv;
+    int p = row_ok ? a.q_pos[(int64_t)b * a.n_suffix + tok] : -1;
+    if (row_ok) p = p < 0 ? 0 : (p > a.max_pos ? a.max_pos : p);
+    int lo = row_ok ? p : INT_MAX, hi = p;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      lo = min(lo, __shfl_xor(lo, o, 64));
+      hi = max(hi, __shfl_xor(hi, o, 64));
+    }
+    if (lane == 0) {
+      red_lo[wave] = lo;
+      red_hi[wave] = hi;
+    }
+    __syncthreads();
+    pos_min_wg = red_lo[0];
+    pos_max_wg = red_hi[0];
+#pragma unroll
+    for (int i = 1; i < kWaves; ++i) {
+      pos_min_wg = min(pos_min_wg, red_lo[i]);
+      pos_max_wg = max(pos_max_wg, red_hi[i]);
+    }
+    qpos = row_ok ? p : pos_max_wg;
+    ctx = pos_max_wg + 1;   // every visible key is in the cache
+  }
+  const int n_keys = kTable ? pos_max_wg + 1 : ctx + a.n_suffix;
   // this workgroup's key tiles: [t0, t0 + n_tiles) of the (pos_max_wg + 1) visible keys
   const int t0 = split * a.tiles_per_split;
   const int n_tiles = min((pos_max_wg + kKeys) / kKeys - t0, a.tiles_per_split);
-
-  const int r = row0_wg + wave * kRowsPerWave + n;    // this lane's query row
-  const bool row_ok = r < M;
-  const int tok = row_ok ? r / n_rep : a.n_suffix - 1;
-  const int hq = g * n_rep + (row_ok ? r % n_rep : 0);
-  const int qpos = ctx + tok;
 
   const int64_t bh_kv = (((int64_t)l * a.batch + b) * a.n_kv_heads + g) * a.cache_cap;
   const bf16_t* Kg = a.cache_k + bh_kv * kHD;
@@ -138,9 +182,9 @@ prefill_bf16_kernel(PrefillArgs a) {
   // suffix token i of this (request, kv head): row i with a stride of Hkv rows
   const int64_t suf0 = (((int64_t)l * a.batch + b) * a.n_suffix * a.n_kv_heads + g) * kHD;
   const int64_t suf_stride = (int64_t)a.n_kv_heads * kHD;
-  const bf16_t* Ks = a.k_suf + suf0;
-  const bf16_t* Vs = a.v_suf + suf0;
-  if (mt == 0 && split == 0) {   // cache assembly: suffix rows into slots [ctx, ctx + n_suffix)
+  const bf16_t* Ks = kTable ? nullptr : a.k_suf + suf0;
+  const bf16_t* Vs = kTable ? nullptr : a.v_suf + suf0;
+  if (!kTable && mt == 0 && split == 0) {   // cache assembly: suffix rows into slots [ctx, ctx + n_suffix)
     for (int c = tid; c < a.n_suffix * 32; c += kThreads) {
       const int i = c >> 5, part = c & 31;           // row i, 16-byte chunk part % 16 of K or V
       const int64_t src = i * suf_stride + 8 * (part & 15);
@@ -252,7 +296,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   // which float32 sums and bf16 probabilities hold without loss of relative precision.
   auto finish_scores = [&](int t, f32x16_t (&s)[2]) {   // t: global tile index
     const int k0 = t * kKeys;
-    if (k0 + kKeys - 1 > ctx) {
+    if (k0 + kKeys - 1 > pos_min_wg) {
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
@@ -381,13 +425,23 @@ prefill_bf16_kernel(PrefillArgs a) {
 }
 
 // Merge the key-range splits of each query row by log-sum-exp.  grid (rows_total / 4), 256
-// threads: one wave per row, two head dims per lane.
+// threads: one wave per row, two head dims per lane.  With n_valid (table mode), rows of
+// tokens past n_valid[b] are left untouched.
 __global__ void __launch_bounds__(256) prefill_combine_kernel(const float* __restrict__ ws_o,
                                                               const float2* __restrict__ ws_ml,
                                                               int32_t n_splits, int64_t rows_total,
+                                                              const int32_t* __restrict__ n_valid,
+                                                              int32_t n_q, int32_t n_q_heads,
+                                                              int32_t batch,
                                                               bf16_t* __restrict__ out) {
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows_total) return;
+  if (n_valid) {   // row = ((l * B + b) * n_q + i) * Hq + h
+    const int64_t ti = row / n_q_heads;
+    const int i = (int)(ti % n_q);
+    const int b = (int)((ti / n_q) % batch);
+    if (i >= n_valid[b]) return;
+  }
   const int d = 2 * (threadIdx.x & 63);
   float M = -INFINITY;
   for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ws_ml[s * rows_total + row].x);
@@ -448,25 +502,15 @@ size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_
   return (size_t)p.n_splits * rows * (kHD + 2) * sizeof(float);
 }
 
-hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_suf,
-                               const bf16_t* v_suf, bf16_t* cache_k, bf16_t* cache_v,
-                               const int32_t* ctx_len, int32_t max_ctx,
-                               int32_t n_suffix, bf16_t* out, void* workspace, size_t ws_bytes,
-                               hipStream_t stream) {
+namespace {
+
+hipError_t launch(const AttnShape& s, PrefillArgs a, bool table, int32_t n_q, int32_t max_ctx,
+                  void* workspace, size_t ws_bytes, hipStream_t stream) {
   const int n_rep = s.n_q_heads / s.n_kv_heads;
-  const int64_t M = (int64_t)n_suffix * n_rep;
+  const int64_t M = (int64_t)n_q * n_rep;
   if (M == 0 || s.batch == 0 || s.n_layers == 0) return hipSuccess;
-  const SplitPlan p = plan_splits(s, n_suffix, max_ctx);
-  PrefillArgs a;
-  a.q = q;
-  a.k_suf = k_suf;
-  a.v_suf = v_suf;
-  a.cache_k = cache_k;
-  a.cache_v = cache_v;
-  a.ctx_len = ctx_len;
-  a.out = out;
-  a.max_ctx = max_ctx;
-  a.n_suffix = n_suffix;
+  const SplitPlan p = plan_splits(s, n_q, max_ctx);
+  a.n_suffix = n_q;
   a.batch = s.batch;
   a.cache_cap = s.cache_cap;
   a.n_q_heads = s.n_q_heads;
@@ -475,20 +519,59 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
   a.n_splits = p.n_splits;
   a.tiles_per_split = p.tiles_per_split;
   a.n_wg = p.m_tiles * p.n_splits * s.batch * s.n_kv_heads;
-  a.rows_total = (int64_t)s.n_layers * s.batch * n_suffix * s.n_q_heads;
+  a.rows_total = (int64_t)s.n_layers * s.batch * n_q * s.n_q_heads;
   a.ws_o = static_cast<float*>(workspace);
   a.ws_ml = reinterpret_cast<float2*>(a.ws_o + (size_t)p.n_splits * a.rows_total * kHD);
   a.scale_log2 = s.scale_log2;
-  if (p.n_splits > 1 && (workspace == nullptr || ws_bytes < prefill_bf16_workspace(s, n_suffix, max_ctx)))
+  if (p.n_splits > 1 && (workspace == nullptr || ws_bytes < prefill_bf16_workspace(s, n_q, max_ctx)))
     return hipErrorInvalidValue;
   const int per_xcd = (a.n_wg + kNumXcd - 1) / kNumXcd;
   const dim3 grid(per_xcd * kNumXcd, s.n_layers);
-  hipLaunchKernelGGL(prefill_bf16_kernel, grid, dim3(kThreads), 0, stream, a);
+  if (table)
+    hipLaunchKernelGGL(prefill_bf16_kernel<true>, grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(prefill_bf16_kernel<false>, grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   hipLaunchKernelGGL(prefill_combine_kernel, dim3((unsigned)((a.rows_total + 3) / 4)), dim3(256), 0,
-                     stream, a.ws_o, a.ws_ml, p.n_splits, a.rows_total, out);
+                     stream, a.ws_o, a.ws_ml, p.n_splits, a.rows_total,
+                     table ? a.n_valid : nullptr, n_q, s.n_q_heads, s.batch, a.out);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_suf,
+                               const bf16_t* v_suf, bf16_t* cache_k, bf16_t* cache_v,
+                               const int32_t* ctx_len, int32_t max_ctx,
+                               int32_t n_suffix, bf16_t* out, void* workspace, size_t ws_bytes,
+                               hipStream_t stream) {
+  PrefillArgs a = {};
+  a.q = q;
+  a.k_suf = k_suf;
+  a.v_suf = v_suf;
+  a.cache_k = cache_k;
+  a.cache_v = cache_v;
+  a.ctx_len = ctx_len;
+  a.out = out;
+  a.max_ctx = max_ctx;
+  return launch(s, a, false, n_suffix, max_ctx, workspace, ws_bytes, stream);
+}
+
+hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
+                                     const bf16_t* cache_v, const RowPos& pos, int32_t n_q,
+                                     int32_t max_len, bf16_t* out, void* workspace,
+                                     size_t ws_bytes, hipStream_t stream) {
+  PrefillArgs a = {};
+  a.q = q;
+  a.cache_k = const_cast<bf16_t*>(cache_k);
+  a.cache_v = const_cast<bf16_t*>(cache_v);
+  a.q_pos = pos.table;
+  a.n_valid = pos.n_valid;
+  a.max_pos = pos.max_pos;
+  a.out = out;
+  const int32_t max_ctx = max_len > n_q ? max_len - n_q : 0;
+  return launch(s, a, true, n_q, max_ctx, workspace, ws_bytes, stream);
 }
 
 }  // namespace pic

@@ -180,8 +180,7 @@ template <typename T, int HD>
 __global__ void __launch_bounds__(256) append_kernel(const T* __restrict__ k_new, const T* __restrict__ v_new,
                                                      T* __restrict__ cache_k, T* __restrict__ cache_v,
                                                      int n_kv_heads, int32_t batch, int32_t cache_cap,
-                                                     const int32_t* __restrict__ base, int32_t max_base,
-                                                     int32_t offset, int32_t n_new, int64_t n_rows) {
+                                                     RowPos pos, int32_t n_new, int64_t n_rows) {
   constexpr int CPR = HD * sizeof(T) / 16;  // 16-byte chunks per row
   const int64_t n_items = n_rows * CPR;
   for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n_items;
@@ -194,10 +193,8 @@ __global__ void __launch_bounds__(256) append_kernel(const T* __restrict__ k_new
     const int i = (int)(r1 % n_new);
     const int64_t lb = r1 / n_new;  // l * B + b
     const int b = (int)(lb % batch);
-    int32_t bl = base[b];
-    bl = bl < 0 ? 0 : (bl > max_base ? max_base : bl);
-    const int64_t slot = (int64_t)bl + offset + i;
-    if (slot >= cache_cap) continue;
+    const int64_t slot = pos(b, i);
+    if (slot < 0 || slot >= cache_cap) continue;
     const int64_t dst = ((lb * n_kv_heads + h) * cache_cap + slot) * HD;
     const uint4* sk = reinterpret_cast<const uint4*>(k_new + row * HD) + c;
     const uint4* sv = reinterpret_cast<const uint4*>(v_new + row * HD) + c;
@@ -263,15 +260,15 @@ hipError_t launch_compose(pic_dtype dt, int head_dim, int n_layers, int n_kv_hea
 
 hipError_t launch_append(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
                          const void* k_new, const void* v_new, void* cache_k, void* cache_v,
-                         int32_t batch, int32_t cache_cap, const int32_t* base, int32_t max_base,
-                         int32_t offset, int32_t n_new, hipStream_t stream) {
+                         int32_t batch, int32_t cache_cap, const RowPos& pos, int32_t n_new,
+                         hipStream_t stream) {
   const int64_t n_rows = (int64_t)n_layers * batch * n_new * n_kv_heads;
   if (n_rows == 0) return hipSuccess;
   PIC_DISPATCH_TD(dt, head_dim, {
     constexpr int CPR = HD * (int)sizeof(T) / 16;
     hipLaunchKernelGGL((append_kernel<T, HD>), dim3(grid_for(n_rows * CPR, 256)), dim3(256), 0,
                        stream, (const T*)k_new, (const T*)v_new, (T*)cache_k, (T*)cache_v,
-                       n_kv_heads, batch, cache_cap, base, max_base, offset, n_new, n_rows);
+                       n_kv_heads, batch, cache_cap, pos, n_new, n_rows);
   });
   return hipGetLastError();
 }

@@ -47,6 +47,7 @@ class Run:
     model: pic.Model = None
     dev: dict = field(default_factory=dict)
     maps: list = None
+    fmaps: list = None            # general frontier layout: the oracle's per-request maps
 
 
 def setup(w: Workload, requests=None, extra_cap: int = 0, mutate=None) -> Run:
@@ -132,6 +133,66 @@ def oracle_prefill(r: Run, b: int):
     K, V = oracle_compose(r, b)
     out, K2, V2 = O.suffix_prefill(K, V, r.inp["q"][b], r.inp["k_suf"][b], r.inp["v_suf"][b])
     return out, K2, V2
+
+
+# ------------------------------------------------------------------------------------------
+# general frontier layout (inline prefix and spans between documents)
+# ------------------------------------------------------------------------------------------
+
+def setup_frontier(w: Workload, items=None, n_inline_cap=None, mutate=None) -> Run:
+    """Like setup() for a frontier workload: lay.items mixes pool entries with inline spans
+    (-n); the inline tokens' q/k/v are the workload's q/k_suf/v_suf rows, in position order."""
+    lay = S.pool_layout(w)
+    if items is not None:
+        lay.items = items
+    inp = S.host_layer(w, lay, 0)
+    if n_inline_cap is not None:   # ragged layouts: more inline rows than the workload's
+        for name, h in (("q", w.n_q_heads), ("k_suf", w.n_kv_heads), ("v_suf", w.n_kv_heads)):
+            x = S.normal_f32(w, name + "_ragged", (w.batch, n_inline_cap, h, w.head_dim))
+            inp[name] = S.bf16_bits_to_f32(S.f32_to_bf16_bits(x)) if w.dtype == "bf16" else x
+    if mutate is not None:
+        mutate(inp, lay)
+    pool_k = O.store(O.rope(inp["pool_k_raw"], pool_compile_positions(lay), w.rope_theta), w.dtype)
+    fmaps = O.plan_frontier(lay.items, lay.doc_offset, lay.doc_len, lay.doc_compile_pos)
+    total = np.array([m.total_len for m in fmaps], np.int32)
+    cap = int(total.max()) + max(w.decode_steps, 0) + 3
+    r = Run(w, lay, inp, pool_k, total, cap)
+    r.fmaps = fmaps
+    r.model = pic.Model.of(1, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype, w.rope_theta)
+    return r
+
+
+def gpu_frontier(r: Run, sentinel: float = 0.0):
+    """Plan (C ABI), compose, frontier prefill; returns (out [1][B][n][Hq][D], n_inline)."""
+    w, dt = r.w, tdtype(r.w)
+    blocks, total, inl, n_inl = pic.pic_plan_frontier(r.lay.items, r.lay.doc_offset, r.lay.doc_len,
+                                                      r.lay.doc_compile_pos, r.lay.pool_tokens)
+    assert np.array_equal(total, r.ctx)
+    d = gpu_compose(r, blocks=blocks)
+    n = r.inp["q"].shape[1]
+    assert inl.shape[1] <= n
+    pos = np.full((w.batch, n), -1, np.int32)
+    pos[:, : inl.shape[1]] = inl
+    d["pos"] = torch.from_numpy(pos).to(DEV)
+    d["n_valid"] = torch.from_numpy(n_inl.astype(np.int32)).to(DEV)
+    d["q"] = to_dev(r.inp["q"][None], dt)
+    d["k_inl"] = to_dev(r.inp["k_suf"][None], dt)
+    d["v_inl"] = to_dev(r.inp["v_suf"][None], dt)
+    d["out"] = torch.full((1, w.batch, n, w.n_q_heads, w.head_dim), sentinel, dtype=dt, device=DEV)
+    max_len = int(total.max())
+    nbytes = pic.pic_frontier_workspace_bytes(r.model, w.batch, n, max_len)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=DEV)
+    pic.pic_frontier_prefill_attn(r.model, d["q"], d["k_inl"], d["v_inl"], d["cache_k"], d["cache_v"],
+                                  w.batch, r.cap, d["pos"], d["n_valid"], n, max_len, d["out"], ws)
+    return d["out"], n_inl
+
+
+def oracle_frontier(r: Run, b: int):
+    """(out [n_b][Hq][D], K, V [Hkv][total][D]) of request b from the oracle."""
+    f = r.fmaps[b]
+    Kc, Vc = O.compose_request(r.pool_k, r.inp["pool_v"], f.cached, r.w.rope_theta, r.w.dtype)
+    n = f.inline_pos.size
+    return O.frontier_prefill(Kc, Vc, f, r.inp["q"][b][:n], r.inp["k_suf"][b][:n], r.inp["v_suf"][b][:n])
 
 
 def bf16_ulp(x: np.ndarray) -> np.ndarray:

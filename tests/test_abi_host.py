@@ -97,6 +97,50 @@ def test_planner_errors(lib):
     assert "4 blocks needed" in pic.pic_last_error()
 
 
+@settings(max_examples=60, deadline=None)
+@given(st.data())
+def test_frontier_planner_matches_oracle_layout(lib, data):
+    n_pool = data.draw(st.integers(1, 8))
+    lens = np.array(data.draw(st.lists(st.integers(1, 150), min_size=n_pool, max_size=n_pool)))
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+    cpos = np.array(data.draw(st.lists(st.integers(0, 3000), min_size=n_pool, max_size=n_pool)))
+    batch = data.draw(st.integers(1, 4))
+    items = [data.draw(st.lists(st.one_of(st.integers(0, n_pool - 1), st.integers(-70, -1)),
+                                max_size=7)) for _ in range(batch)]
+    blocks, total, inl, n_inl = pic.pic_plan_frontier(items, offs, lens, cpos, int(lens.sum()))
+    maps = O.plan_frontier(items, offs, lens, cpos)
+    got = _expand(blocks, batch)
+    for b, m in enumerate(maps):
+        assert total[b] == m.total_len
+        assert n_inl[b] == m.inline_pos.size
+        assert np.array_equal(inl[b, : n_inl[b]], m.inline_pos)
+        assert np.all(inl[b, n_inl[b]:] == -1)
+        slots = np.array(sorted(got[b]), dtype=np.int64)
+        assert np.array_equal(slots, m.cached.logical_pos)
+        src = np.array([got[b][s][0] for s in slots], dtype=np.int64)
+        delta = np.array([got[b][s][1] for s in slots], dtype=np.int64)
+        assert np.array_equal(src, m.cached.src_token)
+        assert np.array_equal(delta, m.cached.logical_pos - m.cached.compile_pos)
+
+
+def test_frontier_planner_hand_layout_and_errors(lib):
+    blocks, total, inl, n_inl = pic.pic_plan_frontier([[-4, 0, -2, 1, -3]], [0, 8], [8, 5], [0, 0], 13)
+    assert list(total) == [22] and list(n_inl) == [9]
+    assert inl[0].tolist() == [0, 1, 2, 3, 12, 13, 19, 20, 21]
+    assert [tuple(int(x) for x in b) for b in blocks] == [(0, 0, 4, 8, 4), (0, 8, 14, 5, 14)]
+    with pytest.raises(pic.PicError) as e:
+        pic.pic_plan_layout([[-3, 0]], [0], [8], [0], 8)   # inline spans only in the frontier planner
+    assert e.value.status == -6
+    n, tot, ninl = ctypes.c_int32(0), np.zeros(1, np.int32), np.zeros(1, np.int32)
+    P = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    pos = np.zeros(2, np.int32)
+    st_ = lib.pic_plan_frontier(1, P(np.array([2], np.int32)), P(np.array([-3, 0], np.int32)), 1,
+                                P(np.array([0], np.int32)), P(np.array([8], np.int32)),
+                                P(np.array([0], np.int32)), 8, None, 0, ctypes.byref(n), P(tot),
+                                P(pos), 2, P(ninl))
+    assert st_ == -4 and "3 inline tokens, room for 2" in pic.pic_last_error()
+
+
 FAKE = 0x10000          # an aligned, never-dereferenced device address
 MIS = 0x10008           # misaligned
 
@@ -134,6 +178,15 @@ def _decode(lib, m, ws=FAKE, ws_bytes=1 << 30, **kw):
                                a["out"], ws, ws_bytes, None)
 
 
+def _frontier(lib, m, ws_bytes=0, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, ck=FAKE, cv=FAKE, batch=2, cap=600, pos=FAKE, nv=FAKE, n=64,
+             max_len=600, scale=0.0, out=FAKE)
+    a.update(kw)
+    return lib.pic_frontier_prefill_attn(ctypes.byref(m), a["q"], a["k"], a["v"], a["ck"], a["cv"],
+                                         a["batch"], a["cap"], a["pos"], a["nv"], a["n"],
+                                         a["max_len"], a["scale"], a["out"], None, ws_bytes, None)
+
+
 def test_argument_checks_fail_before_any_launch(lib):
     m = _model()
     assert _compose(lib, _model(head_dim=96)) == -2
@@ -151,6 +204,15 @@ def test_argument_checks_fail_before_any_launch(lib):
     assert _prefill(lib, m, scale=-1.0) == -1
     assert _prefill(lib, _model(head_dim=64)) == -2      # bf16 attention: head_dim 128 only
     assert _prefill(lib, m, ns=0) == 0
+
+    assert _frontier(lib, m, max_len=601) == -4          # longer than the cache
+    assert _frontier(lib, m, pos=None) == -1
+    assert _frontier(lib, m, nv=None) == -1
+    assert _frontier(lib, m, k=MIS) == -5
+    assert _frontier(lib, m, n=-1) == -1
+    assert _frontier(lib, m, scale=float("nan")) == -1
+    assert _frontier(lib, _model(head_dim=64)) == -2
+    assert _frontier(lib, m, n=0) == 0
 
     assert _decode(lib, m, step=100) == -4               # 500 + 100 + 1 > 600
     assert _decode(lib, m, ws=None) == -3
