@@ -57,10 +57,8 @@ def compose_bytes(w, ctx, n_layers):
     return int(sum(ctx)) * w.n_kv_heads * n_layers * 4 * w.head_dim * w.elem_bytes
 
 
-def prefill_flops(w, ctx):
+def prefill_flops(w, pairs):
     """4 * Hq * D per visible (query, key) pair (QK^T and PV, 2 flops per multiply-add)."""
-    Ls = w.n_suffix
-    pairs = sum(Ls * c + Ls * (Ls + 1) // 2 for c in ctx)
     return 4 * w.n_q_heads * w.head_dim * pairs
 
 
@@ -81,6 +79,10 @@ def source_hash(rel):
 class DeviceWorkload:
     """Every tensor of one workload, resident on the device, plus the per-step driver.
 
+    Plain workloads: documents back to back after a stored prefix, then n_suffix query tokens
+    (pic_plan_layout, pic_compose, pic_suffix_prefill_attn).  Frontier workloads: an inline
+    prefix and inline spans between the documents (pic_plan_frontier, pic_compose,
+    pic_frontier_prefill_attn over all inline tokens).  Decode steps follow either.
     `layers` < w.n_layers builds a workload with fewer layers of the same per-layer shape.
     """
 
@@ -94,11 +96,29 @@ class DeviceWorkload:
         self.w, self.dev, self.n_dec = w, dev, n_dec
         self.L = L = w.n_layers if layers is None else layers
         self.dt = dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
-        B, Hq, Hkv, D, Ls = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_suffix
+        B, Hq, Hkv, D = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
         self.lay = lay = S.pool_layout(w)
-        self.ctx_host = S.context_lengths(lay)
-        self.max_ctx = int(self.ctx_host.max())
-        self.cap = self.max_ctx + Ls + n_dec
+        self.frontier = w.frontier
+        if self.frontier:
+            _, total, inl, n_inl = pic.pic_plan_frontier(lay.items, lay.doc_offset, lay.doc_len,
+                                                         lay.doc_compile_pos, lay.pool_tokens)
+            self.Ls = Ls = inl.shape[1]
+            self.length_host = total.astype(np.int64)               # positions before decode
+            self.ctx_host = (total - n_inl).astype(np.int32)        # cached (composed) tokens
+            self.pos_host = inl
+            self.pairs = int(sum(int(p) + 1 for b in range(B) for p in inl[b, : n_inl[b]]))
+            self.max_len = int(total.max())
+            self.max_ctx = int(self.ctx_host.max())
+            self.pos_dev = torch.from_numpy(inl).to(dev)
+            self.n_valid_dev = torch.from_numpy(n_inl.astype(np.int32)).to(dev)
+        else:
+            self.Ls = Ls = w.n_suffix
+            self.ctx_host = S.context_lengths(lay)
+            self.max_ctx = int(self.ctx_host.max())
+            self.length_host = self.ctx_host.astype(np.int64) + Ls
+            self.max_len = self.max_ctx + Ls
+            self.pairs = int(sum(Ls * int(c) + Ls * (Ls + 1) // 2 for c in self.ctx_host))
+        self.cap = self.max_len + n_dec
         self.model = pic.Model.of(L, Hq, Hkv, D, w.dtype, w.rope_theta)
         self.m1 = self.model.with_layers(1)
 
@@ -125,14 +145,18 @@ class DeviceWorkload:
                                  device=dev)
         pic.pic_rope_table_init(self.model, self.mad, self.table)
         self.ctx_dev = torch.from_numpy(self.ctx_host.astype(np.int32)).to(dev)
-        self.base_dev = torch.from_numpy((self.ctx_host + Ls).astype(np.int32)).to(dev)
-        self.max_base = self.max_ctx + Ls
-        self.ws_pre = torch.empty(max(pic.pic_prefill_workspace_bytes(self.m1, B, Ls, self.max_ctx), 16),
-                                  dtype=torch.uint8, device=dev)
+        self.base_dev = torch.from_numpy(self.length_host.astype(np.int32)).to(dev)
+        self.max_base = self.max_len
+        if self.frontier:
+            nbytes = pic.pic_frontier_workspace_bytes(self.m1, B, Ls, self.max_len)
+        else:
+            nbytes = pic.pic_prefill_workspace_bytes(self.m1, B, Ls, self.max_ctx)
+        self.ws_pre = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev)
         self.ws_dec = torch.empty(max(pic.pic_decode_workspace_bytes(self.m1, B, self.max_base + n_dec, 0), 16),
                                   dtype=torch.uint8, device=dev)
         n_blocks_max = sum((int(n) + 63) // 64 for r in lay.requests for n in lay.doc_len[r])
-        self.blocks_pinned = torch.empty(n_blocks_max * 5, dtype=torch.int32, pin_memory=True)
+        n_pos = self.pos_host.size if self.frontier else 0
+        self.blocks_pinned = torch.empty(n_blocks_max * 5 + n_pos, dtype=torch.int32, pin_memory=True)
         self.blocks_dev = torch.empty(n_blocks_max * 5, dtype=torch.int32, device=dev)
 
     def step(self, rec: dict | None = None, calib=None):
@@ -142,18 +166,26 @@ class DeviceWorkload:
 
         import paper_2607_28069_amd as pic
 
-        w, L, B, Ls = self.w, self.L, self.w.batch, self.w.n_suffix
+        w, L, B, Ls = self.w, self.L, self.w.batch, self.Ls
         stream = torch.cuda.current_stream()
         ev = lambda: torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         # -- TTFT region
         lay = self.lay
-        blocks, ctx = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len,
-                                          lay.doc_compile_pos, lay.pool_tokens)
+        if self.frontier:
+            blocks, _, inl, _ = pic.pic_plan_frontier(lay.items, lay.doc_offset, lay.doc_len,
+                                                      lay.doc_compile_pos, lay.pool_tokens)
+        else:
+            blocks, _ = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len,
+                                            lay.doc_compile_pos, lay.pool_tokens)
         nb = len(blocks)
-        self.blocks_pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32)))
+        self.blocks_pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32).reshape(-1)))
         self.blocks_dev[: nb * 5].copy_(self.blocks_pinned[: nb * 5], non_blocking=True)
+        if self.frontier:   # the inline positions go to the device with the blocks
+            tail = self.blocks_pinned[nb * 5: nb * 5 + inl.size]
+            tail.copy_(torch.from_numpy(inl.reshape(-1)))
+            self.pos_dev.view(-1).copy_(tail, non_blocking=True)
         e0, e1 = ev(), ev()
         e0.record(stream)
         pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
@@ -163,9 +195,15 @@ class DeviceWorkload:
         for l in range(L if Ls else 0):
             a, b = ev(), ev()
             a.record(stream)
-            pic.pic_suffix_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l], self.cache_k[l],
-                                        self.cache_v[l], B, self.cap, self.ctx_dev, self.max_ctx, Ls,
-                                        self.out[l], self.ws_pre)
+            if self.frontier:
+                pic.pic_frontier_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
+                                              self.cache_k[l], self.cache_v[l], B, self.cap,
+                                              self.pos_dev, self.n_valid_dev, Ls, self.max_len,
+                                              self.out[l], self.ws_pre)
+            else:
+                pic.pic_suffix_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
+                                            self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
+                                            self.max_ctx, Ls, self.out[l], self.ws_pre)
             b.record(stream)
             pre.append((a, b))
         torch.cuda.synchronize()
@@ -213,10 +251,15 @@ def cpu_baseline(w, budget_s):
     while True:
         t0 = time.perf_counter()
         r = b % w.batch
-        m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
-        K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], m, w.rope_theta, w.dtype)
-        if w.n_suffix:
-            O.suffix_prefill(K, V, inp["q"][r], inp["k_suf"][r], inp["v_suf"][r])
+        if w.frontier:
+            f = O.plan_frontier([lay.items[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+            K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], f.cached, w.rope_theta, w.dtype)
+            O.frontier_prefill(K, V, f, inp["q"][r], inp["k_suf"][r], inp["v_suf"][r])
+        else:
+            m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+            K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], m, w.rope_theta, w.dtype)
+            if w.n_suffix:
+                O.suffix_prefill(K, V, inp["q"][r], inp["k_suf"][r], inp["v_suf"][r])
         samples.append(time.perf_counter() - t0)
         b += 1
         if time.perf_counter() > t_end:
@@ -226,7 +269,8 @@ def cpu_baseline(w, budget_s):
     return {
         "value": per_req_layer * w.n_layers * 1e3, "unit": "ms/request", "cores": int(threads),
         "kind": "oracle",
-        "sample": f"{len(samples)} request-layers of {w.name} (plan + compose + suffix prefill in fp64 "
+        "sample": f"{len(samples)} request-layers of {w.name} (plan + compose + "
+                  f"{'inline' if w.frontier else 'suffix'} prefill in fp64 "
                   f"numpy, BLAS threads = cores), mean x {w.n_layers} layers; {sum(samples):.1f} s of CPU work",
     }
 
@@ -269,14 +313,14 @@ def main():
     total_ms = (time.perf_counter() - t_start) * 1e3
 
     mean = lambda x: float(sum(x) / len(x)) if x else 0.0
-    L, B, Ls = wl.L, w.batch, w.n_suffix
+    L, B, Ls = wl.L, w.batch, wl.Ls
     ctx = [int(c) for c in wl.ctx_host]
     ttft_ms = mean(rec["ttft"])
     comp_ms, pre_ms, dec_ms = mean(rec["compose"]), mean(rec["prefill"]), mean(rec["decode"])
     comp_b = compose_bytes(w, ctx, L)
-    pre_f_layer = prefill_flops(w, ctx)
-    # decode step t sees ctx + Ls + t + 1 slots; average over the steps of one bench step
-    dec_b_layer = sum(decode_bytes(w, [c + Ls + t + 1 for c in ctx]) for t in range(n_dec)) / max(n_dec, 1)
+    pre_f_layer = prefill_flops(w, wl.pairs)
+    # decode step t sees length + t + 1 slots; average over the steps of one bench step
+    dec_b_layer = sum(decode_bytes(w, [int(n) + t + 1 for n in wl.length_host]) for t in range(n_dec)) / max(n_dec, 1)
     kernels = {
         "compose": {"bound": "hbm", "achieved": comp_b / (comp_ms * 1e-3) / 1e9 if comp_ms else None,
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "ms_per_launch": comp_ms,
@@ -317,8 +361,10 @@ def main():
         "config": {"workload": w.name, "layers": L, "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "rope_theta": w.rope_theta, "batch": B,
                    "context_tokens": ctx[0] if len(set(ctx)) == 1 else ctx,
-                   "suffix_tokens": Ls, "decode_tokens_per_step": n_dec, "pool_docs": w.pool_docs,
-                   "docs_per_request": w.docs_per_request},
+                   "suffix_tokens": w.n_suffix, "decode_tokens_per_step": n_dec, "pool_docs": w.pool_docs,
+                   "docs_per_request": w.docs_per_request,
+                   **({"inline_prefix": w.inline_prefix, "inline_span": w.inline_span,
+                       "inline_tokens": Ls} if w.frontier else {})},
         "ttft_ms_batch": ttft_ms,
         "prefill_attn_tflops": kernels["suffix_prefill_attn"]["achieved"],
         "rerotate_compose_gbps": kernels["compose"]["achieved"],

@@ -116,7 +116,10 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int w = blockIdx.x;
   const int logical = (w % kNumXcd) * per_xcd + w / kNumXcd;
   if (logical >= a.n_wg) return;
-  const int mt = logical % a.m_tiles;
+  // m-tiles of one (request, kv head) are dispatched one after another (so they stream its
+  // keys concurrently, sharing the XCD's L2), the last one first: later query rows see more
+  // keys, so the longest workgroups start earliest and short ones fill the end of the launch
+  const int mt = a.m_tiles - 1 - logical % a.m_tiles;
   const int split = (logical / a.m_tiles) % a.n_splits;
   const int bg = logical / (a.m_tiles * a.n_splits);
   const int b = bg / a.n_kv_heads, g = bg % a.n_kv_heads;

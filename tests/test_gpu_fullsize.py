@@ -160,3 +160,41 @@ def test_llama8b_decode_256_steps_all_layers():
                 ref = O.attention(q[:, None, :], np.asarray([n + t]), Kt, Vt, np.arange(n + t + 1))[:, 0]
                 assert_attn_close(_host(wl.dout[t, l, r]), ref, w.dtype)
             print(f"[c4] layer {l} request {r} steps 0/1/127/{n_dec - 1} ok", flush=True)
+
+
+def test_llama8b_frontier_32layer_bench_shape():
+    # The 32-layer Llama shape in the general frontier layout (inline 128-token prefix, a
+    # 32-token inline span after each of the 10 documents, 128 query tokens): every inline
+    # token's K/V at its slot, composed documents around them, and attention of sampled inline
+    # tokens (prefix, spans, query) on the first, middle and last layers, plus a decode step.
+    w = synth.get("llama8b_frontier")
+    wl = DeviceWorkload(w, DEV, n_dec=1)
+    wl.step()
+    torch.cuda.synchronize()
+    lay = wl.lay
+    print(f"[frontier] lengths={sorted(set(int(x) for x in wl.length_host))} inline={wl.Ls}", flush=True)
+    toks = np.array([0, 127, 128, 140, 159, 300, 447, 448, 500, 575])
+    for l, r in ((0, 0), (wl.L // 2, 9), (wl.L - 1, 15)):
+        pool_k, pool_v = _host(wl.pool_k[l]), _host(wl.pool_v[l])
+        f = O.plan_frontier([lay.items[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+        Kc, Vc = O.compose_request(pool_k, pool_v, f.cached, w.rope_theta, w.dtype)
+        ks, vs = _host(wl.k_suf[l, r]), _host(wl.v_suf[l, r])
+        T = f.total_len
+        ck, cv = _host(wl.cache_k[l, r]), _host(wl.cache_v[l, r])
+        assert np.array_equal(cv[:, f.cached.logical_pos].view(np.uint32), Vc.view(np.uint32))
+        assert assert_keys_close(ck[:, f.cached.logical_pos], Kc, w.dtype) > 0.999
+        assert np.array_equal(ck[:, f.inline_pos].view(np.uint32),
+                              np.transpose(ks, (1, 0, 2)).view(np.uint32))
+        assert np.array_equal(cv[:, f.inline_pos].view(np.uint32),
+                              np.transpose(vs, (1, 0, 2)).view(np.uint32))
+        # the full cache by position from the oracle's composed rows and the inline inputs
+        K = np.empty((w.n_kv_heads, T, w.head_dim), np.float32)
+        V = np.empty_like(K)
+        K[:, f.cached.logical_pos], V[:, f.cached.logical_pos] = Kc, Vc
+        K[:, f.inline_pos], V[:, f.inline_pos] = np.transpose(ks, (1, 0, 2)), np.transpose(vs, (1, 0, 2))
+        q = np.transpose(_host(wl.q[l, r])[toks], (1, 0, 2))
+        ref = O.attention(q, f.inline_pos[toks], K, V, np.arange(T))
+        assert_attn_close(np.transpose(_host(wl.out[l, r])[toks], (1, 0, 2)), ref, w.dtype)
+        dref, _, _ = O.decode_step(K, V, T, _host(wl.dq[l, r]), _host(wl.dk[l, r]), _host(wl.dv[l, r]))
+        assert_attn_close(_host(wl.dout[0, l, r]), dref, w.dtype)
+        print(f"[frontier] layer {l} request {r} ok", flush=True)
