@@ -28,8 +28,11 @@ stored result is rounded once to its storage type.
 
 Readings where the paper is silent (each one is also pinned by a test):
   * rotate-half pairing of element i with element i + D/2 and inverse
-    frequencies theta_i = base^(-2i/D), no frequency scaling;
-  * one rotary transform shared by all layers;
+    frequencies theta_i = base^(-2i/D), no frequency scaling, by default; the
+    interleaved pairing (2i, 2i+1), explicit (e.g. Llama-3.1 frequency-scaled)
+    frequencies and a different transform per layer ("layer-specific R_l",
+    Sec. 2) are available as options;
+  * one rotary transform shared by all layers unless given per layer;
   * softmax scale 1/sqrt(D); GQA query head h reads kv head h // (Hq/Hkv);
   * a token attends to every position <= its own (itself included).
 """
@@ -80,39 +83,75 @@ def inv_freq(head_dim: int, theta: float) -> np.ndarray:
     return np.power(float(theta), -2.0 * i / head_dim)
 
 
-def _cos_sin(pos, head_dim: int, theta: float):
-    ang = np.asarray(pos, dtype=np.float64)[:, None] * inv_freq(head_dim, theta)[None, :]
+def llama3_inv_freq(head_dim: int, theta: float, factor: float = 8.0, low_freq_factor: float = 1.0,
+                    high_freq_factor: float = 4.0, original_max_position: int = 8192) -> np.ndarray:
+    """Frequency-scaled rotary frequencies of the Llama-3.1 family, float64.
+
+    A frequency whose wavelength 2 pi / theta_i is shorter than original_max_position /
+    high_freq_factor is kept; one whose wavelength exceeds original_max_position /
+    low_freq_factor is divided by `factor`; in between the two are blended linearly in
+    original_max_position / wavelength.
+    """
+    f = inv_freq(head_dim, theta)
+    wavelen = 2.0 * np.pi / f
+    smooth = (original_max_position / wavelen - low_freq_factor) / (high_freq_factor - low_freq_factor)
+    blended = (1.0 - smooth) * f / factor + smooth * f
+    out = np.where(wavelen > original_max_position / low_freq_factor, f / factor, blended)
+    return np.where(wavelen < original_max_position / high_freq_factor, f, out)
+
+
+def _frequencies(head_dim: int, theta: float, freqs) -> np.ndarray:
+    return inv_freq(head_dim, theta) if freqs is None else np.asarray(freqs, np.float64)
+
+
+def _cos_sin(pos, head_dim: int, theta: float, freqs=None):
+    ang = np.asarray(pos, dtype=np.float64)[:, None] * _frequencies(head_dim, theta, freqs)[None, :]
     return np.cos(ang), np.sin(ang)
 
 
-def rope(x, pos, theta: float) -> np.ndarray:
+def _split_pairs(x, pairing: str):
+    """The two members of every rotated pair: (x_i, x_{i+D/2}) or (x_{2i}, x_{2i+1})."""
+    if pairing == "half":
+        h = x.shape[-1] // 2
+        return x[..., :h], x[..., h:]
+    if pairing == "interleaved":
+        return x[..., 0::2], x[..., 1::2]
+    raise ValueError(pairing)
+
+
+def _join_pairs(a, b, pairing: str):
+    if pairing == "half":
+        return np.concatenate([a, b], axis=-1)
+    return np.stack([a, b], axis=-1).reshape(a.shape[:-1] + (2 * a.shape[-1],))
+
+
+def rope(x, pos, theta: float, pairing: str = "half", freqs=None) -> np.ndarray:
     """R(p) x for rows x[..., n, D] at positions pos[n]; float64 result.
 
-    Each pair (x_i, x_{i+D/2}) is turned by the angle p * theta_i:
-    (x_i cos - x_{i+D/2} sin, x_i sin + x_{i+D/2} cos).
+    Pair i of a head (elements i and i + D/2 for "half", 2i and 2i + 1 for "interleaved")
+    is turned by the angle p * theta_i: (x cos - y sin, x sin + y cos).  theta_i is
+    theta^(-2i/D) unless `freqs` gives the D/2 frequencies explicitly.
     """
     x = np.asarray(x, dtype=np.float64)
-    h = x.shape[-1] // 2
-    c, s = _cos_sin(pos, 2 * h, theta)
-    x1, x2 = x[..., :h], x[..., h:]
-    return np.concatenate([x1 * c - x2 * s, x1 * s + x2 * c], axis=-1)
+    c, s = _cos_sin(pos, x.shape[-1], theta, freqs)
+    x1, x2 = _split_pairs(x, pairing)
+    return _join_pairs(x1 * c - x2 * s, x1 * s + x2 * c, pairing)
 
 
-def rope_inverse(x, pos, theta: float) -> np.ndarray:
+def rope_inverse(x, pos, theta: float, pairing: str = "half", freqs=None) -> np.ndarray:
     """R(p)^{-1} x = R(p)^T x (a rotation's inverse is its transpose); float64 result."""
     x = np.asarray(x, dtype=np.float64)
-    h = x.shape[-1] // 2
-    c, s = _cos_sin(pos, 2 * h, theta)
-    x1, x2 = x[..., :h], x[..., h:]
-    return np.concatenate([x1 * c + x2 * s, -x1 * s + x2 * c], axis=-1)
+    c, s = _cos_sin(pos, x.shape[-1], theta, freqs)
+    x1, x2 = _split_pairs(x, pairing)
+    return _join_pairs(x1 * c + x2 * s, -x1 * s + x2 * c, pairing)
 
 
-def rerotate_keys(k, a, b, theta: float) -> np.ndarray:
+def rerotate_keys(k, a, b, theta: float, pairing: str = "half", freqs=None) -> np.ndarray:
     """Eq. 3 taken literally: k_b = R(b) (R(a)^{-1} k_a), two rotations in float64.
 
     k: [..., n, D]; a, b: [n] compile-time and request-time positions.
     """
-    return rope(rope_inverse(k, a, theta), b, theta)
+    return rope(rope_inverse(k, a, theta, pairing, freqs), b, theta, pairing, freqs)
 
 
 # --------------------------------------------------------------------------------------
@@ -192,13 +231,15 @@ def plan_frontier(items_per_request, doc_offset, doc_len, doc_compile_pos) -> li
 # --------------------------------------------------------------------------------------
 
 
-def compose_request(pool_k, pool_v, rmap: RequestMap, theta: float, dtype: str):
+def compose_request(pool_k, pool_v, rmap: RequestMap, theta: float, dtype: str,
+                    pairing: str = "half", freqs=None):
     """One request, one layer.  pool_k/pool_v: [Hkv][pool_tokens][D] (float32 values).
 
-    Returns (K, V) of shape [Hkv][ctx][D], float32 values of the storage type.
+    Returns (K, V) of shape [Hkv][ctx][D], float32 values of the storage type.  `pairing`
+    and `freqs` select the layer's rotary transform (see rope()).
     """
     k_src = np.asarray(pool_k, np.float64)[:, rmap.src_token, :]
-    k = store(rerotate_keys(k_src, rmap.compile_pos, rmap.logical_pos, theta), dtype)
+    k = store(rerotate_keys(k_src, rmap.compile_pos, rmap.logical_pos, theta, pairing, freqs), dtype)
     v = np.asarray(pool_v, np.float32)[:, rmap.src_token, :].copy()
     return k, v
 

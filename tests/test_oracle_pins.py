@@ -279,6 +279,54 @@ def test_composed_cache_equals_full_recompute_single_layer():
 
 
 # ------------------------------------------------------------------------------------
+# reader-side rotary variants: scaled frequencies, interleaved pairing, per-layer transforms
+# ------------------------------------------------------------------------------------
+
+def test_llama3_scaled_frequencies_match_hf_transformers():
+    from transformers import LlamaConfig
+    from transformers.modeling_rope_utils import ROPE_INIT_FUNCTIONS
+    for theta, factor, lo, hi, orig in ((5e5, 8.0, 1.0, 4.0, 8192), (1e4, 4.0, 2.0, 8.0, 4096)):
+        cfg = LlamaConfig(hidden_size=4096, num_attention_heads=32, rope_theta=theta,
+                          max_position_embeddings=131072,
+                          rope_scaling={"rope_type": "llama3", "factor": factor, "low_freq_factor": lo,
+                                        "high_freq_factor": hi, "original_max_position_embeddings": orig})
+        ref, _ = ROPE_INIT_FUNCTIONS["llama3"](cfg, "cpu")
+        got = O.llama3_inv_freq(128, theta, factor, lo, hi, orig)
+        np.testing.assert_allclose(got, ref.double().numpy(), rtol=2e-6, atol=0)
+        # all three regimes occur: kept, divided, blended
+        base = O.inv_freq(128, theta)
+        assert np.any(got == base) and np.any(np.isclose(got, base / factor, rtol=1e-12, atol=0))
+        assert np.any((got < base) & ~np.isclose(got, base / factor, rtol=1e-12, atol=0))
+
+
+def test_interleaved_pairing_matches_complex_multiplication():
+    # pairs (x_2i, x_2i+1) as complex numbers x_2i + i x_2i+1, turned by e^{i p theta_i}
+    D, theta = 64, 1e4
+    x = rng.standard_normal((3, 7, D))
+    pos = np.array([0, 1, 5, 100, 2049, 31337, 7])
+    f = O.llama3_inv_freq(D, theta, 4.0, 1.0, 4.0, 1024)
+    xc = torch.view_as_complex(torch.from_numpy(x).reshape(3, 7, D // 2, 2).contiguous())
+    ang = torch.from_numpy(pos.astype(np.float64))[:, None] * torch.from_numpy(f)[None, :]
+    ref = torch.view_as_real(xc * torch.polar(torch.ones_like(ang), ang)).reshape(3, 7, D).numpy()
+    np.testing.assert_allclose(O.rope(x, pos, theta, "interleaved", f), ref, atol=1e-12)
+    assert not np.allclose(O.rope(x, pos, theta, "half", f), ref, atol=1e-3)
+
+
+@settings(max_examples=40, deadline=None)
+@given(st.sampled_from(["half", "interleaved"]), st.integers(0, 5000), st.integers(-3000, 3000),
+       st.sampled_from([1e4, 5e5, 1e6]), st.booleans())
+def test_rerotation_identity_for_every_variant(pairing, p, d, theta, scaled):
+    f = O.llama3_inv_freq(64, theta) if scaled else None
+    k = rng.standard_normal((2, 1, 64))
+    moved = O.rerotate_keys(O.rope(k, [p], theta, pairing, f), [p], [p + d], theta, pairing, f)
+    np.testing.assert_allclose(moved, O.rope(k, [p + d], theta, pairing, f), atol=1e-9)
+    q = rng.standard_normal(64)
+    lhs = O.rope(q[None], [p], theta, pairing, f)[0] @ O.rope(k[0], [p + d], theta, pairing, f)[0]
+    rhs = q @ O.rope(k[0], [d], theta, pairing, f)[0]
+    assert abs(lhs - rhs) < 1e-9 * (1 + abs(rhs))
+
+
+# ------------------------------------------------------------------------------------
 # general frontier layout (inline prefix and inline spans between documents)
 # ------------------------------------------------------------------------------------
 
