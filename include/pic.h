@@ -60,10 +60,21 @@ typedef enum {
 
 typedef enum { PIC_F32 = 0, PIC_BF16 = 1 } pic_dtype;
 
-/* Attention shape of the decoder whose caches are served. head_dim must be 64 or 128;
-   n_q_heads must be a multiple of n_kv_heads.  rope_theta is the RoPE base: pair i of a
-   head (elements i and i + D/2) turns by p * rope_theta^(-2i/D) at position p, the same
-   transform in every layer. */
+/* Which two elements of a head form rotary pair i. */
+typedef enum {
+  PIC_ROPE_HALF = 0,        /* elements i and i + D/2 (rotate-half; Llama, Qwen) */
+  PIC_ROPE_INTERLEAVED = 1  /* elements 2i and 2i + 1 */
+} pic_rope_pairing;
+
+/* Attention shape and rotary transform of the decoder whose caches are served.  head_dim
+   must be 64 or 128; n_q_heads must be a multiple of n_kv_heads.  At position p, rotary
+   pair i of a head turns by p * theta_i, with theta_i = rope_theta^(-2i/D) (the tables
+   pic_rope_table_init builds) or the frequencies given to pic_rope_table_init_freq (e.g.
+   Llama-3.1 frequency scaling).
+     rope_pairing  PIC_ROPE_HALF (0, the default) or PIC_ROPE_INTERLEAVED
+     rope_tables   0 or 1: one transform for every layer; n_layers: layer l has its own
+                   frequencies (a layer-specific R_l, Sec. 2) and the delta-angle table
+                   holds one block per layer */
 typedef struct {
   int32_t n_layers;
   int32_t n_q_heads;
@@ -71,6 +82,8 @@ typedef struct {
   int32_t head_dim;
   pic_dtype dtype;
   double rope_theta;
+  int32_t rope_pairing;
+  int32_t rope_tables;
 } pic_model;
 
 /* Most tokens one gather block carries. */
@@ -133,20 +146,38 @@ pic_status pic_plan_frontier(int32_t batch, const int32_t* n_items, const int32_
 
 /* ---- 2a. delta-angle table (Sec. 2, Eq. 3: R(b) R(a)^-1 = R(b - a)) ----
    Table of (cos, sin) of delta * theta_i for delta = 0..max_abs_delta and i = 0..D/2-1,
-   float32 pairs laid out [max_abs_delta + 1][D/2][2]; angles and cos/sin are evaluated in
-   float64 and rounded once.  Negative shifts use the same row with sin negated.
+   float32 pairs laid out [n_tables][max_abs_delta + 1][D/2][2] (n_tables = rope_tables if
+   it exceeds 1, else 1); angles and cos/sin are evaluated in float64 and rounded once.
+   Negative shifts use the same row with sin negated.
    pic_rope_table_bytes returns the size (0 for an unsupported model or a negative or too
-   large max_abs_delta, at most 1 << 20).  pic_rope_table_init fills `table` on `stream`. */
+   large max_abs_delta, at most 1 << 20).  pic_rope_table_init fills every block from
+   rope_theta; pic_rope_table_init_freq from inv_freq [host, n_tables x D/2], finite and
+   >= 0 (block l from row l).  Both enqueue on `stream`. */
 size_t pic_rope_table_bytes(const pic_model* model, int32_t max_abs_delta);
 pic_status pic_rope_table_init(const pic_model* model, int32_t max_abs_delta, void* table,
                                size_t table_bytes, void* stream);
+pic_status pic_rope_table_init_freq(const pic_model* model, const double* inv_freq,
+                                    int32_t max_abs_delta, void* table, size_t table_bytes,
+                                    void* stream);
+
+/* Host helper: the frequency-scaled rotary frequencies of the Llama-3.1 family for
+   pic_rope_table_init_freq.  Starting from theta_i = theta^(-2i/D): a frequency whose
+   wavelength 2 pi / theta_i is below original_max_position / high_freq_factor is kept, one
+   above original_max_position / low_freq_factor is divided by factor, and in between the
+   two are blended linearly in original_max_position / wavelength.  Writes D/2 values to
+   inv_freq [host]; fails with PIC_ERR_INVALID_ARG for a head_dim other than 64 or 128 or
+   non-positive / inconsistent factors (high_freq_factor must exceed low_freq_factor). */
+pic_status pic_rope_llama3_freq(int32_t head_dim, double theta, double factor,
+                                double low_freq_factor, double high_freq_factor,
+                                double original_max_position, double* inv_freq);
 
 /* ---- 2b. standalone key re-rotation (Sec. 2, Eq. 3) ----
    k_out[t][h] = R(delta[t]) k_in[t][h] for t < n_tokens, h < n_heads; rows of head_dim.
    k_in/k_out [n_tokens][n_heads][D] (may be the same buffer), delta [n_tokens] device int32
    with |delta| <= max_abs_delta (a larger entry is clamped to the table), table from
-   pic_rope_table_init for this model and max_abs_delta.  model->n_layers is ignored
-   (fold layers into n_tokens). */
+   pic_rope_table_init(_freq) for this model and max_abs_delta.  model->n_layers is ignored
+   (fold layers into n_tokens); the first table block is used, so with per-layer tables
+   pass a pointer to layer l's block (l * (max_abs_delta + 1) * D/2 float pairs in). */
 pic_status pic_rerotate_keys(const pic_model* model, const void* k_in, void* k_out,
                              int64_t n_tokens, int32_t n_heads, const int32_t* delta,
                              const void* table, int32_t max_abs_delta, void* stream);

@@ -23,6 +23,7 @@ STATUS = {0: "PIC_OK", -1: "PIC_ERR_INVALID_ARG", -2: "PIC_ERR_UNSUPPORTED", -3:
 
 # Every symbol include/pic.h declares.
 EXPORTS = ("pic_plan_layout", "pic_plan_frontier", "pic_rope_table_bytes", "pic_rope_table_init",
+           "pic_rope_table_init_freq", "pic_rope_llama3_freq",
            "pic_rerotate_keys", "pic_compose", "pic_prefill_workspace_bytes",
            "pic_suffix_prefill_attn", "pic_frontier_workspace_bytes", "pic_frontier_prefill_attn",
            "pic_decode_workspace_bytes", "pic_decode_attn", "pic_status_string", "pic_last_error",
@@ -35,19 +36,28 @@ class PicError(RuntimeError):
         self.status = status
 
 
+PIC_ROPE_HALF, PIC_ROPE_INTERLEAVED = 0, 1
+
+
 class Model(ctypes.Structure):
-    """pic_model: attention shape of the served decoder."""
+    """pic_model: attention shape and rotary transform of the served decoder."""
     _fields_ = [("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
-                ("dtype", ctypes.c_int), ("rope_theta", ctypes.c_double)]
+                ("dtype", ctypes.c_int), ("rope_theta", ctypes.c_double),
+                ("rope_pairing", ctypes.c_int32), ("rope_tables", ctypes.c_int32)]
 
     @classmethod
-    def of(cls, n_layers, n_q_heads, n_kv_heads, head_dim, dtype, rope_theta):
+    def of(cls, n_layers, n_q_heads, n_kv_heads, head_dim, dtype, rope_theta, pairing="half",
+           per_layer_tables=False):
         dt = {"f32": PIC_F32, "bf16": PIC_BF16}.get(dtype, dtype)
-        return cls(n_layers, n_q_heads, n_kv_heads, head_dim, dt, float(rope_theta))
+        pr = {"half": PIC_ROPE_HALF, "interleaved": PIC_ROPE_INTERLEAVED}.get(pairing, pairing)
+        return cls(n_layers, n_q_heads, n_kv_heads, head_dim, dt, float(rope_theta), pr,
+                   n_layers if per_layer_tables else 1)
 
     def with_layers(self, n):
-        return Model(n, self.n_q_heads, self.n_kv_heads, self.head_dim, self.dtype, self.rope_theta)
+        """The same decoder restricted to n layers (per-layer tables: the first n blocks)."""
+        return Model(n, self.n_q_heads, self.n_kv_heads, self.head_dim, self.dtype, self.rope_theta,
+                     self.rope_pairing, n if self.rope_tables > 1 else self.rope_tables)
 
 
 BLOCK_DTYPE = np.dtype([("request", np.int32), ("src_token", np.int32), ("dst_slot", np.int32),
@@ -71,6 +81,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "pic_plan_frontier": (ctypes.c_int, [I32, P, P, I32, P, P, P, I64, P, I32, P, P, P, I32, P]),
         "pic_rope_table_bytes": (SZ, [MP, I32]),
         "pic_rope_table_init": (ctypes.c_int, [MP, I32, P, SZ, P]),
+        "pic_rope_table_init_freq": (ctypes.c_int, [MP, P, I32, P, SZ, P]),
+        "pic_rope_llama3_freq": (ctypes.c_int, [I32, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                                ctypes.c_double, ctypes.c_double, P]),
         "pic_rerotate_keys": (ctypes.c_int, [MP, P, P, I64, I32, P, P, I32, P]),
         "pic_compose": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, P, I32, I32, P]),
         "pic_prefill_workspace_bytes": (SZ, [MP, I32, I32, I32]),
@@ -175,6 +188,23 @@ def pic_rope_table_bytes(model: Model, max_abs_delta: int) -> int:
 def pic_rope_table_init(model: Model, max_abs_delta: int, table, stream=None):
     _check(load().pic_rope_table_init(ctypes.byref(model), max_abs_delta, _ptr(table),
                                       table.numel() * table.element_size(), _stream(stream)))
+
+
+def pic_rope_table_init_freq(model: Model, inv_freq, max_abs_delta: int, table, stream=None):
+    """inv_freq: host array [n_tables][D/2] (or [D/2] for one table) of rotary frequencies."""
+    f = np.ascontiguousarray(inv_freq, dtype=np.float64)
+    _check(load().pic_rope_table_init_freq(ctypes.byref(model), f.ctypes.data_as(ctypes.c_void_p),
+                                           max_abs_delta, _ptr(table),
+                                           table.numel() * table.element_size(), _stream(stream)))
+
+
+def pic_rope_llama3_freq(head_dim, theta, factor=8.0, low_freq_factor=1.0, high_freq_factor=4.0,
+                         original_max_position=8192) -> np.ndarray:
+    out = np.zeros(head_dim // 2, np.float64)
+    _check(load().pic_rope_llama3_freq(int(head_dim), float(theta), float(factor), float(low_freq_factor),
+                                       float(high_freq_factor), float(original_max_position),
+                                       out.ctypes.data_as(ctypes.c_void_p)))
+    return out
 
 
 def pic_rerotate_keys(model: Model, k_in, k_out, n_tokens, n_heads, delta, table, max_abs_delta,

@@ -62,8 +62,15 @@ pic_status check_model(const pic_model* m) {
     return fail(PIC_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", m->head_dim);
   if (m->dtype != PIC_F32 && m->dtype != PIC_BF16)
     return fail(PIC_ERR_UNSUPPORTED, "dtype %d", (int)m->dtype);
+  if (m->rope_pairing != PIC_ROPE_HALF && m->rope_pairing != PIC_ROPE_INTERLEAVED)
+    return fail(PIC_ERR_INVALID_ARG, "rope_pairing %d", m->rope_pairing);
+  if (m->rope_tables < 0 || (m->rope_tables > 1 && m->rope_tables != m->n_layers))
+    return fail(PIC_ERR_INVALID_ARG, "rope_tables %d (0, 1 or n_layers = %d)", m->rope_tables,
+                m->n_layers);
   return PIC_OK;
 }
+
+int32_t n_tables(const pic_model* m) { return m->rope_tables > 1 ? m->rope_tables : 1; }
 
 constexpr int32_t kMaxAbsDelta = 1 << 20;
 
@@ -242,14 +249,14 @@ PIC_API pic_status pic_plan_frontier(int32_t batch, const int32_t* n_items, cons
 PIC_API size_t pic_rope_table_bytes(const pic_model* model, int32_t max_abs_delta) {
   if (check_model(model) != PIC_OK) return 0;
   if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta) return 0;
-  return (size_t)(max_abs_delta + 1) * (model->head_dim / 2) * sizeof(float) * 2;
+  return (size_t)n_tables(model) * (max_abs_delta + 1) * (model->head_dim / 2) * sizeof(float) * 2;
 }
 
-PIC_API pic_status pic_rope_table_init(const pic_model* model, int32_t max_abs_delta, void* table,
-                                       size_t table_bytes, void* stream) {
-  PIC_CHECK(check_model(model));
-  if (!(model->rope_theta > 1.0) || !std::isfinite(model->rope_theta))
-    return fail(PIC_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
+namespace {
+
+// Fills every table block from inv_freq (row l for block l, or row 0 for all when `shared`).
+pic_status fill_tables(const pic_model* model, const double* inv_freq, bool shared,
+                       int32_t max_abs_delta, void* table, size_t table_bytes, void* stream) {
   if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
     return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
   PIC_CHECK(check_ptr(table, "table"));
@@ -257,12 +264,72 @@ PIC_API pic_status pic_rope_table_init(const pic_model* model, int32_t max_abs_d
   if (table_bytes < need)
     return fail(PIC_ERR_CAPACITY, "table needs %zu bytes, got %zu", need, table_bytes);
   const int half = model->head_dim / 2;
+  const int64_t block = (int64_t)(max_abs_delta + 1) * half;
+  for (int32_t t = 0; t < n_tables(model); ++t)
+    PIC_CHECK(hip_status(pic::launch_rope_table(inv_freq + (shared ? 0 : (int64_t)t * half), half,
+                                                max_abs_delta,
+                                                static_cast<float2*>(table) + t * block,
+                                                (hipStream_t)stream),
+                         "rope table launch"));
+  return ok();
+}
+
+}  // namespace
+
+PIC_API pic_status pic_rope_table_init(const pic_model* model, int32_t max_abs_delta, void* table,
+                                       size_t table_bytes, void* stream) {
+  PIC_CHECK(check_model(model));
+  if (!(model->rope_theta > 1.0) || !std::isfinite(model->rope_theta))
+    return fail(PIC_ERR_INVALID_ARG, "rope_theta must be finite and > 1");
+  const int half = model->head_dim / 2;
   double inv_freq[64];
   for (int i = 0; i < half; ++i)
     inv_freq[i] = std::pow(model->rope_theta, -2.0 * i / model->head_dim);
-  return hip_status(pic::launch_rope_table(inv_freq, half, max_abs_delta,
-                                           static_cast<float2*>(table), (hipStream_t)stream),
-                    "rope table launch");
+  return fill_tables(model, inv_freq, true, max_abs_delta, table, table_bytes, stream);
+}
+
+PIC_API pic_status pic_rope_table_init_freq(const pic_model* model, const double* inv_freq,
+                                            int32_t max_abs_delta, void* table,
+                                            size_t table_bytes, void* stream) {
+  PIC_CHECK(check_model(model));
+  if (!inv_freq) return fail(PIC_ERR_INVALID_ARG, "inv_freq is NULL");
+  const int64_t n = (int64_t)n_tables(model) * (model->head_dim / 2);
+  for (int64_t i = 0; i < n; ++i)
+    if (!(inv_freq[i] >= 0.0) || !std::isfinite(inv_freq[i]))
+      return fail(PIC_ERR_INVALID_ARG, "inv_freq[%lld] must be finite and >= 0", (long long)i);
+  return fill_tables(model, inv_freq, false, max_abs_delta, table, table_bytes, stream);
+}
+
+PIC_API pic_status pic_rope_llama3_freq(int32_t head_dim, double theta, double factor,
+                                        double low_freq_factor, double high_freq_factor,
+                                        double original_max_position, double* inv_freq) {
+  if (head_dim != 64 && head_dim != 128)
+    return fail(PIC_ERR_INVALID_ARG, "head_dim %d (supported: 64, 128)", head_dim);
+  if (!inv_freq) return fail(PIC_ERR_INVALID_ARG, "inv_freq is NULL");
+  if (!(theta > 1.0) || !(factor > 0.0) || !(low_freq_factor > 0.0) ||
+      !(high_freq_factor > low_freq_factor) || !(original_max_position > 0.0) ||
+      !std::isfinite(theta) || !std::isfinite(factor) || !std::isfinite(high_freq_factor) ||
+      !std::isfinite(original_max_position))
+    return fail(PIC_ERR_INVALID_ARG, "inconsistent frequency-scaling parameters");
+  const double pi = 3.14159265358979323846;
+  const double long_wave = original_max_position / low_freq_factor;   // divided by factor above
+  const double short_wave = original_max_position / high_freq_factor; // kept below
+  for (int i = 0; i < head_dim / 2; ++i) {
+    const double f = std::pow(theta, -2.0 * i / head_dim);
+    const double wavelength = 2.0 * pi / f;
+    double g;
+    if (wavelength < short_wave) {
+      g = f;
+    } else if (wavelength > long_wave) {
+      g = f / factor;
+    } else {
+      const double t = (original_max_position / wavelength - low_freq_factor) /
+                       (high_freq_factor - low_freq_factor);
+      g = t * f + (1.0 - t) * f / factor;
+    }
+    inv_freq[i] = g;
+  }
+  return ok();
 }
 
 PIC_API pic_status pic_rerotate_keys(const pic_model* model, const void* k_in, void* k_out,
@@ -277,7 +344,8 @@ PIC_API pic_status pic_rerotate_keys(const pic_model* model, const void* k_in, v
   PIC_CHECK(check_ptr(k_out, "k_out"));
   PIC_CHECK(check_ptr(table, "table"));
   if (!delta) return fail(PIC_ERR_INVALID_ARG, "delta is NULL");
-  return hip_status(pic::launch_rerotate(model->dtype, model->head_dim, k_in, k_out,
+  return hip_status(pic::launch_rerotate(model->dtype, model->head_dim,
+                                         model->rope_pairing == PIC_ROPE_INTERLEAVED, k_in, k_out,
                                          n_tokens * n_heads, n_heads, delta,
                                          static_cast<const float2*>(table), max_abs_delta,
                                          (hipStream_t)stream),
@@ -302,11 +370,13 @@ PIC_API pic_status pic_compose(const pic_model* model, const void* pool_k, const
   PIC_CHECK(check_ptr(cache_v, "cache_v"));
   PIC_CHECK(check_ptr(table, "table"));
   if (!blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
-  return hip_status(pic::launch_compose(model->dtype, model->head_dim, model->n_layers,
-                                        model->n_kv_heads, pool_k, pool_v, pool_tokens, blocks,
-                                        n_blocks, static_cast<const float2*>(table),
-                                        max_abs_delta, cache_k, cache_v, batch, cache_cap,
-                                        (hipStream_t)stream),
+  const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+  return hip_status(pic::launch_compose(model->dtype, model->head_dim,
+                                        model->rope_pairing == PIC_ROPE_INTERLEAVED,
+                                        model->n_layers, model->n_kv_heads, pool_k, pool_v,
+                                        pool_tokens, blocks, n_blocks,
+                                        static_cast<const float2*>(table), stride, max_abs_delta,
+                                        cache_k, cache_v, batch, cache_cap, (hipStream_t)stream),
                     "compose launch");
 }
 

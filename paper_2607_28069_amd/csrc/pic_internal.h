@@ -30,15 +30,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 hipError_t launch_rope_table(const double* inv_freq_host, int half, int32_t max_abs_delta,
                              float2* table, hipStream_t stream);
 
-hipError_t launch_rerotate(pic_dtype dt, int head_dim, const void* k_in, void* k_out,
-                           int64_t n_rows, int32_t n_heads, const int32_t* delta,
+hipError_t launch_rerotate(pic_dtype dt, int head_dim, bool interleaved, const void* k_in,
+                           void* k_out, int64_t n_rows, int32_t n_heads, const int32_t* delta,
                            const float2* table, int32_t max_abs_delta, hipStream_t stream);
 
-hipError_t launch_compose(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
-                          const void* pool_k, const void* pool_v, int64_t pool_tokens,
-                          const pic_block* blocks, int32_t n_blocks, const float2* table,
-                          int32_t max_abs_delta, void* cache_k, void* cache_v, int32_t batch,
-                          int32_t cache_cap, hipStream_t stream);
+// table_stride: float2 entries between consecutive layers' tables (0: one shared table).
+hipError_t launch_compose(pic_dtype dt, int head_dim, bool interleaved, int n_layers,
+                          int n_kv_heads, const void* pool_k, const void* pool_v,
+                          int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                          const float2* table, int64_t table_stride, int32_t max_abs_delta,
+                          void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
+                          hipStream_t stream);
 
 // Logical position (= cache slot) of row i of request b among n per-request rows (suffix
 // tokens, inline tokens, a decode token): either base[b] clamped to [0, max_base], plus

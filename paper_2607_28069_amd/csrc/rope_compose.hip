@@ -1,14 +1,16 @@
 // RoPE relocation of cached keys and composition of document caches (Sec. 2, Eq. 3; App. C.1).
 //
 // A key compiled at position a moves to position b by R(b) R(a)^-1 = R(b - a): each pair
-// (x_i, x_{i+D/2}) turns by delta * theta_i.  Both positions run contiguously through a
-// document, so one delta serves a whole gather block and its cos/sin row is loaded once per
-// workgroup from a table built in float64.  Values are copied unchanged.
+// turns by delta * theta_i.  Both positions run contiguously through a document, so one delta
+// serves a whole gather block and its cos/sin row is loaded once per workgroup from a table
+// built in float64 (one table, or one per layer for a layer-specific transform).  Values are
+// copied unchanged.
 //
 // Memory traffic is the whole cost (6 flops per 2 elements), so every access is a 16-byte
-// vector and a row of D elements is split across lanes such that one lane owns element
-// chunk [c, c + VEC) of both halves: the two members of every rotated pair sit in the
-// same lane.
+// vector and a row of D elements is split across lanes such that the two members of every
+// rotated pair sit in the same lane: for the rotate-half pairing (x_i, x_{i+D/2}) a lane owns
+// element chunk [c, c + VEC) of both halves; for the interleaved pairing (x_2i, x_2i+1) it
+// owns the 2 VEC consecutive elements of pairs [c, c + VEC).
 #include "pic_internal.h"
 
 namespace pic {
@@ -80,23 +82,44 @@ __device__ __forceinline__ void load_cs(const float2* table, int32_t delta, int 
   }
 }
 
-template <int VEC>
+__device__ __forceinline__ void turn(float& a, float& b, float c, float s) {
+  const float x = a, y = b;
+  a = fmaf(x, c, -(y * s));
+  b = fmaf(x, s, y * c);
+}
+
+// Pair i of the lane's VEC pairs turned by (cs[i], sn[i]).  IL = false: pair i is
+// (x1[i], x2[i]) (rotate-half chunks); IL = true: x1, x2 are consecutive elements and pair i
+// is elements (2i, 2i + 1) of their concatenation.
+template <int VEC, bool IL>
 __device__ __forceinline__ void rotate(float (&x1)[VEC], float (&x2)[VEC], const float (&cs)[VEC],
                                        const float (&sn)[VEC]) {
 #pragma unroll
   for (int i = 0; i < VEC; ++i) {
-    const float a = x1[i], b = x2[i];
-    x1[i] = fmaf(a, cs[i], -(b * sn[i]));
-    x2[i] = fmaf(a, sn[i], b * cs[i]);
+    if constexpr (IL) {
+      float* x = i < VEC / 2 ? x1 : x2;
+      const int e = 2 * (i % (VEC / 2));
+      turn(x[e], x[e + 1], cs[i], sn[i]);
+    } else {
+      turn(x1[i], x2[i], cs[i], sn[i]);
+    }
   }
 }
 
+// Element offsets of the lane's two 16-byte vectors for pair chunk c0 (see rotate()).
+template <int VEC, int HALF, bool IL>
+__device__ __forceinline__ int off1(int c0) { return IL ? 2 * c0 : c0; }
+template <int VEC, int HALF, bool IL>
+__device__ __forceinline__ int off2(int c0) { return IL ? 2 * c0 + VEC : HALF + c0; }
+
 // grid (n_blocks, Hkv, L), 256 threads.  One workgroup moves one gather block of one kv head.
-template <typename T, int HD>
+// Layer l reads its cos/sin from table + l * table_stride (0: one table for all layers).
+template <typename T, int HD, bool IL>
 __global__ void __launch_bounds__(256) compose_kernel(
     const T* __restrict__ pool_k, const T* __restrict__ pool_v, int64_t pool_tokens,
-    const pic_block* __restrict__ blocks, const float2* __restrict__ table, int32_t max_abs_delta,
-    T* __restrict__ cache_k, T* __restrict__ cache_v, int32_t batch, int32_t cache_cap) {
+    const pic_block* __restrict__ blocks, const float2* __restrict__ table, int64_t table_stride,
+    int32_t max_abs_delta, T* __restrict__ cache_k, T* __restrict__ cache_v, int32_t batch,
+    int32_t cache_cap) {
   using V = Vec16<T>;
   constexpr int VEC = V::N;
   constexpr int HALF = HD / 2;
@@ -117,7 +140,8 @@ __global__ void __launch_bounds__(256) compose_kernel(
   const int c0 = j * VEC;
 
   float cs[VEC], sn[VEC];
-  load_cs<VEC, HALF>(table, blk.delta, c0, cs, sn);
+  load_cs<VEC, HALF>(table + l * table_stride, blk.delta, c0, cs, sn);
+  const int o1 = off1<VEC, HALF, IL>(c0), o2 = off2<VEC, HALF, IL>(c0);
 
   const int64_t src_row0 = ((int64_t)l * Hkv + h) * pool_tokens + blk.src_token;
   const int64_t dst_row0 = (((int64_t)l * batch + blk.request) * Hkv + h) * cache_cap + blk.dst_slot;
@@ -128,28 +152,28 @@ __global__ void __launch_bounds__(256) compose_kernel(
     const int t = r0 + p * RPP;
     if (t < blk.n_tokens) {
       const int64_t s = (src_row0 + t) * HD;
-      V::load(pool_k + s + c0, k1[p]);
-      V::load(pool_k + s + HALF + c0, k2[p]);
-      V::load(pool_v + s + c0, v1[p]);
-      V::load(pool_v + s + HALF + c0, v2[p]);
+      V::load(pool_k + s + o1, k1[p]);
+      V::load(pool_k + s + o2, k2[p]);
+      V::load(pool_v + s + o1, v1[p]);
+      V::load(pool_v + s + o2, v2[p]);
     }
   }
 #pragma unroll
   for (int p = 0; p < PASSES; ++p) {
     const int t = r0 + p * RPP;
     if (t < blk.n_tokens) {
-      rotate<VEC>(k1[p], k2[p], cs, sn);
+      rotate<VEC, IL>(k1[p], k2[p], cs, sn);
       const int64_t d = (dst_row0 + t) * HD;
-      V::store(cache_k + d + c0, k1[p]);
-      V::store(cache_k + d + HALF + c0, k2[p]);
-      V::store(cache_v + d + c0, v1[p]);
-      V::store(cache_v + d + HALF + c0, v2[p]);
+      V::store(cache_k + d + o1, k1[p]);
+      V::store(cache_k + d + o2, k2[p]);
+      V::store(cache_v + d + o1, v1[p]);
+      V::store(cache_v + d + o2, v2[p]);
     }
   }
 }
 
 // rows [n_tokens][n_heads][HD]; one (row, chunk) per thread, grid-stride.
-template <typename T, int HD>
+template <typename T, int HD, bool IL>
 __global__ void __launch_bounds__(256) rerotate_kernel(const T* k_in, T* k_out, int64_t n_rows,
                                                        int32_t n_heads, const int32_t* __restrict__ delta,
                                                        const float2* __restrict__ table,
@@ -167,11 +191,12 @@ __global__ void __launch_bounds__(256) rerotate_kernel(const T* k_in, T* k_out, 
     d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
     float cs[VEC], sn[VEC], x1[VEC], x2[VEC];
     load_cs<VEC, HALF>(table, d, c0, cs, sn);
-    V::load(k_in + row * HD + c0, x1);
-    V::load(k_in + row * HD + HALF + c0, x2);
-    rotate<VEC>(x1, x2, cs, sn);
-    V::store(k_out + row * HD + c0, x1);
-    V::store(k_out + row * HD + HALF + c0, x2);
+    const int o1 = off1<VEC, HALF, IL>(c0), o2 = off2<VEC, HALF, IL>(c0);
+    V::load(k_in + row * HD + o1, x1);
+    V::load(k_in + row * HD + o2, x2);
+    rotate<VEC, IL>(x1, x2, cs, sn);
+    V::store(k_out + row * HD + o1, x1);
+    V::store(k_out + row * HD + o2, x2);
   }
 }
 
@@ -230,30 +255,40 @@ hipError_t launch_rope_table(const double* inv_freq_host, int half, int32_t max_
     else { using T = bf16_t; constexpr int HD = 128; KERNEL_CALL; }                              \
   } while (0)
 
-hipError_t launch_rerotate(pic_dtype dt, int head_dim, const void* k_in, void* k_out,
-                           int64_t n_rows, int32_t n_heads, const int32_t* delta,
+hipError_t launch_rerotate(pic_dtype dt, int head_dim, bool interleaved, const void* k_in,
+                           void* k_out, int64_t n_rows, int32_t n_heads, const int32_t* delta,
                            const float2* table, int32_t max_abs_delta, hipStream_t stream) {
   if (n_rows == 0) return hipSuccess;
   PIC_DISPATCH_TD(dt, head_dim, {
     constexpr int LPR = HD / 2 / (16 / (int)sizeof(T));
-    hipLaunchKernelGGL((rerotate_kernel<T, HD>), dim3(grid_for(n_rows * LPR, 256)), dim3(256), 0,
-                       stream, (const T*)k_in, (T*)k_out, n_rows, n_heads, delta, table,
-                       max_abs_delta);
+    const dim3 grid(grid_for(n_rows * LPR, 256));
+    if (interleaved)
+      hipLaunchKernelGGL((rerotate_kernel<T, HD, true>), grid, dim3(256), 0, stream, (const T*)k_in,
+                         (T*)k_out, n_rows, n_heads, delta, table, max_abs_delta);
+    else
+      hipLaunchKernelGGL((rerotate_kernel<T, HD, false>), grid, dim3(256), 0, stream, (const T*)k_in,
+                         (T*)k_out, n_rows, n_heads, delta, table, max_abs_delta);
   });
   return hipGetLastError();
 }
 
-hipError_t launch_compose(pic_dtype dt, int head_dim, int n_layers, int n_kv_heads,
-                          const void* pool_k, const void* pool_v, int64_t pool_tokens,
-                          const pic_block* blocks, int32_t n_blocks, const float2* table,
-                          int32_t max_abs_delta, void* cache_k, void* cache_v, int32_t batch,
-                          int32_t cache_cap, hipStream_t stream) {
+hipError_t launch_compose(pic_dtype dt, int head_dim, bool interleaved, int n_layers,
+                          int n_kv_heads, const void* pool_k, const void* pool_v,
+                          int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                          const float2* table, int64_t table_stride, int32_t max_abs_delta,
+                          void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
+                          hipStream_t stream) {
   if (n_blocks == 0 || n_layers == 0) return hipSuccess;
   const dim3 grid(n_blocks, n_kv_heads, n_layers);
   PIC_DISPATCH_TD(dt, head_dim, {
-    hipLaunchKernelGGL((compose_kernel<T, HD>), grid, dim3(256), 0, stream, (const T*)pool_k,
-                       (const T*)pool_v, pool_tokens, blocks, table, max_abs_delta, (T*)cache_k,
-                       (T*)cache_v, batch, cache_cap);
+    if (interleaved)
+      hipLaunchKernelGGL((compose_kernel<T, HD, true>), grid, dim3(256), 0, stream,
+                         (const T*)pool_k, (const T*)pool_v, pool_tokens, blocks, table,
+                         table_stride, max_abs_delta, (T*)cache_k, (T*)cache_v, batch, cache_cap);
+    else
+      hipLaunchKernelGGL((compose_kernel<T, HD, false>), grid, dim3(256), 0, stream,
+                         (const T*)pool_k, (const T*)pool_v, pool_tokens, blocks, table,
+                         table_stride, max_abs_delta, (T*)cache_k, (T*)cache_v, batch, cache_cap);
   });
   return hipGetLastError();
 }

@@ -240,3 +240,39 @@ def test_sizes(lib):
     assert pic.pic_decode_workspace_bytes(m, 64, 16640, 3) == 64 * 32 * 3 * 130 * 4
     assert pic.pic_decode_auto_splits(m, 1, 16640) > 1
     assert pic.pic_prefill_workspace_bytes(_model(dtype="f32", head_dim=64), 1, 16, 272) == 0
+
+
+def test_rotary_variant_arguments(lib):
+    m = _model(n_layers=3)
+    one = pic.pic_rope_table_bytes(m, 100)
+    assert one == 101 * 64 * 8
+    per_layer = pic.Model.of(3, 32, 8, 128, "bf16", 5e5, per_layer_tables=True)
+    assert pic.pic_rope_table_bytes(per_layer, 100) == 3 * one
+    assert per_layer.with_layers(1).rope_tables == 1
+    bad = pic.Model.of(3, 32, 8, 128, "bf16", 5e5)
+    bad.rope_tables = 2                                   # neither 1 nor n_layers
+    assert pic.pic_rope_table_bytes(bad, 100) == 0
+    assert _compose(lib, bad) == -1
+    bad = pic.Model.of(1, 32, 8, 128, "bf16", 5e5)
+    bad.rope_pairing = 2
+    assert _compose(lib, bad) == -1
+    f = np.full(64, 0.5)
+    f[3] = np.nan
+    st_ = lib.pic_rope_table_init_freq(ctypes.byref(m), f.ctypes.data_as(ctypes.c_void_p), 10, FAKE,
+                                       1 << 20, None)
+    assert st_ == -1 and "inv_freq[3]" in pic.pic_last_error()
+    with pytest.raises(pic.PicError):
+        pic.pic_rope_llama3_freq(128, 5e5, 8.0, 4.0, 1.0)  # high_freq_factor <= low_freq_factor
+
+
+def test_llama3_frequencies_match_transformers_and_oracle(lib):
+    from transformers import LlamaConfig
+    from transformers.modeling_rope_utils import ROPE_INIT_FUNCTIONS
+    cfg = LlamaConfig(hidden_size=4096, num_attention_heads=32, rope_theta=5e5,
+                      max_position_embeddings=131072,
+                      rope_scaling={"rope_type": "llama3", "factor": 8.0, "low_freq_factor": 1.0,
+                                    "high_freq_factor": 4.0, "original_max_position_embeddings": 8192})
+    ref, _ = ROPE_INIT_FUNCTIONS["llama3"](cfg, "cpu")
+    got = pic.pic_rope_llama3_freq(128, 5e5)
+    np.testing.assert_allclose(got, ref.double().numpy(), rtol=2e-6, atol=0)
+    np.testing.assert_allclose(got, O.llama3_inv_freq(128, 5e5), rtol=1e-14, atol=0)
