@@ -119,7 +119,8 @@ class DeviceWorkload:
             self.max_len = self.max_ctx + Ls
             self.pairs = int(sum(Ls * int(c) + Ls * (Ls + 1) // 2 for c in self.ctx_host))
         self.cap = self.max_len + n_dec
-        self.model = pic.Model.of(L, Hq, Hkv, D, w.dtype, w.rope_theta)
+        self.model = pic.Model.of(L, Hq, Hkv, D, w.dtype, w.rope_theta, pairing=w.rope_pairing,
+                                  per_layer_tables=w.per_layer_rope)
         self.m1 = self.model.with_layers(1)
 
         def per_layer(tensor, shape):
@@ -143,7 +144,15 @@ class DeviceWorkload:
         self.mad = self.cap
         self.table = torch.empty(pic.pic_rope_table_bytes(self.model, self.mad) // 4, dtype=torch.float32,
                                  device=dev)
-        pic.pic_rope_table_init(self.model, self.mad, self.table)
+        if w.rope_scaling == "llama3":
+            pic.pic_rope_table_init_freq(self.model, pic.pic_rope_llama3_freq(D, w.rope_theta), self.mad,
+                                         self.table)
+        elif w.per_layer_rope:   # theta_i = base^(-2i/D) with each layer's base
+            i = np.arange(D // 2, dtype=np.float64)
+            freqs = np.stack([w.layer_theta(l) ** (-2.0 * i / D) for l in range(L)])
+            pic.pic_rope_table_init_freq(self.model, freqs, self.mad, self.table)
+        else:
+            pic.pic_rope_table_init(self.model, self.mad, self.table)
         self.ctx_dev = torch.from_numpy(self.ctx_host.astype(np.int32)).to(dev)
         self.base_dev = torch.from_numpy(self.length_host.astype(np.int32)).to(dev)
         self.max_base = self.max_len
@@ -245,6 +254,9 @@ def cpu_baseline(w, budget_s):
 
     lay = S.pool_layout(w)
     inp = S.host_layer(w, lay, 0)
+    rope = {"pairing": w.rope_pairing,
+            "freqs": O.llama3_inv_freq(w.head_dim, w.rope_theta) if w.rope_scaling == "llama3"
+            else O.inv_freq(w.head_dim, w.layer_theta(0))}
     samples = []
     t_end = time.perf_counter() + budget_s
     b = 0
@@ -253,11 +265,11 @@ def cpu_baseline(w, budget_s):
         r = b % w.batch
         if w.frontier:
             f = O.plan_frontier([lay.items[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
-            K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], f.cached, w.rope_theta, w.dtype)
+            K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], f.cached, w.rope_theta, w.dtype, **rope)
             O.frontier_prefill(K, V, f, inp["q"][r], inp["k_suf"][r], inp["v_suf"][r])
         else:
             m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
-            K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], m, w.rope_theta, w.dtype)
+            K, V = O.compose_request(inp["pool_k_raw"], inp["pool_v"], m, w.rope_theta, w.dtype, **rope)
             if w.n_suffix:
                 O.suffix_prefill(K, V, inp["q"][r], inp["k_suf"][r], inp["v_suf"][r])
         samples.append(time.perf_counter() - t0)
@@ -364,7 +376,10 @@ def main():
                    "suffix_tokens": w.n_suffix, "decode_tokens_per_step": n_dec, "pool_docs": w.pool_docs,
                    "docs_per_request": w.docs_per_request,
                    **({"inline_prefix": w.inline_prefix, "inline_span": w.inline_span,
-                       "inline_tokens": Ls} if w.frontier else {})},
+                       "inline_tokens": Ls} if w.frontier else {}),
+                   **({"rope_pairing": w.rope_pairing, "rope_scaling": w.rope_scaling,
+                       "rope_local_global": w.local_global}
+                      if (w.rope_pairing != "half" or w.rope_scaling or w.local_global) else {})},
         "ttft_ms_batch": ttft_ms,
         "prefill_attn_tflops": kernels["suffix_prefill_attn"]["achieved"],
         "rerotate_compose_gbps": kernels["compose"]["achieved"],

@@ -37,6 +37,13 @@ class Workload:
     # (stored prefix entry, documents back to back, then the n_suffix query tokens).
     inline_prefix: int = 0
     inline_span: int = 0
+    # Reader-side rotary variants: pairing ("half" = (i, i + D/2), "interleaved" = (2i, 2i+1)),
+    # Llama-3.1 frequency scaling ("llama3": factor 8, low/high frequency factors 1/4, original
+    # context 8192), and per-layer bases (local, global, period): layer l uses the global base
+    # when l % period == period - 1, else the local one.
+    rope_pairing: str = "half"
+    rope_scaling: str | None = None
+    local_global: tuple[float, float, int] | None = None
     seed: int = 0
     notes: str = ""
 
@@ -47,6 +54,16 @@ class Workload:
     @property
     def elem_bytes(self) -> int:
         return 4 if self.dtype == "f32" else 2
+
+    @property
+    def per_layer_rope(self) -> bool:
+        return self.local_global is not None
+
+    def layer_theta(self, layer: int) -> float:
+        if self.local_global is None:
+            return self.rope_theta
+        local, glob, period = self.local_global
+        return glob if layer % period == period - 1 else local
 
     @property
     def frontier(self) -> bool:
@@ -103,6 +120,19 @@ WORKLOADS: dict[str, Workload] = {
         prefix_len=0, n_suffix=128, batch=16, inline_prefix=128, inline_span=32,
         notes="the 32-layer Llama shape with an inline 128-token prefix and a 32-token inline span "
               "after each of the 10 documents (576 inline tokens per request)"),
+    # Reader-side rotary variants on the 32-layer Llama shape.
+    "llama31_32layer": Workload(
+        name="llama31_32layer", dtype="bf16", n_layers=32, n_q_heads=32, n_kv_heads=8,
+        head_dim=128, rope_theta=5e5, pool_docs=64, doc_len=1024, docs_per_request=10,
+        prefix_len=128, n_suffix=128, batch=16, rope_scaling="llama3",
+        notes="the 32-layer Llama shape with Llama-3.1 frequency-scaled RoPE"),
+    "interleaved_localglobal_32layer": Workload(
+        name="interleaved_localglobal_32layer", dtype="bf16", n_layers=32, n_q_heads=32,
+        n_kv_heads=8, head_dim=128, rope_theta=1e4, pool_docs=64, doc_len=1024,
+        docs_per_request=10, prefix_len=128, n_suffix=128, batch=16, rope_pairing="interleaved",
+        local_global=(1e4, 1e6, 6),
+        notes="the 32-layer Llama shape with interleaved pairing and per-layer bases "
+              "(1e4 local, 1e6 on every 6th layer)"),
 }
 
 # Short aliases in the order the workloads are listed above.

@@ -25,12 +25,21 @@ def _host(t):
     return t.detach().float().cpu().numpy()
 
 
+def _rope(w, l):
+    """The oracle's rotary transform of layer l of workload w (pairing and frequencies)."""
+    if w.rope_scaling == "llama3":
+        f = O.llama3_inv_freq(w.head_dim, w.rope_theta)
+    else:
+        f = O.inv_freq(w.head_dim, w.layer_theta(l))
+    return {"pairing": w.rope_pairing, "freqs": f}
+
+
 def _check_request(wl, l, r, tokens=None, decode_steps=0):
     w = wl.w
     lay = wl.lay
     m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
     pool_k, pool_v = _host(wl.pool_k[l]), _host(wl.pool_v[l])
-    K, V = O.compose_request(pool_k, pool_v, m, w.rope_theta, w.dtype)
+    K, V = O.compose_request(pool_k, pool_v, m, w.rope_theta, w.dtype, **_rope(w, l))
     n = m.ctx_len
     ck = _host(wl.cache_k[l, r])
     cv = _host(wl.cache_v[l, r])
@@ -89,7 +98,7 @@ def _check_compose_all_requests(wl, l):
     pool_k, pool_v = _host(wl.pool_k[l]), _host(wl.pool_v[l])
     for r in range(w.batch):
         m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
-        K, V = O.compose_request(pool_k, pool_v, m, w.rope_theta, w.dtype)
+        K, V = O.compose_request(pool_k, pool_v, m, w.rope_theta, w.dtype, **_rope(w, l))
         n = m.ctx_len
         assert np.array_equal(_host(wl.cache_v[l, r])[:, :n].view(np.uint32), V.view(np.uint32)), r
         assert assert_keys_close(_host(wl.cache_k[l, r])[:, :n], K, w.dtype) > 0.999, r
@@ -198,3 +207,19 @@ def test_llama8b_frontier_32layer_bench_shape():
         dref, _, _ = O.decode_step(K, V, T, _host(wl.dq[l, r]), _host(wl.dk[l, r]), _host(wl.dv[l, r]))
         assert_attn_close(_host(wl.dout[0, l, r]), dref, w.dtype)
         print(f"[frontier] layer {l} request {r} ok", flush=True)
+
+
+@pytest.mark.parametrize("name", ["llama31_32layer", "interleaved_localglobal_32layer"])
+def test_rotary_variant_workloads(name):
+    # The 32-layer Llama shape with Llama-3.1 frequency scaling, or with interleaved pairing and
+    # per-layer bases: every request's composed cache on a local and on a global layer, and
+    # attention of one request on the global layer.
+    w = synth.get(name)
+    wl = DeviceWorkload(w, DEV, n_dec=1)
+    wl.step()
+    torch.cuda.synchronize()
+    for l in (0, 5):
+        _check_compose_all_requests(wl, l)
+        print(f"[{name}] layer {l} (base {w.layer_theta(l):g}): all requests composed correctly", flush=True)
+    _check_request(wl, 5, 11, decode_steps=1)
+    print(f"[{name}] layer 5 request 11 ok", flush=True)
