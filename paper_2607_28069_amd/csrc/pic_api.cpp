@@ -448,6 +448,68 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
                     "prefill attention launch");
 }
 
+PIC_API size_t pic_paged_prefill_workspace_bytes(const pic_model* model, int32_t batch,
+                                                 int32_t n_suffix, int32_t max_ctx) {
+  if (check_attn_model(model) != PIC_OK || batch < 0 || n_suffix < 0 || max_ctx < 0) return 0;
+  if (model->dtype != PIC_BF16) return 0;
+  return pic::prefill_bf16_paged_workspace(shape_of(model, batch, max_ctx + n_suffix, 0.f),
+                                           n_suffix, max_ctx);
+}
+
+PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* pool_k,
+                                          const void* pool_v, int64_t pool_tokens,
+                                          const pic_block* blocks, int32_t n_blocks,
+                                          const void* table, int32_t max_abs_delta, const void* q,
+                                          const void* k_suf, const void* v_suf, void* cache_k,
+                                          void* cache_v, int32_t batch, int32_t cache_cap,
+                                          const int32_t* ctx_len, int32_t max_ctx,
+                                          int32_t n_suffix, float scale, void* out,
+                                          void* workspace, size_t ws_bytes, void* stream) {
+  PIC_CHECK(check_attn_model(model));
+  if (model->dtype != PIC_BF16)
+    return fail(PIC_ERR_UNSUPPORTED, "the paged prefill is built for bf16 caches");
+  if (batch < 0 || cache_cap < 0 || max_ctx < 0 || n_suffix < 0 || pool_tokens < 0 || n_blocks < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (!(scale >= 0.f) || !std::isfinite(scale))
+    return fail(PIC_ERR_INVALID_ARG, "scale must be finite and >= 0");
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
+    return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
+  if ((int64_t)max_ctx + n_suffix > cache_cap)
+    return fail(PIC_ERR_CAPACITY, "max_ctx + n_suffix = %lld exceeds cache_cap %d",
+                (long long)max_ctx + n_suffix, cache_cap);
+  if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX)
+    return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
+  if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
+  PIC_CHECK(check_ptr(pool_k, "pool_k"));
+  PIC_CHECK(check_ptr(pool_v, "pool_v"));
+  PIC_CHECK(check_ptr(table, "table"));
+  PIC_CHECK(check_ptr(q, "q"));
+  PIC_CHECK(check_ptr(k_suf, "k_suf"));
+  PIC_CHECK(check_ptr(v_suf, "v_suf"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  PIC_CHECK(check_ptr(out, "out"));
+  if (n_blocks > 0 && !blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
+  if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
+  const size_t need = pic_paged_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
+  if (workspace == nullptr || ws_bytes < need)
+    return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  PIC_CHECK(check_ptr(workspace, "workspace"));
+  const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
+  const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+  return hip_status(pic::launch_prefill_bf16_paged(
+                        s, model->rope_pairing == PIC_ROPE_INTERLEAVED,
+                        static_cast<const pic::bf16_t*>(q), static_cast<const pic::bf16_t*>(k_suf),
+                        static_cast<const pic::bf16_t*>(v_suf), static_cast<pic::bf16_t*>(cache_k),
+                        static_cast<pic::bf16_t*>(cache_v), ctx_len, max_ctx, n_suffix,
+                        static_cast<const pic::bf16_t*>(pool_k),
+                        static_cast<const pic::bf16_t*>(pool_v), pool_tokens, blocks, n_blocks,
+                        static_cast<const float2*>(table), stride, max_abs_delta,
+                        static_cast<pic::bf16_t*>(out), workspace, ws_bytes, (hipStream_t)stream),
+                    "paged prefill launch");
+}
+
 PIC_API size_t pic_frontier_workspace_bytes(const pic_model* model, int32_t batch,
                                             int32_t n_inline, int32_t max_len) {
   if (check_attn_model(model) != PIC_OK || batch < 0 || n_inline < 0 || max_len < 0) return 0;

@@ -31,6 +31,11 @@
 //  * The suffix's own keys/values are read straight from k_suf / v_suf; one workgroup per
 //    (request, kv head) also stores them into cache slots [ctx, ctx + n_suffix) (no separate
 //    append launch, and no workgroup reads those slots from the cache).
+//  * Paged mode (zero-copy composition): the documents' rows come straight from the pool
+//    through the token-level slot map (pool token and position shift of every context slot),
+//    and each wave turns the key rows it loaded by their shift (Eq. 3) in LDS, with the same
+//    float32 arithmetic and rounding as the compose kernel, before the tile is used; the
+//    composed cache is not written.
 #include <climits>
 #include <type_traits>
 
@@ -79,6 +84,16 @@ __device__ __forceinline__ int v_off(int key, int c) { return key * kRowBytes + 
 //  * table (general frontier layout): token i at q_pos[b * n_suffix + i] for i < n_valid[b];
 //    every visible slot, the tokens' own included, is already in the cache.
 struct PrefillArgs {
+  // paged mode: the pool, the slot map and the delta-angle table
+  const bf16_t* pool_k;     // [L][Hkv][pool_tokens][D]
+  const bf16_t* pool_v;
+  int64_t pool_tokens;
+  const int32_t* smap;      // [B][map_cap] pool token of each context slot
+  const int32_t* dmap;      // [B][map_cap] position shift of each context slot
+  int32_t map_cap;
+  const float2* table;      // [L or 1][max_abs_delta + 1][D/2]
+  int64_t table_stride;
+  int32_t max_abs_delta;
   const bf16_t* q;
   const bf16_t* k_suf;      // [L][B][n_suffix][Hkv][D]
   const bf16_t* v_suf;
@@ -100,15 +115,20 @@ struct PrefillArgs {
   float scale_log2;
 };
 
-template <bool kTable>
+constexpr int kModeSuffix = 0, kModeTable = 1, kModePaged = 2;
+
+template <int kMode, bool kInterleaved>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_bf16_kernel(PrefillArgs a) {
+  constexpr bool kTable = kMode == kModeTable, kPaged = kMode == kModePaged;
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
   // loads in flight into one buffer do not alias reads from another.
   __shared__ __attribute__((aligned(16))) uint8_t k_lds0[kTileBytes];
   __shared__ __attribute__((aligned(16))) uint8_t k_lds1[kTileBytes];
   __shared__ __attribute__((aligned(16))) uint8_t v_lds0[kTileBytes];
   __shared__ __attribute__((aligned(16))) uint8_t v_lds1[kTileBytes];
+  // paged mode: each wave's cos/sin of the key rows it turns (4 KB per wave)
+  __shared__ __attribute__((aligned(16))) uint8_t cs_lds[kPaged ? kWaves * 4096 : 16];
 
   // XCD-aware block order: hardware block w runs on XCD w % 8; give each XCD a contiguous
   // range of logical blocks so the m-tiles of one (request, kv head) share an L2.
@@ -175,6 +195,7 @@ prefill_bf16_kernel(PrefillArgs a) {
     ctx = pos_max_wg + 1;   // every visible key is in the cache
   }
   const int n_keys = kTable ? pos_max_wg + 1 : ctx + a.n_suffix;
+  const int ld_row = 4 * wave + (lane >> 4), ld_slot = lane & 15;   // load row within a step
   // this workgroup's key tiles: [t0, t0 + n_tiles) of the (pos_max_wg + 1) visible keys
   const int t0 = split * a.tiles_per_split;
   const int n_tiles = min((pos_max_wg + kKeys) / kKeys - t0, a.tiles_per_split);
@@ -217,13 +238,61 @@ prefill_bf16_kernel(PrefillArgs a) {
   // slot.  The swizzles use key bits 0..3 (K) and 0..1 (V), which do not change with i, so
   // each lane's source offset within one step is a constant.  Rows past the last key (only in the last
   // tile) are clamped to it: their scores are masked, so they enter PV with probability 0.
-  const int ld_row = 4 * wave + (lane >> 4), ld_slot = lane & 15;   // row within a step
   const int k_goff = ld_row * kHD + 8 * (ld_slot ^ k_swz(ld_row));   // elements
   const int v_goff = ld_row * kHD + 8 * (ld_slot ^ v_swz(ld_row));
   const int v_gc = ld_slot ^ v_swz(ld_row), k_gc = ld_slot ^ k_swz(ld_row);
+  // paged mode: pool rows of this (layer, kv head), and the slot map of this request
+  const bf16_t* PKg = kPaged ? a.pool_k + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
+  const bf16_t* PVg = kPaged ? a.pool_v + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
+  const int32_t* smap = kPaged ? a.smap + (int64_t)b * a.map_cap : nullptr;
+  const int32_t* dmap = kPaged ? a.dmap + (int64_t)b * a.map_cap : nullptr;
+  // pool token of load row i (0, 1) of global tile t for this lane (0 past the context)
+  auto map_src = [&](int t, int i) {
+    const int p = t * kKeys + 4 * kWaves * i + ld_row;
+    int32_t v = p < ctx ? smap[p] : 0;
+    return v < 0 ? 0 : (v >= a.pool_tokens ? (int32_t)(a.pool_tokens - 1) : v);
+  };
+  // rotation item of this lane: row 32 i + 4 w + rr (i = lane / 32, rr = (lane / 8) % 4) of
+  // the wave's own load rows, 16-byte chunks c and c + 8 (c = lane % 8)
+  const int rot_row = 32 * (lane >> 5) + 4 * wave + ((lane >> 3) & 3), rot_c = lane & 7;
+  auto map_delta = [&](int t) {   // shift of this lane's rotation row of global tile t (0 past the context)
+    const int p = t * kKeys + rot_row;
+    int32_t d = p < ctx ? dmap[p] : 0;
+    return d < -a.max_abs_delta ? -a.max_abs_delta : (d > a.max_abs_delta ? a.max_abs_delta : d);
+  };
+  // cos/sin of the lane's 8 pair frequencies at |delta| into this wave's cos/sin area:
+  // instruction j moves float pairs (f_j, f_j + 1) to byte j * 1 KB + 16 * lane
+  auto load_cs = [&](int32_t delta) {
+    const int32_t ad = delta < 0 ? -delta : delta;
+    const float2* row = a.table + (int64_t)l * a.table_stride + (int64_t)ad * (kHD / 2);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      // rotate-half: pairs 8c .. 8c + 7 (chunks c and c + 8); interleaved: pairs 4c .. 4c + 3
+      // (chunk c) and 32 + 4c .. 32 + 4c + 3 (chunk c + 8)
+      const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : 32 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
+      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + f),
+                                       (LDS_AS void*)(cs_lds + wave * 4096 + j * 1024), 16, 0, 0);
+    }
+  };
+  int32_t src_v[kLoadSteps], src_k[kLoadSteps], src_f[kLoadSteps];   // rows of tiles t+1, t+2, t+3
+  int32_t d_k = 0, d_f = 0;                                            // rotation shift, tiles t+2, t+3
+
   auto load_tile = [&](const bf16_t* src, uint8_t* dst_tile, int t, bool is_v) {
     const int goff = is_v ? v_goff : k_goff;
-    if ((t + 1) * kKeys <= ctx) {
+    if constexpr (kPaged) {
+      const int c = is_v ? v_gc : k_gc;
+      const bf16_t* suf = is_v ? Vs : Ks;
+      const bf16_t* pool = is_v ? PVg : PKg;
+      const int32_t* rows = is_v ? src_v : src_k;
+#pragma unroll
+      for (int i = 0; i < kLoadSteps; ++i) {
+        const int kk = min(t * kKeys + 4 * kWaves * i + ld_row, n_keys - 1);
+        const bf16_t* row = kk < ctx ? pool + (int64_t)rows[i] * kHD : suf + (kk - ctx) * suf_stride;
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + 8 * c),
+                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
+                                         16, 0, 0);
+      }
+    } else if ((t + 1) * kKeys <= ctx) {
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
         const bf16_t* base = src + (int64_t)(t * kKeys + 4 * kWaves * i) * kHD;   // uniform
@@ -244,6 +313,51 @@ prefill_bf16_kernel(PrefillArgs a) {
                                          16, 0, 0);
       }
     }
+  };
+  // Paged mode: turn this lane's item of the wave's own rows of K tile t (in `kt`, landed)
+  // by its shift, as the compose kernel does: fp32 x cos - y sin, x sin + y cos, rounded to
+  // bf16.  Context rows only: suffix rows and clamped rows stay as loaded.
+  auto rotate_own = [&](uint8_t* kt, int t, int32_t delta) {
+    if (t * kKeys + rot_row >= ctx) return;
+    uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz(rot_row)) << 4);
+    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz(rot_row)) << 4);
+    const u32x4 w1 = *reinterpret_cast<const u32x4*>(p1);
+    const u32x4 w2 = *reinterpret_cast<const u32x4*>(p2);
+    float cs[8], sn[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float4 v = *reinterpret_cast<const float4*>(cs_lds + wave * 4096 + j * 1024 + 16 * lane);
+      cs[2 * j] = v.x;
+      sn[2 * j] = delta < 0 ? -v.y : v.y;
+      cs[2 * j + 1] = v.z;
+      sn[2 * j + 1] = delta < 0 ? -v.w : v.w;
+    }
+    float x1[8], x2[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x1[2 * e] = __uint_as_float(w1[e] << 16);
+      x1[2 * e + 1] = __uint_as_float(w1[e] & 0xFFFF0000u);
+      x2[2 * e] = __uint_as_float(w2[e] << 16);
+      x2[2 * e + 1] = __uint_as_float(w2[e] & 0xFFFF0000u);
+    }
+    auto turn = [](float& u, float& v, float c, float s) {
+      const float x = u, y = v;
+      u = fmaf(x, c, -(y * s));
+      v = fmaf(x, s, y * c);
+    };
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if constexpr (kInterleaved) {   // pairs (2e, 2e + 1) of each chunk; chunk c+8 uses cs[4..7]
+        float* x = k < 4 ? x1 : x2;
+        turn(x[2 * (k & 3)], x[2 * (k & 3) + 1], cs[k], sn[k]);
+      } else {
+        turn(x1[k], x2[k], cs[k], sn[k]);
+      }
+    }
+    *reinterpret_cast<u32x4*>(p1) = u32x4{pack_bf16x2(x1[0], x1[1]), pack_bf16x2(x1[2], x1[3]),
+                                         pack_bf16x2(x1[4], x1[5]), pack_bf16x2(x1[6], x1[7])};
+    *reinterpret_cast<u32x4*>(p2) = u32x4{pack_bf16x2(x2[0], x2[1]), pack_bf16x2(x2[2], x2[3]),
+                                         pack_bf16x2(x2[4], x2[5]), pack_bf16x2(x2[6], x2[7])};
   };
   auto wait_loads = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };   // vmcnt(0)
 
@@ -324,11 +438,42 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
   };
 
-  // ---- prologue: K0, V0, K1 resident; scores of tile 0
-  load_tile(Kg, k_lds0, t0, false);
-  load_tile(Vg, v_lds0, t0, true);
-  if (n_tiles > 1) load_tile(Kg, k_lds1, t0 + 1, false);
-  wait_loads();
+  // ---- prologue: K0, V0, K1 resident (paged: turned); scores of tile 0
+  if constexpr (kPaged) {
+#pragma unroll
+    for (int i = 0; i < kLoadSteps; ++i) {
+      src_k[i] = map_src(t0, i);
+      src_v[i] = map_src(t0, i);
+    }
+    d_k = map_delta(t0);
+    wait_loads();
+    load_tile(Kg, k_lds0, t0, false);
+    load_tile(Vg, v_lds0, t0, true);
+    load_cs(d_k);
+#pragma unroll
+    for (int i = 0; i < kLoadSteps; ++i) src_k[i] = map_src(t0 + 1, i);
+    d_f = map_delta(t0 + 1);
+    wait_loads();
+    rotate_own(k_lds0, t0, d_k);
+    if (n_tiles > 1) {
+      load_tile(Kg, k_lds1, t0 + 1, false);
+      load_cs(d_f);
+      // V(t0 + 1) is loaded by tile 0 and K(t0 + 2) by tile 0: their rows
+#pragma unroll
+      for (int i = 0; i < kLoadSteps; ++i) {
+        src_v[i] = src_k[i];
+        src_k[i] = map_src(t0 + 2, i);
+      }
+      d_k = map_delta(t0 + 2);
+      wait_loads();
+      rotate_own(k_lds1, t0 + 1, d_f);
+    }
+  } else {
+    load_tile(Kg, k_lds0, t0, false);
+    load_tile(Vg, v_lds0, t0, true);
+    if (n_tiles > 1) load_tile(Kg, k_lds1, t0 + 1, false);
+    wait_loads();
+  }
   __syncthreads();
   f32x16_t s_a[2], s_b[2];   // scores of the current / next tile, swapped every tile
   scores(k_lds0, s_a);
@@ -348,6 +493,13 @@ prefill_bf16_kernel(PrefillArgs a) {
     uint8_t* const v_free = P ? v_lds0 : v_lds1;   // receives V(t+1)
     if (t + 2 < n_tiles) load_tile(Kg, k_free, t0 + t + 2, false);
     if (t + 1 < n_tiles) load_tile(Vg, v_free, t0 + t + 1, true);
+    if constexpr (kPaged) {
+      if (t + 2 < n_tiles) load_cs(d_k);
+      // the rows of tile t + 3 (K issued by the next tile) and its shifts
+#pragma unroll
+      for (int i = 0; i < kLoadSteps; ++i) src_f[i] = map_src(t0 + t + 3, i);
+      d_f = map_delta(t0 + t + 3);
+    }
 
     // (scores of a tile past the last one are computed on stale LDS and dropped)
     snext[0] = f32x16_t{};
@@ -391,6 +543,15 @@ prefill_bf16_kernel(PrefillArgs a) {
 
     if (t + 1 < n_tiles) finish_scores(t0 + t + 1, snext);
     wait_loads();
+    if constexpr (kPaged) {
+      if (t + 2 < n_tiles) rotate_own(k_free, t0 + t + 2, d_k);
+#pragma unroll
+      for (int i = 0; i < kLoadSteps; ++i) {
+        src_v[i] = src_k[i];
+        src_k[i] = src_f[i];
+      }
+      d_k = d_f;
+    }
     __syncthreads();
   };
 
@@ -507,8 +668,36 @@ size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_
 
 namespace {
 
-hipError_t launch(const AttnShape& s, PrefillArgs a, bool table, int32_t n_q, int32_t max_ctx,
-                  void* workspace, size_t ws_bytes, hipStream_t stream) {
+// Token-level slot map (App. C.1) of the paged mode: every context slot of every request
+// gets the pool token and the position shift of the gather block covering it.
+__global__ void __launch_bounds__(256) map_clear_kernel(int32_t* smap, int32_t* dmap, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    smap[i] = 0;
+    dmap[i] = 0;
+  }
+}
+
+// grid (n_blocks), 64 threads: one gather block per workgroup, invalid blocks skipped.
+__global__ void __launch_bounds__(64) map_expand_kernel(const pic_block* __restrict__ blocks,
+                                                        int32_t batch, int32_t map_cap,
+                                                        int32_t* smap, int32_t* dmap) {
+  const pic_block blk = blocks[blockIdx.x];
+  if (blk.request < 0 || blk.request >= batch || blk.n_tokens <= 0 ||
+      blk.n_tokens > PIC_BLOCK_TOKENS || blk.dst_slot < 0 ||
+      (int64_t)blk.dst_slot + blk.n_tokens > map_cap)
+    return;
+  const int t = threadIdx.x;
+  if (t < blk.n_tokens) {
+    const int64_t i = (int64_t)blk.request * map_cap + blk.dst_slot + t;
+    smap[i] = blk.src_token + t;
+    dmap[i] = blk.delta;
+  }
+}
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved, int32_t n_q,
+                  int32_t max_ctx, void* workspace, size_t ws_bytes, hipStream_t stream) {
   const int n_rep = s.n_q_heads / s.n_kv_heads;
   const int64_t M = (int64_t)n_q * n_rep;
   if (M == 0 || s.batch == 0 || s.n_layers == 0) return hipSuccess;
@@ -530,15 +719,19 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, bool table, int32_t n_q, in
     return hipErrorInvalidValue;
   const int per_xcd = (a.n_wg + kNumXcd - 1) / kNumXcd;
   const dim3 grid(per_xcd * kNumXcd, s.n_layers);
-  if (table)
-    hipLaunchKernelGGL(prefill_bf16_kernel<true>, grid, dim3(kThreads), 0, stream, a);
+  if (mode == kModeTable)
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModePaged && interleaved)
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModePaged, true>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModePaged)
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModePaged, false>), grid, dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(prefill_bf16_kernel<false>, grid, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   hipLaunchKernelGGL(prefill_combine_kernel, dim3((unsigned)((a.rows_total + 3) / 4)), dim3(256), 0,
                      stream, a.ws_o, a.ws_ml, p.n_splits, a.rows_total,
-                     table ? a.n_valid : nullptr, n_q, s.n_q_heads, s.batch, a.out);
+                     mode == kModeTable ? a.n_valid : nullptr, n_q, s.n_q_heads, s.batch, a.out);
   return hipGetLastError();
 }
 
@@ -558,7 +751,7 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
   a.ctx_len = ctx_len;
   a.out = out;
   a.max_ctx = max_ctx;
-  return launch(s, a, false, n_suffix, max_ctx, workspace, ws_bytes, stream);
+  return launch(s, a, kModeSuffix, false, n_suffix, max_ctx, workspace, ws_bytes, stream);
 }
 
 hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,
@@ -574,7 +767,61 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
   a.max_pos = pos.max_pos;
   a.out = out;
   const int32_t max_ctx = max_len > n_q ? max_len - n_q : 0;
-  return launch(s, a, true, n_q, max_ctx, workspace, ws_bytes, stream);
+  return launch(s, a, kModeTable, false, n_q, max_ctx, workspace, ws_bytes, stream);
+}
+
+size_t prefill_bf16_paged_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
+  return align256(prefill_bf16_workspace(s, n_suffix, max_ctx)) +
+         2 * align256((size_t)s.batch * (max_ctx > 0 ? max_ctx : 1) * sizeof(int32_t));
+}
+
+hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const bf16_t* q,
+                                     const bf16_t* k_suf, const bf16_t* v_suf, bf16_t* cache_k,
+                                     bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
+                                     int32_t n_suffix, const bf16_t* pool_k, const bf16_t* pool_v,
+                                     int64_t pool_tokens, const pic_block* blocks,
+                                     int32_t n_blocks, const float2* table, int64_t table_stride,
+                                     int32_t max_abs_delta, bf16_t* out, void* workspace,
+                                     size_t ws_bytes, hipStream_t stream) {
+  if ((int64_t)n_suffix * (s.n_q_heads / s.n_kv_heads) == 0 || s.batch == 0 || s.n_layers == 0)
+    return hipSuccess;
+  if (workspace == nullptr || ws_bytes < prefill_bf16_paged_workspace(s, n_suffix, max_ctx))
+    return hipErrorInvalidValue;
+  const size_t split_ws = align256(prefill_bf16_workspace(s, n_suffix, max_ctx));
+  const int32_t map_cap = max_ctx > 0 ? max_ctx : 1;
+  const size_t map_bytes = align256((size_t)s.batch * map_cap * sizeof(int32_t));
+  int32_t* smap = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + split_ws);
+  int32_t* dmap = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + split_ws + map_bytes);
+  const int64_t n_map = (int64_t)s.batch * map_cap;
+  int64_t g = (n_map + 255) / 256;
+  g = g < 1 ? 1 : (g > 65536 ? 65536 : g);
+  hipLaunchKernelGGL(map_clear_kernel, dim3((unsigned)g), dim3(256), 0, stream, smap, dmap, n_map);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (n_blocks > 0) {
+    hipLaunchKernelGGL(map_expand_kernel, dim3(n_blocks), dim3(64), 0, stream, blocks, s.batch, map_cap,
+                       smap, dmap);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  PrefillArgs a = {};
+  a.pool_k = pool_k;
+  a.pool_v = pool_v;
+  a.pool_tokens = pool_tokens;
+  a.smap = smap;
+  a.dmap = dmap;
+  a.map_cap = map_cap;
+  a.table = table;
+  a.table_stride = table_stride;
+  a.max_abs_delta = max_abs_delta;
+  a.q = q;
+  a.k_suf = k_suf;
+  a.v_suf = v_suf;
+  a.cache_k = cache_k;
+  a.cache_v = cache_v;
+  a.ctx_len = ctx_len;
+  a.out = out;
+  a.max_ctx = max_ctx;
+  return launch(s, a, kModePaged, interleaved, n_suffix, max_ctx, workspace, split_ws, stream);
 }
 
 }  // namespace pic

@@ -1,0 +1,105 @@
+"""GPU parity of the zero-copy (paged) suffix prefill: attention reading the documents' K/V
+straight from the pool through the gather blocks, keys turned on load (App. C.1 token map;
+Sec. 2, Eq. 3).  It computes exactly what compose + suffix prefill compute, with the same
+float32 arithmetic and bf16 rounding, so its outputs must be bit-identical to that path's and
+within the attention tolerance of the oracle; the composed document slots stay untouched.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_28069_amd as pic
+import synth
+from oracle import pic_oracle as O
+from synth import inputs as S
+
+from gpu_path import (DEV, assert_attn_close, gpu_compose, gpu_prefill, host, oracle_prefill, setup,
+                      tdtype, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, layers=1):
+    """Paged prefill of run r on fresh (zeroed) caches; returns (out, cache_k, cache_v)."""
+    w, d, dt = r.w, r.dev, tdtype(r.w)
+    m = model or r.model
+    shape = (layers, w.batch, w.n_kv_heads, r.cap, w.head_dim)
+    ck = torch.zeros(shape, dtype=dt, device=DEV) if cache_k is None else cache_k
+    cv = torch.zeros(shape, dtype=dt, device=DEV) if cache_v is None else cache_v
+    out = torch.zeros((layers, w.batch, w.n_suffix, w.n_q_heads, w.head_dim), dtype=dt, device=DEV)
+    max_ctx = int(r.ctx.max())
+    ws = torch.empty(pic.pic_paged_prefill_workspace_bytes(m, w.batch, w.n_suffix, max_ctx),
+                     dtype=torch.uint8, device=DEV)
+    pic.pic_paged_prefill_attn(m, d["pool_k"] if pool_k is None else pool_k,
+                               d["pool_v"] if pool_v is None else pool_v, r.lay.pool_tokens, d["blocks"],
+                               d["blocks"].numel() // 5, d["table"], d["mad"], d["q"], d["k_suf"], d["v_suf"],
+                               ck, cv, w.batch, r.cap, d["ctx"], max_ctx, w.n_suffix, out, ws)
+    return out, ck, cv
+
+
+def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m):
+    w = r.w
+    assert torch.equal(out_p, out_m), "paged outputs differ from compose + prefill"
+    for b in range(w.batch):
+        c = int(r.ctx[b])
+        sl = slice(c, c + w.n_suffix)
+        assert torch.equal(ck_p[:, b, :, sl], ck_m[:, b, :, sl]) and torch.equal(cv_p[:, b, :, sl], cv_m[:, b, :, sl])
+        assert not ck_p[:, b, :, :c].any() and not cv_p[:, b, :, :c].any(), "document slots were written"
+
+
+@pytest.mark.parametrize("name", ["c2", "ragged"])
+def test_paged_prefill_equals_compose_then_prefill(name):
+    if name == "c2":
+        w = synth.get("c2")
+        r = setup(w)
+    else:   # uneven contexts, a prefix-only request, n_rep 7, tails that are not tile multiples
+        w = dataclasses.replace(synth.get("c2"), name="ragged", n_q_heads=28, n_kv_heads=4, pool_docs=5,
+                                doc_len=77, docs_per_request=4, n_suffix=37, prefix_len=13, batch=3,
+                                doc_len_jitter=(1, 150))
+        lay = S.pool_layout(w)
+        r = setup(w, requests=[[lay.prefix_entry, 3, 0, 4], [lay.prefix_entry], [2, 1, 0, 3, 4]], extra_cap=5)
+    gpu_compose(r)
+    out_m = gpu_prefill(r).clone()
+    out_p, ck_p, cv_p = _paged(r)
+    torch.cuda.synchronize()
+    _check_against_materialized(r, out_p, ck_p, cv_p, r.dev["cache_k"], r.dev["cache_v"], out_m)
+    got = host(out_p)[0]
+    for b in range(w.batch):
+        ref, _, _ = oracle_prefill(r, b)
+        assert_attn_close(got[b], ref, "bf16")
+    print(f"[{name}] paged == materialized, oracle ok (ctx {[int(c) for c in r.ctx]})", flush=True)
+
+
+@pytest.mark.parametrize("pairing", ["half", "interleaved"])
+def test_paged_prefill_with_rotary_variants(pairing):
+    # two layers with their own frequencies in one call; pool layer 1 differs from layer 0
+    w = synth.get("c2")
+    r = setup(w)
+    d = gpu_compose(r)
+    D = w.head_dim
+    m2 = pic.Model.of(2, w.n_q_heads, w.n_kv_heads, D, "bf16", w.rope_theta, pairing=pairing,
+                      per_layer_tables=True)
+    f = np.stack([pic.pic_rope_llama3_freq(D, 5e5), O.inv_freq(D, 1e4)])
+    mad = d["mad"]
+    table = torch.empty(pic.pic_rope_table_bytes(m2, mad) // 4, dtype=torch.float32, device=DEV)
+    pic.pic_rope_table_init_freq(m2, f, mad, table)
+    pk = torch.cat([d["pool_k"], d["pool_k"].flip(-1)], 0).contiguous()
+    pv = torch.cat([d["pool_v"], d["pool_v"] * 2], 0).contiguous()
+    dt = tdtype(w)
+    for name in ("q", "k_suf", "v_suf"):
+        d[name] = torch.cat([to_dev(r.inp[name][None], dt)] * 2, 0).contiguous()
+    shape = (2, w.batch, w.n_kv_heads, r.cap, D)
+    ck_m, cv_m = torch.zeros(shape, dtype=dt, device=DEV), torch.zeros(shape, dtype=dt, device=DEV)
+    pic.pic_compose(m2, pk, pv, r.lay.pool_tokens, d["blocks"], d["blocks"].numel() // 5, table, mad, ck_m, cv_m,
+                    w.batch, r.cap)
+    out_m = torch.zeros((2, w.batch, w.n_suffix, w.n_q_heads, D), dtype=dt, device=DEV)
+    ws = torch.empty(max(pic.pic_prefill_workspace_bytes(m2, w.batch, w.n_suffix, int(r.ctx.max())), 16),
+                     dtype=torch.uint8, device=DEV)
+    pic.pic_suffix_prefill_attn(m2, d["q"], d["k_suf"], d["v_suf"], ck_m, cv_m, w.batch, r.cap, d["ctx"],
+                                int(r.ctx.max()), w.n_suffix, out_m, ws)
+    d["table"] = table
+    out_p, ck_p, cv_p = _paged(r, model=m2, pool_k=pk, pool_v=pv, layers=2)
+    torch.cuda.synchronize()
+    _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m)
