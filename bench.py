@@ -43,6 +43,9 @@ def parse(argv=None):
                    help="decode tokens per step (default: the workload's decode steps, else 1)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    p.add_argument("--paged", action="store_true",
+                   help="zero-copy TTFT: the prefill reads the documents from the pool through the "
+                        "gather map; the composed cache is built after the first token, for decode")
     p.add_argument("--copy-calib-gib", type=float, default=0.0,
                    help="also run a plain device copy of this size per step (counter calibration)")
     return p.parse_args(argv)
@@ -86,7 +89,7 @@ class DeviceWorkload:
     `layers` < w.n_layers builds a workload with fewer layers of the same per-layer shape.
     """
 
-    def __init__(self, w, dev, n_dec: int, layers: int | None = None):
+    def __init__(self, w, dev, n_dec: int, layers: int | None = None, paged: bool = False):
         import numpy as np
         import torch
 
@@ -94,6 +97,7 @@ class DeviceWorkload:
         from synth import inputs as S
 
         self.w, self.dev, self.n_dec = w, dev, n_dec
+        self.paged = paged
         self.L = L = w.n_layers if layers is None else layers
         self.dt = dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
         B, Hq, Hkv, D = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
@@ -160,6 +164,10 @@ class DeviceWorkload:
             nbytes = pic.pic_frontier_workspace_bytes(self.m1, B, Ls, self.max_len)
         else:
             nbytes = pic.pic_prefill_workspace_bytes(self.m1, B, Ls, self.max_ctx)
+        if paged:
+            assert not self.frontier and w.dtype == "bf16", "the paged prefill serves the plain bf16 layout"
+            self.slot_src = torch.empty((B, max(self.max_ctx, 1)), dtype=torch.int32, device=dev)
+            self.slot_delta = torch.empty_like(self.slot_src)
         self.ws_pre = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev)
         self.ws_dec = torch.empty(max(pic.pic_decode_workspace_bytes(self.m1, B, self.max_base + n_dec, 0), 16),
                                   dtype=torch.uint8, device=dev)
@@ -196,15 +204,26 @@ class DeviceWorkload:
             tail.copy_(torch.from_numpy(inl.reshape(-1)))
             self.pos_dev.view(-1).copy_(tail, non_blocking=True)
         e0, e1 = ev(), ev()
-        e0.record(stream)
-        pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
-                        self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
-        e1.record(stream)
+        if not self.paged:
+            e0.record(stream)
+            pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
+                            self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
+            e1.record(stream)
         pre = []
+        block = (self.mad + 1) * (w.head_dim // 2) * 2 if self.model.rope_tables > 1 else 0
+        if self.paged:   # the token-level slot map, shared by every layer
+            pic.pic_build_slot_map(self.blocks_dev, nb, B, self.slot_src.shape[1], self.slot_src,
+                                   self.slot_delta)
         for l in range(L if Ls else 0):
             a, b = ev(), ev()
             a.record(stream)
-            if self.frontier:
+            if self.paged:
+                pic.pic_paged_prefill_attn(self.m1, self.pool_k[l], self.pool_v[l], lay.pool_tokens,
+                                           self.slot_src, self.slot_delta, self.slot_src.shape[1],
+                                           self.table[l * block:], self.mad, self.q[l],
+                                           self.k_suf[l], self.v_suf[l], self.cache_k[l], self.cache_v[l], B,
+                                           self.cap, self.ctx_dev, self.max_ctx, Ls, self.out[l], self.ws_pre)
+            elif self.frontier:
                 pic.pic_frontier_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
                                               self.cache_k[l], self.cache_v[l], B, self.cap,
                                               self.pos_dev, self.n_valid_dev, Ls, self.max_len,
@@ -217,6 +236,11 @@ class DeviceWorkload:
             pre.append((a, b))
         torch.cuda.synchronize()
         t1 = time.perf_counter()
+        if self.paged:   # the composed cache, for decoding, after the first token
+            e0.record(stream)
+            pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
+                            self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
+            e1.record(stream)
         # -- decode
         dec = []
         for t in range(self.n_dec):
@@ -307,7 +331,7 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     n_dec = args.decode_tokens if args.decode_tokens is not None else (w.decode_steps or 1)
-    wl = DeviceWorkload(w, dev, n_dec)
+    wl = DeviceWorkload(w, dev, n_dec, paged=args.paged)
     calib = None
     if args.copy_calib_gib > 0:
         n = int(args.copy_calib_gib * (1 << 30)) // 2
@@ -375,6 +399,8 @@ def main():
                    "context_tokens": ctx[0] if len(set(ctx)) == 1 else ctx,
                    "suffix_tokens": w.n_suffix, "decode_tokens_per_step": n_dec, "pool_docs": w.pool_docs,
                    "docs_per_request": w.docs_per_request,
+                   **({"ttft_path": "paged (zero-copy prefill; cache composed after the first token)"}
+                      if args.paged else {}),
                    **({"inline_prefix": w.inline_prefix, "inline_span": w.inline_span,
                        "inline_tokens": Ls} if w.frontier else {}),
                    **({"rope_pairing": w.rope_pairing, "rope_scaling": w.rope_scaling,

@@ -211,26 +211,32 @@ pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const 
                                    void* workspace, size_t ws_bytes, void* stream);
 
 /* ---- 3c. zero-copy (paged) suffix prefill (App. C.1 token map; Sec. 2, Eq. 3) ----
-   The result of pic_compose followed by pic_suffix_prefill_attn, without writing the composed
-   cache: attention reads the documents' K/V straight from the pool through the gather blocks
-   and turns each key by its block's shift on load (same float32 arithmetic and bf16 rounding
-   as pic_compose, so outputs are bit-identical).  Only the suffix K/V are stored (slots
-   [ctx_len[b], ctx_len[b] + n_suffix)); a later pic_compose fills the document slots for
-   decoding.  bf16 only.
-     pool_k, pool_v, pool_tokens, blocks, n_blocks, table, max_abs_delta  as for pic_compose
+   pic_build_slot_map expands gather blocks into the token-level map from cache slots to the
+   pool: slot_src[b][p] / slot_delta[b][p] = pool token and position shift of slot p of
+   request b ([batch][map_cap] device int32; slots no block covers get 0 / 0; blocks outside
+   batch or map_cap are skipped).  One map serves every layer.
+   pic_paged_prefill_attn computes what pic_compose followed by pic_suffix_prefill_attn
+   computes, without writing the composed cache: attention reads the documents' K/V straight
+   from the pool through the slot map and turns each key by its shift on load (same float32
+   arithmetic and bf16 rounding as pic_compose, so outputs are bit-identical).  Only the
+   suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)); a later pic_compose fills
+   the document slots for decoding.  bf16 only.
+     pool_k, pool_v, pool_tokens, table, max_abs_delta   as for pic_compose
+     slot_src, slot_delta, map_cap   the map; map_cap >= max_ctx (entries are clamped to the
+                                     pool and to max_abs_delta)
      q, k_suf, v_suf, cache_k, cache_v, batch, cache_cap, ctx_len, max_ctx, n_suffix, scale,
-     out  as for pic_suffix_prefill_attn (ctx_len must match the blocks' layout)
-     workspace  pic_paged_prefill_workspace_bytes(...) bytes (never 0: it holds the slot map) */
-size_t pic_paged_prefill_workspace_bytes(const pic_model* model, int32_t batch, int32_t n_suffix,
-                                         int32_t max_ctx);
+     out, workspace   as for pic_suffix_prefill_attn (same workspace size) */
+pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch,
+                              int32_t map_cap, int32_t* slot_src, int32_t* slot_delta,
+                              void* stream);
 pic_status pic_paged_prefill_attn(const pic_model* model, const void* pool_k, const void* pool_v,
-                                  int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
-                                  const void* table, int32_t max_abs_delta, const void* q,
-                                  const void* k_suf, const void* v_suf, void* cache_k,
-                                  void* cache_v, int32_t batch, int32_t cache_cap,
-                                  const int32_t* ctx_len, int32_t max_ctx, int32_t n_suffix,
-                                  float scale, void* out, void* workspace, size_t ws_bytes,
-                                  void* stream);
+                                  int64_t pool_tokens, const int32_t* slot_src,
+                                  const int32_t* slot_delta, int32_t map_cap, const void* table,
+                                  int32_t max_abs_delta, const void* q, const void* k_suf,
+                                  const void* v_suf, void* cache_k, void* cache_v, int32_t batch,
+                                  int32_t cache_cap, const int32_t* ctx_len, int32_t max_ctx,
+                                  int32_t n_suffix, float scale, void* out, void* workspace,
+                                  size_t ws_bytes, void* stream);
 
 /* ---- 3b. frontier prefill (App. C.1: inline KVs interleaved with the prepared states at
    their logical slots; a query never sees a logically later position) ----

@@ -25,7 +25,7 @@ STATUS = {0: "PIC_OK", -1: "PIC_ERR_INVALID_ARG", -2: "PIC_ERR_UNSUPPORTED", -3:
 EXPORTS = ("pic_plan_layout", "pic_plan_frontier", "pic_rope_table_bytes", "pic_rope_table_init",
            "pic_rope_table_init_freq", "pic_rope_llama3_freq",
            "pic_rerotate_keys", "pic_compose", "pic_prefill_workspace_bytes",
-           "pic_suffix_prefill_attn", "pic_paged_prefill_workspace_bytes", "pic_paged_prefill_attn",
+           "pic_suffix_prefill_attn", "pic_build_slot_map", "pic_paged_prefill_attn",
            "pic_frontier_workspace_bytes", "pic_frontier_prefill_attn",
            "pic_decode_workspace_bytes", "pic_decode_attn", "pic_status_string", "pic_last_error",
            "pic_decode_auto_splits")
@@ -89,9 +89,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "pic_compose": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, P, I32, I32, P]),
         "pic_prefill_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_suffix_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, P, P, SZ, P]),
-        "pic_paged_prefill_workspace_bytes": (SZ, [MP, I32, I32, I32]),
-        "pic_paged_prefill_attn": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, P, P, P, P, I32, I32, P,
-                                                  I32, I32, F, P, P, SZ, P]),
+        "pic_build_slot_map": (ctypes.c_int, [P, I32, I32, I32, P, P, P]),
+        "pic_paged_prefill_attn": (ctypes.c_int, [MP, P, P, I64, P, P, I32, P, I32, P, P, P, P, P, I32, I32,
+                                                  P, I32, I32, F, P, P, SZ, P]),
         "pic_frontier_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_frontier_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, P, I32, I32, F, P, P, SZ, P]),
         "pic_decode_workspace_bytes": (SZ, [MP, I32, I32, I32]),
@@ -238,19 +238,21 @@ def pic_suffix_prefill_attn(model: Model, q, k_suf, v_suf, cache_k, cache_v, bat
                                           _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
-def pic_paged_prefill_workspace_bytes(model: Model, batch, n_suffix, max_ctx) -> int:
-    return load().pic_paged_prefill_workspace_bytes(ctypes.byref(model), batch, n_suffix, max_ctx)
+def pic_build_slot_map(blocks, n_blocks, batch, map_cap, slot_src, slot_delta, stream=None):
+    _check(load().pic_build_slot_map(_ptr(blocks), int(n_blocks), int(batch), int(map_cap), _ptr(slot_src),
+                                     _ptr(slot_delta), _stream(stream)))
 
 
-def pic_paged_prefill_attn(model: Model, pool_k, pool_v, pool_tokens, blocks, n_blocks, table, max_abs_delta,
-                           q, k_suf, v_suf, cache_k, cache_v, batch, cache_cap, ctx_len, max_ctx, n_suffix,
-                           out, workspace, scale=0.0, stream=None):
+def pic_paged_prefill_attn(model: Model, pool_k, pool_v, pool_tokens, slot_src, slot_delta, map_cap, table,
+                           max_abs_delta, q, k_suf, v_suf, cache_k, cache_v, batch, cache_cap, ctx_len, max_ctx,
+                           n_suffix, out, workspace=None, scale=0.0, stream=None):
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().pic_paged_prefill_attn(ctypes.byref(model), _ptr(pool_k), _ptr(pool_v), int(pool_tokens),
-                                         _ptr(blocks), int(n_blocks), _ptr(table), int(max_abs_delta), _ptr(q),
-                                         _ptr(k_suf), _ptr(v_suf), _ptr(cache_k), _ptr(cache_v), int(batch),
-                                         int(cache_cap), _ptr(ctx_len), int(max_ctx), int(n_suffix),
-                                         float(scale), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
+                                         _ptr(slot_src), _ptr(slot_delta), int(map_cap), _ptr(table),
+                                         int(max_abs_delta), _ptr(q), _ptr(k_suf), _ptr(v_suf), _ptr(cache_k),
+                                         _ptr(cache_v), int(batch), int(cache_cap), _ptr(ctx_len), int(max_ctx),
+                                         int(n_suffix), float(scale), _ptr(out), _ptr(workspace), ws_bytes,
+                                         _stream(stream)))
 
 
 def pic_frontier_workspace_bytes(model: Model, batch, n_inline, max_len) -> int:

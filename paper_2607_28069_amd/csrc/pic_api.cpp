@@ -448,27 +448,32 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
                     "prefill attention launch");
 }
 
-PIC_API size_t pic_paged_prefill_workspace_bytes(const pic_model* model, int32_t batch,
-                                                 int32_t n_suffix, int32_t max_ctx) {
-  if (check_attn_model(model) != PIC_OK || batch < 0 || n_suffix < 0 || max_ctx < 0) return 0;
-  if (model->dtype != PIC_BF16) return 0;
-  return pic::prefill_bf16_paged_workspace(shape_of(model, batch, max_ctx + n_suffix, 0.f),
-                                           n_suffix, max_ctx);
+PIC_API pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch,
+                                      int32_t map_cap, int32_t* slot_src, int32_t* slot_delta,
+                                      void* stream) {
+  if (n_blocks < 0 || batch < 0 || map_cap < 0) return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if ((int64_t)batch * map_cap == 0) return ok();
+  if (n_blocks > 0 && !blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
+  if (!slot_src || !slot_delta) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL");
+  return hip_status(pic::launch_slot_map(blocks, n_blocks, batch, map_cap, slot_src, slot_delta,
+                                         (hipStream_t)stream),
+                    "slot map launch");
 }
 
 PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* pool_k,
                                           const void* pool_v, int64_t pool_tokens,
-                                          const pic_block* blocks, int32_t n_blocks,
-                                          const void* table, int32_t max_abs_delta, const void* q,
-                                          const void* k_suf, const void* v_suf, void* cache_k,
-                                          void* cache_v, int32_t batch, int32_t cache_cap,
-                                          const int32_t* ctx_len, int32_t max_ctx,
-                                          int32_t n_suffix, float scale, void* out,
-                                          void* workspace, size_t ws_bytes, void* stream) {
+                                          const int32_t* slot_src, const int32_t* slot_delta,
+                                          int32_t map_cap, const void* table, int32_t max_abs_delta,
+                                          const void* q, const void* k_suf, const void* v_suf,
+                                          void* cache_k, void* cache_v, int32_t batch,
+                                          int32_t cache_cap, const int32_t* ctx_len,
+                                          int32_t max_ctx, int32_t n_suffix, float scale,
+                                          void* out, void* workspace, size_t ws_bytes,
+                                          void* stream) {
   PIC_CHECK(check_attn_model(model));
   if (model->dtype != PIC_BF16)
     return fail(PIC_ERR_UNSUPPORTED, "the paged prefill is built for bf16 caches");
-  if (batch < 0 || cache_cap < 0 || max_ctx < 0 || n_suffix < 0 || pool_tokens < 0 || n_blocks < 0)
+  if (batch < 0 || cache_cap < 0 || max_ctx < 0 || n_suffix < 0 || pool_tokens < 0 || map_cap < 0)
     return fail(PIC_ERR_INVALID_ARG, "negative size");
   if (!(scale >= 0.f) || !std::isfinite(scale))
     return fail(PIC_ERR_INVALID_ARG, "scale must be finite and >= 0");
@@ -477,6 +482,9 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
   if ((int64_t)max_ctx + n_suffix > cache_cap)
     return fail(PIC_ERR_CAPACITY, "max_ctx + n_suffix = %lld exceeds cache_cap %d",
                 (long long)max_ctx + n_suffix, cache_cap);
+  if (map_cap < max_ctx)
+    return fail(PIC_ERR_CAPACITY, "map_cap %d is below max_ctx %d", map_cap, max_ctx);
+  if (max_ctx > 0 && pool_tokens == 0) return fail(PIC_ERR_RANGE, "empty pool");
   if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX)
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
@@ -490,12 +498,11 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
   PIC_CHECK(check_ptr(cache_k, "cache_k"));
   PIC_CHECK(check_ptr(cache_v, "cache_v"));
   PIC_CHECK(check_ptr(out, "out"));
-  if (n_blocks > 0 && !blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
+  if (!slot_src || !slot_delta) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL");
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
-  const size_t need = pic_paged_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
-  if (workspace == nullptr || ws_bytes < need)
+  const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
+  if (need > 0 && (workspace == nullptr || ws_bytes < need))
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
-  PIC_CHECK(check_ptr(workspace, "workspace"));
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
   return hip_status(pic::launch_prefill_bf16_paged(
@@ -504,9 +511,10 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
                         static_cast<const pic::bf16_t*>(v_suf), static_cast<pic::bf16_t*>(cache_k),
                         static_cast<pic::bf16_t*>(cache_v), ctx_len, max_ctx, n_suffix,
                         static_cast<const pic::bf16_t*>(pool_k),
-                        static_cast<const pic::bf16_t*>(pool_v), pool_tokens, blocks, n_blocks,
-                        static_cast<const float2*>(table), stride, max_abs_delta,
-                        static_cast<pic::bf16_t*>(out), workspace, ws_bytes, (hipStream_t)stream),
+                        static_cast<const pic::bf16_t*>(pool_v), pool_tokens, slot_src, slot_delta,
+                        map_cap > 0 ? map_cap : 1, static_cast<const float2*>(table), stride,
+                        max_abs_delta, static_cast<pic::bf16_t*>(out), workspace, ws_bytes,
+                        (hipStream_t)stream),
                     "paged prefill launch");
 }
 

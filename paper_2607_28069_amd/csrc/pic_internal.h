@@ -99,17 +99,21 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
                                      int32_t max_len, bf16_t* out, void* workspace,
                                      size_t ws_bytes, hipStream_t stream);
 
-// Zero-copy composition: the documents' K/V are read from the pool through the gather blocks
-// (keys turned on load by their block's shift); only the suffix rows are stored into the cache.
-size_t prefill_bf16_paged_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx);
+// Token-level slot map: slot_src / slot_delta [batch][map_cap] = pool token and position shift
+// of every slot the gather blocks cover (0 / 0 elsewhere).
+hipError_t launch_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch, int32_t map_cap,
+                           int32_t* slot_src, int32_t* slot_delta, hipStream_t stream);
+// Zero-copy composition: the documents' K/V are read from the pool through the slot map (keys
+// turned on load by their shift); only the suffix rows are stored into the cache.  Workspace as
+// for launch_prefill_bf16.
 hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const bf16_t* q,
                                      const bf16_t* k_suf, const bf16_t* v_suf, bf16_t* cache_k,
                                      bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
                                      int32_t n_suffix, const bf16_t* pool_k, const bf16_t* pool_v,
-                                     int64_t pool_tokens, const pic_block* blocks,
-                                     int32_t n_blocks, const float2* table, int64_t table_stride,
-                                     int32_t max_abs_delta, bf16_t* out, void* workspace,
-                                     size_t ws_bytes, hipStream_t stream);
+                                     int64_t pool_tokens, const int32_t* slot_src,
+                                     const int32_t* slot_delta, int32_t map_cap, const float2* table,
+                                     int64_t table_stride, int32_t max_abs_delta, bf16_t* out,
+                                     void* workspace, size_t ws_bytes, hipStream_t stream);
 
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len);
 size_t decode_bf16_workspace(const AttnShape& s, int32_t max_len, int32_t n_splits);

@@ -262,8 +262,12 @@ prefill_bf16_kernel(PrefillArgs a) {
   };
   // cos/sin of the lane's 8 pair frequencies at |delta| into this wave's cos/sin area:
   // instruction j moves float pairs (f_j, f_j + 1) to byte j * 1 KB + 16 * lane
+  // (a lane reloads only when its |shift| changes: a document keeps one shift for all its tiles)
+  int32_t cs_held = -1;   // |shift| whose cos/sin this lane's area holds
   auto load_cs = [&](int32_t delta) {
     const int32_t ad = delta < 0 ? -delta : delta;
+    if (ad == cs_held) return;
+    cs_held = ad;
     const float2* row = a.table + (int64_t)l * a.table_stride + (int64_t)ad * (kHD / 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -694,8 +698,6 @@ __global__ void __launch_bounds__(64) map_expand_kernel(const pic_block* __restr
   }
 }
 
-size_t align256(size_t x) { return (x + 255) / 256 * 256; }
-
 hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved, int32_t n_q,
                   int32_t max_ctx, void* workspace, size_t ws_bytes, hipStream_t stream) {
   const int n_rep = s.n_q_heads / s.n_kv_heads;
@@ -770,39 +772,28 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
   return launch(s, a, kModeTable, false, n_q, max_ctx, workspace, ws_bytes, stream);
 }
 
-size_t prefill_bf16_paged_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
-  return align256(prefill_bf16_workspace(s, n_suffix, max_ctx)) +
-         2 * align256((size_t)s.batch * (max_ctx > 0 ? max_ctx : 1) * sizeof(int32_t));
+hipError_t launch_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch, int32_t map_cap,
+                           int32_t* smap, int32_t* dmap, hipStream_t stream) {
+  const int64_t n_map = (int64_t)batch * map_cap;
+  if (n_map == 0) return hipSuccess;
+  int64_t g = (n_map + 255) / 256;
+  g = g < 1 ? 1 : (g > 65536 ? 65536 : g);
+  hipLaunchKernelGGL(map_clear_kernel, dim3((unsigned)g), dim3(256), 0, stream, smap, dmap, n_map);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || n_blocks == 0) return e;
+  hipLaunchKernelGGL(map_expand_kernel, dim3(n_blocks), dim3(64), 0, stream, blocks, batch, map_cap,
+                     smap, dmap);
+  return hipGetLastError();
 }
 
 hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const bf16_t* q,
                                      const bf16_t* k_suf, const bf16_t* v_suf, bf16_t* cache_k,
                                      bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
                                      int32_t n_suffix, const bf16_t* pool_k, const bf16_t* pool_v,
-                                     int64_t pool_tokens, const pic_block* blocks,
-                                     int32_t n_blocks, const float2* table, int64_t table_stride,
+                                     int64_t pool_tokens, const int32_t* smap, const int32_t* dmap,
+                                     int32_t map_cap, const float2* table, int64_t table_stride,
                                      int32_t max_abs_delta, bf16_t* out, void* workspace,
                                      size_t ws_bytes, hipStream_t stream) {
-  if ((int64_t)n_suffix * (s.n_q_heads / s.n_kv_heads) == 0 || s.batch == 0 || s.n_layers == 0)
-    return hipSuccess;
-  if (workspace == nullptr || ws_bytes < prefill_bf16_paged_workspace(s, n_suffix, max_ctx))
-    return hipErrorInvalidValue;
-  const size_t split_ws = align256(prefill_bf16_workspace(s, n_suffix, max_ctx));
-  const int32_t map_cap = max_ctx > 0 ? max_ctx : 1;
-  const size_t map_bytes = align256((size_t)s.batch * map_cap * sizeof(int32_t));
-  int32_t* smap = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + split_ws);
-  int32_t* dmap = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace) + split_ws + map_bytes);
-  const int64_t n_map = (int64_t)s.batch * map_cap;
-  int64_t g = (n_map + 255) / 256;
-  g = g < 1 ? 1 : (g > 65536 ? 65536 : g);
-  hipLaunchKernelGGL(map_clear_kernel, dim3((unsigned)g), dim3(256), 0, stream, smap, dmap, n_map);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (n_blocks > 0) {
-    hipLaunchKernelGGL(map_expand_kernel, dim3(n_blocks), dim3(64), 0, stream, blocks, s.batch, map_cap,
-                       smap, dmap);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
   PrefillArgs a = {};
   a.pool_k = pool_k;
   a.pool_v = pool_v;
@@ -821,7 +812,7 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
   a.ctx_len = ctx_len;
   a.out = out;
   a.max_ctx = max_ctx;
-  return launch(s, a, kModePaged, interleaved, n_suffix, max_ctx, workspace, split_ws, stream);
+  return launch(s, a, kModePaged, interleaved, n_suffix, max_ctx, workspace, ws_bytes, stream);
 }
 
 }  // namespace pic

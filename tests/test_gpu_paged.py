@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
 
 
 def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, layers=1):
-    """Paged prefill of run r on fresh (zeroed) caches; returns (out, cache_k, cache_v)."""
+    """Slot map + paged prefill of run r on fresh (zeroed) caches; returns (out, cache_k, cache_v)."""
     w, d, dt = r.w, r.dev, tdtype(r.w)
     m = model or r.model
     shape = (layers, w.batch, w.n_kv_heads, r.cap, w.head_dim)
@@ -30,12 +30,22 @@ def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, 
     cv = torch.zeros(shape, dtype=dt, device=DEV) if cache_v is None else cache_v
     out = torch.zeros((layers, w.batch, w.n_suffix, w.n_q_heads, w.head_dim), dtype=dt, device=DEV)
     max_ctx = int(r.ctx.max())
-    ws = torch.empty(pic.pic_paged_prefill_workspace_bytes(m, w.batch, w.n_suffix, max_ctx),
+    map_cap = max_ctx + 7                                   # any capacity >= max_ctx
+    smap = torch.full((w.batch, map_cap), -5, dtype=torch.int32, device=DEV)
+    dmap = torch.full((w.batch, map_cap), 123, dtype=torch.int32, device=DEV)
+    pic.pic_build_slot_map(d["blocks"], d["blocks"].numel() // 5, w.batch, map_cap, smap, dmap)
+    ws = torch.empty(max(pic.pic_prefill_workspace_bytes(m, w.batch, w.n_suffix, max_ctx), 16),
                      dtype=torch.uint8, device=DEV)
     pic.pic_paged_prefill_attn(m, d["pool_k"] if pool_k is None else pool_k,
-                               d["pool_v"] if pool_v is None else pool_v, r.lay.pool_tokens, d["blocks"],
-                               d["blocks"].numel() // 5, d["table"], d["mad"], d["q"], d["k_suf"], d["v_suf"],
-                               ck, cv, w.batch, r.cap, d["ctx"], max_ctx, w.n_suffix, out, ws)
+                               d["pool_v"] if pool_v is None else pool_v, r.lay.pool_tokens, smap, dmap, map_cap,
+                               d["table"], d["mad"], d["q"], d["k_suf"], d["v_suf"], ck, cv, w.batch, r.cap,
+                               d["ctx"], max_ctx, w.n_suffix, out, ws)
+    # the map: pool token and shift of every composed slot, 0 / 0 past each context
+    sm, dm = smap.cpu().numpy(), dmap.cpu().numpy()
+    for b, mp in enumerate(r.maps):
+        n = mp.ctx_len
+        assert np.array_equal(sm[b, :n], mp.src_token) and np.array_equal(dm[b, :n], mp.logical_pos - mp.compile_pos)
+        assert not sm[b, n:].any() and not dm[b, n:].any()
     return out, ck, cv
 
 
