@@ -105,6 +105,8 @@ struct PrefillArgs {
   int32_t max_pos;          // table mode: positions are clamped to [0, max_pos]
   bf16_t* out;
   int32_t max_ctx, n_suffix, batch, cache_cap, n_q_heads, n_kv_heads;
+  int32_t n_rep;            // n_q_heads / n_kv_heads
+  uint64_t rep_magic;       // ceil(2^32 / n_rep): x / n_rep = (x * rep_magic) >> 32 for x < 2^27
   int32_t m_tiles;          // ceil(n_suffix * n_rep / kRowsPerWG)
   int32_t n_splits;         // key-range splits per (m-tile, request, kv head)
   int32_t tiles_per_split;  // key tiles per split
@@ -145,7 +147,10 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int b = bg / a.n_kv_heads, g = bg % a.n_kv_heads;
   const int l = blockIdx.y;
 
-  const int n_rep = a.n_q_heads / a.n_kv_heads;
+  // (divisions by n_rep as multiply-highs: uniform operands then stay in scalar registers,
+  // and with them every tile count, mask decision and load path derived from them)
+  const int n_rep = a.n_rep;
+  auto div_rep = [&](int x) { return (int)(((uint64_t)(uint32_t)x * a.rep_magic) >> 32); };
   const int M = a.n_suffix * n_rep;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -155,16 +160,16 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int row0_wg = mt * kRowsPerWG;
   const int r = row0_wg + wave * kRowsPerWave + n;    // this lane's query row
   bool row_ok = r < M;
-  const int tok = row_ok ? r / n_rep : a.n_suffix - 1;
-  const int hq = g * n_rep + (row_ok ? r % n_rep : 0);
+  const int tok = row_ok ? div_rep(r) : a.n_suffix - 1;
+  const int hq = g * n_rep + (row_ok ? r - div_rep(r) * n_rep : 0);
   // ctx: keys below it come from the cache (suffix mode: the composed context);
   // pos_min_wg / pos_max_wg: nearest / furthest position of this workgroup's query rows
   int ctx, qpos, pos_min_wg, pos_max_wg;
   if constexpr (!kTable) {
     ctx = a.ctx_len[b];
     ctx = ctx < 0 ? 0 : (ctx > a.max_ctx ? a.max_ctx : ctx);
-    pos_min_wg = ctx + row0_wg / n_rep;
-    pos_max_wg = ctx + (min(row0_wg + kRowsPerWG, M) - 1) / n_rep;
+    pos_min_wg = ctx + div_rep(row0_wg);
+    pos_max_wg = ctx + div_rep(min(row0_wg + kRowsPerWG, M) - 1);
     qpos = ctx + tok;
   } else {
     __shared__ int red_lo[kWaves], red_hi[kWaves];
@@ -705,6 +710,9 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
   if (M == 0 || s.batch == 0 || s.n_layers == 0) return hipSuccess;
   const SplitPlan p = plan_splits(s, n_q, max_ctx);
   a.n_suffix = n_q;
+  a.n_rep = n_rep;
+  a.rep_magic = ((uint64_t(1) << 32) + n_rep - 1) / n_rep;
+  if (M >= (int64_t(1) << 27)) return hipErrorInvalidValue;   // beyond the exact range of the division
   a.batch = s.batch;
   a.cache_cap = s.cache_cap;
   a.n_q_heads = s.n_q_heads;
