@@ -406,7 +406,8 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
   if ((int64_t)max_ctx + n_suffix > cache_cap)
     return fail(PIC_ERR_CAPACITY, "max_ctx + n_suffix = %lld exceeds cache_cap %d",
                 (long long)max_ctx + n_suffix, cache_cap);
-  if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX)
+  if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX ||
+      (int64_t)n_suffix * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
   if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
@@ -485,7 +486,8 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
   if (map_cap < max_ctx)
     return fail(PIC_ERR_CAPACITY, "map_cap %d is below max_ctx %d", map_cap, max_ctx);
   if (max_ctx > 0 && pool_tokens == 0) return fail(PIC_ERR_RANGE, "empty pool");
-  if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX)
+  if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX ||
+      (int64_t)n_suffix * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
   if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
@@ -540,7 +542,8 @@ PIC_API pic_status pic_frontier_prefill_attn(const pic_model* model, const void*
     return fail(PIC_ERR_INVALID_ARG, "scale must be finite and >= 0");
   if (max_len > cache_cap)
     return fail(PIC_ERR_CAPACITY, "max_len %d exceeds cache_cap %d", max_len, cache_cap);
-  if ((int64_t)batch * model->n_q_heads * n_inline > INT32_MAX)
+  if ((int64_t)batch * model->n_q_heads * n_inline > INT32_MAX ||
+      (int64_t)n_inline * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
   if (batch == 0 || n_inline == 0 || model->n_layers == 0 || max_len == 0) return ok();
