@@ -156,6 +156,15 @@ def test_llama8b_decode_256_steps_all_layers():
                 assert torch.equal(app, new[l, r][:, None, :].expand_as(app)), (l, r)
     print("[c4] appended regions bit-exact", flush=True)
     lay = wl.lay
+    for l in (0, L // 2, L - 1):                       # composed context, sampled requests
+        pool_k, pool_v = _host(wl.pool_k[l]), _host(wl.pool_v[l])
+        for r in (5, 21, 42):
+            m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+            K, V = O.compose_request(pool_k, pool_v, m, w.rope_theta, w.dtype, **_rope(w, l))
+            n = m.ctx_len
+            assert np.array_equal(_host(wl.cache_v[l, r])[:, :n].view(np.uint32), V.view(np.uint32))
+            assert assert_keys_close(_host(wl.cache_k[l, r])[:, :n], K, w.dtype) > 0.999
+    print("[c4] composed contexts of layers 0/15/31 x requests 5/21/42 ok", flush=True)
     for l, reqs in ((0, (0, 63)), (L - 1, (0, 63, 17))):
         pool_k, pool_v = _host(wl.pool_k[l]), _host(wl.pool_v[l])
         for r in reqs:
