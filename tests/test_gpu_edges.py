@@ -1,0 +1,75 @@
+"""Degenerate and extreme cases on the GPU, against the oracle: a request that composes
+nothing (empty context: the suffix attends only to itself), a single-token suffix, a single
+suffix token with a one-token context, keys moved by the largest supported shift, and calls
+that have nothing to do (they launch nothing and leave outputs untouched)."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_28069_amd as pic
+import synth
+from oracle import pic_oracle as O
+from synth import inputs as S
+
+from gpu_path import (DEV, assert_attn_close, assert_keys_close, gpu_compose, gpu_decode, gpu_prefill, host,
+                      oracle_prefill, setup, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("n_suffix", [1, 37])
+def test_empty_and_tiny_contexts(n_suffix):
+    w = dataclasses.replace(synth.get("c2"), name="edges", pool_docs=3, doc_len=1, docs_per_request=1,
+                            n_suffix=n_suffix, prefix_len=0, batch=3, decode_steps=2)
+    r = setup(w, requests=[[], [0], [2, 1, 0]])          # contexts 0, 1 and 3 tokens
+    assert list(r.ctx) == [0, 1, 3]
+    gpu_compose(r)
+    out = host(gpu_prefill(r))[0]
+    for b in range(w.batch):
+        ref, _, _ = oracle_prefill(r, b)
+        assert_attn_close(out[b], ref, "bf16")
+    outs = [host(o)[0] for o in gpu_decode(r, 2)]
+    for b in range(w.batch):
+        _, K, V = oracle_prefill(r, b)
+        length = r.ctx[b] + w.n_suffix
+        for t in range(2):
+            ref, K, V = O.decode_step(K, V, length, r.inp["dq"][t][b], r.inp["dk"][t][b], r.inp["dv"][t][b])
+            length += 1
+            assert_attn_close(outs[t][b], ref, "bf16")
+
+
+def test_largest_shift():
+    # keys compiled at position 0 and moved to positions near the table's limit (2^20)
+    for dtype, D in (("f32", 64), ("bf16", 128)):
+        m = pic.Model.of(1, 4, 2, D, dtype, 5e5)
+        mad = 1 << 20
+        n, H = 64, 2
+        rng = np.random.default_rng(11)
+        k = O.store(rng.standard_normal((n, H, D)), dtype)
+        a = np.zeros(n, np.int64)
+        b = mad - rng.integers(0, 1000, n)
+        b[::2] *= -1                                       # also the largest negative shifts
+        table = torch.empty(pic.pic_rope_table_bytes(m, mad) // 4, dtype=torch.float32, device=DEV)
+        pic.pic_rope_table_init(m, mad, table)
+        dt = torch.float32 if dtype == "f32" else torch.bfloat16
+        kin = to_dev(k, dt)
+        kout = torch.empty_like(kin)
+        pic.pic_rerotate_keys(m, kin, kout, n, H, torch.from_numpy((b - a).astype(np.int32)).to(DEV), table, mad)
+        ref = O.store(O.rerotate_keys(np.transpose(k, (1, 0, 2)), a, b, 5e5), dtype)
+        assert_keys_close(np.transpose(host(kout), (1, 0, 2)), ref, dtype)
+
+
+def test_calls_with_nothing_to_do_leave_outputs_untouched():
+    w = synth.get("c2")
+    m = pic.Model.of(1, w.n_q_heads, w.n_kv_heads, w.head_dim, "bf16", w.rope_theta)
+    out = torch.full((1, 2, 4, w.n_q_heads, w.head_dim), 3.0, dtype=torch.bfloat16, device=DEV)
+    ck = torch.full((1, 2, w.n_kv_heads, 16, w.head_dim), 5.0, dtype=torch.bfloat16, device=DEV)
+    cv = ck.clone()
+    ctx = torch.zeros(2, dtype=torch.int32, device=DEV)
+    pic.pic_suffix_prefill_attn(m, out, out, out, ck, cv, 2, 16, ctx, 4, 0, out)      # no suffix tokens
+    pic.pic_suffix_prefill_attn(m, out, out, out, ck, cv, 0, 16, ctx, 4, 4, out)      # empty batch
+    pic.pic_compose(m, ck, cv, 16, ctx, 0, ctx, 16, ck, cv, 2, 16)                    # no blocks
+    torch.cuda.synchronize()
+    assert torch.all(out == 3.0) and torch.all(ck == 5.0) and torch.all(cv == 5.0)
