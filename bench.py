@@ -264,6 +264,107 @@ class DeviceWorkload:
             rec["decode"] += [a.elapsed_time(b) for a, b in dec]
 
 
+def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
+    """TTFT (ms) of requests served alone, batch 1: the paper's per-request synchronized wall
+    clock (App. C.2), where the batched figure divides a batch's time by its size.
+
+    Each of the first n_requests requests is planned, composed into a one-request cache and
+    prefilled by itself (paged workloads: slot map + paged prefill), reps times after one
+    untimed pass; the pool, suffix inputs and rotary table are those of the batched workload.
+    A lone request's per-layer launches are short, so the launch sequence after the plan is
+    also recorded once per request as a HIP graph and replayed (the plan and the copy of its
+    gather blocks stay in the timed region).  Returns (eager mean, graph-replay mean)."""
+    import numpy as np
+    import torch
+
+    import paper_2607_28069_amd as pic
+
+    w, L, Ls, dev = wl.w, wl.L, wl.Ls, wl.dev
+    if Ls == 0:
+        return None, None
+    lay, D, Hkv = wl.lay, w.head_dim, w.n_kv_heads
+    cache_k = torch.zeros((L, 1, Hkv, wl.cap, D), dtype=wl.dt, device=dev)
+    cache_v = torch.zeros_like(cache_k)
+    if wl.frontier:
+        nbytes = pic.pic_frontier_workspace_bytes(wl.m1, 1, Ls, wl.max_len)
+    else:
+        nbytes = pic.pic_prefill_workspace_bytes(wl.m1, 1, Ls, wl.max_ctx)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev)
+    blocks_dev = torch.empty_like(wl.blocks_dev)
+    pinned = torch.empty_like(wl.blocks_pinned)
+    pos_dev = torch.empty((1, Ls), dtype=torch.int32, device=dev)
+    if wl.paged:
+        slot_src = torch.empty((1, wl.slot_src.shape[1]), dtype=torch.int32, device=dev)
+        slot_delta = torch.empty_like(slot_src)
+    block = (wl.mad + 1) * (D // 2) * 2 if wl.model.rope_tables > 1 else 0
+
+    def plan(i):   # host plan + asynchronous copy of its blocks (and inline positions)
+        if wl.frontier:
+            blocks, total, inl, _ = pic.pic_plan_frontier([lay.items[i]], lay.doc_offset, lay.doc_len,
+                                                          lay.doc_compile_pos, lay.pool_tokens)
+            n_keys = int(total[0])
+        else:
+            blocks, ctx = pic.pic_plan_layout([lay.requests[i]], lay.doc_offset, lay.doc_len,
+                                              lay.doc_compile_pos, lay.pool_tokens)
+            n_keys = int(ctx[0])
+        nb = len(blocks)
+        pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32).reshape(-1)))
+        blocks_dev[: nb * 5].copy_(pinned[: nb * 5], non_blocking=True)
+        if wl.frontier:
+            tail = pinned[nb * 5: nb * 5 + inl.size]
+            tail.copy_(torch.from_numpy(inl.reshape(-1)))
+            pos_dev.view(-1)[: inl.size].copy_(tail, non_blocking=True)
+        return nb, n_keys
+
+    def launches(views, ctx_i, nv_i, nb, n_keys):   # compose (or slot map) + every layer's prefill
+        if wl.paged:
+            pic.pic_build_slot_map(blocks_dev, nb, 1, slot_src.shape[1], slot_src, slot_delta)
+        else:
+            pic.pic_compose(wl.model, wl.pool_k, wl.pool_v, lay.pool_tokens, blocks_dev, nb, wl.table,
+                            wl.mad, cache_k, cache_v, 1, wl.cap)
+        for q, k, v, ck, cv, out, pk, pv, tab in views:
+            if wl.paged:
+                pic.pic_paged_prefill_attn(wl.m1, pk, pv, lay.pool_tokens, slot_src, slot_delta,
+                                           slot_src.shape[1], tab, wl.mad, q, k, v, ck, cv, 1, wl.cap,
+                                           ctx_i, n_keys, Ls, out, ws)
+            elif wl.frontier:
+                pic.pic_frontier_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, pos_dev, nv_i, Ls, n_keys,
+                                              out, ws)
+            else:
+                pic.pic_suffix_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, ctx_i, n_keys, Ls, out, ws)
+
+    eager, graphed = [], []
+    stream = torch.cuda.current_stream()
+    for i in range(min(n_requests, w.batch)):
+        sl = slice(i, i + 1)
+        # per-layer views of request i, made once (a serving loop holds such pointers)
+        views = [(wl.q[l][sl], wl.k_suf[l][sl], wl.v_suf[l][sl], cache_k[l], cache_v[l], wl.out[l][sl],
+                  wl.pool_k[l], wl.pool_v[l], wl.table[l * block:]) for l in range(L)]
+        ctx_i, nv_i = wl.ctx_dev[sl], (wl.n_valid_dev[sl] if wl.frontier else None)
+        for rep in range(reps + 1):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            launches(views, ctx_i, nv_i, *plan(i))
+            stream.synchronize()
+            if rep:
+                eager.append((time.perf_counter() - t0) * 1e3)
+        nb, n_keys = plan(i)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            launches(views, ctx_i, nv_i, nb, n_keys)
+        for rep in range(reps + 1):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            assert plan(i) == (nb, n_keys)
+            g.replay()
+            stream.synchronize()
+            if rep:
+                graphed.append((time.perf_counter() - t0) * 1e3)
+        del g
+    return float(sum(eager) / len(eager)), float(sum(graphed) / len(graphed))
+
+
 # ------------------------------------------------------------------------------------------
 # CPU oracle baseline (bounded sample)
 # ------------------------------------------------------------------------------------------
@@ -407,6 +508,7 @@ def main():
                        "rope_local_global": w.local_global}
                       if (w.rope_pairing != "half" or w.rope_scaling or w.local_global) else {})},
         "ttft_ms_batch": ttft_ms,
+        **dict(zip(("ttft_ms_single_request", "ttft_ms_single_request_graph"), single_request_ttft(wl))),
         "prefill_attn_tflops": kernels["suffix_prefill_attn"]["achieved"],
         "rerotate_compose_gbps": kernels["compose"]["achieved"],
         "decode_gbps": kernels["decode_attn"]["achieved"],

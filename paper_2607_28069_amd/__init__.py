@@ -113,8 +113,14 @@ def _check(status: int):
 
 
 def _ptr(t):
+    """Device address of a tensor argument (None -> NULL).  The library reads every buffer as a
+    dense array in GPU memory, so host tensors and strided views are refused here."""
     if t is None:
         return None
+    if not t.is_cuda:
+        raise ValueError("device buffer expected: got a host tensor")
+    if not t.is_contiguous():
+        raise ValueError("device buffer must be contiguous")
     return t.data_ptr()
 
 

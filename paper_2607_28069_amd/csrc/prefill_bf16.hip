@@ -638,9 +638,10 @@ struct SplitPlan {
 
 // Key-range splits: enough workgroups to cover the 256 compute units in whole rounds, each
 // split keeping at least 8 key tiles.  Cost in units of one workgroup-tile (~2 us):
-// rounds * tiles per split, plus, for split runs, the fp32 partials each split writes and the
-// combine reads back (520 bytes per query row, twice, at ~4 TB/s) and one tile per split.
-// Ties (within 3%) go to fewer splits.
+// rounds * tiles per split, plus, for split runs, one tile (the combine launch; the splits'
+// own prologues run in parallel) and the fp32 partials each split writes and the combine
+// reads back (520 bytes per query row, twice, at ~4 TB/s).  Ties (within 3%) go to fewer
+// splits.
 SplitPlan plan_splits(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
   SplitPlan p;
   const int64_t M = (int64_t)n_suffix * (s.n_q_heads / s.n_kv_heads);
@@ -650,11 +651,11 @@ SplitPlan plan_splits(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
   const int tiles = (max_ctx + n_suffix + kKeys - 1) / kKeys;
   int best = 1;
   double best_cost = 1e30;
-  for (int sp = 1; sp <= 8; ++sp) {
+  for (int sp = 1; sp <= 32; ++sp) {
     const int tps = (tiles + sp - 1) / sp;
     if (sp > 1 && tps < 8) break;
     const int64_t rounds = (base * sp + 255) / 256;
-    const double partials = sp > 1 ? sp * (1.0 + rows * 2.0 * (kHD + 2) * 4 / 4e12 / 2e-6) : 0.0;
+    const double partials = sp > 1 ? 1.0 + sp * rows * 2.0 * (kHD + 2) * 4 / 4e12 / 2e-6 : 0.0;
     const double cost = (double)rounds * tps + partials;
     if (cost < best_cost * 0.97) {
       best_cost = cost;

@@ -276,3 +276,16 @@ def test_llama3_frequencies_match_transformers_and_oracle(lib):
     got = pic.pic_rope_llama3_freq(128, 5e5)
     np.testing.assert_allclose(got, ref.double().numpy(), rtol=2e-6, atol=0)
     np.testing.assert_allclose(got, O.llama3_inv_freq(128, 5e5), rtol=1e-14, atol=0)
+
+
+def test_binding_refuses_host_and_strided_buffers(lib):
+    # The library reads every tensor argument as a dense device array: the binding stops a
+    # host tensor or a strided view before any call is made.
+    import torch
+    m = pic.Model.of(1, 4, 2, 64, "f32", 1e4)
+    host = torch.zeros(16, 64)
+    with pytest.raises(ValueError, match="host tensor"):
+        pic.pic_rerotate_keys(m, host, host, 16, 1, None, None, 0)
+    with pytest.raises(ValueError, match="host tensor"):
+        pic._ptr(host[::2])
+    assert pic._ptr(None) is None

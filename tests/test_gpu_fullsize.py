@@ -256,3 +256,33 @@ def test_paged_prefill_full_size(name):
     for l, r in ((0, 0), (wl.L - 1, w.batch - 1)):
         _check_request(wl, l, r, tokens=[0, 1, 64, w.n_suffix - 1], decode_steps=1)
         print(f"[{name} paged] layer {l} request {r} ok", flush=True)
+
+
+def test_llama8b_single_request_path():
+    # A request served alone (batch 1) has 16 (m-tile, kv head) units, so its prefill runs
+    # split over ~15 key ranges with a combine (the batched launch needs none).  The
+    # benchmark's single-request path -- eager, then replayed from a recorded graph -- on two
+    # layers of the 32-layer shape, against the oracle on sampled tokens (every head).
+    from bench import single_request_ttft
+    w = synth.get("c3")
+    wl = DeviceWorkload(w, DEV, n_dec=1, layers=2)
+    assert wl.ws_pre.numel() >= 16
+    import paper_2607_28069_amd as pic
+    assert pic.pic_prefill_workspace_bytes(wl.m1, 1, w.n_suffix, wl.max_ctx) > 0
+    wl.out.zero_()
+    single_request_ttft(wl, n_requests=1, reps=1)
+    torch.cuda.synchronize()
+    lay, r, Ls = wl.lay, 0, w.n_suffix
+    m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+    toks = np.array([0, 1, 63, 64, 127])
+    for l in range(2):
+        K, V = O.compose_request(_host(wl.pool_k[l]), _host(wl.pool_v[l]), m, w.rope_theta, w.dtype,
+                                 **_rope(w, l))
+        n = m.ctx_len
+        Kf = np.concatenate([K, np.transpose(_host(wl.k_suf[l, r]), (1, 0, 2))], axis=1)
+        Vf = np.concatenate([V, np.transpose(_host(wl.v_suf[l, r]), (1, 0, 2))], axis=1)
+        q = np.transpose(_host(wl.q[l, r])[toks], (1, 0, 2))
+        ref = O.attention(q, n + toks, Kf, Vf, np.arange(n + Ls))
+        got = np.transpose(_host(wl.out[l, r])[toks], (1, 0, 2))
+        assert_attn_close(got, ref, w.dtype)
+        print(f"[c3 single request] layer {l} ok", flush=True)
