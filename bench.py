@@ -168,6 +168,9 @@ class DeviceWorkload:
             assert not self.frontier and w.dtype == "bf16", "the paged prefill serves the plain bf16 layout"
             self.slot_src = torch.empty((B, max(self.max_ctx, 1)), dtype=torch.int32, device=dev)
             self.slot_delta = torch.empty_like(self.slot_src)
+            # whole-run tiles: read unturned, queries turned instead
+            self.tile_map = torch.empty((B, pic.pic_slot_map_tiles(self.slot_src.shape[1]), 2),
+                                        dtype=torch.int32, device=dev)
         self.ws_pre = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev)
         self.ws_dec = torch.empty(max(pic.pic_decode_workspace_bytes(self.m1, B, self.max_base + n_dec, 0), 16),
                                   dtype=torch.uint8, device=dev)
@@ -209,20 +212,20 @@ class DeviceWorkload:
             pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
                             self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
             e1.record(stream)
-        pre = []
         block = (self.mad + 1) * (w.head_dim // 2) * 2 if self.model.rope_tables > 1 else 0
         if self.paged:   # the token-level slot map, shared by every layer
             pic.pic_build_slot_map(self.blocks_dev, nb, B, self.slot_src.shape[1], self.slot_src,
-                                   self.slot_delta)
+                                   self.slot_delta, self.tile_map)
+        p0, p1 = ev(), ev()
+        p0.record(stream)
         for l in range(L if Ls else 0):
-            a, b = ev(), ev()
-            a.record(stream)
             if self.paged:
                 pic.pic_paged_prefill_attn(self.m1, self.pool_k[l], self.pool_v[l], lay.pool_tokens,
                                            self.slot_src, self.slot_delta, self.slot_src.shape[1],
                                            self.table[l * block:], self.mad, self.q[l],
                                            self.k_suf[l], self.v_suf[l], self.cache_k[l], self.cache_v[l], B,
-                                           self.cap, self.ctx_dev, self.max_ctx, Ls, self.out[l], self.ws_pre)
+                                           self.cap, self.ctx_dev, self.max_ctx, Ls, self.out[l], self.ws_pre,
+                                           tile_map=self.tile_map)
             elif self.frontier:
                 pic.pic_frontier_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
                                               self.cache_k[l], self.cache_v[l], B, self.cap,
@@ -232,8 +235,7 @@ class DeviceWorkload:
                 pic.pic_suffix_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
                                             self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
                                             self.max_ctx, Ls, self.out[l], self.ws_pre)
-            b.record(stream)
-            pre.append((a, b))
+        p1.record(stream)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         if self.paged:   # the composed cache, for decoding, after the first token
@@ -242,16 +244,14 @@ class DeviceWorkload:
                             self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
             e1.record(stream)
         # -- decode
-        dec = []
+        d0, d1 = ev(), ev()
+        d0.record(stream)
         for t in range(self.n_dec):
             for l in range(L):
-                a, b = ev(), ev()
-                a.record(stream)
                 pic.pic_decode_attn(self.m1, self.dq[l], self.dk[l], self.dv[l], self.cache_k[l],
                                     self.cache_v[l], B, self.cap, self.base_dev, t, self.max_base,
                                     self.dout[t, l], self.ws_dec)
-                b.record(stream)
-                dec.append((a, b))
+        d1.record(stream)
         if calib is not None:
             calib[1].copy_(calib[0])
         torch.cuda.synchronize()
@@ -260,8 +260,11 @@ class DeviceWorkload:
             rec["ttft"].append((t1 - t0) * 1e3)
             rec["step"].append((t2 - t0) * 1e3)
             rec["compose"].append(e0.elapsed_time(e1))
-            rec["prefill"] += [a.elapsed_time(b) for a, b in pre]
-            rec["decode"] += [a.elapsed_time(b) for a, b in dec]
+            # per-call means over back-to-back launch sequences (one event pair per sequence)
+            if L and Ls:
+                rec["prefill"].append(p0.elapsed_time(p1) / L)
+            if L and self.n_dec:
+                rec["decode"].append(d0.elapsed_time(d1) / (L * self.n_dec))
 
 
 def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
@@ -296,6 +299,7 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
     if wl.paged:
         slot_src = torch.empty((1, wl.slot_src.shape[1]), dtype=torch.int32, device=dev)
         slot_delta = torch.empty_like(slot_src)
+        tile_map = torch.empty((1,) + tuple(wl.tile_map.shape[1:]), dtype=torch.int32, device=dev)
     block = (wl.mad + 1) * (D // 2) * 2 if wl.model.rope_tables > 1 else 0
 
     def plan(i):   # host plan + asynchronous copy of its blocks (and inline positions)
@@ -318,7 +322,7 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
 
     def launches(views, ctx_i, nv_i, nb, n_keys):   # compose (or slot map) + every layer's prefill
         if wl.paged:
-            pic.pic_build_slot_map(blocks_dev, nb, 1, slot_src.shape[1], slot_src, slot_delta)
+            pic.pic_build_slot_map(blocks_dev, nb, 1, slot_src.shape[1], slot_src, slot_delta, tile_map)
         else:
             pic.pic_compose(wl.model, wl.pool_k, wl.pool_v, lay.pool_tokens, blocks_dev, nb, wl.table,
                             wl.mad, cache_k, cache_v, 1, wl.cap)
@@ -326,7 +330,7 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
             if wl.paged:
                 pic.pic_paged_prefill_attn(wl.m1, pk, pv, lay.pool_tokens, slot_src, slot_delta,
                                            slot_src.shape[1], tab, wl.mad, q, k, v, ck, cv, 1, wl.cap,
-                                           ctx_i, n_keys, Ls, out, ws)
+                                           ctx_i, n_keys, Ls, out, ws, tile_map=tile_map)
             elif wl.frontier:
                 pic.pic_frontier_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, pos_dev, nv_i, Ls, n_keys,
                                               out, ws)

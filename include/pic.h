@@ -214,13 +214,23 @@ pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const 
    pic_build_slot_map expands gather blocks into the token-level map from cache slots to the
    pool: slot_src[b][p] / slot_delta[b][p] = pool token and position shift of slot p of
    request b ([batch][map_cap] device int32; slots no block covers get 0 / 0; blocks outside
-   batch or map_cap are skipped).  One map serves every layer.
+   batch or map_cap are skipped).  With tile_map (device int32, may be NULL) it also writes,
+   for every 64-slot tile T = slots [64 T, 64 T + 64) of request b,
+   tile_map[(b * ceil(map_cap / 64) + T) * 2 + {0, 1}] = (src, shift) when those slots are pool
+   tokens src .. src + 63 under one shift, else (-1, 0).  One map serves every layer.
    pic_paged_prefill_attn computes what pic_compose followed by pic_suffix_prefill_attn
    computes, without writing the composed cache: attention reads the documents' K/V straight
-   from the pool through the slot map and turns each key by its shift on load (same float32
-   arithmetic and bf16 rounding as pic_compose, so outputs are bit-identical).  Only the
-   suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)); a later pic_compose fills
-   the document slots for decoding.  bf16 only.
+   from the pool through the slot map.
+   * tile_map NULL: every key is turned by its shift on load, with the float32 arithmetic and
+     bf16 rounding of pic_compose, so outputs are bit-identical to compose + prefill.
+   * tile_map from pic_build_slot_map (same blocks, batch and map_cap): a context tile that is
+     one pool run under one shift is loaded in one piece, unturned, and the queries are turned
+     by -shift for its scores instead (<R(-d) q, k> = <q, R(d) k>: RoPE's relative property
+     applied to Eq. 3), in float32 with one bf16 rounding of the turned query; other tiles take
+     the per-key path.  Outputs then match compose + prefill to within bf16 rounding, not bit
+     for bit.  Entries outside the pool, the table or the context are treated as (-1, 0).
+   Only the suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)); a later
+   pic_compose fills the document slots for decoding.  bf16 only.
      pool_k, pool_v, pool_tokens, table, max_abs_delta   as for pic_compose
      slot_src, slot_delta, map_cap   the map; map_cap >= max_ctx (entries are clamped to the
                                      pool and to max_abs_delta)
@@ -228,10 +238,11 @@ pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const 
      out, workspace   as for pic_suffix_prefill_attn (same workspace size) */
 pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch,
                               int32_t map_cap, int32_t* slot_src, int32_t* slot_delta,
-                              void* stream);
+                              int32_t* tile_map, void* stream);
 pic_status pic_paged_prefill_attn(const pic_model* model, const void* pool_k, const void* pool_v,
                                   int64_t pool_tokens, const int32_t* slot_src,
-                                  const int32_t* slot_delta, int32_t map_cap, const void* table,
+                                  const int32_t* slot_delta, int32_t map_cap,
+                                  const int32_t* tile_map, const void* table,
                                   int32_t max_abs_delta, const void* q, const void* k_suf,
                                   const void* v_suf, void* cache_k, void* cache_v, int32_t batch,
                                   int32_t cache_cap, const int32_t* ctx_len, int32_t max_ctx,

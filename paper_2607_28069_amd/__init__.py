@@ -89,8 +89,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "pic_compose": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, P, I32, I32, P]),
         "pic_prefill_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_suffix_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, P, P, SZ, P]),
-        "pic_build_slot_map": (ctypes.c_int, [P, I32, I32, I32, P, P, P]),
-        "pic_paged_prefill_attn": (ctypes.c_int, [MP, P, P, I64, P, P, I32, P, I32, P, P, P, P, P, I32, I32,
+        "pic_build_slot_map": (ctypes.c_int, [P, I32, I32, I32, P, P, P, P]),
+        "pic_paged_prefill_attn": (ctypes.c_int, [MP, P, P, I64, P, P, I32, P, P, I32, P, P, P, P, P, I32, I32,
                                                   P, I32, I32, F, P, P, SZ, P]),
         "pic_frontier_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_frontier_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, P, I32, I32, F, P, P, SZ, P]),
@@ -244,17 +244,26 @@ def pic_suffix_prefill_attn(model: Model, q, k_suf, v_suf, cache_k, cache_v, bat
                                           _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
-def pic_build_slot_map(blocks, n_blocks, batch, map_cap, slot_src, slot_delta, stream=None):
+def pic_slot_map_tiles(map_cap) -> int:
+    """64-slot tiles per request in a tile map of `map_cap` slots."""
+    return (int(map_cap) + PIC_BLOCK_TOKENS - 1) // PIC_BLOCK_TOKENS
+
+
+def pic_build_slot_map(blocks, n_blocks, batch, map_cap, slot_src, slot_delta, tile_map=None, stream=None):
+    """tile_map: None, or int32 [batch][pic_slot_map_tiles(map_cap)][2]."""
     _check(load().pic_build_slot_map(_ptr(blocks), int(n_blocks), int(batch), int(map_cap), _ptr(slot_src),
-                                     _ptr(slot_delta), _stream(stream)))
+                                     _ptr(slot_delta), _ptr(tile_map), _stream(stream)))
 
 
 def pic_paged_prefill_attn(model: Model, pool_k, pool_v, pool_tokens, slot_src, slot_delta, map_cap, table,
                            max_abs_delta, q, k_suf, v_suf, cache_k, cache_v, batch, cache_cap, ctx_len, max_ctx,
-                           n_suffix, out, workspace=None, scale=0.0, stream=None):
+                           n_suffix, out, workspace=None, scale=0.0, stream=None, tile_map=None):
+    """tile_map None: keys turned one by one (bit-identical to compose + prefill); a tile map from
+    pic_build_slot_map: whole-run tiles turn the queries instead."""
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().pic_paged_prefill_attn(ctypes.byref(model), _ptr(pool_k), _ptr(pool_v), int(pool_tokens),
-                                         _ptr(slot_src), _ptr(slot_delta), int(map_cap), _ptr(table),
+                                         _ptr(slot_src), _ptr(slot_delta), int(map_cap), _ptr(tile_map),
+                                         _ptr(table),
                                          int(max_abs_delta), _ptr(q), _ptr(k_suf), _ptr(v_suf), _ptr(cache_k),
                                          _ptr(cache_v), int(batch), int(cache_cap), _ptr(ctx_len), int(max_ctx),
                                          int(n_suffix), float(scale), _ptr(out), _ptr(workspace), ws_bytes,

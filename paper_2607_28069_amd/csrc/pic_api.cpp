@@ -451,20 +451,21 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
 
 PIC_API pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch,
                                       int32_t map_cap, int32_t* slot_src, int32_t* slot_delta,
-                                      void* stream) {
+                                      int32_t* tile_map, void* stream) {
   if (n_blocks < 0 || batch < 0 || map_cap < 0) return fail(PIC_ERR_INVALID_ARG, "negative size");
   if ((int64_t)batch * map_cap == 0) return ok();
   if (n_blocks > 0 && !blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
   if (!slot_src || !slot_delta) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL");
   return hip_status(pic::launch_slot_map(blocks, n_blocks, batch, map_cap, slot_src, slot_delta,
-                                         (hipStream_t)stream),
+                                         tile_map, (hipStream_t)stream),
                     "slot map launch");
 }
 
 PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* pool_k,
                                           const void* pool_v, int64_t pool_tokens,
                                           const int32_t* slot_src, const int32_t* slot_delta,
-                                          int32_t map_cap, const void* table, int32_t max_abs_delta,
+                                          int32_t map_cap, const int32_t* tile_map,
+                                          const void* table, int32_t max_abs_delta,
                                           const void* q, const void* k_suf, const void* v_suf,
                                           void* cache_k, void* cache_v, int32_t batch,
                                           int32_t cache_cap, const int32_t* ctx_len,
@@ -514,7 +515,7 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
                         static_cast<pic::bf16_t*>(cache_v), ctx_len, max_ctx, n_suffix,
                         static_cast<const pic::bf16_t*>(pool_k),
                         static_cast<const pic::bf16_t*>(pool_v), pool_tokens, slot_src, slot_delta,
-                        map_cap > 0 ? map_cap : 1, static_cast<const float2*>(table), stride,
+                        map_cap > 0 ? map_cap : 1, tile_map, static_cast<const float2*>(table), stride,
                         max_abs_delta, static_cast<pic::bf16_t*>(out), workspace, ws_bytes,
                         (hipStream_t)stream),
                     "paged prefill launch");

@@ -100,18 +100,24 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
                                      size_t ws_bytes, hipStream_t stream);
 
 // Token-level slot map: slot_src / slot_delta [batch][map_cap] = pool token and position shift
-// of every slot the gather blocks cover (0 / 0 elsewhere).
+// of every slot the gather blocks cover (0 / 0 elsewhere).  With tile_map (may be NULL):
+// [batch][slot_map_tiles(map_cap)][2] = (src, shift) for every 64-slot tile that is pool tokens
+// src .. src + 63 under one shift, (-1, 0) for any other tile.
+int32_t slot_map_tiles(int32_t map_cap);
 hipError_t launch_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch, int32_t map_cap,
-                           int32_t* slot_src, int32_t* slot_delta, hipStream_t stream);
+                           int32_t* slot_src, int32_t* slot_delta, int32_t* tile_map,
+                           hipStream_t stream);
 // Zero-copy composition: the documents' K/V are read from the pool through the slot map (keys
-// turned on load by their shift); only the suffix rows are stored into the cache.  Workspace as
-// for launch_prefill_bf16.
+// turned on load by their shift); only the suffix rows are stored into the cache.  With a tile
+// map, whole-run tiles are loaded in one piece and the queries are turned by -shift for them
+// instead.  Workspace as for launch_prefill_bf16.
 hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const bf16_t* q,
                                      const bf16_t* k_suf, const bf16_t* v_suf, bf16_t* cache_k,
                                      bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
                                      int32_t n_suffix, const bf16_t* pool_k, const bf16_t* pool_v,
                                      int64_t pool_tokens, const int32_t* slot_src,
-                                     const int32_t* slot_delta, int32_t map_cap, const float2* table,
+                                     const int32_t* slot_delta, int32_t map_cap,
+                                     const int32_t* tile_map, const float2* table,
                                      int64_t table_stride, int32_t max_abs_delta, bf16_t* out,
                                      void* workspace, size_t ws_bytes, hipStream_t stream);
 

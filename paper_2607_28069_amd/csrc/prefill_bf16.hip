@@ -32,10 +32,14 @@
 //    (request, kv head) also stores them into cache slots [ctx, ctx + n_suffix) (no separate
 //    append launch, and no workgroup reads those slots from the cache).
 //  * Paged mode (zero-copy composition): the documents' rows come straight from the pool
-//    through the token-level slot map (pool token and position shift of every context slot),
-//    and each wave turns the key rows it loaded by their shift (Eq. 3) in LDS, with the same
-//    float32 arithmetic and rounding as the compose kernel, before the tile is used; the
-//    composed cache is not written.
+//    through the token-level slot map (pool token and position shift of every context slot);
+//    the composed cache is not written.  A key tile that is one pool run under one shift (the
+//    tile map says so) is loaded like a cache tile and the wave turns its queries by -shift
+//    for that tile's scores instead of turning 64 keys (RoPE's relative property; the turned
+//    operand is rebuilt from an unturned copy in LDS whenever the shift changes).  Any other
+//    tile is loaded row by row and each wave turns the key rows it loaded by their shift
+//    (Eq. 3) in LDS, with the same float32 arithmetic and rounding as the compose kernel,
+//    before the tile is used.
 #include <climits>
 #include <type_traits>
 
@@ -91,6 +95,9 @@ struct PrefillArgs {
   const int32_t* smap;      // [B][map_cap] pool token of each context slot
   const int32_t* dmap;      // [B][map_cap] position shift of each context slot
   int32_t map_cap;
+  const int32_t* tmap;      // [B][map_tiles][2] (pool token of a tile's first key, shift) of
+                            // tiles that are one pool run with one shift, else (-1, 0); or NULL
+  int32_t map_tiles;
   const float2* table;      // [L or 1][max_abs_delta + 1][D/2]
   int64_t table_stride;
   int32_t max_abs_delta;
@@ -124,13 +131,16 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
 prefill_bf16_kernel(PrefillArgs a) {
   constexpr bool kTable = kMode == kModeTable, kPaged = kMode == kModePaged;
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
-  // loads in flight into one buffer do not alias reads from another.
-  __shared__ __attribute__((aligned(16))) uint8_t k_lds0[kTileBytes];
-  __shared__ __attribute__((aligned(16))) uint8_t k_lds1[kTileBytes];
-  __shared__ __attribute__((aligned(16))) uint8_t v_lds0[kTileBytes];
-  __shared__ __attribute__((aligned(16))) uint8_t v_lds1[kTileBytes];
+  // loads in flight into one buffer do not alias reads from another.  (The larger alignment
+  // places them first, at the bottom of LDS, ahead of the paged mode's bigger areas.)
+  __shared__ __attribute__((aligned(4096))) uint8_t k_lds0[kTileBytes];
+  __shared__ __attribute__((aligned(4096))) uint8_t k_lds1[kTileBytes];
+  __shared__ __attribute__((aligned(4096))) uint8_t v_lds0[kTileBytes];
+  __shared__ __attribute__((aligned(4096))) uint8_t v_lds1[kTileBytes];
   // paged mode: each wave's cos/sin of the key rows it turns (4 KB per wave)
   __shared__ __attribute__((aligned(16))) uint8_t cs_lds[kPaged ? kWaves * 4096 : 16];
+  // paged mode: each wave's unturned Q^T operand (8 KB per wave), the source of every turn
+  __shared__ __attribute__((aligned(16))) uint8_t q_lds[kPaged ? kWaves * 8192 : 16];
 
   // XCD-aware block order: hardware block w runs on XCD w % 8; give each XCD a contiguous
   // range of logical blocks so the m-tiles of one (request, kv head) share an L2.
@@ -236,6 +246,11 @@ prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0});
   }
+  if constexpr (kPaged) {   // keep the unturned operand (lane-private slots)
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      *reinterpret_cast<u32x4*>(q_lds + wave * 8192 + (ks * 64 + lane) * 16) = __builtin_bit_cast(u32x4, qop[ks]);
+  }
 
   // ---- global -> LDS tile loads.  Instruction i of wave w writes 1 KB of LDS = tile rows
   // 4 (kWaves i + w) .. +3, lane `lane` landing at byte 16 * lane: row 4 kWaves i + 4 w +
@@ -252,23 +267,30 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int32_t* smap = kPaged ? a.smap + (int64_t)b * a.map_cap : nullptr;
   const int32_t* dmap = kPaged ? a.dmap + (int64_t)b * a.map_cap : nullptr;
   // pool token of load row i (0, 1) of global tile t for this lane (0 past the context)
-  auto map_src = [&](int t, int i) {
-    const int p = t * kKeys + 4 * kWaves * i + ld_row;
-    int32_t v = p < ctx ? smap[p] : 0;
+  // (map entries are loaded raw and checked after the tile's loads have landed: a use right
+  // after the load would make the wave wait for every load in flight, the tile's included)
+  auto raw_src = [&](int t, int i) -> int32_t {   // ctx > 0
+    return smap[min(t * kKeys + 4 * kWaves * i + ld_row, ctx - 1)];
+  };
+  auto fin_src = [&](int t, int i, int32_t v) -> int32_t {
+    if (t * kKeys + 4 * kWaves * i + ld_row >= ctx) v = 0;
     return v < 0 ? 0 : (v >= a.pool_tokens ? (int32_t)(a.pool_tokens - 1) : v);
   };
+  auto map_src = [&](int t, int i) { return ctx > 0 ? fin_src(t, i, raw_src(t, i)) : 0; };
   // rotation item of this lane: row 32 i + 4 w + rr (i = lane / 32, rr = (lane / 8) % 4) of
   // the wave's own load rows, 16-byte chunks c and c + 8 (c = lane % 8)
   const int rot_row = 32 * (lane >> 5) + 4 * wave + ((lane >> 3) & 3), rot_c = lane & 7;
-  auto map_delta = [&](int t) {   // shift of this lane's rotation row of global tile t (0 past the context)
-    const int p = t * kKeys + rot_row;
-    int32_t d = p < ctx ? dmap[p] : 0;
+  // shift of this lane's rotation row of global tile t (0 past the context)
+  auto raw_delta = [&](int t) -> int32_t { return dmap[min(t * kKeys + rot_row, ctx - 1)]; };   // ctx > 0
+  auto fin_delta = [&](int t, int32_t d) -> int32_t {
+    if (t * kKeys + rot_row >= ctx) d = 0;
     return d < -a.max_abs_delta ? -a.max_abs_delta : (d > a.max_abs_delta ? a.max_abs_delta : d);
   };
+  auto map_delta = [&](int t) { return ctx > 0 ? fin_delta(t, raw_delta(t)) : 0; };
   // cos/sin of the lane's 8 pair frequencies at |delta| into this wave's cos/sin area:
   // instruction j moves float pairs (f_j, f_j + 1) to byte j * 1 KB + 16 * lane
   // (a lane reloads only when its |shift| changes: a document keeps one shift for all its tiles)
-  int32_t cs_held = -1;   // |shift| whose cos/sin this lane's area holds
+  int32_t cs_held = -1;   // |shift| whose per-lane cos/sin this lane's area holds (-1: none)
   auto load_cs = [&](int32_t delta) {
     const int32_t ad = delta < 0 ? -delta : delta;
     if (ad == cs_held) return;
@@ -283,12 +305,123 @@ prefill_bf16_kernel(PrefillArgs a) {
                                        (LDS_AS void*)(cs_lds + wave * 4096 + j * 1024), 16, 0, 0);
     }
   };
+  // Paged mode, whole-run tiles: when the 64 keys of context tile T are pool tokens
+  // src .. src + 63 with one shift delta (the tile map says so, and the run lies inside the
+  // pool, the table and the context), the tile is loaded like a cache tile (one base address)
+  // and, instead of turning its 64 keys by delta, the wave turns its queries by -delta for
+  // that tile's scores: <R(-delta) q, k> = <q, R(delta) k> (Eq. 3 and RoPE's relative
+  // property).  Other tiles take the per-key path.  Returns src (uniform), or -1.
+  // The tile map entries are read 64 tiles at a time (lane j: tile win + j) and taken out
+  // with readlane, so a tile costs no memory instruction for them.
+  int32_t win = INT_MIN / 2, w_src = -1, w_del = 0;
+  auto tile_run = [&](int T, int32_t& delta) -> int32_t {   // T uniform
+    delta = 0;
+    if (a.tmap == nullptr || T >= a.map_tiles || (T + 1) * kKeys > ctx) return -1;
+    if (T < win || T >= win + 64) {   // refill the window
+      win = T;
+      const int Tj = T + lane;
+      if (Tj < a.map_tiles) {
+        const int2 e = *reinterpret_cast<const int2*>(a.tmap + ((int64_t)b * a.map_tiles + Tj) * 2);
+        w_src = e.x;
+        w_del = e.y;
+      } else {
+        w_src = -1;
+        w_del = 0;
+      }
+    }
+    const int32_t src = __builtin_amdgcn_readlane(w_src, T - win);
+    const int32_t d = __builtin_amdgcn_readlane(w_del, T - win);
+    if (src < 0 || (int64_t)src + kKeys > a.pool_tokens || d < -a.max_abs_delta || d > a.max_abs_delta)
+      return -1;
+    delta = d;
+    return src;
+  };
+  // Turn the Q^T operand (from its unturned copy) by -shift, in float32, rounded to bf16.
+  // The cos/sin row of |shift| must have been staged in this wave's cos/sin area
+  // (stage_row, landed); shift 0 restores the unturned operand.
+  int32_t q_shift = 0;   // shift the operand is turned by (uniform)
+  auto stage_row = [&](int32_t shift) {
+    const int32_t ad = shift < 0 ? -shift : shift;
+    const float2* row = a.table + (int64_t)l * a.table_stride + (int64_t)ad * (kHD / 2);
+    if (lane < kHD / 4)   // 32 lanes x 16 bytes = the row's 64 (cos, sin) pairs
+      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + 2 * lane),
+                                       (LDS_AS void*)(cs_lds + wave * 4096), 16, 0, 0);
+    cs_held = -1;
+  };
+  auto turn_q = [&](int32_t shift) {
+    if (shift == q_shift) return;
+    q_shift = shift;
+    const uint8_t* qs = q_lds + wave * 8192 + lane * 16;
+    if (shift == 0) {
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(qs + ks * 1024));
+      return;
+    }
+    const float sg = shift < 0 ? -1.f : 1.f;   // sin(shift theta) = sg * sin(|shift| theta)
+    const float4* row = reinterpret_cast<const float4*>(cs_lds + wave * 4096);
+    cs_held = -1;
+    auto unpack = [](u32x4 w, float (&x)[8]) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[2 * e] = __uint_as_float(w[e] << 16);
+        x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+      }
+    };
+    auto pack = [](const float (&x)[8]) {
+      return as_bf16x8(u32x4{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                             pack_bf16x2(x[6], x[7])});
+    };
+    // (x, y) -> (x cos + y sin, y cos - x sin): the pair turned by -shift
+    auto turn = [](float& x, float& y, float c, float sn) {
+      const float u = x, v = y;
+      x = fmaf(u, c, v * sn);
+      y = fmaf(v, c, -(u * sn));
+    };
+    if constexpr (!kInterleaved) {
+      // pairs (d, d + 64): chunks ks and ks + 4, frequencies 16 ks + 8 hh + j
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        float x[8], y[8];
+        unpack(*reinterpret_cast<const u32x4*>(qs + ks * 1024), x);
+        unpack(*reinterpret_cast<const u32x4*>(qs + (ks + 4) * 1024), y);
+#pragma unroll
+        for (int j4 = 0; j4 < 4; ++j4) {
+          const float4 cs = row[8 * ks + 4 * hh + j4];
+          turn(x[2 * j4], y[2 * j4], cs.x, sg * cs.y);
+          turn(x[2 * j4 + 1], y[2 * j4 + 1], cs.z, sg * cs.w);
+        }
+        qop[ks] = pack(x);
+        qop[ks + 4] = pack(y);
+      }
+    } else {
+      // pairs (2i, 2i + 1) inside each chunk: frequencies 8 ks + 4 hh + m
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        float x[8];
+        unpack(*reinterpret_cast<const u32x4*>(qs + ks * 1024), x);
+#pragma unroll
+        for (int m2 = 0; m2 < 2; ++m2) {
+          const float4 cs = row[4 * ks + 2 * hh + m2];
+          turn(x[4 * m2], x[4 * m2 + 1], cs.x, sg * cs.y);
+          turn(x[4 * m2 + 2], x[4 * m2 + 3], cs.z, sg * cs.w);
+        }
+        qop[ks] = pack(x);
+      }
+    }
+  };
   int32_t src_v[kLoadSteps], src_k[kLoadSteps], src_f[kLoadSteps];   // rows of tiles t+1, t+2, t+3
   int32_t d_k = 0, d_f = 0;                                            // rotation shift, tiles t+2, t+3
 
-  auto load_tile = [&](const bf16_t* src, uint8_t* dst_tile, int t, bool is_v) {
+  auto load_tile = [&](const bf16_t* src, uint8_t* dst_tile, int t, bool is_v, int32_t run = -1) {
     const int goff = is_v ? v_goff : k_goff;
-    if constexpr (kPaged) {
+    if (kPaged && run >= 0) {   // a whole-run tile: pool rows run .. run + 63
+      const bf16_t* base = (is_v ? PVg : PKg) + (int64_t)run * kHD;   // uniform
+#pragma unroll
+      for (int i = 0; i < kLoadSteps; ++i)
+        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(base + (4 * kWaves * i) * kHD + goff),
+                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
+                                         16, 0, 0);
+    } else if constexpr (kPaged) {
       const int c = is_v ? v_gc : k_gc;
       const bf16_t* suf = is_v ? Vs : Ks;
       const bf16_t* pool = is_v ? PVg : PKg;
@@ -448,7 +581,17 @@ prefill_bf16_kernel(PrefillArgs a) {
   };
 
   // ---- prologue: K0, V0, K1 resident (paged: turned); scores of tile 0
+  // paged mode: whole-run descriptors of tiles t+1 (V, and the scores computed during tile t)
+  // and t+2 (K) as the tile loop enters tile t, with their shifts
+  int32_t run_v = -1, run_k = -1, del_v = 0, del_k = 0;
   if constexpr (kPaged) {
+    int32_t del0 = 0, del1 = 0;
+    const int32_t run0 = tile_run(t0, del0), run1 = n_tiles > 1 ? tile_run(t0 + 1, del1) : -1;
+    if (run0 >= 0 && del0 != 0) {   // the operand for the scores of tile 0
+      stage_row(del0);
+      wait_loads();
+      turn_q(del0);
+    }
 #pragma unroll
     for (int i = 0; i < kLoadSteps; ++i) {
       src_k[i] = map_src(t0, i);
@@ -456,17 +599,17 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
     d_k = map_delta(t0);
     wait_loads();
-    load_tile(Kg, k_lds0, t0, false);
-    load_tile(Vg, v_lds0, t0, true);
-    load_cs(d_k);
+    load_tile(Kg, k_lds0, t0, false, run0);
+    load_tile(Vg, v_lds0, t0, true, run0);
+    if (run0 < 0) load_cs(d_k);
 #pragma unroll
     for (int i = 0; i < kLoadSteps; ++i) src_k[i] = map_src(t0 + 1, i);
     d_f = map_delta(t0 + 1);
     wait_loads();
-    rotate_own(k_lds0, t0, d_k);
+    if (run0 < 0) rotate_own(k_lds0, t0, d_k);
     if (n_tiles > 1) {
-      load_tile(Kg, k_lds1, t0 + 1, false);
-      load_cs(d_f);
+      load_tile(Kg, k_lds1, t0 + 1, false, run1);
+      if (run1 < 0) load_cs(d_f);
       // V(t0 + 1) is loaded by tile 0 and K(t0 + 2) by tile 0: their rows
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
@@ -475,7 +618,16 @@ prefill_bf16_kernel(PrefillArgs a) {
       }
       d_k = map_delta(t0 + 2);
       wait_loads();
-      rotate_own(k_lds1, t0 + 1, d_f);
+      if (run1 < 0) rotate_own(k_lds1, t0 + 1, d_f);
+    }
+    run_v = run1;
+    del_v = del1;
+    run_k = n_tiles > 2 ? tile_run(t0 + 2, del_k) : -1;
+    // the row the first tile turns the operand with, for the scores of tile 1 (the cos/sin
+    // area is free: tile 1 is a whole run, so nothing rotates with it)
+    if (run_v >= 0 && del_v != 0 && del_v != q_shift) {
+      stage_row(del_v);
+      wait_loads();
     }
   } else {
     load_tile(Kg, k_lds0, t0, false);
@@ -500,14 +652,28 @@ prefill_bf16_kernel(PrefillArgs a) {
     uint8_t* const k_free = P ? k_lds1 : k_lds0;   // receives K(t+2)
     const uint8_t* const v_cur = P ? v_lds1 : v_lds0;   // holds V(t)
     uint8_t* const v_free = P ? v_lds0 : v_lds1;   // receives V(t+1)
-    if (t + 2 < n_tiles) load_tile(Kg, k_free, t0 + t + 2, false);
-    if (t + 1 < n_tiles) load_tile(Vg, v_free, t0 + t + 1, true);
+    // paged: the operand for the scores of tile t + 1, computed below (its cos/sin row, if
+    // any, was staged during the previous tile; read before this tile's cos/sin loads)
+    int32_t run_f = -1, del_f = 0;   // paged: tile t + 3 (K issued by the next tile)
     if constexpr (kPaged) {
-      if (t + 2 < n_tiles) load_cs(d_k);
-      // the rows of tile t + 3 (K issued by the next tile) and its shifts
+      turn_q(run_v >= 0 ? del_v : 0);
+      if (t + 3 < n_tiles) run_f = tile_run(t0 + t + 3, del_f);
+    }
+    if (t + 2 < n_tiles) load_tile(Kg, k_free, t0 + t + 2, false, run_k);
+    if (t + 1 < n_tiles) load_tile(Vg, v_free, t0 + t + 1, true, run_v);
+    int32_t rdl_f = 0;   // raw shift of this lane's rotation row of tile t + 3
+    if constexpr (kPaged) {
+      if (t + 2 < n_tiles && run_k < 0) load_cs(d_k);
+      // the row the next tile turns the operand with (tile t + 2 is a whole run, so nothing
+      // uses the cos/sin area during this tile)
+      if (run_k >= 0 && del_k != 0 && del_k != q_shift) stage_row(del_k);
+      // tile t + 3 not a whole run: the rows and shifts of its keys, loaded now and checked
+      // once the tile's loads have landed
+      if (run_f < 0 && ctx > 0) {
 #pragma unroll
-      for (int i = 0; i < kLoadSteps; ++i) src_f[i] = map_src(t0 + t + 3, i);
-      d_f = map_delta(t0 + t + 3);
+        for (int i = 0; i < kLoadSteps; ++i) src_f[i] = raw_src(t0 + t + 3, i);
+        rdl_f = raw_delta(t0 + t + 3);
+      }
     }
 
     // (scores of a tile past the last one are computed on stale LDS and dropped)
@@ -553,13 +719,18 @@ prefill_bf16_kernel(PrefillArgs a) {
     if (t + 1 < n_tiles) finish_scores(t0 + t + 1, snext);
     wait_loads();
     if constexpr (kPaged) {
-      if (t + 2 < n_tiles) rotate_own(k_free, t0 + t + 2, d_k);
+      if (t + 2 < n_tiles && run_k < 0) rotate_own(k_free, t0 + t + 2, d_k);
+      const bool rows_f = run_f < 0 && ctx > 0;
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
         src_v[i] = src_k[i];
-        src_k[i] = src_f[i];
+        src_k[i] = rows_f ? fin_src(t0 + t + 3, i, src_f[i]) : 0;
       }
-      d_k = d_f;
+      d_k = rows_f ? fin_delta(t0 + t + 3, rdl_f) : 0;
+      run_v = run_k;
+      del_v = del_k;
+      run_k = run_f;
+      del_k = del_f;
     }
     __syncthreads();
   };
@@ -704,6 +875,34 @@ __global__ void __launch_bounds__(64) map_expand_kernel(const pic_block* __restr
   }
 }
 
+// grid over (request, 64-slot tile), 256 threads: a tile whose 64 slots map to pool tokens
+// src .. src + 63 with one shift is recorded as (src, shift), any other tile as (-1, 0).
+__global__ void __launch_bounds__(256) map_tiles_kernel(const int32_t* __restrict__ smap,
+                                                        const int32_t* __restrict__ dmap,
+                                                        int64_t n_tiles, int32_t map_cap,
+                                                        int32_t map_tiles, int32_t* tmap) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_tiles;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t b = i / map_tiles;
+    const int32_t k0 = (int32_t)(i - b * map_tiles) * kKeys;
+    int32_t src = -1, d = 0;
+    if (k0 + kKeys <= map_cap) {
+      const int32_t* sm = smap + b * map_cap + k0;
+      const int32_t* dm = dmap + b * map_cap + k0;
+      src = sm[0];
+      d = dm[0];
+      bool run = src >= 0;
+      for (int j = 1; j < kKeys && run; ++j) run = sm[j] == src + j && dm[j] == d;
+      if (!run) {
+        src = -1;
+        d = 0;
+      }
+    }
+    tmap[2 * i] = src;
+    tmap[2 * i + 1] = d;
+  }
+}
+
 hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved, int32_t n_q,
                   int32_t max_ctx, void* workspace, size_t ws_bytes, hipStream_t stream) {
   const int n_rep = s.n_q_heads / s.n_kv_heads;
@@ -781,17 +980,30 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
   return launch(s, a, kModeTable, false, n_q, max_ctx, workspace, ws_bytes, stream);
 }
 
+int32_t slot_map_tiles(int32_t map_cap) { return (map_cap + kKeys - 1) / kKeys; }
+
 hipError_t launch_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch, int32_t map_cap,
-                           int32_t* smap, int32_t* dmap, hipStream_t stream) {
+                           int32_t* smap, int32_t* dmap, int32_t* tmap, hipStream_t stream) {
   const int64_t n_map = (int64_t)batch * map_cap;
   if (n_map == 0) return hipSuccess;
   int64_t g = (n_map + 255) / 256;
   g = g < 1 ? 1 : (g > 65536 ? 65536 : g);
   hipLaunchKernelGGL(map_clear_kernel, dim3((unsigned)g), dim3(256), 0, stream, smap, dmap, n_map);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || n_blocks == 0) return e;
-  hipLaunchKernelGGL(map_expand_kernel, dim3(n_blocks), dim3(64), 0, stream, blocks, batch, map_cap,
-                     smap, dmap);
+  if (e != hipSuccess) return e;
+  if (n_blocks > 0) {
+    hipLaunchKernelGGL(map_expand_kernel, dim3(n_blocks), dim3(64), 0, stream, blocks, batch, map_cap,
+                       smap, dmap);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (tmap == nullptr) return hipSuccess;
+  const int32_t mt = slot_map_tiles(map_cap);
+  const int64_t n_tiles = (int64_t)batch * mt;
+  int64_t gt = (n_tiles + 255) / 256;
+  gt = gt < 1 ? 1 : (gt > 65536 ? 65536 : gt);
+  hipLaunchKernelGGL(map_tiles_kernel, dim3((unsigned)gt), dim3(256), 0, stream, smap, dmap, n_tiles,
+                     map_cap, mt, tmap);
   return hipGetLastError();
 }
 
@@ -800,7 +1012,8 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
                                      bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
                                      int32_t n_suffix, const bf16_t* pool_k, const bf16_t* pool_v,
                                      int64_t pool_tokens, const int32_t* smap, const int32_t* dmap,
-                                     int32_t map_cap, const float2* table, int64_t table_stride,
+                                     int32_t map_cap, const int32_t* tmap, const float2* table,
+                                     int64_t table_stride,
                                      int32_t max_abs_delta, bf16_t* out, void* workspace,
                                      size_t ws_bytes, hipStream_t stream) {
   PrefillArgs a = {};
@@ -810,6 +1023,8 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
   a.smap = smap;
   a.dmap = dmap;
   a.map_cap = map_cap;
+  a.tmap = tmap;
+  a.map_tiles = slot_map_tiles(map_cap);
   a.table = table;
   a.table_stride = table_stride;
   a.max_abs_delta = max_abs_delta;

@@ -187,6 +187,17 @@ def _frontier(lib, m, ws_bytes=0, **kw):
                                          a["max_len"], a["scale"], a["out"], None, ws_bytes, None)
 
 
+def _paged(lib, m, ws_bytes=1 << 30, **kw):
+    a = dict(pool_k=FAKE, pool_v=FAKE, pool_tokens=1000, smap=FAKE, dmap=FAKE, map_cap=500, tmap=FAKE,
+             table=FAKE, mad=600, q=FAKE, k=FAKE, v=FAKE, ck=FAKE, cv=FAKE, batch=2, cap=600, ctx=FAKE,
+             max_ctx=500, ns=64, scale=0.0, out=FAKE, ws=FAKE)
+    a.update(kw)
+    return lib.pic_paged_prefill_attn(ctypes.byref(m), a["pool_k"], a["pool_v"], a["pool_tokens"], a["smap"],
+                                      a["dmap"], a["map_cap"], a["tmap"], a["table"], a["mad"], a["q"], a["k"],
+                                      a["v"], a["ck"], a["cv"], a["batch"], a["cap"], a["ctx"], a["max_ctx"],
+                                      a["ns"], a["scale"], a["out"], a["ws"], ws_bytes, None)
+
+
 def test_argument_checks_fail_before_any_launch(lib):
     m = _model()
     assert _compose(lib, _model(head_dim=96)) == -2
@@ -213,6 +224,21 @@ def test_argument_checks_fail_before_any_launch(lib):
     assert _frontier(lib, m, scale=float("nan")) == -1
     assert _frontier(lib, _model(head_dim=64)) == -2
     assert _frontier(lib, m, n=0) == 0
+
+    assert _paged(lib, m, map_cap=499) == -4             # the map must cover max_ctx
+    assert _paged(lib, m, max_ctx=580) == -4             # 580 + 64 > cache_cap 600
+    assert _paged(lib, m, smap=None) == -1
+    assert _paged(lib, m, ctx=None) == -1
+    assert _paged(lib, m, mad=-1) == -6
+    assert _paged(lib, m, pool_tokens=0) == -6           # documents but no pool
+    assert _paged(lib, m, q=MIS) == -5
+    assert _paged(lib, _model(dtype="f32")) == -2
+    assert _paged(lib, m, ws=None, ws_bytes=0, max_ctx=4000, map_cap=4000, cap=5000) == -3   # split-K
+    assert _paged(lib, m, batch=0) == 0
+    assert lib.pic_build_slot_map(FAKE, 4, 2, 500, None, FAKE, FAKE, None) == -1
+    assert lib.pic_build_slot_map(None, 4, 2, 500, FAKE, FAKE, None, None) == -1
+    assert lib.pic_build_slot_map(FAKE, -1, 2, 500, FAKE, FAKE, None, None) == -1
+    assert lib.pic_build_slot_map(FAKE, 4, 0, 500, FAKE, FAKE, FAKE, None) == 0   # empty map
 
     assert _decode(lib, m, step=100) == -4               # 500 + 100 + 1 > 600
     assert _decode(lib, m, ws=None) == -3

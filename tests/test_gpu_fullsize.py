@@ -236,14 +236,19 @@ def test_rotary_variant_workloads(name):
 
 @pytest.mark.parametrize("name", ["c3", "c5"])
 def test_paged_prefill_full_size(name):
-    # The bench's zero-copy TTFT path at full size: every layer's paged prefill output equals,
-    # bit for bit, the suffix prefill over the cache composed afterwards; sampled requests
-    # against the oracle.
+    # The bench's zero-copy TTFT path at full size (whole-run tiles turn the queries; the others
+    # their keys): every layer's paged prefill output within the attention tolerance of the
+    # suffix prefill over the cache composed afterwards; sampled requests against the oracle.
     import paper_2607_28069_amd as pic
+    from gpu_path import host
     w = synth.get(name)
     wl = DeviceWorkload(w, DEV, n_dec=1, layers=4 if name == "c5" else None, paged=True)
     wl.step()
     torch.cuda.synchronize()
+    tm = wl.tile_map.cpu().numpy()
+    n_run = int((tm[..., 0] >= 0).sum())
+    print(f"[{name} paged] whole-run tiles {n_run} of {tm.shape[0] * tm.shape[1]}", flush=True)
+    assert n_run > 0
     paged = wl.out.clone()
     ws = torch.empty(max(pic.pic_prefill_workspace_bytes(wl.m1, w.batch, w.n_suffix, wl.max_ctx), 16),
                      dtype=torch.uint8, device=DEV)
@@ -251,8 +256,10 @@ def test_paged_prefill_full_size(name):
         pic.pic_suffix_prefill_attn(wl.m1, wl.q[l], wl.k_suf[l], wl.v_suf[l], wl.cache_k[l], wl.cache_v[l],
                                     w.batch, wl.cap, wl.ctx_dev, wl.max_ctx, w.n_suffix, wl.out[l], ws)
     torch.cuda.synchronize()
-    assert torch.equal(paged, wl.out), "paged prefill differs from compose + prefill"
-    print(f"[{name} paged] all {wl.L} layers bit-identical to compose + prefill", flush=True)
+    for l in range(wl.L):
+        assert_attn_close(host(paged[l]), host(wl.out[l]), w.dtype)
+    print(f"[{name} paged] all {wl.L} layers within tolerance of compose + prefill", flush=True)
+    wl.out.copy_(paged)
     for l, r in ((0, 0), (wl.L - 1, w.batch - 1)):
         _check_request(wl, l, r, tokens=[0, 1, 64, w.n_suffix - 1], decode_steps=1)
         print(f"[{name} paged] layer {l} request {r} ok", flush=True)

@@ -43,7 +43,7 @@ def test_graph_replays_match_eager():
                   per_layer("dv", (steps, B, Hkv, D)))
     cache_k = torch.zeros((L, B, Hkv, cap, D), dtype=dt, device=dev)
     cache_v = torch.zeros_like(cache_k)
-    out, pout = torch.zeros((L, B, Ls, Hq, D), dtype=dt, device=dev), torch.zeros((L, B, Ls, Hq, D), dtype=dt, device=dev)
+    out, pout, rout = (torch.zeros((L, B, Ls, Hq, D), dtype=dt, device=dev) for _ in range(3))
     dout = torch.zeros((L, steps, B, Hq, D), dtype=dt, device=dev)
     table = torch.empty(pic.pic_rope_table_bytes(model, cap) // 4, dtype=torch.float32, device=dev)
     pic.pic_rope_table_init(model, cap, table)
@@ -56,29 +56,34 @@ def test_graph_replays_match_eager():
                          dtype=torch.uint8, device=dev)
     slot_src = torch.empty((B, max_ctx), dtype=torch.int32, device=dev)
     slot_delta = torch.empty_like(slot_src)
+    tile_map = torch.empty((B, pic.pic_slot_map_tiles(max_ctx), 2), dtype=torch.int32, device=dev)
     assert pic.pic_prefill_workspace_bytes(m1, B, Ls, max_ctx) > 0   # the split-K combine is recorded too
 
     def path():
         pic.pic_compose(model, pool_k, pool_v, lay.pool_tokens, blocks_dev, len(blocks), table, cap, cache_k,
                         cache_v, B, cap)
-        pic.pic_build_slot_map(blocks_dev, len(blocks), B, max_ctx, slot_src, slot_delta)
+        pic.pic_build_slot_map(blocks_dev, len(blocks), B, max_ctx, slot_src, slot_delta, tile_map)
         for l in range(L):
             pic.pic_suffix_prefill_attn(m1, q[l], k_suf[l], v_suf[l], cache_k[l], cache_v[l], B, cap, ctx_dev,
                                         max_ctx, Ls, out[l], ws_pre)
             pic.pic_paged_prefill_attn(m1, pool_k[l], pool_v[l], lay.pool_tokens, slot_src, slot_delta, max_ctx,
                                        table, cap, q[l], k_suf[l], v_suf[l], cache_k[l], cache_v[l], B, cap,
                                        ctx_dev, max_ctx, Ls, pout[l], ws_pre)
+            pic.pic_paged_prefill_attn(m1, pool_k[l], pool_v[l], lay.pool_tokens, slot_src, slot_delta, max_ctx,
+                                       table, cap, q[l], k_suf[l], v_suf[l], cache_k[l], cache_v[l], B, cap,
+                                       ctx_dev, max_ctx, Ls, rout[l], ws_pre, tile_map=tile_map)
         for t in range(steps):
             for l in range(L):
                 pic.pic_decode_attn(m1, dq[l][t], dk[l][t], dv[l][t], cache_k[l], cache_v[l], B, cap, base_dev,
                                     t, max_ctx + Ls, dout[l][t], ws_dec, n_splits=2)
 
-    results = (out, pout, dout, cache_k, cache_v)
+    results = (out, pout, rout, dout, cache_k, cache_v, tile_map)
     path()
     torch.cuda.synchronize()
     ref = [x.clone() for x in results]
     assert torch.equal(ref[0], ref[1])            # paged prefill == compose + prefill
-    assert ref[2].abs().sum().item() > 0
+    assert (ref[6][..., 0] >= 0).any()            # whole-run tiles were recorded
+    assert ref[3].abs().sum().item() > 0
 
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
@@ -90,6 +95,7 @@ def test_graph_replays_match_eager():
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        for name, x, y in zip(("out", "paged out", "decode out", "cache_k", "cache_v"), results, ref):
+        for name, x, y in zip(("out", "paged out", "paged out (whole-run tiles)", "decode out", "cache_k",
+                               "cache_v", "tile map"), results, ref):
             assert torch.equal(x, y), f"replay {replay}: {name} differs from the eager run"
         print(f"replay {replay} matches", flush=True)

@@ -1,8 +1,14 @@
 """GPU parity of the zero-copy (paged) suffix prefill: attention reading the documents' K/V
-straight from the pool through the gather blocks, keys turned on load (App. C.1 token map;
-Sec. 2, Eq. 3).  It computes exactly what compose + suffix prefill compute, with the same
-float32 arithmetic and bf16 rounding, so its outputs must be bit-identical to that path's and
-within the attention tolerance of the oracle; the composed document slots stay untouched.
+straight from the pool through the gather blocks (App. C.1 token map; Sec. 2, Eq. 3).
+
+* Without a tile map every key is turned on load with the float32 arithmetic and bf16
+  rounding of compose, so the outputs must be bit-identical to compose + suffix prefill.
+* With the tile map, key tiles that are one pool run under one shift are read unturned and the
+  queries are turned by -shift instead (RoPE's relative property); the outputs must then be
+  within the attention tolerance of compose + prefill and of the oracle.  The tile map itself
+  is checked entry by entry.
+In both modes the suffix rows stored into the cache are bit-exact and the composed document
+slots stay untouched.
 """
 import dataclasses
 
@@ -21,8 +27,24 @@ from gpu_path import (DEV, assert_attn_close, gpu_compose, gpu_prefill, host, or
 pytestmark = pytest.mark.gpu
 
 
-def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, layers=1):
-    """Slot map + paged prefill of run r on fresh (zeroed) caches; returns (out, cache_k, cache_v)."""
+def _expected_tile_map(sm, dm, map_cap):
+    """(src, shift) of every 64-slot tile that is one pool run under one shift, else (-1, 0)."""
+    B, T = sm.shape[0], pic.pic_slot_map_tiles(map_cap)
+    out = np.tile(np.array([-1, 0], np.int32), (B, T, 1))
+    for b in range(B):
+        for t in range(T):
+            k0 = 64 * t
+            if k0 + 64 > map_cap:
+                continue
+            src, d = int(sm[b, k0]), int(dm[b, k0])
+            if src >= 0 and np.array_equal(sm[b, k0:k0 + 64], src + np.arange(64)) and (dm[b, k0:k0 + 64] == d).all():
+                out[b, t] = (src, d)
+    return out
+
+
+def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, layers=1, runs=False):
+    """Slot map + paged prefill of run r on fresh (zeroed) caches; returns (out, cache_k, cache_v).
+    runs: also build the tile map and pass it (whole-run tiles turn the queries)."""
     w, d, dt = r.w, r.dev, tdtype(r.w)
     m = model or r.model
     shape = (layers, w.batch, w.n_kv_heads, r.cap, w.head_dim)
@@ -33,25 +55,34 @@ def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, 
     map_cap = max_ctx + 7                                   # any capacity >= max_ctx
     smap = torch.full((w.batch, map_cap), -5, dtype=torch.int32, device=DEV)
     dmap = torch.full((w.batch, map_cap), 123, dtype=torch.int32, device=DEV)
-    pic.pic_build_slot_map(d["blocks"], d["blocks"].numel() // 5, w.batch, map_cap, smap, dmap)
+    tmap = (torch.full((w.batch, pic.pic_slot_map_tiles(map_cap), 2), 77, dtype=torch.int32, device=DEV)
+            if runs else None)
+    pic.pic_build_slot_map(d["blocks"], d["blocks"].numel() // 5, w.batch, map_cap, smap, dmap, tmap)
     ws = torch.empty(max(pic.pic_prefill_workspace_bytes(m, w.batch, w.n_suffix, max_ctx), 16),
                      dtype=torch.uint8, device=DEV)
     pic.pic_paged_prefill_attn(m, d["pool_k"] if pool_k is None else pool_k,
                                d["pool_v"] if pool_v is None else pool_v, r.lay.pool_tokens, smap, dmap, map_cap,
                                d["table"], d["mad"], d["q"], d["k_suf"], d["v_suf"], ck, cv, w.batch, r.cap,
-                               d["ctx"], max_ctx, w.n_suffix, out, ws)
+                               d["ctx"], max_ctx, w.n_suffix, out, ws, tile_map=tmap)
     # the map: pool token and shift of every composed slot, 0 / 0 past each context
     sm, dm = smap.cpu().numpy(), dmap.cpu().numpy()
     for b, mp in enumerate(r.maps):
         n = mp.ctx_len
         assert np.array_equal(sm[b, :n], mp.src_token) and np.array_equal(dm[b, :n], mp.logical_pos - mp.compile_pos)
         assert not sm[b, n:].any() and not dm[b, n:].any()
+    if runs:
+        tm = tmap.cpu().numpy()
+        assert np.array_equal(tm, _expected_tile_map(sm, dm, map_cap)), "tile map"
+        _paged.runs = int((tm[..., 0] >= 0).sum()), int((tm[..., 0] < 0).sum())
     return out, ck, cv
 
 
-def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m):
+def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=True):
     w = r.w
-    assert torch.equal(out_p, out_m), "paged outputs differ from compose + prefill"
+    if exact:
+        assert torch.equal(out_p, out_m), "paged outputs differ from compose + prefill"
+    else:
+        assert_attn_close(host(out_p), host(out_m), "bf16")
     for b in range(w.batch):
         c = int(r.ctx[b])
         sl = slice(c, c + w.n_suffix)
@@ -59,31 +90,39 @@ def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m):
         assert not ck_p[:, b, :, :c].any() and not cv_p[:, b, :, :c].any(), "document slots were written"
 
 
-@pytest.mark.parametrize("name", ["c2", "ragged"])
-def test_paged_prefill_equals_compose_then_prefill(name):
+@pytest.mark.parametrize("runs", [False, True], ids=["per-key", "whole-runs"])
+@pytest.mark.parametrize("name", ["c2", "ragged", "mixed"])
+def test_paged_prefill_equals_compose_then_prefill(name, runs):
     if name == "c2":
         w = synth.get("c2")
         r = setup(w)
-    else:   # uneven contexts, a prefix-only request, n_rep 7, tails that are not tile multiples
-        w = dataclasses.replace(synth.get("c2"), name="ragged", n_q_heads=28, n_kv_heads=4, pool_docs=5,
+    else:   # uneven contexts, a prefix-only request, n_rep 7, tails that are not tile multiples;
+            # ragged: documents of 7..81 tokens (no tile is one run), mixed: 151..238 tokens
+            # (whole-run tiles inside documents, mixed tiles at their boundaries)
+        w = dataclasses.replace(synth.get("c2"), name=name, n_q_heads=28, n_kv_heads=4, pool_docs=5,
                                 doc_len=77, docs_per_request=4, n_suffix=37, prefix_len=13, batch=3,
-                                doc_len_jitter=(1, 150))
+                                doc_len_jitter=(1, 150) if name == "ragged" else (60, 300))
         lay = S.pool_layout(w)
         r = setup(w, requests=[[lay.prefix_entry, 3, 0, 4], [lay.prefix_entry], [2, 1, 0, 3, 4]], extra_cap=5)
     gpu_compose(r)
     out_m = gpu_prefill(r).clone()
-    out_p, ck_p, cv_p = _paged(r)
+    out_p, ck_p, cv_p = _paged(r, runs=runs)
     torch.cuda.synchronize()
-    _check_against_materialized(r, out_p, ck_p, cv_p, r.dev["cache_k"], r.dev["cache_v"], out_m)
+    _check_against_materialized(r, out_p, ck_p, cv_p, r.dev["cache_k"], r.dev["cache_v"], out_m, exact=not runs)
     got = host(out_p)[0]
     for b in range(w.batch):
         ref, _, _ = oracle_prefill(r, b)
         assert_attn_close(got[b], ref, "bf16")
-    print(f"[{name}] paged == materialized, oracle ok (ctx {[int(c) for c in r.ctx]})", flush=True)
+    if runs:   # c2: context tiles are whole runs; ragged: none is; mixed: both kinds
+        n_run, n_other = _paged.runs
+        assert (n_run > 0 or name == "ragged") and (n_other > 0 or name == "c2"), _paged.runs
+    print(f"[{name}] paged ({'whole-run tiles ' + str(_paged.runs) if runs else 'per-key'}) vs materialized "
+          f"and oracle ok (ctx {[int(c) for c in r.ctx]})", flush=True)
 
 
+@pytest.mark.parametrize("runs", [False, True], ids=["per-key", "whole-runs"])
 @pytest.mark.parametrize("pairing", ["half", "interleaved"])
-def test_paged_prefill_with_rotary_variants(pairing):
+def test_paged_prefill_with_rotary_variants(pairing, runs):
     # two layers with their own frequencies in one call; pool layer 1 differs from layer 0
     w = synth.get("c2")
     r = setup(w)
@@ -110,6 +149,6 @@ def test_paged_prefill_with_rotary_variants(pairing):
     pic.pic_suffix_prefill_attn(m2, d["q"], d["k_suf"], d["v_suf"], ck_m, cv_m, w.batch, r.cap, d["ctx"],
                                 int(r.ctx.max()), w.n_suffix, out_m, ws)
     d["table"] = table
-    out_p, ck_p, cv_p = _paged(r, model=m2, pool_k=pk, pool_v=pv, layers=2)
+    out_p, ck_p, cv_p = _paged(r, model=m2, pool_k=pk, pool_v=pv, layers=2, runs=runs)
     torch.cuda.synchronize()
-    _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m)
+    _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=not runs)
