@@ -44,6 +44,11 @@ class Workload:
     rope_pairing: str = "half"
     rope_scaling: str | None = None
     local_global: tuple[float, float, int] | None = None
+    # Learned block boundaries (KV Packet / Joint): (header, trailer) tokens.  One shared
+    # header entry, compiled at positions 0 .. header-1, precedes every document in a request;
+    # each document entry carries its own trailer and was compiled after the header (its first
+    # token at position `header`).
+    boundary: tuple[int, int] | None = None
     seed: int = 0
     notes: str = ""
 
@@ -133,6 +138,19 @@ WORKLOADS: dict[str, Workload] = {
         local_global=(1e4, 1e6, 6),
         notes="the 32-layer Llama shape with interleaved pairing and per-layer bases "
               "(1e4 local, 1e6 on every 6th layer)"),
+    # Learned block boundaries around every document (KV Packet / Joint serving layout).
+    "llama8b_joint_1layer": Workload(
+        name="llama8b_joint_1layer", dtype="bf16", n_layers=1, n_q_heads=32, n_kv_heads=8,
+        head_dim=128, rope_theta=5e5, pool_docs=16, doc_len=512, docs_per_request=8,
+        prefix_len=64, n_suffix=64, batch=4, boundary=(8, 8),
+        notes="the 1-layer Llama shape with an 8-token shared header before and an 8-token trailer "
+              "after every document"),
+    "llama8b_joint": Workload(
+        name="llama8b_joint", dtype="bf16", n_layers=32, n_q_heads=32, n_kv_heads=8,
+        head_dim=128, rope_theta=5e5, pool_docs=64, doc_len=1024, docs_per_request=10,
+        prefix_len=128, n_suffix=128, batch=16, boundary=(8, 8),
+        notes="the 32-layer Llama shape with an 8-token shared header before and an 8-token trailer "
+              "after every document (10 528-token contexts)"),
 }
 
 # Short aliases in the order the workloads are listed above.

@@ -60,29 +60,39 @@ class PoolLayout:
     prefix_entry: int             # index of the instruction-prefix entry, or -1
     requests: list[list[int]]     # per request: pool entries in logical order
     items: list[list[int]] | None = None   # frontier layouts: entries (>= 0) and inline spans (-n)
+    header_entry: int = -1        # boundary layouts: the shared header entry, else -1
 
 
 def pool_layout(w: Workload) -> PoolLayout:
-    """Pool = the workload's documents, then (if any) one shared instruction prefix.
+    """Pool = the workload's documents, then (if any) one shared instruction prefix, then
+    (boundary layouts) one shared header.
 
-    Documents are compiled independently starting at position 0.  The prefix is
-    stored already at its request-time position 0.  Each request lists the pool
-    entries it composes, prefix first.
+    Documents are compiled independently starting at position 0 (boundary layouts: at
+    position `header`, after the header, with their trailer tokens appended).  The prefix is
+    stored already at its request-time position 0.  Each request lists the pool entries it
+    composes, prefix first (boundary layouts: the header before every document).
     """
     if w.doc_len_jitter is not None:
         lo, hi = w.doc_len_jitter
         lens = host_stream(w, "doc_len").integers(lo, hi + 1, size=w.pool_docs)
     else:
         lens = np.full(w.pool_docs, w.doc_len, dtype=np.int64)
-    lens = list(int(x) for x in lens)
-    prefix_entry = -1
+    header, trailer = w.boundary if w.boundary is not None else (0, 0)
+    lens = list(int(x) + trailer for x in lens)
+    cpos = [header] * len(lens)
+    prefix_entry = header_entry = -1
     if w.prefix_len > 0:
         prefix_entry = len(lens)
         lens.append(w.prefix_len)
+        cpos.append(0)
+    if header > 0:
+        header_entry = len(lens)
+        lens.append(header)
+        cpos.append(0)
     lens_a = np.asarray(lens, dtype=np.int32)
     offs = np.zeros_like(lens_a)
     offs[1:] = np.cumsum(lens_a[:-1])
-    compile_pos = np.zeros_like(lens_a)
+    compile_pos = np.asarray(cpos, dtype=np.int32)
 
     g = host_stream(w, "doc_choice")
     requests = []
@@ -93,6 +103,8 @@ def pool_layout(w: Workload) -> PoolLayout:
             docs = [int(x) for x in g.permutation(w.pool_docs)]
         else:
             docs = [int(x) for x in g.choice(w.pool_docs, size=w.docs_per_request, replace=False)]
+        if header_entry >= 0:
+            docs = [e for d in docs for e in (header_entry, d)]
         requests.append(([prefix_entry] if prefix_entry >= 0 else []) + docs)
     items = None
     if w.frontier:
@@ -101,12 +113,13 @@ def pool_layout(w: Workload) -> PoolLayout:
             it = [-w.inline_prefix] if w.inline_prefix > 0 else []
             for e in entries:
                 it.append(e)
-                if w.inline_span > 0 and e != prefix_entry:
+                if w.inline_span > 0 and e != prefix_entry and e != header_entry:
                     it.append(-w.inline_span)
             if w.n_suffix > 0:
                 it.append(-w.n_suffix)
             items.append(it)
-    return PoolLayout(offs, lens_a, compile_pos, int(lens_a.sum()), prefix_entry, requests, items)
+    return PoolLayout(offs, lens_a, compile_pos, int(lens_a.sum()), prefix_entry, requests, items,
+                      header_entry)
 
 
 def context_lengths(layout: PoolLayout) -> np.ndarray:

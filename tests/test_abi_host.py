@@ -53,7 +53,10 @@ def test_planner_matches_oracle_layout(lib, data):
     offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
     cpos = np.array(data.draw(st.lists(st.integers(0, 3000), min_size=n_pool, max_size=n_pool)))
     batch = data.draw(st.integers(1, 4))
+    # requests of distinct entries, or with repeats (a shared header placed before every
+    # document, as the boundary layouts do)
     reqs = [list(data.draw(st.permutations(range(n_pool)))[: data.draw(st.integers(0, n_pool))])
+            if data.draw(st.booleans()) else data.draw(st.lists(st.integers(0, n_pool - 1), max_size=8))
             for _ in range(batch)]
     blocks, ctx = pic.pic_plan_layout(reqs, offs, lens, cpos, int(lens.sum()))
     maps = O.plan_layout(reqs, offs, lens, cpos)
@@ -65,6 +68,20 @@ def test_planner_matches_oracle_layout(lib, data):
         delta = np.array([got[b][s][1] for s in range(m.ctx_len)], dtype=np.int64)
         assert np.array_equal(src, m.src_token)
         assert np.array_equal(delta, m.logical_pos - m.compile_pos)
+
+
+def test_planner_boundary_workload_matches_oracle(lib):
+    import synth
+    from synth import inputs as S
+    lay = S.pool_layout(synth.get("llama8b_joint"))
+    blocks, ctx = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                      lay.pool_tokens)
+    got = _expand(blocks, len(lay.requests))
+    for b, m in enumerate(O.plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos)):
+        assert ctx[b] == m.ctx_len == 10528
+        src = np.array([got[b][s][0] for s in range(m.ctx_len)], dtype=np.int64)
+        delta = np.array([got[b][s][1] for s in range(m.ctx_len)], dtype=np.int64)
+        assert np.array_equal(src, m.src_token) and np.array_equal(delta, m.logical_pos - m.compile_pos)
 
 
 def test_planner_tiny_workload(lib):

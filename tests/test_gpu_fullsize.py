@@ -79,6 +79,19 @@ def test_llama8b_32layer_bench_configuration():
         print(f"[c3] layer {l} request {r} ok", flush=True)
 
 
+def test_llama8b_joint_bench_configuration():
+    # Learned block boundaries: the shared header composed before each of the 10 documents
+    # (11 placements per request with the prefix), every layer in one compose launch.
+    w = synth.get("llama8b_joint")
+    wl = DeviceWorkload(w, DEV, n_dec=1)
+    wl.step()
+    torch.cuda.synchronize()
+    print(f"[joint] ctx={wl.max_ctx} cap={wl.cap} layers={wl.L}", flush=True)
+    for l, r in ((0, 3), (31, 12)):
+        _check_request(wl, l, r, tokens=[0, 63, 127], decode_steps=1)
+        print(f"[joint] layer {l} request {r} ok", flush=True)
+
+
 def test_llama8b_decode_full_per_layer_shape():
     # 64 requests x 16K composed context from a 256-document pool; 2 of the 32 identical
     # layers (per-layer launches are the same) and 3 of the 256 decode steps.

@@ -91,10 +91,10 @@ def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=T
 
 
 @pytest.mark.parametrize("runs", [False, True], ids=["per-key", "whole-runs"])
-@pytest.mark.parametrize("name", ["c2", "ragged", "mixed"])
+@pytest.mark.parametrize("name", ["c2", "ragged", "mixed", "joint"])
 def test_paged_prefill_equals_compose_then_prefill(name, runs):
-    if name == "c2":
-        w = synth.get("c2")
+    if name in ("c2", "joint"):   # joint: a shared 8-token header before every 520-token document
+        w = synth.get("c2" if name == "c2" else "llama8b_joint_1layer")
         r = setup(w)
     else:   # uneven contexts, a prefix-only request, n_rep 7, tails that are not tile multiples;
             # ragged: documents of 7..81 tokens (no tile is one run), mixed: 151..238 tokens

@@ -31,7 +31,7 @@ def _check_compose(r, d):
     return min(fracs)
 
 
-@pytest.mark.parametrize("name", ["c1", "c2"])
+@pytest.mark.parametrize("name", ["c1", "c2", "llama8b_joint_1layer"])
 def test_compose_and_prefill_small_workloads(name):
     w = synth.get(name)
     r = setup(w)
@@ -70,7 +70,7 @@ def test_composed_keys_equal_keys_rotated_in_place():
     assert np.abs(ck[0][:, : m.ctx_len] - direct).max() <= 1e-5
 
 
-@pytest.mark.parametrize("name", ["c1", "c2"])
+@pytest.mark.parametrize("name", ["c1", "c2", "llama8b_joint_1layer"])
 def test_decode_steps(name):
     w = synth.get(name)
     import dataclasses

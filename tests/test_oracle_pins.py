@@ -278,6 +278,34 @@ def test_composed_cache_equals_full_recompute_single_layer():
     np.testing.assert_allclose(np.transpose(out, (1, 0, 2)), ref, atol=2e-5)
 
 
+def test_boundary_layout_hand_computed_and_equal_to_full_recompute():
+    # Learned block boundaries (KV Packet / Joint): one shared header entry, compiled at
+    # positions 0..2, is placed before every document; each document (with its trailer) was
+    # compiled after the header, from position 3.  Request [prefix, H, B, H, A]:
+    #   prefix [0, 2) delta 0 | H [2, 5) delta 2 | B [5, 11) delta 2 | H [11, 14) delta 11 |
+    #   A [14, 21) delta 11,
+    # and the composed keys equal the raw keys rotated at their logical positions, the
+    # header's at both of its places.
+    Hkv, D, theta = 2, 64, 1e4
+    lens = np.array([7, 6, 2, 3])                 # A (5 + trailer 2), B (4 + 2), prefix, header
+    offs = np.array([0, 7, 13, 15])
+    cpos_e = np.array([3, 3, 0, 0])
+    (m,) = O.plan_layout([[2, 3, 1, 3, 0]], offs, lens, cpos_e)
+    assert m.ctx_len == 21 and np.array_equal(m.logical_pos, np.arange(21))
+    assert np.array_equal(m.src_token, np.r_[13:15, 15:18, 7:13, 15:18, 0:7])
+    assert np.array_equal(m.logical_pos - m.compile_pos, np.r_[[0] * 2, [2] * 3, [2] * 6, [11] * 3, [11] * 7])
+    raw_k = rng.standard_normal((Hkv, 18, D))
+    raw_v = rng.standard_normal((Hkv, 18, D)).astype(np.float32)
+    cpos_t = np.concatenate([np.arange(3, 10), np.arange(3, 9), np.arange(2), np.arange(3)])
+    pool_k = O.round_to_f32(O.rope(raw_k, cpos_t, theta))
+    K, V = O.compose_request(pool_k, raw_v, m, theta, "f32")
+    direct = O.rope(raw_k[:, m.src_token], m.logical_pos, theta)
+    np.testing.assert_allclose(K, direct, atol=1e-5, rtol=0)
+    assert np.array_equal(V, raw_v[:, m.src_token])
+    # the two copies of the header differ (rotated 9 positions apart) but carry the same values
+    assert not np.allclose(K[:, 2:5], K[:, 11:14]) and np.array_equal(V[:, 2:5], V[:, 11:14])
+
+
 # ------------------------------------------------------------------------------------
 # reader-side rotary variants: scaled frequencies, interleaved pairing, per-layer transforms
 # ------------------------------------------------------------------------------------

@@ -45,3 +45,19 @@ def test_requests_draw_distinct_documents():
             assert all(0 <= e < w.pool_docs for e in docs)
         if w.prefix_len:
             assert all(r[0] == lay.prefix_entry for r in lay.requests)
+
+
+def test_boundary_layouts_put_the_shared_header_before_every_document():
+    w = synth.get("llama8b_joint")
+    lay = S.pool_layout(w)
+    h, tr = w.boundary
+    H, P = lay.header_entry, lay.prefix_entry
+    assert lay.doc_len[H] == h and lay.doc_compile_pos[H] == 0
+    assert lay.doc_len[P] == w.prefix_len and lay.doc_compile_pos[P] == 0
+    docs = [e for e in range(len(lay.doc_len)) if e not in (H, P)]
+    assert len(docs) == w.pool_docs
+    assert np.all(lay.doc_len[docs] == w.doc_len + tr) and np.all(lay.doc_compile_pos[docs] == h)
+    for r in lay.requests:
+        assert r[0] == P and r[1::2] == [H] * w.docs_per_request
+        assert len(set(r[2::2])) == w.docs_per_request and H not in r[2::2]
+    assert list(S.context_lengths(lay)) == [w.prefix_len + w.docs_per_request * (h + w.doc_len + tr)] * w.batch
