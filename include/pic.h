@@ -106,7 +106,10 @@ typedef struct {
    logical position 0 in the order given, and splits them into gather blocks.
      batch                      number of requests (>= 1)
      n_entries [host, batch]    entries each request composes (>= 0)
-     entries   [host, sum n]    pool entry ids, request by request, in logical order
+     entries   [host, sum n]    pool entry ids, request by request, in logical order; an entry
+                                may appear more than once (a shared block-boundary header placed
+                                before every document, Sec. 5), each placement getting its own
+                                slots and shift
      n_pool_entries             size of the three per-entry arrays below
      entry_offset [host]        first pool token of each entry
      entry_len    [host]        tokens in each entry (>= 1)
