@@ -42,6 +42,8 @@ def parse(argv=None):
     p.add_argument("--decode-tokens", type=int, default=None,
                    help="decode tokens per step (default: the workload's decode steps, else 1)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-single-request", action="store_true",
+                   help="skip the requests-served-alone timing (profiling runs: only the batched launches)")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
     p.add_argument("--paged", action="store_true",
                    help="zero-copy TTFT: the prefill reads the documents from the pool through the "
@@ -512,7 +514,8 @@ def main():
                        "rope_local_global": w.local_global}
                       if (w.rope_pairing != "half" or w.rope_scaling or w.local_global) else {})},
         "ttft_ms_batch": ttft_ms,
-        **dict(zip(("ttft_ms_single_request", "ttft_ms_single_request_graph"), single_request_ttft(wl))),
+        **dict(zip(("ttft_ms_single_request", "ttft_ms_single_request_graph"),
+                   (None, None) if args.no_single_request else single_request_ttft(wl))),
         "prefill_attn_tflops": kernels["suffix_prefill_attn"]["achieved"],
         "rerotate_compose_gbps": kernels["compose"]["achieved"],
         "decode_gbps": kernels["decode_attn"]["achieved"],
