@@ -213,6 +213,23 @@ pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const 
                                    int32_t max_ctx, int32_t n_suffix, float scale, void* out,
                                    void* workspace, size_t ws_bytes, void* stream);
 
+/* ---- 3a. suffix prefill with fused RoPE (Sec. 5: the Reader turns request-time tokens to
+   their positions; Eq. 3's R(p) from the delta-angle table) ----
+   As pic_suffix_prefill_attn, but q and k_suf are given unrotated: the kernel turns query and
+   key rows of suffix token i of request b by R(ctx_len[b] + i) (the model's pairing and, with
+   per-layer tables, layer l's frequencies) as it loads them, in the float32 arithmetic and bf16
+   rounding of pic_rerotate_keys, and stores the turned keys into the cache.  The result is
+   bit-identical to turning q and k_suf with pic_rerotate_keys first and then calling
+   pic_suffix_prefill_attn.  bf16 only.
+     table, max_abs_delta   a pic_rope_table_init table with max_abs_delta >= max_ctx + n_suffix - 1
+   (other arguments and the workspace as for pic_suffix_prefill_attn) */
+pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q, const void* k_suf,
+                                        const void* v_suf, void* cache_k, void* cache_v,
+                                        int32_t batch, int32_t cache_cap, const int32_t* ctx_len,
+                                        int32_t max_ctx, int32_t n_suffix, const void* table,
+                                        int32_t max_abs_delta, float scale, void* out,
+                                        void* workspace, size_t ws_bytes, void* stream);
+
 /* ---- 3c. zero-copy (paged) suffix prefill (App. C.1 token map; Sec. 2, Eq. 3) ----
    pic_build_slot_map expands gather blocks into the token-level map from cache slots to the
    pool: slot_src[b][p] / slot_delta[b][p] = pool token and position shift of slot p of
@@ -293,6 +310,21 @@ pic_status pic_decode_attn(const pic_model* model, const void* q, const void* k_
                            int32_t cache_cap, const int32_t* base_len, int32_t step,
                            int32_t max_base_len, float scale, int32_t n_splits, void* out,
                            void* workspace, size_t ws_bytes, void* stream);
+
+/* ---- 4a. decode with fused RoPE ----
+   As pic_decode_attn, but q and k_new are given unrotated: the kernel turns them to the new
+   token's position p = base_len[b] + step (the model's pairing; per-layer tables: layer l's
+   frequencies) in the float32 arithmetic and bf16 rounding of pic_rerotate_keys, and stores
+   the turned key into the cache; bit-identical to turning them first and calling
+   pic_decode_attn.  bf16 only.
+     table, max_abs_delta   a pic_rope_table_init table with max_abs_delta >= max_base_len + step
+   (other arguments and the workspace as for pic_decode_attn) */
+pic_status pic_decode_attn_rope(const pic_model* model, const void* q, const void* k_new,
+                                const void* v_new, void* cache_k, void* cache_v, int32_t batch,
+                                int32_t cache_cap, const int32_t* base_len, int32_t step,
+                                int32_t max_base_len, const void* table, int32_t max_abs_delta,
+                                float scale, int32_t n_splits, void* out, void* workspace,
+                                size_t ws_bytes, void* stream);
 
 /* ---- diagnostics ---- */
 const char* pic_status_string(pic_status status);

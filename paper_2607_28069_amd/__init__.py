@@ -25,9 +25,11 @@ STATUS = {0: "PIC_OK", -1: "PIC_ERR_INVALID_ARG", -2: "PIC_ERR_UNSUPPORTED", -3:
 EXPORTS = ("pic_plan_layout", "pic_plan_frontier", "pic_rope_table_bytes", "pic_rope_table_init",
            "pic_rope_table_init_freq", "pic_rope_llama3_freq",
            "pic_rerotate_keys", "pic_compose", "pic_prefill_workspace_bytes",
-           "pic_suffix_prefill_attn", "pic_build_slot_map", "pic_paged_prefill_attn",
+           "pic_suffix_prefill_attn", "pic_suffix_prefill_attn_rope", "pic_build_slot_map",
+           "pic_paged_prefill_attn",
            "pic_frontier_workspace_bytes", "pic_frontier_prefill_attn",
-           "pic_decode_workspace_bytes", "pic_decode_attn", "pic_status_string", "pic_last_error",
+           "pic_decode_workspace_bytes", "pic_decode_attn", "pic_decode_attn_rope", "pic_status_string",
+           "pic_last_error",
            "pic_decode_auto_splits")
 
 
@@ -89,6 +91,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "pic_compose": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, P, I32, I32, P]),
         "pic_prefill_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_suffix_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, P, P, SZ, P]),
+        "pic_suffix_prefill_attn_rope": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, P, I32, F, P, P,
+                                                        SZ, P]),
         "pic_build_slot_map": (ctypes.c_int, [P, I32, I32, I32, P, P, P, P]),
         "pic_paged_prefill_attn": (ctypes.c_int, [MP, P, P, I64, P, P, I32, P, P, I32, P, P, P, P, P, I32, I32,
                                                   P, I32, I32, F, P, P, SZ, P]),
@@ -96,6 +100,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "pic_frontier_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, P, I32, I32, F, P, P, SZ, P]),
         "pic_decode_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_decode_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, I32, P, P, SZ, P]),
+        "pic_decode_attn_rope": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, P, I32, F, I32, P, P, SZ,
+                                                P]),
         "pic_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "pic_last_error": (ctypes.c_char_p, []),
         "pic_decode_auto_splits": (I32, [MP, I32, I32]),
@@ -244,6 +250,18 @@ def pic_suffix_prefill_attn(model: Model, q, k_suf, v_suf, cache_k, cache_v, bat
                                           _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
+def pic_suffix_prefill_attn_rope(model: Model, q, k_suf, v_suf, cache_k, cache_v, batch, cache_cap, ctx_len,
+                                 max_ctx, n_suffix, table, max_abs_delta, out, workspace=None, scale=0.0,
+                                 stream=None):
+    """q / k_suf unrotated: turned to positions ctx_len[b] + i inside the kernel."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().pic_suffix_prefill_attn_rope(ctypes.byref(model), _ptr(q), _ptr(k_suf), _ptr(v_suf),
+                                               _ptr(cache_k), _ptr(cache_v), int(batch), int(cache_cap),
+                                               _ptr(ctx_len), int(max_ctx), int(n_suffix), _ptr(table),
+                                               int(max_abs_delta), float(scale), _ptr(out), _ptr(workspace),
+                                               ws_bytes, _stream(stream)))
+
+
 def pic_slot_map_tiles(map_cap) -> int:
     """64-slot tiles per request in a tile map of `map_cap` slots."""
     return (int(map_cap) + PIC_BLOCK_TOKENS - 1) // PIC_BLOCK_TOKENS
@@ -300,6 +318,18 @@ def pic_decode_attn(model: Model, q, k_new, v_new, cache_k, cache_v, batch, cach
                                   _ptr(base_len), int(step), int(max_base_len), float(scale),
                                   int(n_splits), _ptr(out), _ptr(workspace), ws_bytes,
                                   _stream(stream)))
+
+
+def pic_decode_attn_rope(model: Model, q, k_new, v_new, cache_k, cache_v, batch, cache_cap, base_len, step,
+                         max_base_len, table, max_abs_delta, out, workspace=None, n_splits=0, scale=0.0,
+                         stream=None):
+    """q / k_new unrotated: turned to position base_len[b] + step inside the kernel."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().pic_decode_attn_rope(ctypes.byref(model), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                       _ptr(cache_k), _ptr(cache_v), int(batch), int(cache_cap),
+                                       _ptr(base_len), int(step), int(max_base_len), _ptr(table),
+                                       int(max_abs_delta), float(scale), int(n_splits), _ptr(out),
+                                       _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def pic_status_string(status: int) -> str:

@@ -17,7 +17,10 @@
 //  * the new token's K/V are read straight from k_new/v_new by the wave whose range holds slot p,
 //    and written into the cache by that workgroup (no separate append launch);
 //  * the 4 waves merge by log-sum-exp in LDS; a context split over several workgroups (only when
-//    (request, kv head) pairs alone do not fill the GPU) leaves fp32 partials for a combine pass.
+//    (request, kv head) pairs alone do not fill the GPU) leaves fp32 partials for a combine pass;
+//  * rope variant: q and k_new arrive unrotated and are turned to position p (the delta-angle
+//    table's row p) in registers -- the query once, the new key in the tile that holds it and
+//    where it is stored -- with the float32 arithmetic of the re-rotation kernel.
 #include <type_traits>
 
 #include "pic_internal.h"
@@ -54,9 +57,64 @@ struct DecodeArgs {
   float* ws_ml;           // [L][B][Hq][S][2]
   int32_t batch, cache_cap, n_q_heads, n_kv_heads, max_base, step, n_splits, chunk;
   float scale_log2;
+  const float2* table;    // rope variant: [L or 1][max_abs_delta + 1][D/2] cos/sin rows
+  int64_t table_stride;
+  int32_t max_abs_delta;
 };
 
+// (x, y) turned by (c, s) in the float32 form of the re-rotation kernel.
+__device__ __forceinline__ void rot_pair(float& x, float& y, float c, float s) {
+  const float u = x, v = y;
+  x = fmaf(u, c, -(v * s));
+  y = fmaf(u, s, v * c);
+}
+__device__ __forceinline__ void unpack8(u32x4 w, float (&x)[8]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(w[e] << 16);
+    x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ u32x4 pack8(const float (&x)[8]) {
+  return u32x4{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+               pack_bf16x2(x[6], x[7])};
+}
+// The 16 head dims 32 ks + 8 g4 .. + 8 (ks = 0..3) a lane holds of one row (the A / B operand
+// layout below), turned by row `trow` of the table: rotate-half pairs are chunks ks and ks + 2
+// (frequencies 32 ks + 8 g4 + j), interleaved pairs sit inside a chunk (16 ks + 4 g4 + m).
+template <bool kInterleaved>
+__device__ __forceinline__ void rot_operand(u32x4 (&c)[4], const float2* trow, int g4) {
+  if constexpr (!kInterleaved) {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      float x[8], y[8];
+      unpack8(c[ks], x);
+      unpack8(c[ks + 2], y);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float2 cs = trow[32 * ks + 8 * g4 + j];
+        rot_pair(x[j], y[j], cs.x, cs.y);
+      }
+      c[ks] = pack8(x);
+      c[ks + 2] = pack8(y);
+    }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      float x[8];
+      unpack8(c[ks], x);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const float2 cs = trow[16 * ks + 4 * g4 + m];
+        rot_pair(x[2 * m], x[2 * m + 1], cs.x, cs.y);
+      }
+      c[ks] = pack8(x);
+    }
+  }
+}
+
 // grid (S * B * Hkv, L), 256 threads
+template <bool kRope, bool kInterleaved>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 decode_bf16_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t v_lds0[kWaves * kVTileBytes];
@@ -89,10 +147,34 @@ decode_bf16_kernel(DecodeArgs a) {
 
   // The workgroup holding slot p writes the new token into the cache.  Nobody reads that row
   // from the cache during this launch: the wave whose range holds it reads k_new / v_new.
+  const float2* trow = kRope ? a.table + (int64_t)l * a.table_stride + (int64_t)min(p, a.max_abs_delta) * (kHD / 2)
+                             : nullptr;   // rope variant: cos/sin of position p
   if (p < a.cache_cap && p >= wc0 && p < wc1 && wave == 0 && lane < 32) {
     const int c = lane & 15;
     u32x4* dst = reinterpret_cast<u32x4*>((lane < 16 ? a.cache_k : a.cache_v) + (bh_kv * a.cache_cap + p) * kHD);
-    dst[c] = reinterpret_cast<const u32x4*>(lane < 16 ? Kn : Vn)[c];
+    if (kRope && lane < 16) {   // the new key turned to p: lane c < 8 takes a chunk pair
+      if (c < 8) {
+        // rotate-half: chunks c, c + 8 (frequencies 8 c ..); interleaved: 2 c, 2 c + 1 (8 c ..)
+        const int ca = kInterleaved ? 2 * c : c, cb = kInterleaved ? 2 * c + 1 : c + 8;
+        float x[8], y[8];
+        unpack8(reinterpret_cast<const u32x4*>(Kn)[ca], x);
+        unpack8(reinterpret_cast<const u32x4*>(Kn)[cb], y);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float2 cs = trow[8 * c + i];
+          if constexpr (kInterleaved) {
+            float* z = i < 4 ? x : y;
+            rot_pair(z[2 * (i & 3)], z[2 * (i & 3) + 1], cs.x, cs.y);
+          } else {
+            rot_pair(x[i], y[i], cs.x, cs.y);
+          }
+        }
+        dst[ca] = pack8(x);
+        dst[cb] = pack8(y);
+      }
+    } else {
+      dst[c] = reinterpret_cast<const u32x4*>(lane < 16 ? Kn : Vn)[c];
+    }
   }
 
   const int n = lane & 15, g4 = lane >> 4;
@@ -102,8 +184,12 @@ decode_bf16_kernel(DecodeArgs a) {
     const bool ok = n < n_rep;
     const int64_t qrow = ((int64_t)l * a.batch + b) * a.n_q_heads + g * n_rep + (ok ? n : 0);
     const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + qrow * kHD);
+    u32x4 qv[4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qop[ks] = as_bf16x8(ok ? qp[4 * ks + g4] : u32x4{0, 0, 0, 0});
+    for (int ks = 0; ks < 4; ++ks) qv[ks] = ok ? qp[4 * ks + g4] : u32x4{0, 0, 0, 0};
+    if constexpr (kRope) rot_operand<kInterleaved>(qv, trow, g4);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) qop[ks] = as_bf16x8(qv[ks]);
   }
 
   // K of one tile, straight into the A-operand layout: [mb][ks] = row k0 + 16 mb + n, head
@@ -163,6 +249,13 @@ decode_bf16_kernel(DecodeArgs a) {
     if (k0 + kTile < c1) {
       load_k(k0 + kTile, knext);
       load_v(k0 + kTile, vnext);
+    }
+    if constexpr (kRope) {   // the new token's key, read unrotated from k_new, turned to p
+      if (p >= k0 && p < k0 + kTile) {
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+          if (min(k0 + 16 * mb + n, c1 - 1) == p) rot_operand<kInterleaved>(kcur[mb], trow, g4);
+      }
     }
     f32x4_t sacc[2] = {f32x4_t{}, f32x4_t{}};
 #pragma unroll
@@ -326,7 +419,8 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
                               const bf16_t* v_new, bf16_t* cache_k, bf16_t* cache_v,
                               const int32_t* base_len, int32_t max_base, int32_t step,
                               int32_t n_splits, bf16_t* out, void* workspace, size_t,
-                              hipStream_t stream) {
+                              const float2* rope_table, int64_t table_stride, int32_t max_abs_delta,
+                              bool interleaved, hipStream_t stream) {
   if (s.batch == 0 || s.n_layers == 0) return hipSuccess;
   const int32_t max_len = max_base + step + 1;
   DecodeArgs a;
@@ -350,8 +444,16 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   const int32_t chunk = (max_len + n_splits - 1) / n_splits;
   a.chunk = (chunk + kWaves * kTile - 1) / (kWaves * kTile) * (kWaves * kTile);
   a.scale_log2 = s.scale_log2;
-  hipLaunchKernelGGL(decode_bf16_kernel, dim3(n_splits * s.batch * s.n_kv_heads, s.n_layers),
-                     dim3(256), 0, stream, a);
+  a.table = rope_table;
+  a.table_stride = table_stride;
+  a.max_abs_delta = max_abs_delta;
+  const dim3 grid(n_splits * s.batch * s.n_kv_heads, s.n_layers);
+  if (rope_table == nullptr)
+    hipLaunchKernelGGL((decode_bf16_kernel<false, false>), grid, dim3(256), 0, stream, a);
+  else if (interleaved)
+    hipLaunchKernelGGL((decode_bf16_kernel<true, true>), grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_bf16_kernel<true, false>), grid, dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_splits == 1) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(s.batch * s.n_q_heads, s.n_layers), dim3(64), 0,

@@ -449,6 +449,57 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
                     "prefill attention launch");
 }
 
+PIC_API pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q,
+                                                const void* k_suf, const void* v_suf,
+                                                void* cache_k, void* cache_v, int32_t batch,
+                                                int32_t cache_cap, const int32_t* ctx_len,
+                                                int32_t max_ctx, int32_t n_suffix,
+                                                const void* table, int32_t max_abs_delta,
+                                                float scale, void* out, void* workspace,
+                                                size_t ws_bytes, void* stream) {
+  PIC_CHECK(check_attn_model(model));
+  if (model->dtype != PIC_BF16)
+    return fail(PIC_ERR_UNSUPPORTED, "the fused-RoPE prefill is built for bf16 caches");
+  if (batch < 0 || cache_cap < 0 || max_ctx < 0 || n_suffix < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (!(scale >= 0.f) || !std::isfinite(scale))
+    return fail(PIC_ERR_INVALID_ARG, "scale must be finite and >= 0");
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
+    return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
+  if ((int64_t)max_ctx + n_suffix > cache_cap)
+    return fail(PIC_ERR_CAPACITY, "max_ctx + n_suffix = %lld exceeds cache_cap %d",
+                (long long)max_ctx + n_suffix, cache_cap);
+  if ((int64_t)max_ctx + n_suffix - 1 > max_abs_delta)
+    return fail(PIC_ERR_RANGE, "positions up to %lld need a table with max_abs_delta >= that, got %d",
+                (long long)max_ctx + n_suffix - 1, max_abs_delta);
+  if ((int64_t)batch * model->n_q_heads * n_suffix > INT32_MAX ||
+      (int64_t)n_suffix * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
+    return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
+  if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
+  PIC_CHECK(check_ptr(q, "q"));
+  PIC_CHECK(check_ptr(k_suf, "k_suf"));
+  PIC_CHECK(check_ptr(v_suf, "v_suf"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  PIC_CHECK(check_ptr(table, "table"));
+  PIC_CHECK(check_ptr(out, "out"));
+  if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
+  const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
+  if (need > 0 && (workspace == nullptr || ws_bytes < need))
+    return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
+  const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+  return hip_status(pic::launch_prefill_bf16_rope(
+                        s, model->rope_pairing == PIC_ROPE_INTERLEAVED,
+                        static_cast<const pic::bf16_t*>(q), static_cast<const pic::bf16_t*>(k_suf),
+                        static_cast<const pic::bf16_t*>(v_suf), static_cast<pic::bf16_t*>(cache_k),
+                        static_cast<pic::bf16_t*>(cache_v), ctx_len, max_ctx, n_suffix,
+                        static_cast<const float2*>(table), stride, max_abs_delta,
+                        static_cast<pic::bf16_t*>(out), workspace, ws_bytes, (hipStream_t)stream),
+                    "fused-RoPE prefill launch");
+}
+
 PIC_API pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch,
                                       int32_t map_cap, int32_t* slot_src, int32_t* slot_delta,
                                       int32_t* tile_map, void* stream) {
@@ -456,6 +507,7 @@ PIC_API pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks,
   if ((int64_t)batch * map_cap == 0) return ok();
   if (n_blocks > 0 && !blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
   if (!slot_src || !slot_delta) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL");
+  if (tile_map) PIC_CHECK(check_ptr(tile_map, "tile_map"));
   return hip_status(pic::launch_slot_map(blocks, n_blocks, batch, map_cap, slot_src, slot_delta,
                                          tile_map, (hipStream_t)stream),
                     "slot map launch");
@@ -502,6 +554,7 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
   PIC_CHECK(check_ptr(cache_v, "cache_v"));
   PIC_CHECK(check_ptr(out, "out"));
   if (!slot_src || !slot_delta) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL");
+  if (tile_map) PIC_CHECK(check_ptr(tile_map, "tile_map"));
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
   const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
   if (need > 0 && (workspace == nullptr || ws_bytes < need))
@@ -604,11 +657,13 @@ PIC_API size_t pic_decode_workspace_bytes(const pic_model* model, int32_t batch,
   return pic::decode_bf16_workspace(shape_of(model, batch, max_len, 0.f), max_len, n_splits);
 }
 
-PIC_API pic_status pic_decode_attn(const pic_model* model, const void* q, const void* k_new,
-                                   const void* v_new, void* cache_k, void* cache_v, int32_t batch,
-                                   int32_t cache_cap, const int32_t* base_len, int32_t step,
-                                   int32_t max_base_len, float scale, int32_t n_splits, void* out,
-                                   void* workspace, size_t ws_bytes, void* stream) {
+namespace {
+
+pic_status decode_impl(const pic_model* model, const void* q, const void* k_new, const void* v_new,
+                       void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
+                       const int32_t* base_len, int32_t step, int32_t max_base_len,
+                       const void* table, int32_t max_abs_delta, float scale, int32_t n_splits,
+                       void* out, void* workspace, size_t ws_bytes, void* stream) {
   PIC_CHECK(check_attn_model(model));
   if (batch < 0 || cache_cap < 0 || step < 0 || max_base_len < 0 || n_splits < 0)
     return fail(PIC_ERR_INVALID_ARG, "negative size");
@@ -632,6 +687,14 @@ PIC_API pic_status pic_decode_attn(const pic_model* model, const void* q, const 
   PIC_CHECK(check_ptr(cache_v, "cache_v"));
   PIC_CHECK(check_ptr(out, "out"));
   if (!base_len) return fail(PIC_ERR_INVALID_ARG, "base_len is NULL");
+  if (table) {   // fused RoPE: every position the call turns must be in the table
+    if (model->dtype != PIC_BF16)
+      return fail(PIC_ERR_UNSUPPORTED, "the fused-RoPE decode is built for bf16 caches");
+    PIC_CHECK(check_ptr(table, "table"));
+    if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta || max_len - 1 > max_abs_delta)
+      return fail(PIC_ERR_RANGE, "position %lld needs a table with max_abs_delta >= that, got %d",
+                  (long long)(max_len - 1), max_abs_delta);
+  }
   const hipStream_t st = (hipStream_t)stream;
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   if (model->dtype == PIC_F32) {
@@ -663,6 +726,32 @@ PIC_API pic_status pic_decode_attn(const pic_model* model, const void* q, const 
                                             static_cast<pic::bf16_t*>(cache_k),
                                             static_cast<pic::bf16_t*>(cache_v), base_len,
                                             max_base_len, step, n_splits,
-                                            static_cast<pic::bf16_t*>(out), workspace, ws_bytes, st),
+                                            static_cast<pic::bf16_t*>(out), workspace, ws_bytes,
+                                            static_cast<const float2*>(table),
+                                            n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0,
+                                            max_abs_delta, model->rope_pairing == PIC_ROPE_INTERLEAVED, st),
                     "decode attention launch");
+}
+
+}  // namespace
+
+PIC_API pic_status pic_decode_attn(const pic_model* model, const void* q, const void* k_new,
+                                   const void* v_new, void* cache_k, void* cache_v, int32_t batch,
+                                   int32_t cache_cap, const int32_t* base_len, int32_t step,
+                                   int32_t max_base_len, float scale, int32_t n_splits, void* out,
+                                   void* workspace, size_t ws_bytes, void* stream) {
+  return decode_impl(model, q, k_new, v_new, cache_k, cache_v, batch, cache_cap, base_len, step,
+                     max_base_len, nullptr, 0, scale, n_splits, out, workspace, ws_bytes, stream);
+}
+
+PIC_API pic_status pic_decode_attn_rope(const pic_model* model, const void* q, const void* k_new,
+                                        const void* v_new, void* cache_k, void* cache_v,
+                                        int32_t batch, int32_t cache_cap, const int32_t* base_len,
+                                        int32_t step, int32_t max_base_len, const void* table,
+                                        int32_t max_abs_delta, float scale, int32_t n_splits,
+                                        void* out, void* workspace, size_t ws_bytes, void* stream) {
+  if (!table) return fail(PIC_ERR_INVALID_ARG, "table is NULL");
+  return decode_impl(model, q, k_new, v_new, cache_k, cache_v, batch, cache_cap, base_len, step,
+                     max_base_len, table, max_abs_delta, scale, n_splits, out, workspace, ws_bytes,
+                     stream);
 }

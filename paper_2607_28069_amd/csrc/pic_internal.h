@@ -99,6 +99,16 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
                                      int32_t max_len, bf16_t* out, void* workspace,
                                      size_t ws_bytes, hipStream_t stream);
 
+// Suffix prefill with q / k_suf given unrotated: both are turned to positions ctx_len[b] + i
+// with the delta-angle table (layer l's block at table + l * table_stride) as they are loaded;
+// the cache receives the turned keys.  Positions must be <= max_abs_delta.
+hipError_t launch_prefill_bf16_rope(const AttnShape& s, bool interleaved, const bf16_t* q,
+                                    const bf16_t* k_suf, const bf16_t* v_suf, bf16_t* cache_k,
+                                    bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
+                                    int32_t n_suffix, const float2* table, int64_t table_stride,
+                                    int32_t max_abs_delta, bf16_t* out, void* workspace,
+                                    size_t ws_bytes, hipStream_t stream);
+
 // Token-level slot map: slot_src / slot_delta [batch][map_cap] = pool token and position shift
 // of every slot the gather blocks cover (0 / 0 elsewhere).  With tile_map (may be NULL):
 // [batch][slot_map_tiles(map_cap)][2] = (src, shift) for every 64-slot tile that is pool tokens
@@ -123,11 +133,14 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
 
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len);
 size_t decode_bf16_workspace(const AttnShape& s, int32_t max_len, int32_t n_splits);
-// Also writes k_new / v_new into slot base_len[b] + step of the cache.
+// Also writes k_new / v_new into slot base_len[b] + step of the cache.  With rope_table, q and
+// k_new are given unrotated and turned to that position (table block of layer l at
+// rope_table + l * table_stride; positions <= max_abs_delta).
 hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_new,
                               const bf16_t* v_new, bf16_t* cache_k, bf16_t* cache_v,
                               const int32_t* base_len, int32_t max_base, int32_t step,
                               int32_t n_splits, bf16_t* out, void* workspace, size_t ws_bytes,
-                              hipStream_t stream);
+                              const float2* rope_table, int64_t table_stride, int32_t max_abs_delta,
+                              bool interleaved, hipStream_t stream);
 
 }  // namespace pic

@@ -124,12 +124,48 @@ struct PrefillArgs {
   float scale_log2;
 };
 
-constexpr int kModeSuffix = 0, kModeTable = 1, kModePaged = 2;
+// Rope mode = suffix mode with the suffix queries and keys given unrotated: the kernel turns
+// them to their positions (RoPE at ctx + i, from the delta-angle table) as they are loaded.
+constexpr int kModeSuffix = 0, kModeTable = 1, kModePaged = 2, kModeRope = 3;
+
+// (x, y) turned by the angle with cosine c and sine s, in the float32 arithmetic the compose
+// and re-rotation kernels use, so fused and separate rotations round identically.
+__device__ __forceinline__ void rot_pair(float& x, float& y, float c, float s) {
+  const float u = x, v = y;
+  x = fmaf(u, c, -(v * s));
+  y = fmaf(u, s, v * c);
+}
+__device__ __forceinline__ void unpack8(u32x4 w, float (&x)[8]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(w[e] << 16);
+    x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ u32x4 pack8(const float (&x)[8]) {
+  return u32x4{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+               pack_bf16x2(x[6], x[7])};
+}
+// Pairs of two 16-byte chunks x1, x2 turned by frequencies f0 .. f0 + 7 of table row `row`
+// (cos, sin pairs): rotate-half pairs (x1[i], x2[i]); interleaved pairs (2i, 2i + 1) of x1 then x2.
+template <bool kInterleaved>
+__device__ __forceinline__ void rot_chunks(float (&x1)[8], float (&x2)[8], const float2* row, int f0) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float2 cs = row[f0 + i];
+    if constexpr (kInterleaved) {
+      float* x = i < 4 ? x1 : x2;
+      rot_pair(x[2 * (i & 3)], x[2 * (i & 3) + 1], cs.x, cs.y);
+    } else {
+      rot_pair(x1[i], x2[i], cs.x, cs.y);
+    }
+  }
+}
 
 template <int kMode, bool kInterleaved>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_bf16_kernel(PrefillArgs a) {
-  constexpr bool kTable = kMode == kModeTable, kPaged = kMode == kModePaged;
+  constexpr bool kTable = kMode == kModeTable, kPaged = kMode == kModePaged, kRope = kMode == kModeRope;
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
   // loads in flight into one buffer do not alias reads from another.  (The larger alignment
   // places them first, at the bottom of LDS, ahead of the paged mode's bigger areas.)
@@ -223,7 +259,29 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int64_t suf_stride = (int64_t)a.n_kv_heads * kHD;
   const bf16_t* Ks = kTable ? nullptr : a.k_suf + suf0;
   const bf16_t* Vs = kTable ? nullptr : a.v_suf + suf0;
-  if (!kTable && mt == 0 && split == 0) {   // cache assembly: suffix rows into slots [ctx, ctx + n_suffix)
+  if (kRope && mt == 0 && split == 0) {   // cache assembly with the suffix keys turned to ctx + i
+    const float2* trow0 = a.table + (int64_t)l * a.table_stride;
+    for (int c = tid; c < a.n_suffix * 24; c += kThreads) {
+      const int i = c / 24, part = c - 24 * (c / 24);   // row i: K chunk pair part (< 8), V chunk part - 8
+      if (part < 8) {
+        // rotate-half: chunks part, part + 8; interleaved: chunks 2 part, 2 part + 1 (both:
+        // frequencies 8 part .. 8 part + 7)
+        const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : 64 + 8 * part;
+        float x1[8], x2[8];
+        unpack8(*reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o1), x1);
+        unpack8(*reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o2), x2);
+        const int32_t pos = min(ctx + i, a.max_abs_delta);
+        rot_chunks<kInterleaved>(x1, x2, trow0 + (int64_t)pos * (kHD / 2), 8 * part);
+        bf16_t* dst = a.cache_k + (bh_kv + ctx + i) * kHD;
+        *reinterpret_cast<u32x4*>(dst + o1) = pack8(x1);
+        *reinterpret_cast<u32x4*>(dst + o2) = pack8(x2);
+      } else {
+        const int ch = part - 8;
+        *reinterpret_cast<u32x4*>(a.cache_v + (bh_kv + ctx + i) * kHD + 8 * ch) =
+            *reinterpret_cast<const u32x4*>(Vs + i * suf_stride + 8 * ch);
+      }
+    }
+  } else if (!kTable && mt == 0 && split == 0) {   // cache assembly: suffix rows into slots [ctx, ctx + n_suffix)
     for (int c = tid; c < a.n_suffix * 32; c += kThreads) {
       const int i = c >> 5, part = c & 31;           // row i, 16-byte chunk part % 16 of K or V
       const int64_t src = i * suf_stride + 8 * (part & 15);
@@ -245,6 +303,34 @@ prefill_bf16_kernel(PrefillArgs a) {
     const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + qrow * kHD);
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0});
+  }
+  if constexpr (kRope) {   // queries turned to their positions
+    const float2* trow = a.table + (int64_t)l * a.table_stride + (int64_t)min(qpos, a.max_abs_delta) * (kHD / 2);
+    if constexpr (!kInterleaved) {
+      // pairs (d, d + 64): chunks ks and ks + 4, frequencies 16 ks + 8 hh .. + 7
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        float x1[8], x2[8];
+        unpack8(__builtin_bit_cast(u32x4, qop[ks]), x1);
+        unpack8(__builtin_bit_cast(u32x4, qop[ks + 4]), x2);
+        rot_chunks<false>(x1, x2, trow, 16 * ks + 8 * hh);
+        qop[ks] = as_bf16x8(pack8(x1));
+        qop[ks + 4] = as_bf16x8(pack8(x2));
+      }
+    } else {
+      // pairs (2i, 2i + 1) inside each chunk: dims 16 ks + 8 hh + 2m, frequency 8 ks + 4 hh + m
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        float x[8];
+        unpack8(__builtin_bit_cast(u32x4, qop[ks]), x);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const float2 cs = trow[8 * ks + 4 * hh + m];
+          rot_pair(x[2 * m], x[2 * m + 1], cs.x, cs.y);
+        }
+        qop[ks] = as_bf16x8(pack8(x));
+      }
+    }
   }
   if constexpr (kPaged) {   // keep the unturned operand (lane-private slots)
 #pragma unroll
@@ -502,6 +588,30 @@ prefill_bf16_kernel(PrefillArgs a) {
                                          pack_bf16x2(x2[4], x2[5]), pack_bf16x2(x2[6], x2[7])};
   };
   auto wait_loads = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };   // vmcnt(0)
+  // Rope mode: turn the suffix rows (keys ctx .. n_keys - 1) of K tile t, landed in `kt`, to
+  // their positions; this lane's item is chunks rot_c and rot_c + 8 of row rot_row.
+  auto rope_own = [&](uint8_t* kt, int t) {
+    const int k = t * kKeys + rot_row;
+    if (k < ctx || k >= n_keys) return;
+    uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz(rot_row)) << 4);
+    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz(rot_row)) << 4);
+    float x1[8], x2[8];
+    unpack8(*reinterpret_cast<const u32x4*>(p1), x1);
+    unpack8(*reinterpret_cast<const u32x4*>(p2), x2);
+    const float2* trow = a.table + (int64_t)l * a.table_stride + (int64_t)min(k, a.max_abs_delta) * (kHD / 2);
+    if constexpr (!kInterleaved) {
+      rot_chunks<false>(x1, x2, trow, 8 * rot_c);   // pairs (d, d + 64), frequencies 8 c ..
+    } else {   // pairs inside each chunk: chunk c has frequencies 4 c .., chunk c + 8 32 + 4 c ..
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const float2 c1 = trow[4 * rot_c + m], c2 = trow[32 + 4 * rot_c + m];
+        rot_pair(x1[2 * m], x1[2 * m + 1], c1.x, c1.y);
+        rot_pair(x2[2 * m], x2[2 * m + 1], c2.x, c2.y);
+      }
+    }
+    *reinterpret_cast<u32x4*>(p1) = pack8(x1);
+    *reinterpret_cast<u32x4*>(p2) = pack8(x2);
+  };
 
   // ---- per-lane LDS read offsets, fixed for the whole loop (buffer, 32-row block and
   // 16-row slice steps are immediate offsets)
@@ -634,6 +744,10 @@ prefill_bf16_kernel(PrefillArgs a) {
     load_tile(Vg, v_lds0, t0, true);
     if (n_tiles > 1) load_tile(Kg, k_lds1, t0 + 1, false);
     wait_loads();
+    if constexpr (kRope) {
+      if ((t0 + 1) * kKeys > ctx) rope_own(k_lds0, t0);
+      if (n_tiles > 1 && (t0 + 2) * kKeys > ctx) rope_own(k_lds1, t0 + 1);
+    }
   }
   __syncthreads();
   f32x16_t s_a[2], s_b[2];   // scores of the current / next tile, swapped every tile
@@ -718,6 +832,9 @@ prefill_bf16_kernel(PrefillArgs a) {
 
     if (t + 1 < n_tiles) finish_scores(t0 + t + 1, snext);
     wait_loads();
+    if constexpr (kRope) {
+      if (t + 2 < n_tiles && (t0 + t + 3) * kKeys > ctx) rope_own(k_free, t0 + t + 2);
+    }
     if constexpr (kPaged) {
       if (t + 2 < n_tiles && run_k < 0) rotate_own(k_free, t0 + t + 2, d_k);
       const bool rows_f = run_f < 0 && ctx > 0;
@@ -931,6 +1048,10 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
   const dim3 grid(per_xcd * kNumXcd, s.n_layers);
   if (mode == kModeTable)
     hipLaunchKernelGGL((prefill_bf16_kernel<kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRope && interleaved)
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRope, true>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRope)
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRope, false>), grid, dim3(kThreads), 0, stream, a);
   else if (mode == kModePaged && interleaved)
     hipLaunchKernelGGL((prefill_bf16_kernel<kModePaged, true>), grid, dim3(kThreads), 0, stream, a);
   else if (mode == kModePaged)
@@ -962,6 +1083,27 @@ hipError_t launch_prefill_bf16(const AttnShape& s, const bf16_t* q, const bf16_t
   a.out = out;
   a.max_ctx = max_ctx;
   return launch(s, a, kModeSuffix, false, n_suffix, max_ctx, workspace, ws_bytes, stream);
+}
+
+hipError_t launch_prefill_bf16_rope(const AttnShape& s, bool interleaved, const bf16_t* q,
+                                    const bf16_t* k_suf, const bf16_t* v_suf, bf16_t* cache_k,
+                                    bf16_t* cache_v, const int32_t* ctx_len, int32_t max_ctx,
+                                    int32_t n_suffix, const float2* table, int64_t table_stride,
+                                    int32_t max_abs_delta, bf16_t* out, void* workspace,
+                                    size_t ws_bytes, hipStream_t stream) {
+  PrefillArgs a = {};
+  a.q = q;
+  a.k_suf = k_suf;
+  a.v_suf = v_suf;
+  a.cache_k = cache_k;
+  a.cache_v = cache_v;
+  a.ctx_len = ctx_len;
+  a.out = out;
+  a.max_ctx = max_ctx;
+  a.table = table;
+  a.table_stride = table_stride;
+  a.max_abs_delta = max_abs_delta;
+  return launch(s, a, kModeRope, interleaved, n_suffix, max_ctx, workspace, ws_bytes, stream);
 }
 
 hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const bf16_t* cache_k,

@@ -249,6 +249,8 @@ def test_argument_checks_fail_before_any_launch(lib):
     assert _paged(lib, m, mad=-1) == -6
     assert _paged(lib, m, pool_tokens=0) == -6           # documents but no pool
     assert _paged(lib, m, q=MIS) == -5
+    assert _paged(lib, m, tmap=MIS) == -5
+    assert lib.pic_build_slot_map(FAKE, 4, 2, 500, FAKE, FAKE, MIS, None) == -5
     assert _paged(lib, _model(dtype="f32")) == -2
     assert _paged(lib, m, ws=None, ws_bytes=0, max_ctx=4000, map_cap=4000, cap=5000) == -3   # split-K
     assert _paged(lib, m, batch=0) == 0
@@ -256,6 +258,20 @@ def test_argument_checks_fail_before_any_launch(lib):
     assert lib.pic_build_slot_map(None, 4, 2, 500, FAKE, FAKE, None, None) == -1
     assert lib.pic_build_slot_map(FAKE, -1, 2, 500, FAKE, FAKE, None, None) == -1
     assert lib.pic_build_slot_map(FAKE, 4, 0, 500, FAKE, FAKE, FAKE, None) == 0   # empty map
+
+    # fused RoPE: the table must cover every position the call turns
+    rp = lambda mm, table=FAKE, mad=600, ws_bytes=1 << 30: lib.pic_suffix_prefill_attn_rope(
+        ctypes.byref(mm), FAKE, FAKE, FAKE, FAKE, FAKE, 2, 600, FAKE, 500, 64, table, mad, 0.0, FAKE, FAKE,
+        ws_bytes, None)
+    assert rp(m, mad=562) == -6                          # positions up to 563
+    assert rp(m, table=None) == -1
+    assert rp(m, table=MIS) == -5
+    assert rp(_model(dtype="f32", head_dim=64)) == -2
+    rd = lambda table=FAKE, mad=600: lib.pic_decode_attn_rope(
+        ctypes.byref(m), FAKE, FAKE, FAKE, FAKE, FAKE, 2, 600, FAKE, 3, 500, table, mad, 0.0, 0, FAKE, FAKE,
+        1 << 30, None)
+    assert rd(mad=502) == -6                             # position 503
+    assert rd(table=None) == -1
 
     assert _decode(lib, m, step=100) == -4               # 500 + 100 + 1 > 600
     assert _decode(lib, m, ws=None) == -3
