@@ -45,6 +45,9 @@ def parse(argv=None):
     p.add_argument("--no-single-request", action="store_true",
                    help="skip the requests-served-alone timing (profiling runs: only the batched launches)")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    p.add_argument("--fused-rope", action="store_true",
+                   help="suffix and decode tokens arrive unrotated: the prefill and decode kernels turn them "
+                        "to their positions (pic_suffix_prefill_attn_rope / pic_decode_attn_rope)")
     p.add_argument("--paged", action="store_true",
                    help="zero-copy TTFT: the prefill reads the documents from the pool through the "
                         "gather map; the composed cache is built after the first token, for decode")
@@ -91,7 +94,8 @@ class DeviceWorkload:
     `layers` < w.n_layers builds a workload with fewer layers of the same per-layer shape.
     """
 
-    def __init__(self, w, dev, n_dec: int, layers: int | None = None, paged: bool = False):
+    def __init__(self, w, dev, n_dec: int, layers: int | None = None, paged: bool = False,
+                 fused_rope: bool = False):
         import numpy as np
         import torch
 
@@ -100,6 +104,7 @@ class DeviceWorkload:
 
         self.w, self.dev, self.n_dec = w, dev, n_dec
         self.paged = paged
+        self.fused_rope = fused_rope
         self.L = L = w.n_layers if layers is None else layers
         self.dt = dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
         B, Hq, Hkv, D = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
@@ -162,6 +167,8 @@ class DeviceWorkload:
         self.ctx_dev = torch.from_numpy(self.ctx_host.astype(np.int32)).to(dev)
         self.base_dev = torch.from_numpy(self.length_host.astype(np.int32)).to(dev)
         self.max_base = self.max_len
+        assert not (fused_rope and (paged or self.frontier or w.dtype != "bf16")), \
+            "fused RoPE serves the plain bf16 layout"
         if self.frontier:
             nbytes = pic.pic_frontier_workspace_bytes(self.m1, B, Ls, self.max_len)
         else:
@@ -233,6 +240,11 @@ class DeviceWorkload:
                                               self.cache_k[l], self.cache_v[l], B, self.cap,
                                               self.pos_dev, self.n_valid_dev, Ls, self.max_len,
                                               self.out[l], self.ws_pre)
+            elif self.fused_rope:
+                pic.pic_suffix_prefill_attn_rope(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
+                                                 self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
+                                                 self.max_ctx, Ls, self.table[l * block:], self.mad, self.out[l],
+                                                 self.ws_pre)
             else:
                 pic.pic_suffix_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
                                             self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
@@ -250,9 +262,14 @@ class DeviceWorkload:
         d0.record(stream)
         for t in range(self.n_dec):
             for l in range(L):
-                pic.pic_decode_attn(self.m1, self.dq[l], self.dk[l], self.dv[l], self.cache_k[l],
-                                    self.cache_v[l], B, self.cap, self.base_dev, t, self.max_base,
-                                    self.dout[t, l], self.ws_dec)
+                if self.fused_rope:
+                    pic.pic_decode_attn_rope(self.m1, self.dq[l], self.dk[l], self.dv[l], self.cache_k[l],
+                                             self.cache_v[l], B, self.cap, self.base_dev, t, self.max_base,
+                                             self.table[l * block:], self.mad, self.dout[t, l], self.ws_dec)
+                else:
+                    pic.pic_decode_attn(self.m1, self.dq[l], self.dk[l], self.dv[l], self.cache_k[l],
+                                        self.cache_v[l], B, self.cap, self.base_dev, t, self.max_base,
+                                        self.dout[t, l], self.ws_dec)
         d1.record(stream)
         if calib is not None:
             calib[1].copy_(calib[0])
@@ -336,6 +353,9 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
             elif wl.frontier:
                 pic.pic_frontier_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, pos_dev, nv_i, Ls, n_keys,
                                               out, ws)
+            elif wl.fused_rope:
+                pic.pic_suffix_prefill_attn_rope(wl.m1, q, k, v, ck, cv, 1, wl.cap, ctx_i, n_keys, Ls, tab, wl.mad,
+                                                 out, ws)
             else:
                 pic.pic_suffix_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, ctx_i, n_keys, Ls, out, ws)
 
@@ -438,7 +458,7 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     n_dec = args.decode_tokens if args.decode_tokens is not None else (w.decode_steps or 1)
-    wl = DeviceWorkload(w, dev, n_dec, paged=args.paged)
+    wl = DeviceWorkload(w, dev, n_dec, paged=args.paged, fused_rope=args.fused_rope)
     calib = None
     if args.copy_calib_gib > 0:
         n = int(args.copy_calib_gib * (1 << 30)) // 2
@@ -508,6 +528,8 @@ def main():
                    "docs_per_request": w.docs_per_request,
                    **({"ttft_path": "paged (zero-copy prefill; cache composed after the first token)"}
                       if args.paged else {}),
+                   **({"request_tokens": "unrotated; RoPE fused into the prefill and decode kernels"}
+                      if args.fused_rope else {}),
                    **({"inline_prefix": w.inline_prefix, "inline_span": w.inline_span,
                        "inline_tokens": Ls} if w.frontier else {}),
                    **({"rope_pairing": w.rope_pairing, "rope_scaling": w.rope_scaling,
