@@ -306,3 +306,35 @@ def test_llama8b_single_request_path():
         got = np.transpose(_host(wl.out[l, r])[toks], (1, 0, 2))
         assert_attn_close(got, ref, w.dtype)
         print(f"[c3 single request] layer {l} ok", flush=True)
+
+
+def test_fused_rope_full_size():
+    # The 32-layer Llama shape with unrotated request-time tokens (`bench.py --fused-rope`), two
+    # layers: prefill outputs, caches and a decode step bit-identical to turning q / k with the
+    # re-rotation kernel first and running the plain calls.
+    import paper_2607_28069_amd as pic
+    w = synth.get("c3")
+    wl = DeviceWorkload(w, DEV, n_dec=1, layers=2, fused_rope=True)
+    wl.step()
+    torch.cuda.synchronize()
+    out_f, dout_f = wl.out.clone(), wl.dout.clone()
+    ck_f, cv_f = wl.cache_k.clone(), wl.cache_v.clone()
+    B, Ls, Hq, Hkv, D = w.batch, w.n_suffix, w.n_q_heads, w.n_kv_heads, w.head_dim
+    pos = (wl.ctx_host.astype(np.int64)[:, None] + np.arange(Ls)[None, :]).reshape(-1).astype(np.int32)
+    pos_d = torch.from_numpy(pos).to(DEV)
+    dpos_d = torch.from_numpy(wl.length_host.astype(np.int32)).to(DEV)   # decode step 0
+    wl.fused_rope = False
+    for name, shape, p in (("q", (B * Ls, Hq, D), pos_d), ("k_suf", (B * Ls, Hkv, D), pos_d),
+                           ("dq", (B, Hq, D), dpos_d), ("dk", (B, Hkv, D), dpos_d)):
+        t = getattr(wl, name)
+        for l in range(wl.L):
+            x = t[l].reshape(shape).contiguous()
+            pic.pic_rerotate_keys(wl.m1, x, x, shape[0], shape[1], p, wl.table, wl.mad)
+            t[l].copy_(x.reshape(t[l].shape))
+    wl.step()
+    torch.cuda.synchronize()
+    assert torch.equal(out_f, wl.out), "fused-RoPE prefill differs from turn-then-prefill"
+    assert torch.equal(dout_f, wl.dout), "fused-RoPE decode differs from turn-then-decode"
+    assert torch.equal(ck_f, wl.cache_k) and torch.equal(cv_f, wl.cache_v), "caches differ"
+    print("[c3 fused rope] 2 layers bit-identical to turned inputs + plain calls", flush=True)
+    _check_request(wl, 1, 5, tokens=[0, 127], decode_steps=1)   # the turned-input run vs the oracle
