@@ -173,8 +173,8 @@ prefill_bf16_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(4096))) uint8_t k_lds1[kTileBytes];
   __shared__ __attribute__((aligned(4096))) uint8_t v_lds0[kTileBytes];
   __shared__ __attribute__((aligned(4096))) uint8_t v_lds1[kTileBytes];
-  // paged mode: each wave's cos/sin of the key rows it turns (4 KB per wave)
-  __shared__ __attribute__((aligned(16))) uint8_t cs_lds[kPaged ? kWaves * 4096 : 16];
+  // paged and rope modes: each wave's cos/sin of the key rows it turns (4 KB per wave)
+  __shared__ __attribute__((aligned(16))) uint8_t cs_lds[(kPaged || kRope) ? kWaves * 4096 : 16];
   // paged mode: each wave's unturned Q^T operand (8 KB per wave), the source of every turn
   __shared__ __attribute__((aligned(16))) uint8_t q_lds[kPaged ? kWaves * 8192 : 16];
 
@@ -260,25 +260,56 @@ prefill_bf16_kernel(PrefillArgs a) {
   const bf16_t* Ks = kTable ? nullptr : a.k_suf + suf0;
   const bf16_t* Vs = kTable ? nullptr : a.v_suf + suf0;
   if (kRope && mt == 0 && split == 0) {   // cache assembly with the suffix keys turned to ctx + i
+    // item c: row i = c / 24; part < 8: K chunk pair part (rotate-half: chunks part, part + 8;
+    // interleaved: 2 part, 2 part + 1; both: frequencies 8 part .. 8 part + 7), part >= 8: V
+    // chunk part - 8.  Three items per thread per pass, all loads issued before any math.
     const float2* trow0 = a.table + (int64_t)l * a.table_stride;
-    for (int c = tid; c < a.n_suffix * 24; c += kThreads) {
-      const int i = c / 24, part = c - 24 * (c / 24);   // row i: K chunk pair part (< 8), V chunk part - 8
-      if (part < 8) {
-        // rotate-half: chunks part, part + 8; interleaved: chunks 2 part, 2 part + 1 (both:
-        // frequencies 8 part .. 8 part + 7)
-        const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : 64 + 8 * part;
-        float x1[8], x2[8];
-        unpack8(*reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o1), x1);
-        unpack8(*reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o2), x2);
-        const int32_t pos = min(ctx + i, a.max_abs_delta);
-        rot_chunks<kInterleaved>(x1, x2, trow0 + (int64_t)pos * (kHD / 2), 8 * part);
-        bf16_t* dst = a.cache_k + (bh_kv + ctx + i) * kHD;
-        *reinterpret_cast<u32x4*>(dst + o1) = pack8(x1);
-        *reinterpret_cast<u32x4*>(dst + o2) = pack8(x2);
-      } else {
-        const int ch = part - 8;
-        *reinterpret_cast<u32x4*>(a.cache_v + (bh_kv + ctx + i) * kHD + 8 * ch) =
-            *reinterpret_cast<const u32x4*>(Vs + i * suf_stride + 8 * ch);
+    const int total = a.n_suffix * 24;
+    for (int c0 = tid; c0 < total; c0 += 3 * kThreads) {
+      u32x4 w1[3], w2[3];
+      float4 cs[3][4];
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const int c = c0 + u * kThreads;
+        if (c >= total) continue;
+        const int i = c / 24, part = c - 24 * i;
+        if (part < 8) {
+          const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : 64 + 8 * part;
+          w1[u] = *reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o1);
+          w2[u] = *reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o2);
+          const float4* row = reinterpret_cast<const float4*>(trow0 + (int64_t)min(ctx + i, a.max_abs_delta) * (kHD / 2));
+#pragma unroll
+          for (int j = 0; j < 4; ++j) cs[u][j] = row[4 * part + j];
+        } else {
+          w1[u] = *reinterpret_cast<const u32x4*>(Vs + i * suf_stride + 8 * (part - 8));
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const int c = c0 + u * kThreads;
+        if (c >= total) continue;
+        const int i = c / 24, part = c - 24 * i;
+        if (part < 8) {
+          const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : 64 + 8 * part;
+          float x1[8], x2[8];
+          unpack8(w1[u], x1);
+          unpack8(w2[u], x2);
+          const float2* cs2 = reinterpret_cast<const float2*>(cs[u]);   // frequencies 8 part + 0..7
+#pragma unroll
+          for (int f = 0; f < 8; ++f) {
+            if constexpr (kInterleaved) {
+              float* z = f < 4 ? x1 : x2;
+              rot_pair(z[2 * (f & 3)], z[2 * (f & 3) + 1], cs2[f].x, cs2[f].y);
+            } else {
+              rot_pair(x1[f], x2[f], cs2[f].x, cs2[f].y);
+            }
+          }
+          bf16_t* dst = a.cache_k + (bh_kv + ctx + i) * kHD;
+          *reinterpret_cast<u32x4*>(dst + o1) = pack8(x1);
+          *reinterpret_cast<u32x4*>(dst + o2) = pack8(x2);
+        } else {
+          *reinterpret_cast<u32x4*>(a.cache_v + (bh_kv + ctx + i) * kHD + 8 * (part - 8)) = w1[u];
+        }
       }
     }
   } else if (!kTable && mt == 0 && split == 0) {   // cache assembly: suffix rows into slots [ctx, ctx + n_suffix)
@@ -304,7 +335,9 @@ prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0});
   }
-  if constexpr (kRope) {   // queries turned to their positions
+  // rope mode: queries turned to their positions (called once the first tiles' loads are in
+  // flight, so the table reads overlap them)
+  auto rope_q = [&]() {
     const float2* trow = a.table + (int64_t)l * a.table_stride + (int64_t)min(qpos, a.max_abs_delta) * (kHD / 2);
     if constexpr (!kInterleaved) {
       // pairs (d, d + 64): chunks ks and ks + 4, frequencies 16 ks + 8 hh .. + 7
@@ -331,7 +364,7 @@ prefill_bf16_kernel(PrefillArgs a) {
         qop[ks] = as_bf16x8(pack8(x));
       }
     }
-  }
+  };
   if constexpr (kPaged) {   // keep the unturned operand (lane-private slots)
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
@@ -590,7 +623,18 @@ prefill_bf16_kernel(PrefillArgs a) {
   auto wait_loads = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };   // vmcnt(0)
   // Rope mode: turn the suffix rows (keys ctx .. n_keys - 1) of K tile t, landed in `kt`, to
   // their positions; this lane's item is chunks rot_c and rot_c + 8 of row rot_row.
-  auto rope_own = [&](uint8_t* kt, int t) {
+  auto rope_cs = [&](int t) {   // this lane's cos/sin for its suffix row of K tile t -> cos/sin area
+    const int k = t * kKeys + rot_row;
+    if (k < ctx || k >= n_keys) return;
+    const float2* row = a.table + (int64_t)l * a.table_stride + (int64_t)min(k, a.max_abs_delta) * (kHD / 2);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {   // the frequency pairs the paged key turn uses (see load_cs)
+      const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : 32 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
+      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + f),
+                                       (LDS_AS void*)(cs_lds + wave * 4096 + j * 1024), 16, 0, 0);
+    }
+  };
+  auto rope_own = [&](uint8_t* kt, int t) {   // after rope_cs(t) has landed
     const int k = t * kKeys + rot_row;
     if (k < ctx || k >= n_keys) return;
     uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz(rot_row)) << 4);
@@ -598,15 +642,22 @@ prefill_bf16_kernel(PrefillArgs a) {
     float x1[8], x2[8];
     unpack8(*reinterpret_cast<const u32x4*>(p1), x1);
     unpack8(*reinterpret_cast<const u32x4*>(p2), x2);
-    const float2* trow = a.table + (int64_t)l * a.table_stride + (int64_t)min(k, a.max_abs_delta) * (kHD / 2);
-    if constexpr (!kInterleaved) {
-      rot_chunks<false>(x1, x2, trow, 8 * rot_c);   // pairs (d, d + 64), frequencies 8 c ..
-    } else {   // pairs inside each chunk: chunk c has frequencies 4 c .., chunk c + 8 32 + 4 c ..
+    float cs[8], sn[8];
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const float2 c1 = trow[4 * rot_c + m], c2 = trow[32 + 4 * rot_c + m];
-        rot_pair(x1[2 * m], x1[2 * m + 1], c1.x, c1.y);
-        rot_pair(x2[2 * m], x2[2 * m + 1], c2.x, c2.y);
+    for (int j = 0; j < 4; ++j) {
+      const float4 v = *reinterpret_cast<const float4*>(cs_lds + wave * 4096 + j * 1024 + 16 * lane);
+      cs[2 * j] = v.x;
+      sn[2 * j] = v.y;
+      cs[2 * j + 1] = v.z;
+      sn[2 * j + 1] = v.w;
+    }
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      if constexpr (kInterleaved) {   // chunk c: pairs of frequencies 4 c ..; chunk c + 8: 32 + 4 c ..
+        float* x = f < 4 ? x1 : x2;
+        rot_pair(x[2 * (f & 3)], x[2 * (f & 3) + 1], cs[f], sn[f]);
+      } else {                         // pairs (d, d + 64): frequencies 8 c ..
+        rot_pair(x1[f], x2[f], cs[f], sn[f]);
       }
     }
     *reinterpret_cast<u32x4*>(p1) = pack8(x1);
@@ -743,10 +794,18 @@ prefill_bf16_kernel(PrefillArgs a) {
     load_tile(Kg, k_lds0, t0, false);
     load_tile(Vg, v_lds0, t0, true);
     if (n_tiles > 1) load_tile(Kg, k_lds1, t0 + 1, false);
+    if constexpr (kRope) {
+      if ((t0 + 1) * kKeys > ctx) rope_cs(t0);
+      rope_q();
+    }
     wait_loads();
     if constexpr (kRope) {
       if ((t0 + 1) * kKeys > ctx) rope_own(k_lds0, t0);
-      if (n_tiles > 1 && (t0 + 2) * kKeys > ctx) rope_own(k_lds1, t0 + 1);
+      if (n_tiles > 1 && (t0 + 2) * kKeys > ctx) {
+        rope_cs(t0 + 1);
+        wait_loads();
+        rope_own(k_lds1, t0 + 1);
+      }
     }
   }
   __syncthreads();
@@ -775,6 +834,9 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
     if (t + 2 < n_tiles) load_tile(Kg, k_free, t0 + t + 2, false, run_k);
     if (t + 1 < n_tiles) load_tile(Vg, v_free, t0 + t + 1, true, run_v);
+    if constexpr (kRope) {
+      if (t + 2 < n_tiles && (t0 + t + 3) * kKeys > ctx) rope_cs(t0 + t + 2);
+    }
     int32_t rdl_f = 0;   // raw shift of this lane's rotation row of tile t + 3
     if constexpr (kPaged) {
       if (t + 2 < n_tiles && run_k < 0) load_cs(d_k);
