@@ -204,7 +204,11 @@ pic_status pic_compose(const pic_model* model, const void* pool_k, const void* p
      ctx_len [device, batch]  composed lengths; entries are clamped to [0, max_ctx]
      max_ctx [host]           bound on ctx_len; max_ctx + n_suffix <= cache_cap
      scale                    softmax scale; 0 means 1/sqrt(head_dim)
-     workspace                pic_prefill_workspace_bytes(...) bytes (may be 0 bytes) */
+     workspace                pic_prefill_workspace_bytes(...) bytes (may be 0 bytes)
+   The prefill kernels (this call and 3a-3c) address one cache stream [cache_cap][D], one
+   request's suffix rows [n_suffix][Hkv][D] and one pool head [pool_tokens][D] with 32-bit byte
+   offsets: each of cache_cap, n_suffix * Hkv and pool_tokens must be below 2^24
+   (PIC_ERR_UNSUPPORTED otherwise). */
 size_t pic_prefill_workspace_bytes(const pic_model* model, int32_t batch, int32_t n_suffix,
                                    int32_t max_ctx);
 pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const void* k_suf,

@@ -73,6 +73,17 @@ pic_status check_model(const pic_model* m) {
 int32_t n_tables(const pic_model* m) { return m->rope_tables > 1 ? m->rope_tables : 1; }
 
 constexpr int32_t kMaxAbsDelta = 1 << 20;
+// The bf16 attention kernels address a cache stream (one layer, request and kv head), one
+// request's suffix rows and a pool head (one layer and kv head) with 32-bit byte offsets from
+// a buffer base: each must stay under 2^32 bytes (rows of 256 bytes).
+constexpr int64_t kMaxRows32 = (int64_t(1) << 32) / 256 - 1;
+static pic_status check_rows32(int64_t cache_cap, int64_t suffix_rows, int64_t pool_tokens) {
+  if (cache_cap > kMaxRows32 || suffix_rows > kMaxRows32 || pool_tokens > kMaxRows32)
+    return fail(PIC_ERR_UNSUPPORTED,
+                "a cache stream, a request's suffix rows or a pool head exceeds %lld rows",
+                (long long)kMaxRows32);
+  return ok();
+}
 
 size_t elem_bytes(const pic_model* m) { return m->dtype == PIC_F32 ? 4 : 2; }
 
@@ -410,6 +421,7 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
       (int64_t)n_suffix * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  PIC_CHECK(check_rows32(cache_cap, (int64_t)n_suffix * model->n_kv_heads, 0));
   if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
   PIC_CHECK(check_ptr(q, "q"));
   PIC_CHECK(check_ptr(k_suf, "k_suf"));
@@ -476,6 +488,7 @@ PIC_API pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const vo
       (int64_t)n_suffix * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  PIC_CHECK(check_rows32(cache_cap, (int64_t)n_suffix * model->n_kv_heads, 0));
   if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
   PIC_CHECK(check_ptr(q, "q"));
   PIC_CHECK(check_ptr(k_suf, "k_suf"));
@@ -543,6 +556,7 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
       (int64_t)n_suffix * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  PIC_CHECK(check_rows32(cache_cap, (int64_t)n_suffix * model->n_kv_heads, pool_tokens));
   if (batch == 0 || n_suffix == 0 || model->n_layers == 0) return ok();
   PIC_CHECK(check_ptr(pool_k, "pool_k"));
   PIC_CHECK(check_ptr(pool_v, "pool_v"));
@@ -600,6 +614,7 @@ PIC_API pic_status pic_frontier_prefill_attn(const pic_model* model, const void*
       (int64_t)n_inline * (model->n_q_heads / model->n_kv_heads) >= (int64_t(1) << 27))
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  PIC_CHECK(check_rows32(cache_cap, 0, 0));
   if (batch == 0 || n_inline == 0 || model->n_layers == 0 || max_len == 0) return ok();
   PIC_CHECK(check_ptr(q, "q"));
   PIC_CHECK(check_ptr(k_inl, "k_inl"));

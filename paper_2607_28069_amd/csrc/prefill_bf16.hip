@@ -21,11 +21,14 @@
 //    the accumulator holds them.  V stays row-major in LDS; its A operand (8 keys at one head
 //    dim per lane) comes from two transposing reads (ds_read_b64_tr_b16), which also apply
 //    that key order.
-//  * Tiles move global -> LDS with global_load_lds_dwordx4 (no register staging).  The 16-byte
-//    chunks of a row are XOR-swizzled so that every LDS read is free of bank conflicts.
+//  * Tiles move global -> LDS with buffer_load_dwordx4 ... lds (no register staging).  The
+//    16-byte chunks of a row are XOR-swizzled so that every LDS read is free of bank conflicts.
 //  * Software pipeline, one barrier per tile: K runs one tile ahead of V.  While the matrix
 //    core computes the scores of tile t+1, the vector unit turns the scores of tile t into
-//    probabilities, which then feed the PV products of tile t.
+//    probabilities, which then feed the PV products of tile t.  The tile body is ordered by
+//    hand (scheduling barriers): each LDS operand is read one product ahead of its use, and
+//    the PV products of a tile's last slice are issued after the tile barrier, covering the
+//    latency of the next tile's first reads.
 //  * Workgroups sharing a (request, kv head) key stream are mapped onto the same XCD (blocks
 //    are dealt round-robin over the 8 XCDs), so that stream is fetched into one L2.
 //  * The suffix's own keys/values are read straight from k_suf / v_suf; one workgroup per
@@ -61,6 +64,26 @@ constexpr int kLoadSteps = kKeys / (4 * kWaves);   // 1 KB load instructions per
 
 #define LDS_AS __attribute__((address_space(3)))
 #define GLOBAL_AS __attribute__((address_space(1)))
+
+// Global -> LDS moves go through buffer instructions (buffer_load_dwordx4 ... lds): a wave-
+// uniform base in a buffer resource, a uniform byte offset (soffset) and a per-lane byte
+// offset.  (The global-address form of the same move counts as an access to both memory and
+// LDS, and the compiler then waits for every outstanding load before any LDS read result or
+// any global load result is used; the buffer form keeps those waits to the operands needed.)
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base) {
+  // raw buffer (stride 0), no range limit: every offset the kernel forms is in bounds
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, -1, 0x00020000);
+}
+// 16 bytes per lane from base + soff + voff into LDS at lds + 16 * lane
+__device__ __forceinline__ void dma16(rsrc_t r, uint32_t voff, uint32_t soff, void* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void*)lds, 16, voff, soff, 0, 0);
+}
+// the same move in the indexed form (index 0), for the second of two moves under
+// complementary lane masks, so the compiler cannot fold the two into one
+__device__ __forceinline__ void dma16_other(rsrc_t r, uint32_t voff, void* lds) {
+  __builtin_amdgcn_struct_ptr_buffer_load_lds(r, (LDS_AS void*)lds, 16, 0, voff, 0, 0, 0);
+}
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -384,6 +407,13 @@ prefill_bf16_kernel(PrefillArgs a) {
   const bf16_t* PKg = kPaged ? a.pool_k + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
   const bf16_t* PVg = kPaged ? a.pool_v + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
   const int32_t* smap = kPaged ? a.smap + (int64_t)b * a.map_cap : nullptr;
+  // buffer resources (byte offsets from these bases fit in 32 bits: a cache stream holds
+  // cache_cap rows, the suffix n_suffix * Hkv rows, a pool head pool_tokens rows and a
+  // table (max_abs_delta + 1) rows of 512 bytes, each under 2^32 bytes by the host checks)
+  const rsrc_t r_k = make_rsrc(Kg), r_v = make_rsrc(Vg);
+  const rsrc_t r_ks = make_rsrc(kTable ? Kg : Ks), r_vs = make_rsrc(kTable ? Vg : Vs);
+  const rsrc_t r_pk = make_rsrc(kPaged ? PKg : Kg), r_pv = make_rsrc(kPaged ? PVg : Vg);
+  const rsrc_t r_tab = make_rsrc((kPaged || kRope) ? a.table + (int64_t)l * a.table_stride : (const float2*)Kg);
   const int32_t* dmap = kPaged ? a.dmap + (int64_t)b * a.map_cap : nullptr;
   // pool token of load row i (0, 1) of global tile t for this lane (0 past the context)
   // (map entries are loaded raw and checked after the tile's loads have landed: a use right
@@ -414,14 +444,12 @@ prefill_bf16_kernel(PrefillArgs a) {
     const int32_t ad = delta < 0 ? -delta : delta;
     if (ad == cs_held) return;
     cs_held = ad;
-    const float2* row = a.table + (int64_t)l * a.table_stride + (int64_t)ad * (kHD / 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       // rotate-half: pairs 8c .. 8c + 7 (chunks c and c + 8); interleaved: pairs 4c .. 4c + 3
       // (chunk c) and 32 + 4c .. 32 + 4c + 3 (chunk c + 8)
       const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : 32 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
-      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + f),
-                                       (LDS_AS void*)(cs_lds + wave * 4096 + j * 1024), 16, 0, 0);
+      dma16(r_tab, (uint32_t)(ad * (kHD / 2) + f) * 8u, 0, cs_lds + wave * 4096 + j * 1024);
     }
   };
   // Paged mode, whole-run tiles: when the 64 keys of context tile T are pool tokens
@@ -461,10 +489,8 @@ prefill_bf16_kernel(PrefillArgs a) {
   int32_t q_shift = 0;   // shift the operand is turned by (uniform)
   auto stage_row = [&](int32_t shift) {
     const int32_t ad = shift < 0 ? -shift : shift;
-    const float2* row = a.table + (int64_t)l * a.table_stride + (int64_t)ad * (kHD / 2);
     if (lane < kHD / 4)   // 32 lanes x 16 bytes = the row's 64 (cos, sin) pairs
-      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + 2 * lane),
-                                       (LDS_AS void*)(cs_lds + wave * 4096), 16, 0, 0);
+      dma16(r_tab, 16u * lane, (uint32_t)ad * (kHD / 2) * 8u, cs_lds + wave * 4096);
     cs_held = -1;
   };
   auto turn_q = [&](int32_t shift) {
@@ -531,47 +557,39 @@ prefill_bf16_kernel(PrefillArgs a) {
   int32_t src_v[kLoadSteps], src_k[kLoadSteps], src_f[kLoadSteps];   // rows of tiles t+1, t+2, t+3
   int32_t d_k = 0, d_f = 0;                                            // rotation shift, tiles t+2, t+3
 
-  auto load_tile = [&](const bf16_t* src, uint8_t* dst_tile, int t, bool is_v, int32_t run = -1) {
-    const int goff = is_v ? v_goff : k_goff;
+  auto load_tile = [&](uint8_t* dst_tile, int t, bool is_v, int32_t run = -1) {
+    const uint32_t goff = 2u * (is_v ? v_goff : k_goff);   // bytes
+    const uint32_t coff = 16u * (is_v ? v_gc : k_gc);
+    const rsrc_t rc = is_v ? r_v : r_k, rs = is_v ? r_vs : r_ks;
     if (kPaged && run >= 0) {   // a whole-run tile: pool rows run .. run + 63
-      const bf16_t* base = (is_v ? PVg : PKg) + (int64_t)run * kHD;   // uniform
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i)
-        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(base + (4 * kWaves * i) * kHD + goff),
-                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
-                                         16, 0, 0);
+        dma16(is_v ? r_pv : r_pk, goff, (uint32_t)(run + 4 * kWaves * i) * kRowBytes,
+              dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes);
     } else if constexpr (kPaged) {
-      const int c = is_v ? v_gc : k_gc;
-      const bf16_t* suf = is_v ? Vs : Ks;
-      const bf16_t* pool = is_v ? PVg : PKg;
       const int32_t* rows = is_v ? src_v : src_k;
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
         const int kk = min(t * kKeys + 4 * kWaves * i + ld_row, n_keys - 1);
-        const bf16_t* row = kk < ctx ? pool + (int64_t)rows[i] * kHD : suf + (kk - ctx) * suf_stride;
-        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + 8 * c),
-                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
-                                         16, 0, 0);
+        uint8_t* dst = dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes;
+        // (two separate moves: one move with a per-lane choice of base would need a loop
+        // over the distinct bases)
+        if (kk < ctx) dma16(is_v ? r_pv : r_pk, (uint32_t)rows[i] * kRowBytes + coff, 0, dst);
+        if (kk >= ctx) dma16_other(rs, (uint32_t)((kk - ctx) * suf_stride) * 2u + coff, dst);
       }
     } else if ((t + 1) * kKeys <= ctx) {
 #pragma unroll
-      for (int i = 0; i < kLoadSteps; ++i) {
-        const bf16_t* base = src + (int64_t)(t * kKeys + 4 * kWaves * i) * kHD;   // uniform
-        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(base + goff),
-                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
-                                         16, 0, 0);
-      }
+      for (int i = 0; i < kLoadSteps; ++i)
+        dma16(rc, goff, (uint32_t)(t * kKeys + 4 * kWaves * i) * kRowBytes,
+              dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes);
     } else {
       // a tile reaching the suffix: its keys come from k_suf / v_suf
-      const int c = is_v ? v_gc : k_gc;
-      const bf16_t* suf = is_v ? Vs : Ks;
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
         const int kk = min(t * kKeys + 4 * kWaves * i + ld_row, n_keys - 1);
-        const bf16_t* row = kk < ctx ? src + (int64_t)kk * kHD : suf + (kk - ctx) * suf_stride;
-        __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + 8 * c),
-                                         (LDS_AS void*)(dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes),
-                                         16, 0, 0);
+        uint8_t* dst = dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes;
+        if (kk < ctx) dma16(rc, (uint32_t)kk * kRowBytes + coff, 0, dst);
+        if (kk >= ctx) dma16_other(rs, (uint32_t)((kk - ctx) * suf_stride) * 2u + coff, dst);
       }
     }
   };
@@ -626,12 +644,11 @@ prefill_bf16_kernel(PrefillArgs a) {
   auto rope_cs = [&](int t) {   // this lane's cos/sin for its suffix row of K tile t -> cos/sin area
     const int k = t * kKeys + rot_row;
     if (k < ctx || k >= n_keys) return;
-    const float2* row = a.table + (int64_t)l * a.table_stride + (int64_t)min(k, a.max_abs_delta) * (kHD / 2);
+    const uint32_t row = (uint32_t)min(k, a.max_abs_delta) * (kHD / 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {   // the frequency pairs the paged key turn uses (see load_cs)
       const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : 32 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
-      __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)(row + f),
-                                       (LDS_AS void*)(cs_lds + wave * 4096 + j * 1024), 16, 0, 0);
+      dma16(r_tab, (row + f) * 8u, 0, cs_lds + wave * 4096 + j * 1024);
     }
   };
   auto rope_own = [&](uint8_t* kt, int t) {   // after rope_cs(t) has landed
@@ -698,6 +715,21 @@ prefill_bf16_kernel(PrefillArgs a) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) oacc[i] = f32x16_t{};
   float m_run = -INFINITY, l_part = 0.f;
+  // The PV products of a tile's last slice are issued after the tile barrier, at the start of
+  // the next tile, while that tile's first LDS reads are in flight.  Pending: probabilities
+  // pend_p and V^T operands pend_v (zero before the first tile: the products then add 0).
+  bf16x8_t pend_p = as_bf16x8(u32x4{0, 0, 0, 0});
+  bf16x8_t pend_v[4];
+#pragma unroll
+  for (int db = 0; db < 4; ++db) pend_v[db] = as_bf16x8(u32x4{0, 0, 0, 0});
+  // (not in paged mode, whose loop holds more state: there the slice is issued in its tile)
+  constexpr bool kDefer = !kPaged;
+  auto flush_pending = [&]() {
+    if constexpr (!kDefer) return;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+      oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pend_v[db], pend_p, oacc[db], 0, 0, 0);
+  };
 
   // Both lane halves hold keys of the same query column: (x[l], x[l ^ 32]) as a pair, for
   // all lanes, from one v_permlane32_swap.
@@ -732,6 +764,8 @@ prefill_bf16_kernel(PrefillArgs a) {
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kb2][e]);
     const float m_tile = pair_max(mx) * a.scale_log2;
     if (__any(m_tile > m_run + 8.f)) {
+      flush_pending();   // the pending products belong to the old reference max
+      pend_p = as_bf16x8(u32x4{0, 0, 0, 0});
       const float m_new = fmaxf(m_run, m_tile);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
@@ -760,8 +794,8 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
     d_k = map_delta(t0);
     wait_loads();
-    load_tile(Kg, k_lds0, t0, false, run0);
-    load_tile(Vg, v_lds0, t0, true, run0);
+    load_tile(k_lds0, t0, false, run0);
+    load_tile(v_lds0, t0, true, run0);
     if (run0 < 0) load_cs(d_k);
 #pragma unroll
     for (int i = 0; i < kLoadSteps; ++i) src_k[i] = map_src(t0 + 1, i);
@@ -769,7 +803,7 @@ prefill_bf16_kernel(PrefillArgs a) {
     wait_loads();
     if (run0 < 0) rotate_own(k_lds0, t0, d_k);
     if (n_tiles > 1) {
-      load_tile(Kg, k_lds1, t0 + 1, false, run1);
+      load_tile(k_lds1, t0 + 1, false, run1);
       if (run1 < 0) load_cs(d_f);
       // V(t0 + 1) is loaded by tile 0 and K(t0 + 2) by tile 0: their rows
 #pragma unroll
@@ -791,9 +825,9 @@ prefill_bf16_kernel(PrefillArgs a) {
       wait_loads();
     }
   } else {
-    load_tile(Kg, k_lds0, t0, false);
-    load_tile(Vg, v_lds0, t0, true);
-    if (n_tiles > 1) load_tile(Kg, k_lds1, t0 + 1, false);
+    load_tile(k_lds0, t0, false);
+    load_tile(v_lds0, t0, true);
+    if (n_tiles > 1) load_tile(k_lds1, t0 + 1, false);
     if constexpr (kRope) {
       if ((t0 + 1) * kKeys > ctx) rope_cs(t0);
       rope_q();
@@ -832,8 +866,8 @@ prefill_bf16_kernel(PrefillArgs a) {
       turn_q(run_v >= 0 ? del_v : 0);
       if (t + 3 < n_tiles) run_f = tile_run(t0 + t + 3, del_f);
     }
-    if (t + 2 < n_tiles) load_tile(Kg, k_free, t0 + t + 2, false, run_k);
-    if (t + 1 < n_tiles) load_tile(Vg, v_free, t0 + t + 1, true, run_v);
+    if (t + 2 < n_tiles) load_tile(k_free, t0 + t + 2, false, run_k);
+    if (t + 1 < n_tiles) load_tile(v_free, t0 + t + 1, true, run_v);
     if constexpr (kRope) {
       if (t + 2 < n_tiles && (t0 + t + 3) * kKeys > ctx) rope_cs(t0 + t + 2);
     }
@@ -853,21 +887,34 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
 
     // (scores of a tile past the last one are computed on stale LDS and dropped)
-    snext[0] = f32x16_t{};
-    snext[1] = f32x16_t{};
+    // Hand-ordered body: the K operands of the next tile's score products are read one pair
+    // of products ahead and the V^T operands of slice s4 + 1 while slice s4's PV products
+    // issue, so no matrix product waits on an LDS read issued just before it.  Scheduling
+    // barriers keep this order.
     float psum = 0.f;
     const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
+    auto kread = [&](int ks, int kb2) {
+      return *reinterpret_cast<const u32x4*>(k_next + k_rd[ks] + 32 * kb2 * kRowBytes);
+    };
+    auto vread = [&](int s4, int db, int half) {
+      return __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(v_cur + v_rd[db][half] + 16 * s4 * kRowBytes));
+    };
+    u32x4 kq[8][2];
+    i16x4 vq[4][4][2];
+    kq[0][0] = kread(0, 0);
+    kq[0][1] = kread(0, 1);
+    kq[1][0] = kread(1, 0);
+    kq[1][1] = kread(1, 1);
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      vq[0][db][0] = vread(0, db, 0);
+      vq[0][db][1] = vread(0, db, 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    flush_pending();   // the previous tile's last slice
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) {
-      // a quarter of the next tile's S^T products
-#pragma unroll
-      for (int ks = 2 * s4; ks < 2 * s4 + 2; ++ks)
-#pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2) {
-          const u32x4 kv = *reinterpret_cast<const u32x4*>(k_next + k_rd[ks] + 32 * kb2 * kRowBytes);
-          snext[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qop[ks], snext[kb2], 0, 0, 0);
-        }
-      // probabilities of slice s4 of this tile (keys 16 s4 .. 16 s4 + 15 in accumulator order)
       const int kb2 = s4 >> 1, u = s4 & 1;
       uint32_t pw[4];
 #pragma unroll
@@ -875,19 +922,30 @@ prefill_bf16_kernel(PrefillArgs a) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j], a.scale_log2, -m_run));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j + 1], a.scale_log2, -m_run));
         pw[j] = pack_bf16x2(p0, p1);
-        // row sum of the bf16 probabilities the PV product uses (one v_dot2 per pair)
         psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[j]), ones, psum, false);
+        __builtin_amdgcn_sched_barrier(0);
+        // score product j of this slice: pair ks = 2 s4 + (j >> 1), block kb = j & 1
+        const int ks = 2 * s4 + (j >> 1), kb = j & 1;
+        if (kb == 0) snext[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kq[ks][0]), qop[ks], s4 == 0 && j == 0 ? f32x16_t{} : snext[0], 0, 0, 0);
+        else snext[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kq[ks][1]), qop[ks], s4 == 0 && j == 1 ? f32x16_t{} : snext[1], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (ks + 2 < 8) kq[ks + 2][kb] = kread(ks + 2, kb);
+        __builtin_amdgcn_sched_barrier(0);
       }
       const bf16x8_t pop = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
-      // O^T += V^T P^T for this slice
+      if (s4 == 3 && kDefer) pend_p = pop;
 #pragma unroll
       for (int db = 0; db < 4; ++db) {
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (LDS_AS i16x4*)(v_cur + v_rd[db][0] + 16 * s4 * kRowBytes));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (LDS_AS i16x4*)(v_cur + v_rd[db][1] + 16 * s4 * kRowBytes));
-        const bf16x8_t vv = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pop, oacc[db], 0, 0, 0);
+        if (s4 + 1 < 4) {
+          vq[s4 + 1][db][0] = vread(s4 + 1, db, 0);
+          vq[s4 + 1][db][1] = vread(s4 + 1, db, 1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        const bf16x8_t vv = __builtin_bit_cast(
+            bf16x8_t, __builtin_shufflevector(vq[s4][db][0], vq[s4][db][1], 0, 1, 2, 3, 4, 5, 6, 7));
+        if (s4 < 3 || !kDefer) oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pop, oacc[db], 0, 0, 0);
+        else pend_v[db] = vv;
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     l_part += psum;
@@ -920,6 +978,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   }
 
   // ---- lane holds head dims 32 db + 8 qd + 4 hh + (0..3) of its row
+  flush_pending();   // the last tile's last slice
   const float l_tot = pair_sum(l_part);
   if (!row_ok) return;
   if (a.n_splits == 1) {   // normalise and store bf16

@@ -254,6 +254,13 @@ def test_argument_checks_fail_before_any_launch(lib):
     assert _paged(lib, _model(dtype="f32")) == -2
     assert _paged(lib, m, ws=None, ws_bytes=0, max_ctx=4000, map_cap=4000, cap=5000) == -3   # split-K
     assert _paged(lib, m, batch=0) == 0
+    # the prefill kernels use 32-bit byte offsets: a cache stream, a request's suffix rows and
+    # a pool head each stay below 2^24 rows of 256 bytes
+    assert _prefill(lib, m, cap=1 << 24) == -2
+    assert _frontier(lib, m, cap=1 << 24) == -2
+    assert _paged(lib, m, cap=1 << 24) == -2
+    assert _paged(lib, m, pool_tokens=1 << 24) == -2
+    assert _paged(lib, m, pool_tokens=(1 << 24) - 1) != -2
     assert lib.pic_build_slot_map(FAKE, 4, 2, 500, None, FAKE, FAKE, None) == -1
     assert lib.pic_build_slot_map(None, 4, 2, 500, FAKE, FAKE, None, None) == -1
     assert lib.pic_build_slot_map(FAKE, -1, 2, 500, FAKE, FAKE, None, None) == -1
