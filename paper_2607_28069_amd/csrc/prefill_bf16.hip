@@ -866,8 +866,13 @@ prefill_bf16_kernel(PrefillArgs a) {
       turn_q(run_v >= 0 ? del_v : 0);
       if (t + 3 < n_tiles) run_f = tile_run(t0 + t + 3, del_f);
     }
-    if (t + 2 < n_tiles) load_tile(k_free, t0 + t + 2, false, run_k);
-    if (t + 1 < n_tiles) load_tile(v_free, t0 + t + 1, true, run_v);
+    // this tile's loads (K(t+2), V(t+1)): issued after the first slice outside paged mode,
+    // so the waves' first LDS reads and products of the tile go ahead of them
+    auto issue_loads = [&]() {
+      if (t + 2 < n_tiles) load_tile(k_free, t0 + t + 2, false, run_k);
+      if (t + 1 < n_tiles) load_tile(v_free, t0 + t + 1, true, run_v);
+    };
+    if constexpr (kPaged) issue_loads();
     if constexpr (kRope) {
       if (t + 2 < n_tiles && (t0 + t + 3) * kKeys > ctx) rope_cs(t0 + t + 2);
     }
@@ -945,6 +950,10 @@ prefill_bf16_kernel(PrefillArgs a) {
             bf16x8_t, __builtin_shufflevector(vq[s4][db][0], vq[s4][db][1], 0, 1, 2, 3, 4, 5, 6, 7));
         if (s4 < 3 || !kDefer) oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pop, oacc[db], 0, 0, 0);
         else pend_v[db] = vv;
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (!kPaged) {
+        if (s4 == 0) issue_loads();
         __builtin_amdgcn_sched_barrier(0);
       }
     }
