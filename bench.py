@@ -80,6 +80,21 @@ def source_hash(rel):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+def lookup_traffic(workload, kernel, plain_path=True, path=TRAFFIC_FILE):
+    """Counter-measured HBM bytes per launch of `kernel` on `workload`, or None.
+
+    The figures hold for the kernel source they were profiled on (its hash is stored beside
+    them) and for the plain composed path: a zero-copy or fused-RoPE run launches other
+    instantiations of the kernels, whose traffic was not measured."""
+    if not plain_path or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f).get(workload, {}).get(kernel)
+    if t and t.get("source_sha256_16") == source_hash(KERNEL_SOURCES[kernel]):
+        return t["bytes_per_launch"]
+    return None
+
+
 # ------------------------------------------------------------------------------------------
 # device workload
 # ------------------------------------------------------------------------------------------
@@ -444,7 +459,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
@@ -501,12 +516,7 @@ def main():
         k["ms_per_step"] = k["ms_per_launch"] * k["launches_per_step"]
     dom_name = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dom = kernels[dom_name]
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):   # counter-measured HBM bytes, valid for the profiled source only
-        with open(TRAFFIC_FILE) as f:
-            t = json.load(f).get(w.name, {}).get(dom_name)
-        if t and t.get("source_sha256_16") == source_hash(KERNEL_SOURCES[dom_name]):
-            traffic = t["bytes_per_launch"]
+    traffic = lookup_traffic(w.name, dom_name, plain_path=not (args.paged or args.fused_rope))
     roofline = {"kernel": dom_name, "bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
                 "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
 
