@@ -14,6 +14,8 @@
 //  * O^T = V^T P^T with the same instruction: V moves global -> LDS with global_load_lds_dwordx4
 //    (row-major, chunk-swizzled) and its A operand comes from two transposing reads
 //    (ds_read_b64_tr_b16); the swizzle keeps those reads free of bank conflicts;
+//  * every row is read once per step: the V moves (whole rows per instruction) are non-temporal,
+//    while the K loads, which take a row in four 64-byte pieces, stay cached;
 //  * the new token's K/V are read straight from k_new/v_new by the wave whose range holds slot p,
 //    and written into the cache by that workgroup (no separate append launch);
 //  * the 4 waves merge by log-sum-exp in LDS; a context split over several workgroups (only when
@@ -34,6 +36,7 @@ constexpr int kTile = 32;                          // keys per wave tile
 constexpr int kRowBytes = kHD * 2;                 // 256
 constexpr int kVTileBytes = kTile * kRowBytes;     // 8 KB per wave per buffer
 constexpr int kMinWaveKeys = 64;
+constexpr int kNonTemporal = 2;                    // cache-policy bits of a streaming load
 
 #define LDS_AS __attribute__((address_space(3)))
 #define GLOBAL_AS __attribute__((address_space(1)))
@@ -215,7 +218,8 @@ decode_bf16_kernel(DecodeArgs a) {
       const int c = ld_slot ^ v_swz(rl);
       const bf16_t* src = (row == p ? Vn : Vg + (int64_t)row * kHD) + 8 * c;
       __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)src,
-                                       (LDS_AS void*)(buf + wave * kVTileBytes + 4 * i * kRowBytes), 16, 0, 0);
+                                       (LDS_AS void*)(buf + wave * kVTileBytes + 4 * i * kRowBytes), 16, 0,
+                                       kNonTemporal);
     }
   };
 

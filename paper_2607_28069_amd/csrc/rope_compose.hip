@@ -10,7 +10,8 @@
 // vector and a row of D elements is split across lanes such that the two members of every
 // rotated pair sit in the same lane: for the rotate-half pairing (x_i, x_{i+D/2}) a lane owns
 // element chunk [c, c + VEC) of both halves; for the interleaved pairing (x_2i, x_2i+1) it
-// owns the 2 VEC consecutive elements of pairs [c, c + VEC).
+// owns the 2 VEC consecutive elements of pairs [c, c + VEC).  bf16 output rows are stored
+// non-temporally (written once; the caches stay with the pool rows, which several requests read).
 #include "pic_internal.h"
 
 namespace pic {
@@ -58,13 +59,14 @@ struct Vec16<bf16_t> {
       x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
     }
   }
+  // Non-temporal: an output row is written once and not read again by the launch; streaming
+  // it past the caches keeps them for the pool rows that other requests' blocks read again
+  // (the loads stay ordinary).
   __device__ static void store(bf16_t* p, const float (&x)[8]) {
-    uint4 v;
-    v.x = pack_bf16x2(x[0], x[1]);
-    v.y = pack_bf16x2(x[2], x[3]);
-    v.z = pack_bf16x2(x[4], x[5]);
-    v.w = pack_bf16x2(x[6], x[7]);
-    *reinterpret_cast<uint4*>(p) = v;
+    typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+    const u32x4_nt v = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                        pack_bf16x2(x[6], x[7])};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_nt*>(p));
   }
 };
 
