@@ -3,7 +3,8 @@
 
 One step = one pass of the whole path over one batch of requests:
   plan (host) -> copy of the gather blocks to the device -> compose all layers (re-rotate +
-  gather) -> suffix prefill attention layer by layer -> decode tokens layer by layer.
+  gather; blocks that read the same document run are grouped so that each run is read once)
+  -> suffix prefill attention layer by layer -> decode tokens layer by layer.
 The first four are the cache-hit TTFT region, timed like the paper's TTFT boundary (App. C.2):
 device-synchronised at both ends, starting right before layout construction; projections,
 MLP and LM head have no weights here, so the region holds only the attention path.
@@ -51,6 +52,9 @@ def parse(argv=None):
     p.add_argument("--paged", action="store_true",
                    help="zero-copy TTFT: the prefill reads the documents from the pool through the "
                         "gather map; the composed cache is built after the first token, for decode")
+    p.add_argument("--per-block-compose", action="store_true",
+                   help="compose with pic_compose over the blocks as planned (each composed row reads "
+                        "its pool row) instead of grouping blocks that share a document run")
     p.add_argument("--copy-calib-gib", type=float, default=0.0,
                    help="also run a plain device copy of this size per step (counter calibration)")
     return p.parse_args(argv)
@@ -61,7 +65,9 @@ def parse(argv=None):
 # ------------------------------------------------------------------------------------------
 
 def compose_bytes(w, ctx, n_layers):
-    """K and V rows read from the pool and written to the cache, D elements each."""
+    """K and V rows read from the pool and written to the cache, D elements each (one read per
+    composed row; grouping blocks that share a document run reads fewer, so this rate can
+    exceed the HBM peak)."""
     return int(sum(ctx)) * w.n_kv_heads * n_layers * 4 * w.head_dim * w.elem_bytes
 
 
@@ -103,14 +109,15 @@ class DeviceWorkload:
     """Every tensor of one workload, resident on the device, plus the per-step driver.
 
     Plain workloads: documents back to back after a stored prefix, then n_suffix query tokens
-    (pic_plan_layout, pic_compose, pic_suffix_prefill_attn).  Frontier workloads: an inline
+    (pic_plan_layout, pic_plan_shared + pic_compose_shared, pic_suffix_prefill_attn; with
+    shared_compose=False, pic_compose over the blocks as planned).  Frontier workloads: an inline
     prefix and inline spans between the documents (pic_plan_frontier, pic_compose,
     pic_frontier_prefill_attn over all inline tokens).  Decode steps follow either.
     `layers` < w.n_layers builds a workload with fewer layers of the same per-layer shape.
     """
 
     def __init__(self, w, dev, n_dec: int, layers: int | None = None, paged: bool = False,
-                 fused_rope: bool = False):
+                 fused_rope: bool = False, shared_compose: bool = True):
         import numpy as np
         import torch
 
@@ -120,6 +127,7 @@ class DeviceWorkload:
         self.w, self.dev, self.n_dec = w, dev, n_dec
         self.paged = paged
         self.fused_rope = fused_rope
+        self.shared_compose = shared_compose
         self.L = L = w.n_layers if layers is None else layers
         self.dt = dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
         B, Hq, Hkv, D = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim
@@ -200,8 +208,44 @@ class DeviceWorkload:
                                   dtype=torch.uint8, device=dev)
         n_blocks_max = sum((int(n) + 63) // 64 for r in lay.requests for n in lay.doc_len[r])
         n_pos = self.pos_host.size if self.frontier else 0
-        self.blocks_pinned = torch.empty(n_blocks_max * 5 + n_pos, dtype=torch.int32, pin_memory=True)
+        # staging for one plan: blocks, group starts, inline positions
+        self.blocks_pinned = torch.empty(n_blocks_max * 6 + 1 + n_pos, dtype=torch.int32, pin_memory=True)
         self.blocks_dev = torch.empty(n_blocks_max * 5, dtype=torch.int32, device=dev)
+        self.groups_dev = torch.empty(n_blocks_max + 1, dtype=torch.int32, device=dev)
+
+    def upload(self, blocks, pinned, blocks_dev, groups_dev, inl=None, pos_dev=None):
+        """Asynchronous copy of one plan to the device: its gather blocks (grouped by source run
+        when composing with shared sources, with the group starts) and inline positions.
+        Returns (n_blocks, n_groups)."""
+        import numpy as np
+        import torch
+
+        import paper_2607_28069_amd as pic
+
+        nb, ng, at = len(blocks), 0, len(blocks) * 5
+        if self.shared_compose:
+            blocks, starts = pic.pic_plan_shared(blocks)
+            ng = len(starts) - 1
+            pinned[at: at + ng + 1].copy_(torch.from_numpy(starts))
+            groups_dev[: ng + 1].copy_(pinned[at: at + ng + 1], non_blocking=True)
+            at += ng + 1
+        pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32).reshape(-1)))
+        blocks_dev[: nb * 5].copy_(pinned[: nb * 5], non_blocking=True)
+        if inl is not None:   # the inline positions go to the device with the blocks
+            tail = pinned[at: at + inl.size]
+            tail.copy_(torch.from_numpy(inl.reshape(-1)))
+            pos_dev.view(-1)[: inl.size].copy_(tail, non_blocking=True)
+        return nb, ng
+
+    def compose(self, blocks_dev, groups_dev, nb, ng, cache_k, cache_v, batch):
+        import paper_2607_28069_amd as pic
+
+        if self.shared_compose:
+            pic.pic_compose_shared(self.model, self.pool_k, self.pool_v, self.lay.pool_tokens, blocks_dev, nb,
+                                   groups_dev, ng, self.table, self.mad, cache_k, cache_v, batch, self.cap)
+        else:
+            pic.pic_compose(self.model, self.pool_k, self.pool_v, self.lay.pool_tokens, blocks_dev, nb,
+                            self.table, self.mad, cache_k, cache_v, batch, self.cap)
 
     def step(self, rec: dict | None = None, calib=None):
         """One pass of the path; with `rec`, appends timings (ms) to its lists."""
@@ -223,18 +267,12 @@ class DeviceWorkload:
         else:
             blocks, _ = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len,
                                             lay.doc_compile_pos, lay.pool_tokens)
-        nb = len(blocks)
-        self.blocks_pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32).reshape(-1)))
-        self.blocks_dev[: nb * 5].copy_(self.blocks_pinned[: nb * 5], non_blocking=True)
-        if self.frontier:   # the inline positions go to the device with the blocks
-            tail = self.blocks_pinned[nb * 5: nb * 5 + inl.size]
-            tail.copy_(torch.from_numpy(inl.reshape(-1)))
-            self.pos_dev.view(-1).copy_(tail, non_blocking=True)
+        nb, ng = self.upload(blocks, self.blocks_pinned, self.blocks_dev, self.groups_dev,
+                             inl if self.frontier else None, self.pos_dev if self.frontier else None)
         e0, e1 = ev(), ev()
         if not self.paged:
             e0.record(stream)
-            pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
-                            self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
+            self.compose(self.blocks_dev, self.groups_dev, nb, ng, self.cache_k, self.cache_v, B)
             e1.record(stream)
         block = (self.mad + 1) * (w.head_dim // 2) * 2 if self.model.rope_tables > 1 else 0
         if self.paged:   # the token-level slot map, shared by every layer
@@ -269,8 +307,7 @@ class DeviceWorkload:
         t1 = time.perf_counter()
         if self.paged:   # the composed cache, for decoding, after the first token
             e0.record(stream)
-            pic.pic_compose(self.model, self.pool_k, self.pool_v, lay.pool_tokens, self.blocks_dev, nb,
-                            self.table, self.mad, self.cache_k, self.cache_v, B, self.cap)
+            self.compose(self.blocks_dev, self.groups_dev, nb, ng, self.cache_k, self.cache_v, B)
             e1.record(stream)
         # -- decode
         d0, d1 = ev(), ev()
@@ -328,6 +365,7 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
         nbytes = pic.pic_prefill_workspace_bytes(wl.m1, 1, Ls, wl.max_ctx)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev)
     blocks_dev = torch.empty_like(wl.blocks_dev)
+    groups_dev = torch.empty_like(wl.groups_dev)
     pinned = torch.empty_like(wl.blocks_pinned)
     pos_dev = torch.empty((1, Ls), dtype=torch.int32, device=dev)
     if wl.paged:
@@ -345,21 +383,14 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
             blocks, ctx = pic.pic_plan_layout([lay.requests[i]], lay.doc_offset, lay.doc_len,
                                               lay.doc_compile_pos, lay.pool_tokens)
             n_keys = int(ctx[0])
-        nb = len(blocks)
-        pinned[: nb * 5].copy_(torch.from_numpy(blocks.view(np.int32).reshape(-1)))
-        blocks_dev[: nb * 5].copy_(pinned[: nb * 5], non_blocking=True)
-        if wl.frontier:
-            tail = pinned[nb * 5: nb * 5 + inl.size]
-            tail.copy_(torch.from_numpy(inl.reshape(-1)))
-            pos_dev.view(-1)[: inl.size].copy_(tail, non_blocking=True)
-        return nb, n_keys
+        nb, ng = wl.upload(blocks, pinned, blocks_dev, groups_dev, inl if wl.frontier else None, pos_dev)
+        return nb, ng, n_keys
 
-    def launches(views, ctx_i, nv_i, nb, n_keys):   # compose (or slot map) + every layer's prefill
+    def launches(views, ctx_i, nv_i, nb, ng, n_keys):   # compose (or slot map) + every layer's prefill
         if wl.paged:
             pic.pic_build_slot_map(blocks_dev, nb, 1, slot_src.shape[1], slot_src, slot_delta, tile_map)
         else:
-            pic.pic_compose(wl.model, wl.pool_k, wl.pool_v, lay.pool_tokens, blocks_dev, nb, wl.table,
-                            wl.mad, cache_k, cache_v, 1, wl.cap)
+            wl.compose(blocks_dev, groups_dev, nb, ng, cache_k, cache_v, 1)
         for q, k, v, ck, cv, out, pk, pv, tab in views:
             if wl.paged:
                 pic.pic_paged_prefill_attn(wl.m1, pk, pv, lay.pool_tokens, slot_src, slot_delta,
@@ -389,15 +420,15 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
             stream.synchronize()
             if rep:
                 eager.append((time.perf_counter() - t0) * 1e3)
-        nb, n_keys = plan(i)
+        planned = plan(i)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            launches(views, ctx_i, nv_i, nb, n_keys)
+            launches(views, ctx_i, nv_i, *planned)
         for rep in range(reps + 1):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            assert plan(i) == (nb, n_keys)
+            assert plan(i) == planned
             g.replay()
             stream.synchronize()
             if rep:
@@ -473,7 +504,8 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     n_dec = args.decode_tokens if args.decode_tokens is not None else (w.decode_steps or 1)
-    wl = DeviceWorkload(w, dev, n_dec, paged=args.paged, fused_rope=args.fused_rope)
+    wl = DeviceWorkload(w, dev, n_dec, paged=args.paged, fused_rope=args.fused_rope,
+                        shared_compose=not args.per_block_compose)
     calib = None
     if args.copy_calib_gib > 0:
         n = int(args.copy_calib_gib * (1 << 30)) // 2
@@ -516,7 +548,8 @@ def main():
         k["ms_per_step"] = k["ms_per_launch"] * k["launches_per_step"]
     dom_name = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dom = kernels[dom_name]
-    traffic = lookup_traffic(w.name, dom_name, plain_path=not (args.paged or args.fused_rope))
+    traffic = lookup_traffic(w.name, dom_name,
+                             plain_path=not (args.paged or args.fused_rope or args.per_block_compose))
     roofline = {"kernel": dom_name, "bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
                 "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
 

@@ -196,6 +196,31 @@ pic_status pic_compose(const pic_model* model, const void* pool_k, const void* p
                        const void* table, int32_t max_abs_delta, void* cache_k, void* cache_v,
                        int32_t batch, int32_t cache_cap, void* stream);
 
+/* ---- 2d. composition with shared sources (Sec. 2 link operator; App. C.1) ----
+   A document placed in several requests of a batch is one pool entry, and pic_plan_layout cuts
+   every placement of it into the same source runs.  pic_plan_shared (host only) orders a block
+   list so that blocks reading the same run (equal src_token and n_tokens) are neighbours, and
+   pic_compose_shared reads each such run once per kv head and layer and writes it to all of
+   its blocks: pool reads fall from one per composed row to one per distinct run.  The cache it
+   writes is bit-identical to pic_compose's for the same blocks.
+     blocks [host, n_blocks]            gather blocks (pic_plan_layout / pic_plan_frontier)
+     sorted [host out, n_blocks]        the same blocks, grouped by source run (stable)
+     group_start [host out, n_blocks+1] group g = sorted[group_start[g] .. group_start[g+1]);
+                                        group_start[n_groups] = n_blocks
+     n_groups [host out]                number of groups
+   PIC_ERR_INVALID_ARG for NULL arrays or a negative count. */
+pic_status pic_plan_shared(const pic_block* blocks, int32_t n_blocks, pic_block* sorted,
+                           int32_t* group_start, int32_t* n_groups);
+/* As pic_compose, with blocks [device, n_blocks] = pic_plan_shared's sorted list and
+   group_start [device, n_groups + 1] its group starts.  A block whose source differs from its
+   group's first block is skipped, as is a block out of range (see pic_compose); group starts
+   are clamped to [0, n_blocks].  PIC_ERR_INVALID_ARG also when n_groups > n_blocks. */
+pic_status pic_compose_shared(const pic_model* model, const void* pool_k, const void* pool_v,
+                              int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                              const int32_t* group_start, int32_t n_groups, const void* table,
+                              int32_t max_abs_delta, void* cache_k, void* cache_v, int32_t batch,
+                              int32_t cache_cap, void* stream);
+
 /* ---- 3. suffix prefill (App. C.1: inline KVs interleaved, frontier causal mask) ----
    Appends k_suf/v_suf of request b at cache slots [ctx_len[b], ctx_len[b] + n_suffix), then
    for suffix token i (logical position ctx_len[b] + i) and query head h computes

@@ -24,7 +24,8 @@ STATUS = {0: "PIC_OK", -1: "PIC_ERR_INVALID_ARG", -2: "PIC_ERR_UNSUPPORTED", -3:
 # Every symbol include/pic.h declares.
 EXPORTS = ("pic_plan_layout", "pic_plan_frontier", "pic_rope_table_bytes", "pic_rope_table_init",
            "pic_rope_table_init_freq", "pic_rope_llama3_freq",
-           "pic_rerotate_keys", "pic_compose", "pic_prefill_workspace_bytes",
+           "pic_rerotate_keys", "pic_compose", "pic_plan_shared", "pic_compose_shared",
+           "pic_prefill_workspace_bytes",
            "pic_suffix_prefill_attn", "pic_suffix_prefill_attn_rope", "pic_build_slot_map",
            "pic_paged_prefill_attn",
            "pic_frontier_workspace_bytes", "pic_frontier_prefill_attn",
@@ -89,6 +90,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                 ctypes.c_double, ctypes.c_double, P]),
         "pic_rerotate_keys": (ctypes.c_int, [MP, P, P, I64, I32, P, P, I32, P]),
         "pic_compose": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, P, I32, I32, P]),
+        "pic_plan_shared": (ctypes.c_int, [P, I32, P, P, P]),
+        "pic_compose_shared": (ctypes.c_int, [MP, P, P, I64, P, I32, P, I32, P, I32, P, P, I32, I32, P]),
         "pic_prefill_workspace_bytes": (SZ, [MP, I32, I32, I32]),
         "pic_suffix_prefill_attn": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, P, P, SZ, P]),
         "pic_suffix_prefill_attn_rope": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, P, I32, F, P, P,
@@ -169,6 +172,19 @@ def pic_plan_layout(requests, entry_offset, entry_len, entry_compile_pos, pool_t
     return blocks[: n_blocks.value], ctx
 
 
+def pic_plan_shared(blocks):
+    """Gather blocks -> (blocks grouped by source run, group_start [n_groups + 1])."""
+    blocks = np.ascontiguousarray(blocks, BLOCK_DTYPE)
+    n = len(blocks)
+    out = np.zeros(max(n, 1), BLOCK_DTYPE)
+    starts = np.zeros(n + 1, np.int32)
+    n_groups = ctypes.c_int32(0)
+    _check(load().pic_plan_shared(blocks.ctypes.data_as(ctypes.c_void_p) if n else None, n,
+                                  out.ctypes.data_as(ctypes.c_void_p), starts.ctypes.data_as(ctypes.c_void_p),
+                                  ctypes.byref(n_groups)))
+    return out[:n], starts[: n_groups.value + 1]
+
+
 def pic_plan_frontier(items, entry_offset, entry_len, entry_compile_pos, pool_tokens):
     """items: per request, a list of pool entry ids (>= 0) and inline spans (-n).
 
@@ -228,6 +244,14 @@ def pic_rerotate_keys(model: Model, k_in, k_out, n_tokens, n_heads, delta, table
     _check(load().pic_rerotate_keys(ctypes.byref(model), _ptr(k_in), _ptr(k_out), int(n_tokens),
                                     int(n_heads), _ptr(delta), _ptr(table), max_abs_delta,
                                     _stream(stream)))
+
+
+def pic_compose_shared(model: Model, pool_k, pool_v, pool_tokens, blocks, n_blocks, group_start, n_groups,
+                       table, max_abs_delta, cache_k, cache_v, batch, cache_cap, stream=None):
+    _check(load().pic_compose_shared(ctypes.byref(model), _ptr(pool_k), _ptr(pool_v), int(pool_tokens),
+                                     _ptr(blocks), int(n_blocks), _ptr(group_start), int(n_groups),
+                                     _ptr(table), max_abs_delta, _ptr(cache_k), _ptr(cache_v), int(batch),
+                                     int(cache_cap), _stream(stream)))
 
 
 def pic_compose(model: Model, pool_k, pool_v, pool_tokens, blocks, n_blocks, table, max_abs_delta,

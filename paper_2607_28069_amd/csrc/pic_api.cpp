@@ -2,10 +2,12 @@
 // Every check runs before anything is enqueued; a failing call launches nothing.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
+#include <vector>
 
 #include "pic.h"
 #include "pic_internal.h"
@@ -388,6 +390,62 @@ PIC_API pic_status pic_compose(const pic_model* model, const void* pool_k, const
                                         pool_tokens, blocks, n_blocks,
                                         static_cast<const float2*>(table), stride, max_abs_delta,
                                         cache_k, cache_v, batch, cache_cap, (hipStream_t)stream),
+                    "compose launch");
+}
+
+PIC_API pic_status pic_plan_shared(const pic_block* blocks, int32_t n_blocks, pic_block* sorted,
+                                   int32_t* group_start, int32_t* n_groups) {
+  if (n_blocks < 0) return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (!n_groups || !group_start) return fail(PIC_ERR_INVALID_ARG, "a required host array is NULL");
+  if (n_blocks > 0 && (!blocks || !sorted)) return fail(PIC_ERR_INVALID_ARG, "blocks or sorted is NULL");
+  // stable order by source run: blocks that read the same pool tokens become neighbours
+  std::vector<int32_t> order(n_blocks);
+  for (int32_t i = 0; i < n_blocks; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
+    const pic_block &a = blocks[x], &b = blocks[y];
+    return a.src_token != b.src_token ? a.src_token < b.src_token : a.n_tokens < b.n_tokens;
+  });
+  int32_t ng = 0;
+  for (int32_t i = 0; i < n_blocks; ++i) {
+    const pic_block& b = blocks[order[i]];
+    if (i == 0 || b.src_token != sorted[i - 1].src_token || b.n_tokens != sorted[i - 1].n_tokens)
+      group_start[ng++] = i;
+    sorted[i] = b;
+  }
+  group_start[ng] = n_blocks;
+  *n_groups = ng;
+  return ok();
+}
+
+PIC_API pic_status pic_compose_shared(const pic_model* model, const void* pool_k, const void* pool_v,
+                                      int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                                      const int32_t* group_start, int32_t n_groups,
+                                      const void* table, int32_t max_abs_delta, void* cache_k,
+                                      void* cache_v, int32_t batch, int32_t cache_cap, void* stream) {
+  PIC_CHECK(check_model(model));
+  if (pool_tokens < 0 || n_blocks < 0 || n_groups < 0 || batch < 0 || cache_cap < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (n_groups > n_blocks) return fail(PIC_ERR_INVALID_ARG, "more groups (%d) than blocks (%d)", n_groups, n_blocks);
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
+    return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
+  if (model->n_kv_heads > 65535 || model->n_layers > 65535)
+    return fail(PIC_ERR_UNSUPPORTED, "more than 65535 kv heads or layers in one call");
+  if (n_groups == 0 || model->n_layers == 0) return ok();
+  PIC_CHECK(check_ptr(pool_k, "pool_k"));
+  PIC_CHECK(check_ptr(pool_v, "pool_v"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  PIC_CHECK(check_ptr(table, "table"));
+  if (!blocks) return fail(PIC_ERR_INVALID_ARG, "blocks is NULL");
+  if (!group_start) return fail(PIC_ERR_INVALID_ARG, "group_start is NULL");
+  const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+  return hip_status(pic::launch_compose_shared(model->dtype, model->head_dim,
+                                               model->rope_pairing == PIC_ROPE_INTERLEAVED,
+                                               model->n_layers, model->n_kv_heads, pool_k, pool_v,
+                                               pool_tokens, blocks, n_blocks, group_start, n_groups,
+                                               static_cast<const float2*>(table), stride,
+                                               max_abs_delta, cache_k, cache_v, batch, cache_cap,
+                                               (hipStream_t)stream),
                     "compose launch");
 }
 

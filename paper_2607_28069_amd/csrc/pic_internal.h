@@ -41,6 +41,14 @@ hipError_t launch_compose(pic_dtype dt, int head_dim, bool interleaved, int n_la
                           const float2* table, int64_t table_stride, int32_t max_abs_delta,
                           void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
                           hipStream_t stream);
+// Composition with shared sources: blocks sorted into groups that read one pool run each
+// (group g = blocks [group_start[g], group_start[g + 1])); each run is read once per group.
+hipError_t launch_compose_shared(pic_dtype dt, int head_dim, bool interleaved, int n_layers,
+                                 int n_kv_heads, const void* pool_k, const void* pool_v,
+                                 int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                                 const int32_t* group_start, int32_t n_groups, const float2* table,
+                                 int64_t table_stride, int32_t max_abs_delta, void* cache_k,
+                                 void* cache_v, int32_t batch, int32_t cache_cap, hipStream_t stream);
 
 // Logical position (= cache slot) of row i of request b among n per-request rows (suffix
 // tokens, inline tokens, a decode token): either base[b] clamped to [0, max_base], plus

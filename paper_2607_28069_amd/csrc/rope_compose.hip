@@ -45,6 +45,11 @@ struct Vec16<float> {
   __device__ static void store(float* p, const float (&x)[4]) {
     *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
   }
+  __device__ static uint4 load_raw(const float* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ static void widen(uint4 v, float (&x)[4]) {
+    x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y); x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
+  }
+  __device__ static void store_raw(float* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
 };
 
 template <>
@@ -66,6 +71,20 @@ struct Vec16<bf16_t> {
     typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
     const u32x4_nt v = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
                         pack_bf16x2(x[6], x[7])};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_nt*>(p));
+  }
+  __device__ static uint4 load_raw(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ static void widen(uint4 v, float (&x)[8]) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ static void store_raw(bf16_t* p, uint4 w) {
+    typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+    const u32x4_nt v = {w.x, w.y, w.z, w.w};
     __builtin_nontemporal_store(v, reinterpret_cast<u32x4_nt*>(p));
   }
 };
@@ -170,6 +189,99 @@ __global__ void __launch_bounds__(256) compose_kernel(
       V::store(cache_k + d + o2, k2[p]);
       V::store(cache_v + d + o1, v1[p]);
       V::store(cache_v + d + o2, v2[p]);
+    }
+  }
+}
+
+// grid (n_groups, Hkv, L), 256 threads.  Composition with shared sources: blocks is sorted so
+// that the blocks of group g, [group_start[g], group_start[g + 1]), all read the same pool run
+// (the first block's src_token and n_tokens: one document chunk placed in several requests).
+// One workgroup reads that run of one kv head once and writes it to every block of its group,
+// each with its own shift, in exactly the arithmetic of compose_kernel.  A block that does not
+// share its group's source, or whose request, destination or delta is out of range, is skipped.
+template <typename T, int HD, bool IL>
+__global__ void __launch_bounds__(256) compose_shared_kernel(
+    const T* __restrict__ pool_k, const T* __restrict__ pool_v, int64_t pool_tokens,
+    const pic_block* __restrict__ blocks, const int32_t* __restrict__ group_start, int32_t n_blocks,
+    const float2* __restrict__ table, int64_t table_stride, int32_t max_abs_delta,
+    T* __restrict__ cache_k, T* __restrict__ cache_v, int32_t batch, int32_t cache_cap) {
+  using V = Vec16<T>;
+  constexpr int VEC = V::N;
+  constexpr int HALF = HD / 2;
+  constexpr int LPR = HALF / VEC;          // lanes per row
+  constexpr int RPP = 256 / LPR;           // rows per pass
+  constexpr int PASSES = (PIC_BLOCK_TOKENS + RPP - 1) / RPP;
+
+  int g0 = group_start[blockIdx.x], g1 = group_start[blockIdx.x + 1];
+  g0 = g0 < 0 ? 0 : g0;
+  g1 = g1 > n_blocks ? n_blocks : g1;
+  if (g0 >= g1) return;
+  const pic_block src = blocks[g0];
+  if (src.n_tokens <= 0 || src.n_tokens > PIC_BLOCK_TOKENS || src.src_token < 0 ||
+      (int64_t)src.src_token + src.n_tokens > pool_tokens)
+    return;
+
+  const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
+  const int j = threadIdx.x % LPR, r0 = threadIdx.x / LPR;
+  const int c0 = j * VEC;
+  const int o1 = off1<VEC, HALF, IL>(c0), o2 = off2<VEC, HALF, IL>(c0);
+  const float2* ltable = table + l * table_stride;
+  const int64_t src_row0 = ((int64_t)l * Hkv + h) * pool_tokens + src.src_token;
+
+  // the run's rows, held as loaded (16 bytes per vector; keys widened per destination)
+  uint4 k1[PASSES], k2[PASSES], v1[PASSES], v2[PASSES];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const int t = r0 + p * RPP;
+    if (t < src.n_tokens) {
+      const int64_t s = (src_row0 + t) * HD;
+      k1[p] = V::load_raw(pool_k + s + o1);
+      k2[p] = V::load_raw(pool_k + s + o2);
+      v1[p] = V::load_raw(pool_v + s + o1);
+      v2[p] = V::load_raw(pool_v + s + o2);
+    }
+  }
+  // The next block's descriptor and cos/sin row are read while this block is stored, so a
+  // destination costs no memory round trip of its own.
+  auto cs_of = [&](const pic_block& b, float (&cs)[VEC], float (&sn)[VEC]) {
+    int32_t d = b.delta;   // (an out-of-range block is skipped below; clamp for the read)
+    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
+    load_cs<VEC, HALF>(ltable, d, c0, cs, sn);
+  };
+  pic_block nxt = src;
+  float ncs[VEC], nsn[VEC];
+  cs_of(nxt, ncs, nsn);
+  for (int i = g0; i < g1; ++i) {
+    const pic_block blk = nxt;
+    float cs[VEC], sn[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      cs[e] = ncs[e];
+      sn[e] = nsn[e];
+    }
+    if (i + 1 < g1) {
+      nxt = blocks[i + 1];
+      cs_of(nxt, ncs, nsn);
+    }
+    if (blk.src_token != src.src_token || blk.n_tokens != src.n_tokens || blk.request < 0 ||
+        blk.request >= batch || blk.dst_slot < 0 || (int64_t)blk.dst_slot + blk.n_tokens > cache_cap ||
+        blk.delta > max_abs_delta || blk.delta < -max_abs_delta)
+      continue;
+    const int64_t dst_row0 = (((int64_t)l * batch + blk.request) * Hkv + h) * cache_cap + blk.dst_slot;
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int t = r0 + p * RPP;
+      if (t < blk.n_tokens) {
+        float x1[VEC], x2[VEC];
+        V::widen(k1[p], x1);
+        V::widen(k2[p], x2);
+        rotate<VEC, IL>(x1, x2, cs, sn);
+        const int64_t d = (dst_row0 + t) * HD;
+        V::store(cache_k + d + o1, x1);
+        V::store(cache_k + d + o2, x2);
+        V::store_raw(cache_v + d + o1, v1[p]);
+        V::store_raw(cache_v + d + o2, v2[p]);
+      }
     }
   }
 }
@@ -291,6 +403,29 @@ hipError_t launch_compose(pic_dtype dt, int head_dim, bool interleaved, int n_la
       hipLaunchKernelGGL((compose_kernel<T, HD, false>), grid, dim3(256), 0, stream,
                          (const T*)pool_k, (const T*)pool_v, pool_tokens, blocks, table,
                          table_stride, max_abs_delta, (T*)cache_k, (T*)cache_v, batch, cache_cap);
+  });
+  return hipGetLastError();
+}
+
+hipError_t launch_compose_shared(pic_dtype dt, int head_dim, bool interleaved, int n_layers,
+                                 int n_kv_heads, const void* pool_k, const void* pool_v,
+                                 int64_t pool_tokens, const pic_block* blocks, int32_t n_blocks,
+                                 const int32_t* group_start, int32_t n_groups, const float2* table,
+                                 int64_t table_stride, int32_t max_abs_delta, void* cache_k,
+                                 void* cache_v, int32_t batch, int32_t cache_cap, hipStream_t stream) {
+  if (n_groups == 0 || n_layers == 0) return hipSuccess;
+  const dim3 grid(n_groups, n_kv_heads, n_layers);
+  PIC_DISPATCH_TD(dt, head_dim, {
+    if (interleaved)
+      hipLaunchKernelGGL((compose_shared_kernel<T, HD, true>), grid, dim3(256), 0, stream,
+                         (const T*)pool_k, (const T*)pool_v, pool_tokens, blocks, group_start,
+                         n_blocks, table, table_stride, max_abs_delta, (T*)cache_k, (T*)cache_v,
+                         batch, cache_cap);
+    else
+      hipLaunchKernelGGL((compose_shared_kernel<T, HD, false>), grid, dim3(256), 0, stream,
+                         (const T*)pool_k, (const T*)pool_v, pool_tokens, blocks, group_start,
+                         n_blocks, table, table_stride, max_abs_delta, (T*)cache_k, (T*)cache_v,
+                         batch, cache_cap);
   });
   return hipGetLastError();
 }

@@ -308,6 +308,56 @@ def test_sizes(lib):
     assert pic.pic_prefill_workspace_bytes(_model(dtype="f32", head_dim=64), 1, 16, 272) == 0
 
 
+def test_plan_shared_groups_blocks_by_source():
+    """pic_plan_shared: a stable permutation of the blocks in which every group reads one pool
+    run (equal src_token and n_tokens) and different groups read different runs; on the
+    workloads every document chunk a batch places several times becomes one group."""
+    import synth
+    from synth import inputs as S
+    for name in ("c1", "c2", "c3", "llama8b_joint_1layer", "llama8b_frontier_1layer"):
+        w = synth.get(name)
+        lay = S.pool_layout(w)
+        if w.frontier:
+            blocks = pic.pic_plan_frontier(lay.items, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                           lay.pool_tokens)[0]
+        else:
+            blocks = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                         lay.pool_tokens)[0]
+        sb, gs = pic.pic_plan_shared(blocks)
+        key = lambda b: (int(b["src_token"]), int(b["n_tokens"]))
+        # stable permutation: sorting the input by source run gives the output exactly
+        order = sorted(range(len(blocks)), key=lambda i: key(blocks[i]))
+        assert np.array_equal(sb, blocks[order])
+        assert gs[0] == 0 and gs[-1] == len(blocks) and np.all(np.diff(gs) > 0)
+        runs = [key(sb[gs[g]]) for g in range(len(gs) - 1)]
+        assert len(set(runs)) == len(runs)                       # one group per distinct run
+        for g in range(len(gs) - 1):
+            assert all(key(b) == runs[g] for b in sb[gs[g]:gs[g + 1]])
+        assert len(runs) == len({key(b) for b in blocks})
+    # requests sharing documents share groups: 16 requests x 10 of 64 documents
+    w = synth.get("c3")
+    lay = S.pool_layout(w)
+    blocks = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos, lay.pool_tokens)[0]
+    assert len(blocks) / (len(pic.pic_plan_shared(blocks)[1]) - 1) > 2
+    assert len(pic.pic_plan_shared(blocks[:0])[0]) == 0
+
+
+def test_compose_shared_argument_checks(lib):
+    m = _model()
+    n = ctypes.c_int32(0)
+    starts = (ctypes.c_int32 * 4)()
+    assert lib.pic_plan_shared(None, 3, None, starts, ctypes.byref(n)) == -1
+    assert lib.pic_plan_shared(None, -1, None, starts, ctypes.byref(n)) == -1
+    a = dict(pool_k=FAKE, pool_v=FAKE, pool_tokens=1000, blocks=FAKE, n_blocks=4, starts=FAKE, n_groups=2,
+             table=FAKE, mad=100, ck=FAKE, cv=FAKE, batch=2, cap=1000)
+    call = lambda **kw: lib.pic_compose_shared(ctypes.byref(m), *{**a, **kw}.values(), None)
+    assert call(n_groups=5) == -1                  # more groups than blocks
+    assert call(starts=None) == -1
+    assert call(pool_k=MIS) == -5
+    assert call(mad=1 << 30) == -6
+    assert call(n_groups=0) == 0                   # nothing to do: nothing launched
+
+
 def test_rotary_variant_arguments(lib):
     m = _model(n_layers=3)
     one = pic.pic_rope_table_bytes(m, 100)

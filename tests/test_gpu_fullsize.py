@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+import paper_2607_28069_amd as pic
 import synth
 from bench import DeviceWorkload
 from oracle import pic_oracle as O
@@ -115,6 +116,26 @@ def _check_compose_all_requests(wl, l):
         n = m.ctx_len
         assert np.array_equal(_host(wl.cache_v[l, r])[:, :n].view(np.uint32), V.view(np.uint32)), r
         assert assert_keys_close(_host(wl.cache_k[l, r])[:, :n], K, w.dtype) > 0.999, r
+
+
+@pytest.mark.parametrize("name,layers", [("c3", 2), ("c4", 1), ("c5", 2)])
+def test_compose_shared_equals_per_block_full_size(name, layers):
+    # The bench's compose (blocks grouped by document run, each run read once) against
+    # pic_compose over the blocks as planned, at full per-layer shape: identical caches.
+    w = synth.get(name)
+    a = DeviceWorkload(w, DEV, n_dec=1, layers=layers)
+    b = DeviceWorkload(w, DEV, n_dec=1, layers=layers, shared_compose=False)
+    for wl in (a, b):
+        lay = wl.lay
+        blocks = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                     lay.pool_tokens)[0]
+        nb, ng = wl.upload(blocks, wl.blocks_pinned, wl.blocks_dev, wl.groups_dev)
+        wl.compose(wl.blocks_dev, wl.groups_dev, nb, ng, wl.cache_k, wl.cache_v, w.batch)
+    torch.cuda.synchronize()
+    assert torch.equal(a.pool_k, b.pool_k) and torch.equal(a.pool_v, b.pool_v)
+    assert torch.equal(a.cache_k, b.cache_k) and torch.equal(a.cache_v, b.cache_v)
+    print(f"[{name}] {nb} blocks in {ng} groups: shared compose == per-block compose, {layers} layer(s)",
+          flush=True)
 
 
 def test_llama8b_32layer_compose_all_requests():

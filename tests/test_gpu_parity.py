@@ -259,3 +259,83 @@ def test_non_default_stream_and_layer_batching():
                         d["blocks"], d["blocks"].numel() // 5, d["table"], d["mad"], ck1, cv1,
                         w.batch, r.cap)
         assert torch.equal(ck1[0], ck[l]) and torch.equal(cv1[0], cv[l])
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "llama8b_joint_1layer", "llama8b_frontier_1layer", "ragged"])
+def test_compose_shared_equals_compose(name):
+    """pic_compose_shared over pic_plan_shared's groups writes the cache pic_compose writes, bit
+    for bit, slots no block covers included (both start from the same random contents); and
+    the blocks taken in any order give that cache too."""
+    import dataclasses
+    if name == "ragged":
+        w = dataclasses.replace(synth.get("c2"), name="ragged", n_q_heads=28, n_kv_heads=4, pool_docs=5,
+                                doc_len=77, docs_per_request=4, n_suffix=37, prefix_len=13, batch=3,
+                                doc_len_jitter=(1, 150))
+    else:
+        w = synth.get(name)
+    lay = S.pool_layout(w)
+    if w.frontier:
+        blocks = pic.pic_plan_frontier(lay.items, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                       lay.pool_tokens)[0]
+    else:
+        blocks = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                     lay.pool_tokens)[0]
+    L, dt = 2, tdtype(w)
+    m = pic.Model.of(L, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype, w.rope_theta)
+    cap = int(max(b["dst_slot"] + b["n_tokens"] for b in blocks)) + 5
+    g = torch.Generator(device=DEV).manual_seed(3)
+    pk = torch.randn((L, w.n_kv_heads, lay.pool_tokens, w.head_dim), device=DEV, generator=g).to(dt)
+    pv = torch.randn(pk.shape, device=DEV, generator=g).to(dt)
+    init = torch.randn((L, w.batch, w.n_kv_heads, cap, w.head_dim), device=DEV, generator=g).to(dt)
+    table = torch.empty(pic.pic_rope_table_bytes(m, cap) // 4, dtype=torch.float32, device=DEV)
+    pic.pic_rope_table_init(m, cap, table)
+    dev_blocks = lambda b: torch.from_numpy(np.ascontiguousarray(b).view(np.int32).reshape(-1).copy()).to(DEV)
+    ck, cv = init.clone(), init.clone()
+    pic.pic_compose(m, pk, pv, lay.pool_tokens, dev_blocks(blocks), len(blocks), table, cap, ck, cv, w.batch, cap)
+    rng = np.random.default_rng(1)
+    for order in (np.arange(len(blocks)), rng.permutation(len(blocks))):
+        sb, gs = pic.pic_plan_shared(blocks[order])
+        ck2, cv2 = init.clone(), init.clone()
+        pic.pic_compose_shared(m, pk, pv, lay.pool_tokens, dev_blocks(sb), len(sb), torch.from_numpy(gs).to(DEV),
+                               len(gs) - 1, table, cap, ck2, cv2, w.batch, cap)
+        torch.cuda.synchronize()
+        assert torch.equal(ck, ck2) and torch.equal(cv, cv2), name
+    print(f"[{name}] {len(blocks)} blocks in {len(gs) - 1} groups: shared compose == compose", flush=True)
+
+
+def test_compose_shared_skips_blocks_outside_their_group():
+    """A group whose later block names another source run or an out-of-range destination: that
+    block is skipped (its slots keep their contents), the others are written."""
+    w = synth.get("c2")
+    lay = S.pool_layout(w)
+    blocks = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos, lay.pool_tokens)[0]
+    sb, gs = pic.pic_plan_shared(blocks)
+    big = int(np.argmax(np.diff(gs)))               # a group with several blocks
+    i0, i1 = int(gs[big]), int(gs[big + 1])
+    assert i1 - i0 >= 2
+    bad = sb.copy()
+    bad[i0 + 1]["src_token"] += 1                   # reads another run: skipped
+    bad[i1 - 1]["dst_slot"] = 1 << 30               # destination out of range: skipped
+    m = pic.Model.of(1, w.n_q_heads, w.n_kv_heads, w.head_dim, w.dtype, w.rope_theta)
+    cap = int(max(b["dst_slot"] + b["n_tokens"] for b in blocks)) + 1
+    pk = torch.randn((1, w.n_kv_heads, lay.pool_tokens, w.head_dim), device=DEV).to(torch.bfloat16)
+    pv = torch.randn(pk.shape, device=DEV).to(torch.bfloat16)
+    table = torch.empty(pic.pic_rope_table_bytes(m, cap) // 4, dtype=torch.float32, device=DEV)
+    pic.pic_rope_table_init(m, cap, table)
+    outs = []
+    for lst in (sb, bad):
+        ck = torch.full((1, w.batch, w.n_kv_heads, cap, w.head_dim), 7.0, dtype=torch.bfloat16, device=DEV)
+        cv = ck.clone()
+        pic.pic_compose_shared(m, pk, pv, lay.pool_tokens,
+                               torch.from_numpy(lst.view(np.int32).reshape(-1).copy()).to(DEV), len(lst),
+                               torch.from_numpy(gs).to(DEV), len(gs) - 1, table, cap, ck, cv, w.batch, cap)
+        outs.append((host(ck)[0], host(cv)[0]))
+    torch.cuda.synchronize()
+    for j, (ref, got) in enumerate(zip(outs[0], outs[1])):
+        for i in range(len(sb)):
+            b = sb[i]
+            sl = np.s_[int(b["request"]), :, int(b["dst_slot"]):int(b["dst_slot"]) + int(b["n_tokens"])]
+            if i in (i0 + 1, i1 - 1):
+                assert np.all(got[sl] == 7.0), (j, i)
+            else:
+                assert np.array_equal(got[sl].view(np.uint32), ref[sl].view(np.uint32)), (j, i)

@@ -65,7 +65,16 @@ def test_compose_with_rotary_variants(dtype, D, pairing):
     ck = torch.zeros((L, B, Hkv, cap, D), dtype=dt, device=DEV)
     cv = torch.zeros_like(ck)
     bl = torch.from_numpy(blocks.view(np.int32).reshape(-1).copy()).to(DEV)
-    pic.pic_compose(m, to_dev(pool_k, dt), to_dev(pool_v, dt), T, bl, len(blocks), table, mad, ck, cv, B, cap)
+    dpk, dpv = to_dev(pool_k, dt), to_dev(pool_v, dt)
+    pic.pic_compose(m, dpk, dpv, T, bl, len(blocks), table, mad, ck, cv, B, cap)
+    # shared sources (the two requests place documents 1 and 3 twice): the same cache, bit for bit
+    sb, gs = pic.pic_plan_shared(blocks)
+    assert len(gs) - 1 < len(blocks)
+    ck2, cv2 = torch.zeros_like(ck), torch.zeros_like(cv)
+    pic.pic_compose_shared(m, dpk, dpv, T, torch.from_numpy(sb.view(np.int32).reshape(-1).copy()).to(DEV),
+                           len(sb), torch.from_numpy(gs).to(DEV), len(gs) - 1, table, mad, ck2, cv2, B, cap)
+    torch.cuda.synchronize()
+    assert torch.equal(ck, ck2) and torch.equal(cv, cv2), "shared-source compose differs"
     gk, gv = host(ck), host(cv)
     maps = O.plan_layout(reqs, offs, lens, cpos)
     for l in range(L):
