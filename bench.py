@@ -19,6 +19,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -347,7 +348,9 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
     untimed pass; the pool, suffix inputs and rotary table are those of the batched workload.
     A lone request's per-layer launches are short, so the launch sequence after the plan is
     also recorded once per request as a HIP graph and replayed (the plan and the copy of its
-    gather blocks stay in the timed region).  Returns (eager mean, graph-replay mean)."""
+    gather blocks stay in the timed region).  Returns the medians over all samples (eager,
+    graph replay): an occasional host stall of tens of milliseconds, seen on either path,
+    moves a 20-sample mean by several percent."""
     import numpy as np
     import torch
 
@@ -434,7 +437,7 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
             if rep:
                 graphed.append((time.perf_counter() - t0) * 1e3)
         del g
-    return float(sum(eager) / len(eager)), float(sum(graphed) / len(graphed))
+    return float(statistics.median(eager)), float(statistics.median(graphed))
 
 
 # ------------------------------------------------------------------------------------------
