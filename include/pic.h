@@ -275,11 +275,15 @@ pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q, c
    * tile_map from pic_build_slot_map (same blocks, batch and map_cap): a context tile that is
      one pool run under one shift is loaded in one piece, unturned, and the queries are turned
      by -shift for its scores instead (<R(-d) q, k> = <q, R(d) k>: RoPE's relative property
-     applied to Eq. 3), in float32 with one bf16 rounding of the turned query; other tiles take
-     the per-key path.  Outputs then match compose + prefill to within bf16 rounding, not bit
-     for bit.  Entries outside the pool, the table or the context are treated as (-1, 0).
-   Only the suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)); a later
-   pic_compose fills the document slots for decoding.  bf16 only.
+     applied to Eq. 3), in float32 with one bf16 rounding of the turned query.  Every other
+     context tile (document boundaries off the 64-slot grid, short documents, a partial last
+     tile) is first composed into the cache from the slot map (pic_compose's arithmetic, a
+     launch of its own on the same stream) and read from there.  Outputs then match compose +
+     prefill to within bf16 rounding, not bit for bit.  Entries outside the pool, the table or
+     the context are treated as (-1, 0).
+   The suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)), and with a tile map
+   the non-run context tiles; a later pic_compose (or pic_compose_shared) fills the document
+   slots for decoding.  bf16 only.
      pool_k, pool_v, pool_tokens, table, max_abs_delta   as for pic_compose
      slot_src, slot_delta, map_cap   the map; map_cap >= max_ctx (entries are clamped to the
                                      pool and to max_abs_delta)

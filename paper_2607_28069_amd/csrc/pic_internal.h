@@ -122,6 +122,15 @@ hipError_t launch_prefill_bf16_rope(const AttnShape& s, bool interleaved, const 
 // [batch][slot_map_tiles(map_cap)][2] = (src, shift) for every 64-slot tile that is pool tokens
 // src .. src + 63 under one shift, (-1, 0) for any other tile.
 int32_t slot_map_tiles(int32_t map_cap);
+// The context tiles of a paged prefill that are not whole pool runs (tile map), composed into
+// the cache from the slot map (bf16, head_dim 128; compose arithmetic).
+hipError_t launch_compose_tiles(bool interleaved, int n_layers, int n_kv_heads, const bf16_t* pool_k,
+                                const bf16_t* pool_v, int64_t pool_tokens, const int32_t* smap,
+                                const int32_t* dmap, int32_t map_cap, const int32_t* tmap,
+                                int32_t map_tiles, const int32_t* ctx_len, int32_t max_ctx,
+                                const float2* table, int64_t table_stride, int32_t max_abs_delta,
+                                bf16_t* cache_k, bf16_t* cache_v, int32_t batch, int32_t cache_cap,
+                                hipStream_t stream);
 hipError_t launch_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch, int32_t map_cap,
                            int32_t* slot_src, int32_t* slot_delta, int32_t* tile_map,
                            hipStream_t stream);

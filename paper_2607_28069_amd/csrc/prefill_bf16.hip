@@ -149,7 +149,10 @@ struct PrefillArgs {
 
 // Rope mode = suffix mode with the suffix queries and keys given unrotated: the kernel turns
 // them to their positions (RoPE at ctx + i, from the delta-angle table) as they are loaded.
-constexpr int kModeSuffix = 0, kModeTable = 1, kModePaged = 2, kModeRope = 3;
+// Runs mode = paged mode with a tile map whose non-run context tiles have been composed into
+// the cache beforehand: whole-run tiles come from the pool (queries turned), all others from
+// the cache, so the loop carries no per-key rotation.
+constexpr int kModeSuffix = 0, kModeTable = 1, kModePaged = 2, kModeRope = 3, kModeRuns = 4;
 
 // (x, y) turned by the angle with cosine c and sine s, in the float32 arithmetic the compose
 // and re-rotation kernels use, so fused and separate rotations round identically.
@@ -189,6 +192,7 @@ template <int kMode, bool kInterleaved>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_bf16_kernel(PrefillArgs a) {
   constexpr bool kTable = kMode == kModeTable, kPaged = kMode == kModePaged, kRope = kMode == kModeRope;
+  constexpr bool kRuns = kMode == kModeRuns, kPool = kPaged || kRuns;   // kPool: whole-run tiles from the pool
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
   // loads in flight into one buffer do not alias reads from another.  (The larger alignment
   // places them first, at the bottom of LDS, ahead of the paged mode's bigger areas.)
@@ -197,9 +201,9 @@ prefill_bf16_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(4096))) uint8_t v_lds0[kTileBytes];
   __shared__ __attribute__((aligned(4096))) uint8_t v_lds1[kTileBytes];
   // paged and rope modes: each wave's cos/sin of the key rows it turns (4 KB per wave)
-  __shared__ __attribute__((aligned(16))) uint8_t cs_lds[(kPaged || kRope) ? kWaves * 4096 : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t cs_lds[(kPool || kRope) ? kWaves * 4096 : 16];
   // paged mode: each wave's unturned Q^T operand (8 KB per wave), the source of every turn
-  __shared__ __attribute__((aligned(16))) uint8_t q_lds[kPaged ? kWaves * 8192 : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t q_lds[kPool ? kWaves * 8192 : 16];
 
   // XCD-aware block order: hardware block w runs on XCD w % 8; give each XCD a contiguous
   // range of logical blocks so the m-tiles of one (request, kv head) share an L2.
@@ -388,7 +392,7 @@ prefill_bf16_kernel(PrefillArgs a) {
       }
     }
   };
-  if constexpr (kPaged) {   // keep the unturned operand (lane-private slots)
+  if constexpr (kPool) {   // keep the unturned operand (lane-private slots)
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
       *reinterpret_cast<u32x4*>(q_lds + wave * 8192 + (ks * 64 + lane) * 16) = __builtin_bit_cast(u32x4, qop[ks]);
@@ -404,16 +408,16 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int v_goff = ld_row * kHD + 8 * (ld_slot ^ v_swz(ld_row));
   const int v_gc = ld_slot ^ v_swz(ld_row), k_gc = ld_slot ^ k_swz(ld_row);
   // paged mode: pool rows of this (layer, kv head), and the slot map of this request
-  const bf16_t* PKg = kPaged ? a.pool_k + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
-  const bf16_t* PVg = kPaged ? a.pool_v + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
+  const bf16_t* PKg = kPool ? a.pool_k + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
+  const bf16_t* PVg = kPool ? a.pool_v + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
   const int32_t* smap = kPaged ? a.smap + (int64_t)b * a.map_cap : nullptr;
   // buffer resources (byte offsets from these bases fit in 32 bits: a cache stream holds
   // cache_cap rows, the suffix n_suffix * Hkv rows, a pool head pool_tokens rows and a
   // table (max_abs_delta + 1) rows of 512 bytes, each under 2^32 bytes by the host checks)
   const rsrc_t r_k = make_rsrc(Kg), r_v = make_rsrc(Vg);
   const rsrc_t r_ks = make_rsrc(kTable ? Kg : Ks), r_vs = make_rsrc(kTable ? Vg : Vs);
-  const rsrc_t r_pk = make_rsrc(kPaged ? PKg : Kg), r_pv = make_rsrc(kPaged ? PVg : Vg);
-  const rsrc_t r_tab = make_rsrc((kPaged || kRope) ? a.table + (int64_t)l * a.table_stride : (const float2*)Kg);
+  const rsrc_t r_pk = make_rsrc(kPool ? PKg : Kg), r_pv = make_rsrc(kPool ? PVg : Vg);
+  const rsrc_t r_tab = make_rsrc((kPool || kRope) ? a.table + (int64_t)l * a.table_stride : (const float2*)Kg);
   const int32_t* dmap = kPaged ? a.dmap + (int64_t)b * a.map_cap : nullptr;
   // pool token of load row i (0, 1) of global tile t for this lane (0 past the context)
   // (map entries are loaded raw and checked after the tile's loads have landed: a use right
@@ -561,7 +565,7 @@ prefill_bf16_kernel(PrefillArgs a) {
     const uint32_t goff = 2u * (is_v ? v_goff : k_goff);   // bytes
     const uint32_t coff = 16u * (is_v ? v_gc : k_gc);
     const rsrc_t rc = is_v ? r_v : r_k, rs = is_v ? r_vs : r_ks;
-    if (kPaged && run >= 0) {   // a whole-run tile: pool rows run .. run + 63
+    if (kPool && run >= 0) {   // a whole-run tile: pool rows run .. run + 63
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i)
         dma16(is_v ? r_pv : r_pk, goff, (uint32_t)(run + 4 * kWaves * i) * kRowBytes,
@@ -824,6 +828,23 @@ prefill_bf16_kernel(PrefillArgs a) {
       stage_row(del_v);
       wait_loads();
     }
+  } else if constexpr (kRuns) {
+    int32_t del0 = 0, del1 = 0;
+    const int32_t run0 = tile_run(t0, del0), run1 = n_tiles > 1 ? tile_run(t0 + 1, del1) : -1;
+    if (run0 >= 0 && del0 != 0) {   // the operand for the scores of tile 0
+      stage_row(del0);
+      wait_loads();
+      turn_q(del0);
+    }
+    load_tile(k_lds0, t0, false, run0);
+    load_tile(v_lds0, t0, true, run0);
+    if (n_tiles > 1) load_tile(k_lds1, t0 + 1, false, run1);
+    run_v = run1;
+    del_v = del1;
+    run_k = n_tiles > 2 ? tile_run(t0 + 2, del_k) : -1;
+    // the row the first tile turns the operand with, for the scores of tile 1
+    if (run_v >= 0 && del_v != 0 && del_v != q_shift) stage_row(del_v);
+    wait_loads();
   } else {
     load_tile(k_lds0, t0, false);
     load_tile(v_lds0, t0, true);
@@ -862,7 +883,7 @@ prefill_bf16_kernel(PrefillArgs a) {
     // paged: the operand for the scores of tile t + 1, computed below (its cos/sin row, if
     // any, was staged during the previous tile; read before this tile's cos/sin loads)
     int32_t run_f = -1, del_f = 0;   // paged: tile t + 3 (K issued by the next tile)
-    if constexpr (kPaged) {
+    if constexpr (kPool) {
       turn_q(run_v >= 0 ? del_v : 0);
       if (t + 3 < n_tiles) run_f = tile_run(t0 + t + 3, del_f);
     }
@@ -877,11 +898,13 @@ prefill_bf16_kernel(PrefillArgs a) {
       if (t + 2 < n_tiles && (t0 + t + 3) * kKeys > ctx) rope_cs(t0 + t + 2);
     }
     int32_t rdl_f = 0;   // raw shift of this lane's rotation row of tile t + 3
-    if constexpr (kPaged) {
-      if (t + 2 < n_tiles && run_k < 0) load_cs(d_k);
+    if constexpr (kPool) {
+      if (kPaged && t + 2 < n_tiles && run_k < 0) load_cs(d_k);
       // the row the next tile turns the operand with (tile t + 2 is a whole run, so nothing
       // uses the cos/sin area during this tile)
       if (run_k >= 0 && del_k != 0 && del_k != q_shift) stage_row(del_k);
+    }
+    if constexpr (kPaged) {
       // tile t + 3 not a whole run: the rows and shifts of its keys, loaded now and checked
       // once the tile's loads have landed
       if (run_f < 0 && ctx > 0) {
@@ -973,6 +996,8 @@ prefill_bf16_kernel(PrefillArgs a) {
         src_k[i] = rows_f ? fin_src(t0 + t + 3, i, src_f[i]) : 0;
       }
       d_k = rows_f ? fin_delta(t0 + t + 3, rdl_f) : 0;
+    }
+    if constexpr (kPool) {
       run_v = run_k;
       del_v = del_k;
       run_k = run_f;
@@ -1184,6 +1209,10 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
     hipLaunchKernelGGL((prefill_bf16_kernel<kModeRope, false>), grid, dim3(kThreads), 0, stream, a);
   else if (mode == kModePaged && interleaved)
     hipLaunchKernelGGL((prefill_bf16_kernel<kModePaged, true>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRuns && interleaved)
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRuns, true>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRuns)
+    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRuns, false>), grid, dim3(kThreads), 0, stream, a);
   else if (mode == kModePaged)
     hipLaunchKernelGGL((prefill_bf16_kernel<kModePaged, false>), grid, dim3(kThreads), 0, stream, a);
   else
@@ -1308,7 +1337,16 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
   a.ctx_len = ctx_len;
   a.out = out;
   a.max_ctx = max_ctx;
-  return launch(s, a, kModePaged, interleaved, n_suffix, max_ctx, workspace, ws_bytes, stream);
+  if (tmap == nullptr)   // every tile read through the slot map, keys turned in LDS
+    return launch(s, a, kModePaged, interleaved, n_suffix, max_ctx, workspace, ws_bytes, stream);
+  // with a tile map: the tiles that are not whole runs are composed into the cache first, then
+  // the prefill reads whole runs from the pool and everything else from the cache
+  const hipError_t e = launch_compose_tiles(interleaved, s.n_layers, s.n_kv_heads, pool_k, pool_v,
+                                            pool_tokens, smap, dmap, map_cap, tmap, a.map_tiles,
+                                            ctx_len, max_ctx, table, table_stride, max_abs_delta,
+                                            cache_k, cache_v, s.batch, s.cache_cap, stream);
+  if (e != hipSuccess) return e;
+  return launch(s, a, kModeRuns, interleaved, n_suffix, max_ctx, workspace, ws_bytes, stream);
 }
 
 }  // namespace pic

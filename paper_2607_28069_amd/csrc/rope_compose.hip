@@ -286,6 +286,67 @@ __global__ void __launch_bounds__(256) compose_shared_kernel(
   }
 }
 
+// grid (batch * map_tiles, Hkv, L), 256 threads.  Zero-copy prefill with a tile map: the
+// prefill reads a context tile straight from the pool when it is one pool run under one shift
+// (tile map entry (src, delta) with src >= 0, the run inside the pool, |delta| within the
+// table and the tile inside the context: the test the prefill applies); every other context
+// tile is composed here into the cache from the slot map, row by row, with compose_kernel's
+// arithmetic, so the prefill can read it from there.  Whole-run tiles are left alone.
+template <typename T, int HD, bool IL>
+__global__ void __launch_bounds__(256) compose_tiles_kernel(
+    const T* __restrict__ pool_k, const T* __restrict__ pool_v, int64_t pool_tokens,
+    const int32_t* __restrict__ smap, const int32_t* __restrict__ dmap, int32_t map_cap,
+    const int32_t* __restrict__ tmap, int32_t map_tiles, const int32_t* __restrict__ ctx_len,
+    int32_t max_ctx, const float2* __restrict__ table, int64_t table_stride,
+    int32_t max_abs_delta, T* __restrict__ cache_k, T* __restrict__ cache_v, int32_t batch,
+    int32_t cache_cap) {
+  using V = Vec16<T>;
+  constexpr int VEC = V::N;
+  constexpr int HALF = HD / 2;
+  constexpr int LPR = HALF / VEC;
+  constexpr int RPP = 256 / LPR;
+  constexpr int PASSES = (PIC_BLOCK_TOKENS + RPP - 1) / RPP;
+
+  const int b = blockIdx.x / map_tiles, tile = blockIdx.x - b * map_tiles;
+  int ctx = ctx_len[b];
+  ctx = ctx < 0 ? 0 : (ctx > max_ctx ? max_ctx : ctx);
+  const int s0 = tile * PIC_BLOCK_TOKENS;
+  if (s0 >= ctx) return;
+  const int32_t src = tmap[((int64_t)b * map_tiles + tile) * 2];
+  const int32_t dl = tmap[((int64_t)b * map_tiles + tile) * 2 + 1];
+  if (s0 + PIC_BLOCK_TOKENS <= ctx && src >= 0 && (int64_t)src + PIC_BLOCK_TOKENS <= pool_tokens &&
+      dl >= -max_abs_delta && dl <= max_abs_delta)
+    return;   // a whole run: the prefill reads it from the pool
+
+  const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
+  const int j = threadIdx.x % LPR, r0 = threadIdx.x / LPR;
+  const int c0 = j * VEC;
+  const int o1 = off1<VEC, HALF, IL>(c0), o2 = off2<VEC, HALF, IL>(c0);
+  const float2* ltable = table + l * table_stride;
+  const int64_t pool0 = ((int64_t)l * Hkv + h) * pool_tokens;
+  const int64_t dst0 = (((int64_t)l * batch + b) * Hkv + h) * cache_cap;
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const int slot = s0 + r0 + p * RPP;
+    if (slot >= ctx) continue;
+    int32_t st = smap[(int64_t)b * map_cap + slot];
+    st = st < 0 ? 0 : (st >= pool_tokens ? (int32_t)(pool_tokens - 1) : st);
+    int32_t d = dmap[(int64_t)b * map_cap + slot];
+    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
+    float cs[VEC], sn[VEC], x1[VEC], x2[VEC];
+    load_cs<VEC, HALF>(ltable, d, c0, cs, sn);
+    const int64_t sr = (pool0 + st) * HD, dr = (dst0 + slot) * HD;
+    V::load(pool_k + sr + o1, x1);
+    V::load(pool_k + sr + o2, x2);
+    const uint4 w1 = V::load_raw(pool_v + sr + o1), w2 = V::load_raw(pool_v + sr + o2);
+    rotate<VEC, IL>(x1, x2, cs, sn);
+    V::store(cache_k + dr + o1, x1);
+    V::store(cache_k + dr + o2, x2);
+    V::store_raw(cache_v + dr + o1, w1);
+    V::store_raw(cache_v + dr + o2, w2);
+  }
+}
+
 // rows [n_tokens][n_heads][HD]; one (row, chunk) per thread, grid-stride.
 template <typename T, int HD, bool IL>
 __global__ void __launch_bounds__(256) rerotate_kernel(const T* k_in, T* k_out, int64_t n_rows,
@@ -427,6 +488,26 @@ hipError_t launch_compose_shared(pic_dtype dt, int head_dim, bool interleaved, i
                          n_blocks, table, table_stride, max_abs_delta, (T*)cache_k, (T*)cache_v,
                          batch, cache_cap);
   });
+  return hipGetLastError();
+}
+
+hipError_t launch_compose_tiles(bool interleaved, int n_layers, int n_kv_heads, const bf16_t* pool_k,
+                                const bf16_t* pool_v, int64_t pool_tokens, const int32_t* smap,
+                                const int32_t* dmap, int32_t map_cap, const int32_t* tmap,
+                                int32_t map_tiles, const int32_t* ctx_len, int32_t max_ctx,
+                                const float2* table, int64_t table_stride, int32_t max_abs_delta,
+                                bf16_t* cache_k, bf16_t* cache_v, int32_t batch, int32_t cache_cap,
+                                hipStream_t stream) {
+  if ((int64_t)batch * map_tiles == 0 || n_layers == 0) return hipSuccess;
+  const dim3 grid((unsigned)((int64_t)batch * map_tiles), n_kv_heads, n_layers);
+  if (interleaved)
+    hipLaunchKernelGGL((compose_tiles_kernel<bf16_t, 128, true>), grid, dim3(256), 0, stream, pool_k, pool_v,
+                       pool_tokens, smap, dmap, map_cap, tmap, map_tiles, ctx_len, max_ctx, table,
+                       table_stride, max_abs_delta, cache_k, cache_v, batch, cache_cap);
+  else
+    hipLaunchKernelGGL((compose_tiles_kernel<bf16_t, 128, false>), grid, dim3(256), 0, stream, pool_k, pool_v,
+                       pool_tokens, smap, dmap, map_cap, tmap, map_tiles, ctx_len, max_ctx, table,
+                       table_stride, max_abs_delta, cache_k, cache_v, batch, cache_cap);
   return hipGetLastError();
 }
 

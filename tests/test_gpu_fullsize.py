@@ -270,8 +270,9 @@ def test_rotary_variant_workloads(name):
 
 @pytest.mark.parametrize("name", ["c3", "c5"])
 def test_paged_prefill_full_size(name):
-    # The bench's zero-copy TTFT path at full size (whole-run tiles turn the queries; the others
-    # their keys): every layer's paged prefill output within the attention tolerance of the
+    # The bench's zero-copy TTFT path at full size (whole-run tiles read from the pool with the
+    # queries turned; the others composed into the cache first and read from there): every
+    # layer's paged prefill output within the attention tolerance of the
     # suffix prefill over the cache composed afterwards; sampled requests against the oracle.
     import paper_2607_28069_amd as pic
     from gpu_path import host

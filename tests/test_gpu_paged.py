@@ -7,8 +7,10 @@ straight from the pool through the gather blocks (App. C.1 token map; Sec. 2, Eq
   queries are turned by -shift instead (RoPE's relative property); the outputs must then be
   within the attention tolerance of compose + prefill and of the oracle.  The tile map itself
   is checked entry by entry.
-In both modes the suffix rows stored into the cache are bit-exact and the composed document
-slots stay untouched.
+In both modes the suffix rows stored into the cache are bit-exact.  Without a tile map the
+composed document slots stay untouched; with it, the context tiles that are not whole runs are
+composed into the cache first (bit-identical to compose, so the prefill reads them from there)
+and the whole-run tiles stay untouched.
 """
 import dataclasses
 
@@ -74,10 +76,13 @@ def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, 
         tm = tmap.cpu().numpy()
         assert np.array_equal(tm, _expected_tile_map(sm, dm, map_cap)), "tile map"
         _paged.runs = int((tm[..., 0] >= 0).sum()), int((tm[..., 0] < 0).sum())
+        _paged.tmap = tm
     return out, ck, cv
 
 
-def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=True):
+def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=True, tmap=None):
+    """tmap (whole-run mode): context tiles marked as runs stay untouched, the others hold the
+    composed rows bit for bit."""
     w = r.w
     if exact:
         assert torch.equal(out_p, out_m), "paged outputs differ from compose + prefill"
@@ -87,7 +92,16 @@ def _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=T
         c = int(r.ctx[b])
         sl = slice(c, c + w.n_suffix)
         assert torch.equal(ck_p[:, b, :, sl], ck_m[:, b, :, sl]) and torch.equal(cv_p[:, b, :, sl], cv_m[:, b, :, sl])
-        assert not ck_p[:, b, :, :c].any() and not cv_p[:, b, :, :c].any(), "document slots were written"
+        if tmap is None:
+            assert not ck_p[:, b, :, :c].any() and not cv_p[:, b, :, :c].any(), "document slots were written"
+            continue
+        for t in range((c + 63) // 64):
+            ts = slice(64 * t, min(64 * t + 64, c))
+            if tmap[b, t, 0] >= 0:
+                assert not ck_p[:, b, :, ts].any() and not cv_p[:, b, :, ts].any(), f"run tile {t} written"
+            else:
+                assert torch.equal(ck_p[:, b, :, ts], ck_m[:, b, :, ts]) and \
+                    torch.equal(cv_p[:, b, :, ts], cv_m[:, b, :, ts]), f"tile {t} not composed"
 
 
 @pytest.mark.parametrize("runs", [False, True], ids=["per-key", "whole-runs"])
@@ -108,7 +122,8 @@ def test_paged_prefill_equals_compose_then_prefill(name, runs):
     out_m = gpu_prefill(r).clone()
     out_p, ck_p, cv_p = _paged(r, runs=runs)
     torch.cuda.synchronize()
-    _check_against_materialized(r, out_p, ck_p, cv_p, r.dev["cache_k"], r.dev["cache_v"], out_m, exact=not runs)
+    _check_against_materialized(r, out_p, ck_p, cv_p, r.dev["cache_k"], r.dev["cache_v"], out_m, exact=not runs,
+                                tmap=_paged.tmap if runs else None)
     got = host(out_p)[0]
     for b in range(w.batch):
         ref, _, _ = oracle_prefill(r, b)
@@ -151,4 +166,5 @@ def test_paged_prefill_with_rotary_variants(pairing, runs):
     d["table"] = table
     out_p, ck_p, cv_p = _paged(r, model=m2, pool_k=pk, pool_v=pv, layers=2, runs=runs)
     torch.cuda.synchronize()
-    _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=not runs)
+    _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=not runs,
+                                tmap=_paged.tmap if runs else None)
