@@ -273,6 +273,18 @@ prefill_bf16_kernel(PrefillArgs a) {
     ctx = pos_max_wg + 1;   // every visible key is in the cache
   }
   const int n_keys = kTable ? pos_max_wg + 1 : ctx + a.n_suffix;
+  // table mode: the wave's furthest query position.  A tile that starts past it holds no key
+  // any of the wave's rows sees, so the wave skips the products and exponentials of every
+  // tile from there on (it still moves its share of each tile and meets each barrier).  Rows
+  // of different inline spans share a workgroup, so on the general frontier layout waves
+  // whose spans end early skip whole tiles.
+  int wave_max = INT_MAX;
+  if constexpr (kTable) {
+    int wm = row_ok ? qpos : -1;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) wm = max(wm, __shfl_xor(wm, o, 64));
+    wave_max = __builtin_amdgcn_readfirstlane(wm);
+  }
   const int ld_row = 4 * wave + (lane >> 4), ld_slot = lane & 15;   // load row within a step
   // this workgroup's key tiles: [t0, t0 + n_tiles) of the (pos_max_wg + 1) visible keys
   const int t0 = split * a.tiles_per_split;
@@ -1006,9 +1018,27 @@ prefill_bf16_kernel(PrefillArgs a) {
     __syncthreads();
   };
 
-  for (int t = 0; t < n_tiles; t += 2) {
+  // local tiles [0, t_live) hold keys some row of this wave sees (all of them outside table mode)
+  const int t_live = !kTable ? n_tiles
+                             : (wave_max < t0 * kKeys ? 0 : min(n_tiles, wave_max / kKeys - t0 + 1));
+  for (int t = 0; t < t_live; t += 2) {
     tile(t, std::integral_constant<int, 0>{}, s_a, s_b);
-    if (t + 1 < n_tiles) tile(t + 1, std::integral_constant<int, 1>{}, s_b, s_a);
+    if (t + 1 < t_live) tile(t + 1, std::integral_constant<int, 1>{}, s_b, s_a);
+  }
+  if constexpr (kTable) {   // the rest: this wave's share of the loads and the barriers only
+    auto idle = [&](int t, auto parity) {
+      constexpr int P = decltype(parity)::value;
+      flush_pending();   // the last computed tile's last slice (then nothing is pending)
+      pend_p = as_bf16x8(u32x4{0, 0, 0, 0});
+      if (t + 2 < n_tiles) load_tile(P ? k_lds1 : k_lds0, t0 + t + 2, false);
+      if (t + 1 < n_tiles) load_tile(P ? v_lds0 : v_lds1, t0 + t + 1, true);
+      wait_loads();
+      __syncthreads();
+    };
+    for (int t = t_live; t < n_tiles; ++t) {
+      if (t & 1) idle(t, std::integral_constant<int, 1>{});
+      else idle(t, std::integral_constant<int, 0>{});
+    }
   }
 
   // ---- lane holds head dims 32 db + 8 qd + 4 hh + (0..3) of its row
