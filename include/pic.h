@@ -206,7 +206,8 @@ pic_status pic_compose(const pic_model* model, const void* pool_k, const void* p
      blocks [host, n_blocks]            gather blocks (pic_plan_layout / pic_plan_frontier)
      sorted [host out, n_blocks]        the same blocks, grouped by source run (stable)
      group_start [host out, n_blocks+1] group g = sorted[group_start[g] .. group_start[g+1]);
-                                        group_start[n_groups] = n_blocks
+                                        group_start[n_groups] = n_blocks; a run placed more
+                                        than 8 times spans several groups of at most 8 blocks
      n_groups [host out]                number of groups
    PIC_ERR_INVALID_ARG for NULL arrays or a negative count. */
 pic_status pic_plan_shared(const pic_block* blocks, int32_t n_blocks, pic_block* sorted,

@@ -405,11 +405,19 @@ PIC_API pic_status pic_plan_shared(const pic_block* blocks, int32_t n_blocks, pi
     const pic_block &a = blocks[x], &b = blocks[y];
     return a.src_token != b.src_token ? a.src_token < b.src_token : a.n_tokens < b.n_tokens;
   });
-  int32_t ng = 0;
+  // a group holds at most kMaxGroup blocks: its workgroup stores them one after another, so a
+  // run placed very often (a shared block-boundary header precedes every document of every
+  // request) becomes several groups instead of one long serial tail
+  constexpr int32_t kMaxGroup = 8;
+  int32_t ng = 0, in_group = 0;
   for (int32_t i = 0; i < n_blocks; ++i) {
     const pic_block& b = blocks[order[i]];
-    if (i == 0 || b.src_token != sorted[i - 1].src_token || b.n_tokens != sorted[i - 1].n_tokens)
+    if (i == 0 || b.src_token != sorted[i - 1].src_token || b.n_tokens != sorted[i - 1].n_tokens ||
+        in_group == kMaxGroup) {
       group_start[ng++] = i;
+      in_group = 0;
+    }
+    ++in_group;
     sorted[i] = b;
   }
   group_start[ng] = n_blocks;

@@ -286,6 +286,93 @@ __global__ void __launch_bounds__(256) compose_shared_kernel(
   }
 }
 
+// compose_shared_kernel for interleaved pairs on bf16 rows of 128 elements: a pair (x_2i,
+// x_2i+1) sits inside one 16-byte chunk, so 16 lanes cover a row chunk by chunk and every load
+// and store instruction of a wave moves 4 whole rows (1 KB contiguous).  (The generic layout,
+// whose lanes hold pairs of neighbouring chunks, leaves every store instruction writing half of
+// each 32-byte sector.)  Same arithmetic as compose_kernel: bit-identical results.
+__global__ void __launch_bounds__(256) compose_shared_il_rows_kernel(
+    const bf16_t* __restrict__ pool_k, const bf16_t* __restrict__ pool_v, int64_t pool_tokens,
+    const pic_block* __restrict__ blocks, const int32_t* __restrict__ group_start, int32_t n_blocks,
+    const float2* __restrict__ table, int64_t table_stride, int32_t max_abs_delta,
+    bf16_t* __restrict__ cache_k, bf16_t* __restrict__ cache_v, int32_t batch, int32_t cache_cap) {
+  using V = Vec16<bf16_t>;
+  constexpr int HD = 128, HALF = 64;
+  constexpr int RPP = 16;                                   // rows per pass
+  constexpr int PASSES = PIC_BLOCK_TOKENS / RPP;
+
+  int g0 = group_start[blockIdx.x], g1 = group_start[blockIdx.x + 1];
+  g0 = g0 < 0 ? 0 : g0;
+  g1 = g1 > n_blocks ? n_blocks : g1;
+  if (g0 >= g1) return;
+  const pic_block src = blocks[g0];
+  if (src.n_tokens <= 0 || src.n_tokens > PIC_BLOCK_TOKENS || src.src_token < 0 ||
+      (int64_t)src.src_token + src.n_tokens > pool_tokens)
+    return;
+
+  const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
+  const int j = threadIdx.x & 15, r0 = threadIdx.x >> 4;   // chunk j = pairs 4 j .. 4 j + 3
+  const float2* ltable = table + l * table_stride;
+  const int64_t src_row0 = ((int64_t)l * Hkv + h) * pool_tokens + src.src_token;
+
+  uint4 k[PASSES], v[PASSES];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const int t = r0 + p * RPP;
+    if (t < src.n_tokens) {
+      const int64_t sr = (src_row0 + t) * HD + 8 * j;
+      k[p] = V::load_raw(pool_k + sr);
+      v[p] = V::load_raw(pool_v + sr);
+    }
+  }
+  auto cs_of = [&](const pic_block& b, float (&cs)[4], float (&sn)[4]) {
+    int32_t d = b.delta;
+    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
+    const int32_t ad = d < 0 ? -d : d;
+    const float2* row = ltable + (int64_t)ad * HALF + 4 * j;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float2 t = row[i];
+      cs[i] = t.x;
+      sn[i] = d < 0 ? -t.y : t.y;
+    }
+  };
+  pic_block nxt = src;
+  float ncs[4], nsn[4];
+  cs_of(nxt, ncs, nsn);
+  for (int i = g0; i < g1; ++i) {
+    const pic_block blk = nxt;
+    float cs[4], sn[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      cs[e] = ncs[e];
+      sn[e] = nsn[e];
+    }
+    if (i + 1 < g1) {
+      nxt = blocks[i + 1];
+      cs_of(nxt, ncs, nsn);
+    }
+    if (blk.src_token != src.src_token || blk.n_tokens != src.n_tokens || blk.request < 0 ||
+        blk.request >= batch || blk.dst_slot < 0 || (int64_t)blk.dst_slot + blk.n_tokens > cache_cap ||
+        blk.delta > max_abs_delta || blk.delta < -max_abs_delta)
+      continue;
+    const int64_t dst_row0 = (((int64_t)l * batch + blk.request) * Hkv + h) * cache_cap + blk.dst_slot;
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int t = r0 + p * RPP;
+      if (t < blk.n_tokens) {
+        float x[8];
+        V::widen(k[p], x);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) turn(x[2 * q], x[2 * q + 1], cs[q], sn[q]);
+        const int64_t dr = (dst_row0 + t) * HD + 8 * j;
+        V::store(cache_k + dr, x);
+        V::store_raw(cache_v + dr, v[p]);
+      }
+    }
+  }
+}
+
 // grid (batch * map_tiles, Hkv, L), 256 threads.  Zero-copy prefill with a tile map: the
 // prefill reads a context tile straight from the pool when it is one pool run under one shift
 // (tile map entry (src, delta) with src >= 0, the run inside the pool, |delta| within the
@@ -476,6 +563,12 @@ hipError_t launch_compose_shared(pic_dtype dt, int head_dim, bool interleaved, i
                                  void* cache_v, int32_t batch, int32_t cache_cap, hipStream_t stream) {
   if (n_groups == 0 || n_layers == 0) return hipSuccess;
   const dim3 grid(n_groups, n_kv_heads, n_layers);
+  if (interleaved && dt == PIC_BF16 && head_dim == 128) {   // whole-row moves
+    hipLaunchKernelGGL(compose_shared_il_rows_kernel, grid, dim3(256), 0, stream, (const bf16_t*)pool_k,
+                       (const bf16_t*)pool_v, pool_tokens, blocks, group_start, n_blocks, table, table_stride,
+                       max_abs_delta, (bf16_t*)cache_k, (bf16_t*)cache_v, batch, cache_cap);
+    return hipGetLastError();
+  }
   PIC_DISPATCH_TD(dt, head_dim, {
     if (interleaved)
       hipLaunchKernelGGL((compose_shared_kernel<T, HD, true>), grid, dim3(256), 0, stream,

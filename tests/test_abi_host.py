@@ -330,10 +330,15 @@ def test_plan_shared_groups_blocks_by_source():
         assert np.array_equal(sb, blocks[order])
         assert gs[0] == 0 and gs[-1] == len(blocks) and np.all(np.diff(gs) > 0)
         runs = [key(sb[gs[g]]) for g in range(len(gs) - 1)]
-        assert len(set(runs)) == len(runs)                       # one group per distinct run
         for g in range(len(gs) - 1):
             assert all(key(b) == runs[g] for b in sb[gs[g]:gs[g + 1]])
-        assert len(runs) == len({key(b) for b in blocks})
+        # one group per distinct run, split into groups of at most 8 blocks
+        counts = {}
+        for b in blocks:
+            counts[key(b)] = counts.get(key(b), 0) + 1
+        assert np.all(np.diff(gs) <= 8)
+        assert len(runs) == sum((c + 7) // 8 for c in counts.values())
+        assert all(runs[g] != runs[g + 1] or gs[g + 1] - gs[g] == 8 for g in range(len(runs) - 1))
     # requests sharing documents share groups: 16 requests x 10 of 64 documents
     w = synth.get("c3")
     lay = S.pool_layout(w)
