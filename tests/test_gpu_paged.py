@@ -137,10 +137,20 @@ def test_paged_prefill_equals_compose_then_prefill(name, runs):
 
 @pytest.mark.parametrize("runs", [False, True], ids=["per-key", "whole-runs"])
 @pytest.mark.parametrize("pairing", ["half", "interleaved"])
-def test_paged_prefill_with_rotary_variants(pairing, runs):
-    # two layers with their own frequencies in one call; pool layer 1 differs from layer 0
-    w = synth.get("c2")
-    r = setup(w)
+@pytest.mark.parametrize("layout", ["c2", "mixed"])
+def test_paged_prefill_with_rotary_variants(pairing, runs, layout):
+    # two layers with their own frequencies in one call; pool layer 1 differs from layer 0.
+    # mixed: documents of 60..300 tokens, so with the tile map some context tiles are composed
+    # into the cache first (both pairings, per-layer tables) and the others read from the pool
+    if layout == "c2":
+        w = synth.get("c2")
+        r = setup(w)
+    else:
+        w = dataclasses.replace(synth.get("c2"), name="mixed", n_q_heads=28, n_kv_heads=4, pool_docs=5,
+                                doc_len=77, docs_per_request=4, n_suffix=37, prefix_len=13, batch=3,
+                                doc_len_jitter=(60, 300))
+        lay = S.pool_layout(w)
+        r = setup(w, requests=[[lay.prefix_entry, 3, 0, 4], [lay.prefix_entry], [2, 1, 0, 3, 4]], extra_cap=5)
     d = gpu_compose(r)
     D = w.head_dim
     m2 = pic.Model.of(2, w.n_q_heads, w.n_kv_heads, D, "bf16", w.rope_theta, pairing=pairing,
@@ -168,3 +178,9 @@ def test_paged_prefill_with_rotary_variants(pairing, runs):
     torch.cuda.synchronize()
     _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=not runs,
                                 tmap=_paged.tmap if runs else None)
+    if runs and layout == "mixed":   # both kinds of context tile occur: some were composed first
+        tm = _paged.tmap
+        ctx_tiles = [(b, t) for b in range(w.batch) for t in range((int(r.ctx[b]) + 63) // 64)]
+        assert any(tm[b, t, 0] >= 0 for b, t in ctx_tiles) and any(tm[b, t, 0] < 0 for b, t in ctx_tiles)
+    print(f"[{pairing}, {layout}, {'tile map' if runs else 'per-key'}] two layers with their own "
+          f"frequencies: paged == compose + prefill", flush=True)
