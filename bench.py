@@ -57,6 +57,11 @@ def parse(argv=None):
     p.add_argument("--per-block-compose", action="store_true",
                    help="compose with pic_compose over the blocks as planned (each composed row reads "
                         "its pool row) instead of grouping blocks that share a document run")
+    p.add_argument("--no-extra", action="store_true",
+                   help="skip the extra workload legs (profiling runs of one workload)")
+    p.add_argument("--extra", default="c5,c4,rerotate",
+                   help="extra legs after the headline: workloads (their own short step counts) and "
+                        "'rerotate' (standalone key re-rotation)")
     p.add_argument("--copy-calib-gib", type=float, default=0.0,
                    help="also run a plain device copy of this size per step (counter calibration)")
     return p.parse_args(argv)
@@ -71,6 +76,24 @@ def compose_bytes(w, ctx, n_layers):
     composed row; grouping blocks that share a document run reads fewer, so this rate can
     exceed the HBM peak)."""
     return int(sum(ctx)) * w.n_kv_heads * n_layers * 4 * w.head_dim * w.elem_bytes
+
+
+def compose_moved_bytes(w, blocks, group_start, n_layers):
+    """Bytes the compose launch must move: every composed K and V row written once, and the
+    pool rows read once per group of blocks that share a source run (one group per block when
+    blocks are composed from their own pool rows).  This is the rate a roofline fraction is
+    taken on; compose_bytes is the per-composed-row unit, which counts a repeated read."""
+    rows_w = int(blocks["n_tokens"].sum())
+    if group_start is None:
+        rows_r = rows_w
+    else:
+        rows_r = int(blocks["n_tokens"][group_start[:-1]].sum())
+    return (rows_r + rows_w) * w.n_kv_heads * n_layers * 2 * w.head_dim * w.elem_bytes
+
+
+def rerotate_bytes(n_tokens, n_heads, head_dim, elem_bytes):
+    """Standalone re-rotation: every key row read and written once, plus one int32 shift per token."""
+    return n_tokens * (n_heads * 2 * head_dim * elem_bytes + 4)
 
 
 def prefill_flops(w, pairs):
@@ -214,6 +237,17 @@ class DeviceWorkload:
         self.blocks_pinned = torch.empty(n_blocks_max * 6 + 1 + n_pos, dtype=torch.int32, pin_memory=True)
         self.blocks_dev = torch.empty(n_blocks_max * 5, dtype=torch.int32, device=dev)
         self.groups_dev = torch.empty(n_blocks_max + 1, dtype=torch.int32, device=dev)
+        # bytes one compose launch moves (the plan is the same every step)
+        if self.frontier:
+            blocks0 = pic.pic_plan_frontier(lay.items, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                            lay.pool_tokens)[0]
+        else:
+            blocks0 = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                          lay.pool_tokens)[0]
+        starts0 = None
+        if shared_compose:
+            blocks0, starts0 = pic.pic_plan_shared(blocks0)
+        self.compose_moved = compose_moved_bytes(w, blocks0, starts0, L)
 
     def upload(self, blocks, pinned, blocks_dev, groups_dev, inl=None, pos_dev=None):
         """Asynchronous copy of one plan to the device: its gather blocks (grouped by source run
@@ -490,6 +524,135 @@ def cpu_baseline(w, budget_s):
 
 # ------------------------------------------------------------------------------------------
 
+def measure(w, dev, steps, warmup, n_dec, *, paged=False, fused_rope=False, per_block=False,
+            single=True, calib_gib=0.0, plain_path=True):
+    """Runs `warmup` + `steps` bench steps of workload w and returns (workload, figures)."""
+    import torch
+
+    wl = DeviceWorkload(w, dev, n_dec, paged=paged, fused_rope=fused_rope, shared_compose=not per_block)
+    calib = None
+    if calib_gib > 0:
+        n = int(calib_gib * (1 << 30)) // 2
+        calib = (torch.empty(n, dtype=torch.bfloat16, device=dev).normal_(),
+                 torch.empty(n, dtype=torch.bfloat16, device=dev))
+
+    rec = {"compose": [], "prefill": [], "decode": [], "ttft": [], "step": []}
+    # no garbage-collector pauses inside the host-timed regions (collected before, enabled after)
+    gc.collect()
+    gc.disable()
+    try:
+        for _ in range(warmup):
+            wl.step(None, calib)
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        for _ in range(steps):
+            wl.step(rec, calib)
+        torch.cuda.synchronize()
+        total_ms = (time.perf_counter() - t_start) * 1e3
+        single_ms = single_request_ttft(wl) if single else (None, None)
+    finally:
+        gc.enable()
+
+    mean = lambda x: float(sum(x) / len(x)) if x else 0.0
+    L, B, Ls = wl.L, w.batch, wl.Ls
+    ctx = [int(c) for c in wl.ctx_host]
+    ttft_ms = mean(rec["ttft"])
+    comp_ms, pre_ms, dec_ms = mean(rec["compose"]), mean(rec["prefill"]), mean(rec["decode"])
+    comp_unit_b = compose_bytes(w, ctx, L)
+    comp_b = wl.compose_moved
+    pre_f_layer = prefill_flops(w, wl.pairs)
+    # decode step t sees length + t + 1 slots; average over the steps of one bench step
+    dec_b_layer = sum(decode_bytes(w, [int(n) + t + 1 for n in wl.length_host]) for t in range(n_dec)) / max(n_dec, 1)
+    kernels = {
+        "compose": {"bound": "hbm", "achieved": comp_b / (comp_ms * 1e-3) / 1e9 if comp_ms else None,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "ms_per_launch": comp_ms,
+                    "per_launch": comp_b, "launches_per_step": 1,
+                    "per_launch_note": "pool rows read once per group of blocks sharing a source run + every "
+                                       "composed row written (K and V)",
+                    "per_composed_row_bytes": comp_unit_b,
+                    "per_composed_row_gbps": comp_unit_b / (comp_ms * 1e-3) / 1e9 if comp_ms else None},
+        "suffix_prefill_attn": {"bound": "mfma",
+                                "achieved": pre_f_layer / (pre_ms * 1e-3) / 1e12 if pre_ms else None,
+                                "peak": BF16_MFMA_PEAK_TFS, "unit": "TFLOP/s", "ms_per_launch": pre_ms,
+                                "per_launch": pre_f_layer, "launches_per_step": L if Ls else 0},
+        "decode_attn": {"bound": "hbm", "achieved": dec_b_layer / (dec_ms * 1e-3) / 1e9 if dec_ms else None,
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "ms_per_launch": dec_ms,
+                        "per_launch": dec_b_layer, "launches_per_step": L * n_dec},
+    }
+    for k in kernels.values():
+        k["frac"] = (k["achieved"] / k["peak"]) if k["achieved"] else None
+        k["ms_per_step"] = k["ms_per_launch"] * k["launches_per_step"]
+    dom_name = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    dom = kernels[dom_name]
+    traffic = lookup_traffic(w.name, dom_name, plain_path=plain_path)
+    roofline = {"kernel": dom_name, "bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
+                "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
+    fig = {"ttft_ms_batch": ttft_ms, "ttft_ms_per_request": ttft_ms / B,
+           "ttft_ms_single_request": single_ms[0], "ttft_ms_single_request_graph": single_ms[1],
+           "ms_per_step": total_ms / steps, "steps": steps, "warmup": warmup, "decode_tokens_per_step": n_dec,
+           "context_tokens": ctx[0] if len(set(ctx)) == 1 else ctx, "batch": B, "layers": L,
+           "kernels": kernels, "roofline": roofline}
+    return wl, fig
+
+
+def rerotate_leg(dev, reps=10, warmup=3):
+    """Standalone re-rotation (Sec. 2, Eq. 3) of a key set the size of the 32-layer Llama
+    workload's composed context keys: 16 requests x 10368 tokens x 32 layers as [tokens][8 kv
+    heads][128] bf16 rows, turned in place, one shift per token (constant over 64-token runs,
+    like a document's blocks).  Timed with HIP events on the launch stream."""
+    import numpy as np
+    import torch
+
+    import paper_2607_28069_amd as pic
+
+    w = __import__("synth").get("c3")
+    H, D = w.n_kv_heads, w.head_dim
+    n_tok = w.batch * (w.prefix_len + w.docs_per_request * w.doc_len) * w.n_layers
+    mad = 16384
+    model = pic.Model.of(1, w.n_q_heads, H, D, w.dtype, w.rope_theta)
+    table = torch.empty(pic.pic_rope_table_bytes(model, mad) // 4, dtype=torch.float32, device=dev)
+    pic.pic_rope_table_init(model, mad, table)
+    keys = torch.empty((n_tok, H, D), dtype=torch.bfloat16, device=dev).normal_()
+    delta = torch.from_numpy(((np.arange(n_tok) // 64 * 1031) % (2 * mad + 1) - mad).astype(np.int32)).to(dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        pic.pic_rerotate_keys(model, keys, keys, n_tok, H, delta, table, mad)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        pic.pic_rerotate_keys(model, keys, keys, n_tok, H, delta, table, mad)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = rerotate_bytes(n_tok, H, D, 2)
+    del keys, delta, table
+    return {"kernel": "rerotate_kernel", "tokens": n_tok, "heads": H, "head_dim": D, "dtype": "bf16",
+            "ms_per_launch": ms, "per_launch": nbytes, "bound": "hbm",
+            "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+
+def _brief(name, fig):
+    """The figures of one extra workload leg, flattened for the JSON line."""
+    k = fig["kernels"]
+    out = {"workload": name, "ttft_ms_per_request": fig["ttft_ms_per_request"],
+           "ttft_ms_single_request": fig["ttft_ms_single_request"],
+           "ttft_ms_single_request_graph": fig["ttft_ms_single_request_graph"],
+           "compose_ms": k["compose"]["ms_per_launch"], "compose_gbps": k["compose"]["achieved"],
+           "compose_frac": k["compose"]["frac"],
+           "compose_gbps_per_composed_row": k["compose"]["per_composed_row_gbps"],
+           "steps": fig["steps"], "warmup": fig["warmup"], "batch": fig["batch"], "layers": fig["layers"],
+           "context_tokens": fig["context_tokens"], "decode_tokens_per_step": fig["decode_tokens_per_step"]}
+    if k["suffix_prefill_attn"]["launches_per_step"]:
+        out.update(prefill_us_per_layer=k["suffix_prefill_attn"]["ms_per_launch"] * 1e3,
+                   prefill_tflops=k["suffix_prefill_attn"]["achieved"], prefill_frac=k["suffix_prefill_attn"]["frac"])
+    if k["decode_attn"]["launches_per_step"]:
+        out.update(decode_us_per_layer=k["decode_attn"]["ms_per_launch"] * 1e3,
+                   decode_gbps=k["decode_attn"]["achieved"], decode_frac=k["decode_attn"]["frac"])
+    return out
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -508,66 +671,19 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     n_dec = args.decode_tokens if args.decode_tokens is not None else (w.decode_steps or 1)
-    wl = DeviceWorkload(w, dev, n_dec, paged=args.paged, fused_rope=args.fused_rope,
-                        shared_compose=not args.per_block_compose)
-    calib = None
-    if args.copy_calib_gib > 0:
-        n = int(args.copy_calib_gib * (1 << 30)) // 2
-        calib = (torch.empty(n, dtype=torch.bfloat16, device=dev).normal_(),
-                 torch.empty(n, dtype=torch.bfloat16, device=dev))
-
-    rec = {"compose": [], "prefill": [], "decode": [], "ttft": [], "step": []}
-    # no garbage-collector pauses inside the host-timed regions (collected before, enabled after)
-    gc.collect()
-    gc.disable()
-    for _ in range(args.warmup):
-        wl.step(None, calib)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        wl.step(rec, calib)
-    torch.cuda.synchronize()
-    total_ms = (time.perf_counter() - t_start) * 1e3
-    single = (None, None) if args.no_single_request else single_request_ttft(wl)
-    gc.enable()
-
-    mean = lambda x: float(sum(x) / len(x)) if x else 0.0
+    wl, fig = measure(w, dev, args.steps, args.warmup, n_dec, paged=args.paged, fused_rope=args.fused_rope,
+                      per_block=args.per_block_compose, single=not args.no_single_request,
+                      calib_gib=args.copy_calib_gib,
+                      plain_path=not (args.paged or args.fused_rope or args.per_block_compose))
+    kernels = fig["kernels"]
     L, B, Ls = wl.L, w.batch, wl.Ls
     ctx = [int(c) for c in wl.ctx_host]
-    ttft_ms = mean(rec["ttft"])
-    comp_ms, pre_ms, dec_ms = mean(rec["compose"]), mean(rec["prefill"]), mean(rec["decode"])
-    comp_b = compose_bytes(w, ctx, L)
-    pre_f_layer = prefill_flops(w, wl.pairs)
-    # decode step t sees length + t + 1 slots; average over the steps of one bench step
-    dec_b_layer = sum(decode_bytes(w, [int(n) + t + 1 for n in wl.length_host]) for t in range(n_dec)) / max(n_dec, 1)
-    kernels = {
-        "compose": {"bound": "hbm", "achieved": comp_b / (comp_ms * 1e-3) / 1e9 if comp_ms else None,
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "ms_per_launch": comp_ms,
-                    "per_launch": comp_b, "launches_per_step": 1},
-        "suffix_prefill_attn": {"bound": "mfma",
-                                "achieved": pre_f_layer / (pre_ms * 1e-3) / 1e12 if pre_ms else None,
-                                "peak": BF16_MFMA_PEAK_TFS, "unit": "TFLOP/s", "ms_per_launch": pre_ms,
-                                "per_launch": pre_f_layer, "launches_per_step": L if Ls else 0},
-        "decode_attn": {"bound": "hbm", "achieved": dec_b_layer / (dec_ms * 1e-3) / 1e9 if dec_ms else None,
-                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "ms_per_launch": dec_ms,
-                        "per_launch": dec_b_layer, "launches_per_step": L * n_dec},
-    }
-    for k in kernels.values():
-        k["frac"] = (k["achieved"] / k["peak"]) if k["achieved"] else None
-        k["ms_per_step"] = k["ms_per_launch"] * k["launches_per_step"]
-    dom_name = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
-    dom = kernels[dom_name]
-    traffic = lookup_traffic(w.name, dom_name,
-                             plain_path=not (args.paged or args.fused_rope or args.per_block_compose))
-    roofline = {"kernel": dom_name, "bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
-                "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
-
     res = {
         "metric": METRIC,
-        "value": ttft_ms / B,
+        "value": fig["ttft_ms_per_request"],
         "unit": "ms/request",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": total_ms / args.steps,
+        "ms_per_step": fig["ms_per_step"],
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -587,17 +703,46 @@ def main():
                    **({"rope_pairing": w.rope_pairing, "rope_scaling": w.rope_scaling,
                        "rope_local_global": w.local_global}
                       if (w.rope_pairing != "half" or w.rope_scaling or w.local_global) else {})},
-        "ttft_ms_batch": ttft_ms,
-        **dict(zip(("ttft_ms_single_request", "ttft_ms_single_request_graph"),
-                   single)),
+        "ttft_ms_batch": fig["ttft_ms_batch"],
+        "ttft_ms_single_request": fig["ttft_ms_single_request"],
+        "ttft_ms_single_request_graph": fig["ttft_ms_single_request_graph"],
         "prefill_attn_tflops": kernels["suffix_prefill_attn"]["achieved"],
+        # compose rate over the bytes the launch moves (distinct source runs read + all rows
+        # written); the per-composed-row figure counts one pool read per composed row
         "rerotate_compose_gbps": kernels["compose"]["achieved"],
+        "rerotate_compose_gbps_per_composed_row": kernels["compose"]["per_composed_row_gbps"],
         "decode_gbps": kernels["decode_attn"]["achieved"],
-        "roofline": roofline,
+        "roofline": fig["roofline"],
         "kernels": kernels,
     }
+    del wl
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget_s)
+    extras = [] if args.no_extra else [x for x in args.extra.split(",") if x]
+    legs = {}
+    for name in extras:
+        if name == "rerotate":
+            legs["rerotate_keys"] = rerotate_leg(dev)
+        else:
+            we = synth.get(name)
+            if we.name == w.name:
+                continue
+            # the decode-heavy workload: a few of its decode steps at full shape
+            nd = min(4, we.decode_steps) if we.decode_steps else 1
+            wle, fe = measure(we, dev, 3 if we.decode_steps else 5, 2 if we.decode_steps else 3, nd,
+                              single=bool(we.n_suffix))
+            legs[we.name] = _brief(we.name, fe)
+            del wle
+        torch.cuda.empty_cache()
+        print(f"[bench] extra leg {name} done", file=sys.stderr, flush=True)
+    if legs:
+        res["extra_workloads"] = legs
+        for name, leg in legs.items():   # flat copies of the headline figures of each leg
+            for key in ("ttft_ms_per_request", "ttft_ms_single_request", "prefill_tflops", "prefill_frac",
+                        "compose_ms", "compose_frac", "decode_gbps", "decode_frac", "achieved", "frac"):
+                if leg.get(key) is not None:
+                    res[f"{name}_{key}"] = leg[key]
     print(json.dumps(res), flush=True)
 
 

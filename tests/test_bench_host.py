@@ -64,3 +64,38 @@ def test_committed_traffic_figures_are_well_formed():
             assert v["read_bytes"] == pytest.approx(v["fetch_size_kib"] * 1024 * v["fetch_scale"])
             assert v["write_bytes"] == pytest.approx(v["write_size_kib"] * 1024 * v["write_scale"])
             assert all("rocprofv3 --pmc" in c for c in v["commands"])
+
+
+def test_compose_moved_bytes_counts_each_shared_run_once():
+    # The compose launch reads every distinct 64-token source run once per group of at most 8
+    # placements and writes every placement: counted here from the layout with a Counter,
+    # independently of the planner's grouping.
+    import collections
+
+    import paper_2607_28069_amd as pic
+    from synth import inputs as S
+    w = synth.get("c3")
+    lay = S.pool_layout(w)
+    runs = collections.Counter()
+    rows_w = 0
+    for req in lay.requests:
+        for e in req:
+            off, n = int(lay.doc_offset[e]), int(lay.doc_len[e])
+            for t in range(0, n, 64):
+                runs[(off + t, min(64, n - t))] += 1
+                rows_w += min(64, n - t)
+    rows_r = sum(n * -(-c // 8) for (_, n), c in runs.items())
+    unit = w.n_kv_heads * w.n_layers * 2 * w.head_dim * w.elem_bytes
+    blocks, _ = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len, lay.doc_compile_pos,
+                                    lay.pool_tokens)
+    sorted_blocks, starts = pic.pic_plan_shared(blocks)
+    assert bench.compose_moved_bytes(w, sorted_blocks, starts, w.n_layers) == (rows_r + rows_w) * unit
+    # per-block compose reads what it writes: the per-composed-row unit
+    ctx = S.context_lengths(lay)
+    assert bench.compose_moved_bytes(w, blocks, None, w.n_layers) == bench.compose_bytes(w, ctx, w.n_layers)
+    assert rows_r < rows_w / 2   # 16 requests share the prefix and draw 10 of 64 documents
+
+
+def test_rerotate_bytes():
+    # one key row read and written per (token, head), one int32 shift per token
+    assert bench.rerotate_bytes(1000, 8, 128, 2) == 1000 * (8 * 512 + 4)

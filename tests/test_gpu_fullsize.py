@@ -154,8 +154,8 @@ def test_llama8b_32layer_compose_all_requests():
 def test_qwen7b_32k_all_layers():
     # 8 requests x ~32K context (32 jittered documents in per-request order), 256 suffix
     # tokens, all 28 layers: every request's composed cache on the last layer; attention of
-    # sampled suffix tokens (first and last, tile edges) and one decode step on the first,
-    # middle and last layers.
+    # every suffix token (all 7 m-tiles of 256 query rows, every head) and one decode step on
+    # the first, middle and last layers.
     w = synth.get("c5")
     wl = DeviceWorkload(w, DEV, n_dec=1)
     wl.step()
@@ -164,8 +164,8 @@ def test_qwen7b_32k_all_layers():
     _check_compose_all_requests(wl, wl.L - 1)
     print(f"[c5] layer {wl.L - 1}: all {w.batch} requests composed correctly", flush=True)
     for l, r in ((0, 0), (wl.L // 2, 5), (wl.L - 1, 7)):
-        _check_request(wl, l, r, tokens=[0, 1, 63, 64, 100, 255], decode_steps=1)
-        print(f"[c5] layer {l} request {r} ok", flush=True)
+        _check_request(wl, l, r, decode_steps=1)
+        print(f"[c5] layer {l} request {r} ok (all {w.n_suffix} suffix tokens)", flush=True)
 
 
 def test_llama8b_decode_256_steps_all_layers():
@@ -304,7 +304,7 @@ def test_llama8b_single_request_path():
     # A request served alone (batch 1) has 16 (m-tile, kv head) units, so its prefill runs
     # split over ~15 key ranges with a combine (the batched launch needs none).  The
     # benchmark's single-request path -- eager, then replayed from a recorded graph -- on two
-    # layers of the 32-layer shape, against the oracle on sampled tokens (every head).
+    # layers of the 32-layer shape, against the oracle on every suffix token and head.
     from bench import single_request_ttft
     w = synth.get("c3")
     wl = DeviceWorkload(w, DEV, n_dec=1, layers=2)
@@ -316,7 +316,7 @@ def test_llama8b_single_request_path():
     torch.cuda.synchronize()
     lay, r, Ls = wl.lay, 0, w.n_suffix
     m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
-    toks = np.array([0, 1, 63, 64, 127])
+    toks = np.arange(Ls)
     for l in range(2):
         K, V = O.compose_request(_host(wl.pool_k[l]), _host(wl.pool_v[l]), m, w.rope_theta, w.dtype,
                                  **_rope(w, l))

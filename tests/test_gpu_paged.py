@@ -178,6 +178,16 @@ def test_paged_prefill_with_rotary_variants(pairing, runs, layout):
     torch.cuda.synchronize()
     _check_against_materialized(r, out_p, ck_p, cv_p, ck_m, cv_m, out_m, exact=not runs,
                                 tmap=_paged.tmap if runs else None)
+    # and against the oracle: each layer's own frequencies (the oracle's Llama-3.1 scaling and
+    # plain base 1e4) and the pairing, over that layer's pool rows
+    fo = [O.llama3_inv_freq(D, 5e5), O.inv_freq(D, 1e4)]
+    pk_h, pv_h, got = host(pk), host(pv), host(out_p)
+    for l in range(2):
+        for b in range(w.batch):
+            K, V = O.compose_request(pk_h[l], pv_h[l], r.maps[b], w.rope_theta, "bf16", pairing=pairing,
+                                     freqs=fo[l])
+            ref, _, _ = O.suffix_prefill(K, V, r.inp["q"][b], r.inp["k_suf"][b], r.inp["v_suf"][b])
+            assert_attn_close(got[l, b], ref, "bf16")
     if runs and layout == "mixed":   # both kinds of context tile occur: some were composed first
         tm = _paged.tmap
         ctx_tiles = [(b, t) for b in range(w.batch) for t in range((int(r.ctx[b]) + 63) // 64)]
