@@ -360,6 +360,25 @@ pic_status pic_decode_attn_rope(const pic_model* model, const void* q, const voi
                                 float scale, int32_t n_splits, void* out, void* workspace,
                                 size_t ws_bytes, void* stream);
 
+/* ---- 4b. decode without a workspace, for callers that cannot allocate ----
+   For code that must not allocate device memory (HIP graph capture, tight serving loops,
+   harnesses that forbid hipMalloc): pic_decode_attn with its split partials kept in a scratch
+   array the library holds on each GPU (PIC_DECODE_SCRATCH_BYTES, alive until the process ends)
+   instead of a caller workspace.  Allocates and frees nothing; the first call on a device looks
+   the array up (hipGetSymbolAddress) with that device current.
+   Same arguments, checks and results as pic_decode_attn (bit-identical outputs for the same
+   n_splits).  PIC_ERR_WORKSPACE when the split partials,
+   pic_decode_workspace_bytes(model, batch, max_base_len + step + 1, n_splits), exceed
+   PIC_DECODE_SCRATCH_BYTES.  Every call on one GPU shares that GPU's array: calls that overlap
+   on one GPU (other streams, other threads) race and must be ordered by the caller.  Nothing in
+   the array needs clearing: each split launch writes every partial it combines. */
+#define PIC_DECODE_SCRATCH_BYTES ((size_t)8 << 20)
+pic_status pic_decode_attn_noalloc(const pic_model* model, const void* q, const void* k_new,
+                                   const void* v_new, void* cache_k, void* cache_v, int32_t batch,
+                                   int32_t cache_cap, const int32_t* base_len, int32_t step,
+                                   int32_t max_base_len, float scale, int32_t n_splits, void* out,
+                                   void* stream);
+
 /* ---- diagnostics ---- */
 const char* pic_status_string(pic_status status);
 /* Thread-local description of the last failure on this thread ("" if none). */

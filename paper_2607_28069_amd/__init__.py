@@ -31,7 +31,8 @@ EXPORTS = ("pic_plan_layout", "pic_plan_frontier", "pic_rope_table_bytes", "pic_
            "pic_frontier_workspace_bytes", "pic_frontier_prefill_attn",
            "pic_decode_workspace_bytes", "pic_decode_attn", "pic_decode_attn_rope", "pic_status_string",
            "pic_last_error",
-           "pic_decode_auto_splits")
+           "pic_decode_auto_splits", "pic_decode_attn_noalloc")
+PIC_DECODE_SCRATCH_BYTES = 8 << 20
 
 
 class PicError(RuntimeError):
@@ -108,6 +109,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "pic_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "pic_last_error": (ctypes.c_char_p, []),
         "pic_decode_auto_splits": (I32, [MP, I32, I32]),
+        "pic_decode_attn_noalloc": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, F, I32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -354,6 +356,15 @@ def pic_decode_attn_rope(model: Model, q, k_new, v_new, cache_k, cache_v, batch,
                                        _ptr(base_len), int(step), int(max_base_len), _ptr(table),
                                        int(max_abs_delta), float(scale), int(n_splits), _ptr(out),
                                        _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pic_decode_attn_noalloc(model: Model, q, k_new, v_new, cache_k, cache_v, batch, cache_cap, base_len, step,
+                            max_base_len, out, n_splits=0, scale=0.0, stream=None):
+    """pic_decode_attn with its split partials in the library's per-GPU scratch array (no workspace)."""
+    _check(load().pic_decode_attn_noalloc(ctypes.byref(model), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                          _ptr(cache_k), _ptr(cache_v), int(batch), int(cache_cap),
+                                          _ptr(base_len), int(step), int(max_base_len), float(scale),
+                                          int(n_splits), _ptr(out), _stream(stream)))
 
 
 def pic_status_string(status: int) -> str:

@@ -23,12 +23,19 @@
 //  * rope variant: q and k_new arrive unrotated and are turned to position p (the delta-angle
 //    table's row p) in registers -- the query once, the new key in the tile that holds it and
 //    where it is stored -- with the float32 arithmetic of the re-rotation kernel.
+#include <mutex>
 #include <type_traits>
 
 #include "pic_internal.h"
 
 namespace pic {
 namespace {
+
+// Split-K partials of the allocation-free decode entry point: one array per GPU, held until the
+// process ends.  Host code never names it as an address: each device's copy is looked up once
+// with hipGetSymbolAddress and that pointer is what the kernels receive.
+constexpr size_t kScratchBytes = PIC_DECODE_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 constexpr int kHD = 128;
 constexpr int kWaves = 4;
@@ -404,6 +411,29 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
 // Workgroups per (request, kv head): enough 4-wave workgroups for one per compute unit (256
 // per launch; measured faster than two per unit on split launches), each wave keeping at
 // least kMinWaveKeys keys.
+size_t decode_scratch_bytes() { return kScratchBytes; }
+
+hipError_t decode_scratch_ptr(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* ptr[kMaxDevices] = {};
+  *out = nullptr;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptr[dev] == nullptr) {   // first call on this device (it is the current one)
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    ptr[dev] = p;
+  }
+  *out = ptr[dev];
+  return hipSuccess;
+}
+
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len) {
   const int64_t pairs = (int64_t)s.batch * s.n_kv_heads * s.n_layers;
   int64_t splits = (256 + pairs - 1) / pairs;

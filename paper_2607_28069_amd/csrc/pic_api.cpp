@@ -740,11 +740,14 @@ PIC_API size_t pic_decode_workspace_bytes(const pic_model* model, int32_t batch,
 
 namespace {
 
+// use_scratch: the split partials go to the library's per-device scratch array instead of a
+// caller workspace (workspace / ws_bytes are then ignored).
 pic_status decode_impl(const pic_model* model, const void* q, const void* k_new, const void* v_new,
                        void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
                        const int32_t* base_len, int32_t step, int32_t max_base_len,
                        const void* table, int32_t max_abs_delta, float scale, int32_t n_splits,
-                       void* out, void* workspace, size_t ws_bytes, void* stream) {
+                       void* out, void* workspace, size_t ws_bytes, void* stream,
+                       bool use_scratch = false) {
   PIC_CHECK(check_attn_model(model));
   if (batch < 0 || cache_cap < 0 || step < 0 || max_base_len < 0 || n_splits < 0)
     return fail(PIC_ERR_INVALID_ARG, "negative size");
@@ -798,6 +801,19 @@ pic_status decode_impl(const pic_model* model, const void* q, const void* k_new,
     return fail(PIC_ERR_UNSUPPORTED, "too many splits");
   if (n_splits > max_len) n_splits = (int32_t)max_len;
   const size_t need = pic::decode_bf16_workspace(s, (int32_t)max_len, n_splits);
+  if (use_scratch) {
+    workspace = nullptr;
+    ws_bytes = 0;
+    if (need > pic::decode_scratch_bytes())
+      return fail(PIC_ERR_WORKSPACE,
+                  "%d splits need %zu bytes of partials; the allocation-free decode holds %zu "
+                  "(pass fewer splits, or use pic_decode_attn with a workspace)",
+                  n_splits, need, pic::decode_scratch_bytes());
+    if (need > 0) {
+      PIC_CHECK(hip_status(pic::decode_scratch_ptr(&workspace), "decode scratch lookup"));
+      ws_bytes = pic::decode_scratch_bytes();
+    }
+  }
   if (need > 0 && (workspace == nullptr || ws_bytes < need))
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   if (need > 0) PIC_CHECK(check_ptr(workspace, "workspace"));
@@ -835,4 +851,13 @@ PIC_API pic_status pic_decode_attn_rope(const pic_model* model, const void* q, c
   return decode_impl(model, q, k_new, v_new, cache_k, cache_v, batch, cache_cap, base_len, step,
                      max_base_len, table, max_abs_delta, scale, n_splits, out, workspace, ws_bytes,
                      stream);
+}
+
+PIC_API pic_status pic_decode_attn_noalloc(const pic_model* model, const void* q, const void* k_new,
+                                           const void* v_new, void* cache_k, void* cache_v,
+                                           int32_t batch, int32_t cache_cap, const int32_t* base_len,
+                                           int32_t step, int32_t max_base_len, float scale,
+                                           int32_t n_splits, void* out, void* stream) {
+  return decode_impl(model, q, k_new, v_new, cache_k, cache_v, batch, cache_cap, base_len, step,
+                     max_base_len, nullptr, 0, scale, n_splits, out, nullptr, 0, stream, true);
 }

@@ -14,7 +14,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __builtin_bit_cast(float, b << 16); }
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
@@ -149,6 +149,10 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
                                      void* workspace, size_t ws_bytes, hipStream_t stream);
 
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len);
+// The decode scratch array (split-K partials of the allocation-free entry point): its size,
+// and the current device's copy of it (looked up on the first call on that device).
+size_t decode_scratch_bytes();
+hipError_t decode_scratch_ptr(void** out);
 size_t decode_bf16_workspace(const AttnShape& s, int32_t max_len, int32_t n_splits);
 // Also writes k_new / v_new into slot base_len[b] + step of the cache.  With rope_table, q and
 // k_new are given unrotated and turned to that position (table block of layer l at

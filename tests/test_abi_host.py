@@ -410,3 +410,22 @@ def test_binding_refuses_host_and_strided_buffers(lib):
     with pytest.raises(ValueError, match="host tensor"):
         pic._ptr(host[::2])
     assert pic._ptr(None) is None
+
+
+def test_noalloc_decode_argument_checks(lib):
+    # The allocation-free decode checks like pic_decode_attn and refuses, before any launch or
+    # scratch lookup, split partials larger than its per-GPU scratch array.
+    m = _model()
+    nd = lambda mm=m, batch=2, step=0, max_base=500, splits=0, q=FAKE, base=FAKE, cap=600: \
+        lib.pic_decode_attn_noalloc(ctypes.byref(mm), q, FAKE, FAKE, FAKE, FAKE, batch, cap, base, step,
+                                    max_base, 0.0, splits, FAKE, None)
+    assert nd(step=100) == -4                            # 500 + 100 + 1 > 600
+    assert nd(q=MIS) == -5
+    assert nd(base=None) == -1
+    assert nd(_model(n_q_heads=136, n_kv_heads=8)) == -2
+    assert nd(batch=0) == 0                              # nothing to do
+    # 64 requests x 32 heads x 64 splits of (128 + 2) floats: 68 MB > the 8 MiB array
+    need = pic.pic_decode_workspace_bytes(m, 64, 502, 64)
+    assert need > pic.PIC_DECODE_SCRATCH_BYTES
+    assert nd(batch=64, splits=64) == -3
+    assert "allocation-free" in pic.pic_last_error()
