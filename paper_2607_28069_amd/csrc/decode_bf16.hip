@@ -26,6 +26,7 @@
 #include <mutex>
 #include <type_traits>
 
+#include "pic_bounds.h"
 #include "pic_internal.h"
 
 namespace pic {
@@ -43,6 +44,7 @@ constexpr int kTile = 32;                          // keys per wave tile
 constexpr int kRowBytes = kHD * 2;                 // 256
 constexpr int kVTileBytes = kTile * kRowBytes;     // 8 KB per wave per buffer
 constexpr int kMinWaveKeys = 64;
+static_assert(kWaves == kDecodeWaves && kMinWaveKeys == kDecodeMinWaveKeys, "host split planner tiling");
 constexpr int kNonTemporal = 2;                    // cache-policy bits of a streaming load
 
 #define LDS_AS __attribute__((address_space(3)))
@@ -138,8 +140,7 @@ decode_bf16_kernel(DecodeArgs a) {
   const int l = blockIdx.y;
   const int n_rep = a.n_q_heads / a.n_kv_heads;
 
-  int32_t base = a.base_len[b];
-  base = base < 0 ? 0 : (base > a.max_base ? a.max_base : base);
+  const int32_t base = clamp_len(a.base_len[b], a.max_base);
   const int p = base + a.step;                       // the new token's slot
   int n_vis = p + 1;
   if (n_vis > a.cache_cap) n_vis = a.cache_cap;
@@ -408,9 +409,6 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
 
 }  // namespace
 
-// Workgroups per (request, kv head): enough 4-wave workgroups for one per compute unit (256
-// per launch; measured faster than two per unit on split launches), each wave keeping at
-// least kMinWaveKeys keys.
 size_t decode_scratch_bytes() { return kScratchBytes; }
 
 hipError_t decode_scratch_ptr(void** out) {
@@ -432,21 +430,6 @@ hipError_t decode_scratch_ptr(void** out) {
   }
   *out = ptr[dev];
   return hipSuccess;
-}
-
-int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len) {
-  const int64_t pairs = (int64_t)s.batch * s.n_kv_heads * s.n_layers;
-  int64_t splits = (256 + pairs - 1) / pairs;
-  const int64_t max_splits = (max_len + kWaves * kMinWaveKeys - 1) / (kWaves * kMinWaveKeys);
-  if (splits > max_splits) splits = max_splits;
-  if (splits < 1) splits = 1;
-  return (int32_t)splits;
-}
-
-size_t decode_bf16_workspace(const AttnShape& s, int32_t, int32_t n_splits) {
-  if (n_splits <= 1) return 0;
-  const size_t rows = (size_t)s.n_layers * s.batch * s.n_q_heads * n_splits;
-  return rows * (kHD + 2) * sizeof(float);
 }
 
 hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t* k_new,

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "pic.h"
+#include "pic_bounds.h"
 
 namespace pic {
 
@@ -61,15 +62,12 @@ struct RowPos {
   const int32_t* n_valid = nullptr;
   int32_t n = 0, max_pos = 0;
 
-  __device__ __forceinline__ int64_t operator()(int b, int i) const {
+  PIC_HD int64_t operator()(int b, int i) const {
     if (table) {
       if (i >= n_valid[b]) return -1;
-      const int32_t p = table[(int64_t)b * n + i];
-      return p < 0 ? 0 : (p > max_pos ? max_pos : p);
+      return clamp_len(table[(int64_t)b * n + i], max_pos);
     }
-    int32_t bl = base[b];
-    bl = bl < 0 ? 0 : (bl > max_base ? max_base : bl);
-    return (int64_t)bl + offset + i;
+    return (int64_t)clamp_len(base[b], max_base) + offset + i;
   }
 };
 
@@ -84,6 +82,22 @@ struct AttnShape {
   int n_layers, n_q_heads, n_kv_heads, head_dim, batch, cache_cap;
   float scale_log2;  // softmax scale * log2(e)
 };
+
+// Tiling the host planner (pic_plan.cpp) shares with the bf16 attention kernels (each kernel
+// file checks its own constants against these).
+constexpr int kAttnHeadDim = 128;          // head_dim of the bf16 attention kernels
+constexpr int kPrefillRowsPerWG = 256;     // query rows per prefill workgroup
+constexpr int kPrefillKeys = 64;           // keys per prefill tile
+constexpr int kPrefillMaxSplits = 32;      // most key-range splits the planner picks
+constexpr int kDecodeWaves = 4;            // waves per decode workgroup
+constexpr int kDecodeMinWaveKeys = 64;     // fewest keys a decode wave is given
+
+// Key-range split of a prefill launch: m-tiles of query rows, splits per (m-tile, request,
+// kv head) and key tiles per split.
+struct SplitPlan {
+  int m_tiles, n_splits, tiles_per_split;
+};
+SplitPlan plan_prefill_splits(const AttnShape& s, int32_t n_suffix, int32_t max_ctx);
 
 // fp32 attention, one query row per workgroup.  Rows [L][B][n_q][Hq]: query token i of
 // request b sits at position pos(b, i) and sees slots [0, that position]; rows without a

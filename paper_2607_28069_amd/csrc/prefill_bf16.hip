@@ -31,9 +31,9 @@
 //    latency of the next tile's first reads.
 //  * Workgroups sharing a (request, kv head) key stream are mapped onto the same XCD (blocks
 //    are dealt round-robin over the 8 XCDs), so that stream is fetched into one L2.
-//  * The suffix's own keys/values are read straight from k_suf / v_suf; one workgroup per
-//    (request, kv head) also stores them into cache slots [ctx, ctx + n_suffix) (no separate
-//    append launch, and no workgroup reads those slots from the cache).
+//  * The suffix's own keys/values are read straight from k_suf / v_suf; the workgroups of a
+//    (request, kv head) also store them into cache slots [ctx, ctx + n_suffix), each a share
+//    of the rows (no separate append launch, and no workgroup reads those slots from the cache).
 //  * Paged mode (zero-copy composition): the documents' rows come straight from the pool
 //    through the token-level slot map (pool token and position shift of every context slot);
 //    the composed cache is not written.  A key tile that is one pool run under one shift (the
@@ -46,6 +46,7 @@
 #include <climits>
 #include <type_traits>
 
+#include "pic_bounds.h"
 #include "pic_internal.h"
 
 namespace pic {
@@ -61,6 +62,7 @@ constexpr int kRowBytes = kHD * 2;             // 256
 constexpr int kTileBytes = kKeys * kRowBytes;  // 16 KB
 constexpr int kNumXcd = 8;
 constexpr int kLoadSteps = kKeys / (4 * kWaves);   // 1 KB load instructions per wave per tile
+static_assert(kRowsPerWG == kPrefillRowsPerWG && kKeys == kPrefillKeys, "host split planner tiling");
 
 #define LDS_AS __attribute__((address_space(3)))
 #define GLOBAL_AS __attribute__((address_space(1)))
@@ -142,7 +144,7 @@ struct PrefillArgs {
   int32_t tiles_per_split;  // key tiles per split
   int32_t n_wg;             // m_tiles * n_splits * batch * n_kv_heads
   int64_t rows_total;       // L * batch * n_suffix * Hq (query rows of one split's partials)
-  float* ws_o;              // [n_splits][rows_total][D] unnormalised partial outputs
+  bf16_t* ws_o;             // [n_splits][rows_total][D] each split's normalised output
   float2* ws_ml;            // [n_splits][rows_total] (reference max, row sum)
   float scale_log2;
 };
@@ -239,8 +241,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   // pos_min_wg / pos_max_wg: nearest / furthest position of this workgroup's query rows
   int ctx, qpos, pos_min_wg, pos_max_wg;
   if constexpr (!kTable) {
-    ctx = a.ctx_len[b];
-    ctx = ctx < 0 ? 0 : (ctx > a.max_ctx ? a.max_ctx : ctx);
+    ctx = clamp_len(a.ctx_len[b], a.max_ctx);
     pos_min_wg = ctx + div_rep(row0_wg);
     pos_max_wg = ctx + div_rep(min(row0_wg + kRowsPerWG, M) - 1);
     qpos = ctx + tok;
@@ -298,13 +299,19 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int64_t suf_stride = (int64_t)a.n_kv_heads * kHD;
   const bf16_t* Ks = kTable ? nullptr : a.k_suf + suf0;
   const bf16_t* Vs = kTable ? nullptr : a.v_suf + suf0;
-  if (kRope && mt == 0 && split == 0) {   // cache assembly with the suffix keys turned to ctx + i
+  // Cache assembly: the suffix rows go into slots [ctx, ctx + n_suffix), shared out over the
+  // (request, kv head)'s workgroups (every m-tile and split stores a contiguous share of the
+  // rows), so no workgroup carries the whole store ahead of its key loop.
+  const int asm_parts = a.m_tiles * a.n_splits, asm_part = split * a.m_tiles + mt;
+  const int asm_per = (a.n_suffix + asm_parts - 1) / asm_parts;
+  const int asm_i0 = min(asm_part * asm_per, a.n_suffix), asm_i1 = min(asm_i0 + asm_per, a.n_suffix);
+  if (kRope) {   // with the suffix keys turned to ctx + i
     // item c: row i = c / 24; part < 8: K chunk pair part (rotate-half: chunks part, part + 8;
     // interleaved: 2 part, 2 part + 1; both: frequencies 8 part .. 8 part + 7), part >= 8: V
     // chunk part - 8.  Three items per thread per pass, all loads issued before any math.
     const float2* trow0 = a.table + (int64_t)l * a.table_stride;
-    const int total = a.n_suffix * 24;
-    for (int c0 = tid; c0 < total; c0 += 3 * kThreads) {
+    const int total = asm_i1 * 24;
+    for (int c0 = asm_i0 * 24 + tid; c0 < total; c0 += 3 * kThreads) {
       u32x4 w1[3], w2[3];
       float4 cs[3][4];
 #pragma unroll
@@ -351,12 +358,25 @@ prefill_bf16_kernel(PrefillArgs a) {
         }
       }
     }
-  } else if (!kTable && mt == 0 && split == 0) {   // cache assembly: suffix rows into slots [ctx, ctx + n_suffix)
-    for (int c = tid; c < a.n_suffix * 32; c += kThreads) {
-      const int i = c >> 5, part = c & 31;           // row i, 16-byte chunk part % 16 of K or V
-      const int64_t src = i * suf_stride + 8 * (part & 15);
-      bf16_t* dst = (part < 16 ? a.cache_k : a.cache_v) + (bh_kv + ctx + i) * kHD + 8 * (part & 15);
-      *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>((part < 16 ? Ks : Vs) + src);
+  } else if (!kTable) {
+    // item c: row i = c / 32, 16-byte chunk c % 16 of K (c % 32 < 16) or V; eight items per
+    // thread per pass, the loads issued before the stores
+    constexpr int kU = 8;
+    const int total = asm_i1 * 32;
+    for (int c0 = asm_i0 * 32 + tid; c0 < total; c0 += kU * kThreads) {
+      u32x4 w[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int c = c0 + u * kThreads, i = c >> 5, part = c & 31;
+        if (c < total)
+          w[u] = *reinterpret_cast<const u32x4*>((part < 16 ? Ks : Vs) + i * suf_stride + 8 * (part & 15));
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int c = c0 + u * kThreads, i = c >> 5, part = c & 31;
+        if (c < total)
+          *reinterpret_cast<u32x4*>((part < 16 ? a.cache_k : a.cache_v) + (bh_kv + ctx + i) * kHD + 8 * (part & 15)) = w[u];
+      }
     }
   }
   const int64_t qrow = (((int64_t)l * a.batch + b) * a.n_suffix + tok) * a.n_q_heads + hq;
@@ -439,7 +459,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   };
   auto fin_src = [&](int t, int i, int32_t v) -> int32_t {
     if (t * kKeys + 4 * kWaves * i + ld_row >= ctx) v = 0;
-    return v < 0 ? 0 : (v >= a.pool_tokens ? (int32_t)(a.pool_tokens - 1) : v);
+    return clamp_pool_token(v, a.pool_tokens);
   };
   auto map_src = [&](int t, int i) { return ctx > 0 ? fin_src(t, i, raw_src(t, i)) : 0; };
   // rotation item of this lane: row 32 i + 4 w + rr (i = lane / 32, rr = (lane / 8) % 4) of
@@ -449,7 +469,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   auto raw_delta = [&](int t) -> int32_t { return dmap[min(t * kKeys + rot_row, ctx - 1)]; };   // ctx > 0
   auto fin_delta = [&](int t, int32_t d) -> int32_t {
     if (t * kKeys + rot_row >= ctx) d = 0;
-    return d < -a.max_abs_delta ? -a.max_abs_delta : (d > a.max_abs_delta ? a.max_abs_delta : d);
+    return clamp_delta(d, a.max_abs_delta);
   };
   auto map_delta = [&](int t) { return ctx > 0 ? fin_delta(t, raw_delta(t)) : 0; };
   // cos/sin of the lane's 8 pair frequencies at |delta| into this wave's cos/sin area:
@@ -494,8 +514,7 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
     const int32_t src = __builtin_amdgcn_readlane(w_src, T - win);
     const int32_t d = __builtin_amdgcn_readlane(w_del, T - win);
-    if (src < 0 || (int64_t)src + kKeys > a.pool_tokens || d < -a.max_abs_delta || d > a.max_abs_delta)
-      return -1;
+    if (!tile_run_ok(src, d, T * kKeys, ctx, a.pool_tokens, a.max_abs_delta)) return -1;
     delta = d;
     return src;
   };
@@ -1045,42 +1064,39 @@ prefill_bf16_kernel(PrefillArgs a) {
   flush_pending();   // the last tile's last slice
   const float l_tot = pair_sum(l_part);
   if (!row_ok) return;
-  if (a.n_splits == 1) {   // normalise and store bf16
-    const float inv = 1.f / l_tot;
-    bf16_t* op = a.out + orow * kHD;
+  // normalised and rounded to bf16: the output, or one split's share of it (with its reference
+  // max and row sum, the weights the combine needs)
+  const float inv = 1.f / l_tot;
+  bf16_t* op = a.n_splits == 1 ? a.out + orow * kHD : a.ws_o + (split * a.rows_total + orow) * kHD;
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
+  for (int db = 0; db < 4; ++db)
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        const int d = 32 * db + 8 * qd + 4 * hh;
-        uint2 v;
-        v.x = pack_bf16x2(oacc[db][4 * qd] * inv, oacc[db][4 * qd + 1] * inv);
-        v.y = pack_bf16x2(oacc[db][4 * qd + 2] * inv, oacc[db][4 * qd + 3] * inv);
-        *reinterpret_cast<uint2*>(op + d) = v;
-      }
-  } else {                 // unnormalised partial for the split combine
-    float* op = a.ws_o + (split * a.rows_total + orow) * kHD;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int qd = 0; qd < 4; ++qd)
-        *reinterpret_cast<float4*>(op + 32 * db + 8 * qd + 4 * hh) =
-            make_float4(oacc[db][4 * qd], oacc[db][4 * qd + 1], oacc[db][4 * qd + 2], oacc[db][4 * qd + 3]);
-    if (hh == 0) a.ws_ml[split * a.rows_total + orow] = make_float2(m_run, l_tot);
-  }
+    for (int qd = 0; qd < 4; ++qd) {
+      const int d = 32 * db + 8 * qd + 4 * hh;
+      uint2 v;
+      v.x = pack_bf16x2(oacc[db][4 * qd] * inv, oacc[db][4 * qd + 1] * inv);
+      v.y = pack_bf16x2(oacc[db][4 * qd + 2] * inv, oacc[db][4 * qd + 3] * inv);
+      *reinterpret_cast<uint2*>(op + d) = v;
+    }
+  if (a.n_splits > 1 && hh == 0) a.ws_ml[split * a.rows_total + orow] = make_float2(m_run, l_tot);
 }
 
-// Merge the key-range splits of each query row by log-sum-exp.  grid (rows_total / 4), 256
-// threads: one wave per row, two head dims per lane.  With n_valid (table mode), rows of
-// tokens past n_valid[b] are left untouched.
-__global__ void __launch_bounds__(256) prefill_combine_kernel(const float* __restrict__ ws_o,
+// Merge the key-range splits of each query row by log-sum-exp.  Split s left its output
+// normalised by its own row sum l_s (bf16) with its reference max m_s: the row is
+// sum_s w_s O_s / sum_s w_s with w_s = 2^(m_s - M) l_s, M any common reference.  grid (rows_total / 16), 256 threads:
+// 16 lanes per row, 8 head dims per lane; every split's loads are issued without a branch
+// between them (a split that saw no key of the row, reference max -inf, is dropped by a
+// select: its sums are not finite).  With n_valid (table mode), rows of tokens past
+// n_valid[b] are left untouched.
+constexpr int kCombineRowsPerWG = 16;
+__global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __restrict__ ws_o,
                                                               const float2* __restrict__ ws_ml,
                                                               int32_t n_splits, int64_t rows_total,
                                                               const int32_t* __restrict__ n_valid,
                                                               int32_t n_q, int32_t n_q_heads,
                                                               int32_t batch,
                                                               bf16_t* __restrict__ out) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t row = (int64_t)blockIdx.x * kCombineRowsPerWG + (threadIdx.x >> 4);
   if (row >= rows_total) return;
   if (n_valid) {   // row = ((l * B + b) * n_q + i) * Hq + h
     const int64_t ti = row / n_q_heads;
@@ -1088,66 +1104,37 @@ __global__ void __launch_bounds__(256) prefill_combine_kernel(const float* __res
     const int b = (int)((ti / n_q) % batch);
     if (i >= n_valid[b]) return;
   }
-  const int d = 2 * (threadIdx.x & 63);
-  float M = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ws_ml[s * rows_total + row].x);
-  float den = 0.f, o0 = 0.f, o1 = 0.f;
+  const int d = 8 * (threadIdx.x & 15);
+  // one pass with a running reference max; the unrolled loop keeps several splits' loads in
+  // flight (their values do not depend on the running max)
+  float M = -INFINITY, den = 0.f, o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
   for (int s = 0; s < n_splits; ++s) {
     const float2 ml = ws_ml[s * rows_total + row];
-    if (ml.x == -INFINITY) continue;
-    const float w = __builtin_amdgcn_exp2f(ml.x - M);
-    den += w * ml.y;
-    const float2 o = *reinterpret_cast<const float2*>(ws_o + (s * rows_total + row) * kHD + d);
-    o0 += w * o.x;
-    o1 += w * o.y;
-  }
-  const float inv = 1.f / den;
-  reinterpret_cast<uint32_t*>(out + row * kHD)[threadIdx.x & 63] = pack_bf16x2(o0 * inv, o1 * inv);
-}
-
-struct SplitPlan {
-  int m_tiles, n_splits, tiles_per_split;
-};
-
-// Key-range splits: enough workgroups to cover the 256 compute units in whole rounds, each
-// split keeping at least 8 key tiles.  Cost in units of one workgroup-tile (~2 us):
-// rounds * tiles per split, plus, for split runs, one tile (the combine launch; the splits'
-// own prologues run in parallel) and the fp32 partials each split writes and the combine
-// reads back (520 bytes per query row, twice, at ~4 TB/s).  Ties (within 3%) go to fewer
-// splits.
-SplitPlan plan_splits(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
-  SplitPlan p;
-  const int64_t M = (int64_t)n_suffix * (s.n_q_heads / s.n_kv_heads);
-  p.m_tiles = (int)((M + kRowsPerWG - 1) / kRowsPerWG);
-  const int64_t base = (int64_t)p.m_tiles * s.batch * s.n_kv_heads * s.n_layers;
-  const double rows = (double)s.n_layers * s.batch * n_suffix * s.n_q_heads;
-  const int tiles = (max_ctx + n_suffix + kKeys - 1) / kKeys;
-  int best = 1;
-  double best_cost = 1e30;
-  for (int sp = 1; sp <= 32; ++sp) {
-    const int tps = (tiles + sp - 1) / sp;
-    if (sp > 1 && tps < 8) break;
-    const int64_t rounds = (base * sp + 255) / 256;
-    const double partials = sp > 1 ? 1.0 + sp * rows * 2.0 * (kHD + 2) * 4 / 4e12 / 2e-6 : 0.0;
-    const double cost = (double)rounds * tps + partials;
-    if (cost < best_cost * 0.97) {
-      best_cost = cost;
-      best = sp;
+    const uint4 x = *reinterpret_cast<const uint4*>(ws_o + (s * rows_total + row) * kHD + d);
+    const bool seen = ml.x != -INFINITY;
+    const float m_new = seen ? fmaxf(M, ml.x) : M;
+    const float keep = seen ? __builtin_amdgcn_exp2f(M - m_new) : 1.f;   // 0 while M is -inf
+    const float w = seen ? __builtin_amdgcn_exp2f(ml.x - m_new) * ml.y : 0.f;
+    M = m_new;
+    den = den * keep + w;
+    const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[2 * e] = o[2 * e] * keep + (seen ? w * __uint_as_float(xw[e] << 16) : 0.f);
+      o[2 * e + 1] = o[2 * e + 1] * keep + (seen ? w * __uint_as_float(xw[e] & 0xFFFF0000u) : 0.f);
     }
   }
-  p.n_splits = best;
-  p.tiles_per_split = (tiles + best - 1) / best;
-  return p;
+  const float inv = 1.f / den;
+  uint4 v;
+  v.x = pack_bf16x2(o[0] * inv, o[1] * inv);
+  v.y = pack_bf16x2(o[2] * inv, o[3] * inv);
+  v.z = pack_bf16x2(o[4] * inv, o[5] * inv);
+  v.w = pack_bf16x2(o[6] * inv, o[7] * inv);
+  *reinterpret_cast<uint4*>(out + row * kHD + d) = v;
 }
 
 }  // namespace
-
-size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
-  const SplitPlan p = plan_splits(s, n_suffix, max_ctx);
-  if (p.n_splits == 1) return 0;
-  const size_t rows = (size_t)s.n_layers * s.batch * n_suffix * s.n_q_heads;
-  return (size_t)p.n_splits * rows * (kHD + 2) * sizeof(float);
-}
 
 namespace {
 
@@ -1165,10 +1152,7 @@ __global__ void __launch_bounds__(64) map_expand_kernel(const pic_block* __restr
                                                         int32_t batch, int32_t map_cap,
                                                         int32_t* smap, int32_t* dmap) {
   const pic_block blk = blocks[blockIdx.x];
-  if (blk.request < 0 || blk.request >= batch || blk.n_tokens <= 0 ||
-      blk.n_tokens > PIC_BLOCK_TOKENS || blk.dst_slot < 0 ||
-      (int64_t)blk.dst_slot + blk.n_tokens > map_cap)
-    return;
+  if (!map_block_ok(blk, batch, map_cap)) return;
   const int t = threadIdx.x;
   if (t < blk.n_tokens) {
     const int64_t i = (int64_t)blk.request * map_cap + blk.dst_slot + t;
@@ -1210,7 +1194,7 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
   const int n_rep = s.n_q_heads / s.n_kv_heads;
   const int64_t M = (int64_t)n_q * n_rep;
   if (M == 0 || s.batch == 0 || s.n_layers == 0) return hipSuccess;
-  const SplitPlan p = plan_splits(s, n_q, max_ctx);
+  const SplitPlan p = plan_prefill_splits(s, n_q, max_ctx);
   a.n_suffix = n_q;
   a.n_rep = n_rep;
   a.rep_magic = ((uint64_t(1) << 32) + n_rep - 1) / n_rep;
@@ -1224,8 +1208,8 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
   a.tiles_per_split = p.tiles_per_split;
   a.n_wg = p.m_tiles * p.n_splits * s.batch * s.n_kv_heads;
   a.rows_total = (int64_t)s.n_layers * s.batch * n_q * s.n_q_heads;
-  a.ws_o = static_cast<float*>(workspace);
-  a.ws_ml = reinterpret_cast<float2*>(a.ws_o + (size_t)p.n_splits * a.rows_total * kHD);
+  a.ws_o = static_cast<bf16_t*>(workspace);
+  a.ws_ml = a.ws_o ? reinterpret_cast<float2*>(a.ws_o + (size_t)p.n_splits * a.rows_total * kHD) : nullptr;
   a.scale_log2 = s.scale_log2;
   if (p.n_splits > 1 && (workspace == nullptr || ws_bytes < prefill_bf16_workspace(s, n_q, max_ctx)))
     return hipErrorInvalidValue;
@@ -1249,7 +1233,8 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
     hipLaunchKernelGGL((prefill_bf16_kernel<kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
-  hipLaunchKernelGGL(prefill_combine_kernel, dim3((unsigned)((a.rows_total + 3) / 4)), dim3(256), 0,
+  hipLaunchKernelGGL(prefill_combine_kernel,
+                     dim3((unsigned)((a.rows_total + kCombineRowsPerWG - 1) / kCombineRowsPerWG)), dim3(256), 0,
                      stream, a.ws_o, a.ws_ml, p.n_splits, a.rows_total,
                      mode == kModeTable ? a.n_valid : nullptr, n_q, s.n_q_heads, s.batch, a.out);
   return hipGetLastError();
@@ -1310,8 +1295,6 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
   const int32_t max_ctx = max_len > n_q ? max_len - n_q : 0;
   return launch(s, a, kModeTable, false, n_q, max_ctx, workspace, ws_bytes, stream);
 }
-
-int32_t slot_map_tiles(int32_t map_cap) { return (map_cap + kKeys - 1) / kKeys; }
 
 hipError_t launch_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch, int32_t map_cap,
                            int32_t* smap, int32_t* dmap, int32_t* tmap, hipStream_t stream) {

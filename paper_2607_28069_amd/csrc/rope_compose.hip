@@ -12,6 +12,7 @@
 // element chunk [c, c + VEC) of both halves; for the interleaved pairing (x_2i, x_2i+1) it
 // owns the 2 VEC consecutive elements of pairs [c, c + VEC).  bf16 output rows are stored
 // non-temporally (written once; the caches stay with the pool rows, which several requests read).
+#include "pic_bounds.h"
 #include "pic_internal.h"
 
 namespace pic {
@@ -149,12 +150,7 @@ __global__ void __launch_bounds__(256) compose_kernel(
   constexpr int PASSES = (PIC_BLOCK_TOKENS + RPP - 1) / RPP;
 
   const pic_block blk = blocks[blockIdx.x];
-  if (blk.request < 0 || blk.request >= batch || blk.n_tokens <= 0 ||
-      blk.n_tokens > PIC_BLOCK_TOKENS || blk.src_token < 0 ||
-      (int64_t)blk.src_token + blk.n_tokens > pool_tokens || blk.dst_slot < 0 ||
-      (int64_t)blk.dst_slot + blk.n_tokens > cache_cap || blk.delta > max_abs_delta ||
-      blk.delta < -max_abs_delta)
-    return;
+  if (!block_ok(blk, batch, pool_tokens, cache_cap, max_abs_delta)) return;
 
   const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
   const int j = threadIdx.x % LPR, r0 = threadIdx.x / LPR;
@@ -212,14 +208,11 @@ __global__ void __launch_bounds__(256) compose_shared_kernel(
   constexpr int RPP = 256 / LPR;           // rows per pass
   constexpr int PASSES = (PIC_BLOCK_TOKENS + RPP - 1) / RPP;
 
-  int g0 = group_start[blockIdx.x], g1 = group_start[blockIdx.x + 1];
-  g0 = g0 < 0 ? 0 : g0;
-  g1 = g1 > n_blocks ? n_blocks : g1;
+  int32_t g0, g1;
+  group_range(group_start[blockIdx.x], group_start[blockIdx.x + 1], n_blocks, g0, g1);
   if (g0 >= g1) return;
   const pic_block src = blocks[g0];
-  if (src.n_tokens <= 0 || src.n_tokens > PIC_BLOCK_TOKENS || src.src_token < 0 ||
-      (int64_t)src.src_token + src.n_tokens > pool_tokens)
-    return;
+  if (!block_source_ok(src, pool_tokens)) return;
 
   const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
   const int j = threadIdx.x % LPR, r0 = threadIdx.x / LPR;
@@ -244,9 +237,8 @@ __global__ void __launch_bounds__(256) compose_shared_kernel(
   // The next block's descriptor and cos/sin row are read while this block is stored, so a
   // destination costs no memory round trip of its own.
   auto cs_of = [&](const pic_block& b, float (&cs)[VEC], float (&sn)[VEC]) {
-    int32_t d = b.delta;   // (an out-of-range block is skipped below; clamp for the read)
-    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
-    load_cs<VEC, HALF>(ltable, d, c0, cs, sn);
+    // (an out-of-range block is skipped below; clamp for the read)
+    load_cs<VEC, HALF>(ltable, clamp_delta(b.delta, max_abs_delta), c0, cs, sn);
   };
   pic_block nxt = src;
   float ncs[VEC], nsn[VEC];
@@ -263,10 +255,7 @@ __global__ void __launch_bounds__(256) compose_shared_kernel(
       nxt = blocks[i + 1];
       cs_of(nxt, ncs, nsn);
     }
-    if (blk.src_token != src.src_token || blk.n_tokens != src.n_tokens || blk.request < 0 ||
-        blk.request >= batch || blk.dst_slot < 0 || (int64_t)blk.dst_slot + blk.n_tokens > cache_cap ||
-        blk.delta > max_abs_delta || blk.delta < -max_abs_delta)
-      continue;
+    if (!shared_block_ok(blk, src, batch, cache_cap, max_abs_delta)) continue;
     const int64_t dst_row0 = (((int64_t)l * batch + blk.request) * Hkv + h) * cache_cap + blk.dst_slot;
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
@@ -301,14 +290,11 @@ __global__ void __launch_bounds__(256) compose_shared_il_rows_kernel(
   constexpr int RPP = 16;                                   // rows per pass
   constexpr int PASSES = PIC_BLOCK_TOKENS / RPP;
 
-  int g0 = group_start[blockIdx.x], g1 = group_start[blockIdx.x + 1];
-  g0 = g0 < 0 ? 0 : g0;
-  g1 = g1 > n_blocks ? n_blocks : g1;
+  int32_t g0, g1;
+  group_range(group_start[blockIdx.x], group_start[blockIdx.x + 1], n_blocks, g0, g1);
   if (g0 >= g1) return;
   const pic_block src = blocks[g0];
-  if (src.n_tokens <= 0 || src.n_tokens > PIC_BLOCK_TOKENS || src.src_token < 0 ||
-      (int64_t)src.src_token + src.n_tokens > pool_tokens)
-    return;
+  if (!block_source_ok(src, pool_tokens)) return;
 
   const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
   const int j = threadIdx.x & 15, r0 = threadIdx.x >> 4;   // chunk j = pairs 4 j .. 4 j + 3
@@ -326,8 +312,7 @@ __global__ void __launch_bounds__(256) compose_shared_il_rows_kernel(
     }
   }
   auto cs_of = [&](const pic_block& b, float (&cs)[4], float (&sn)[4]) {
-    int32_t d = b.delta;
-    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
+    const int32_t d = clamp_delta(b.delta, max_abs_delta);
     const int32_t ad = d < 0 ? -d : d;
     const float2* row = ltable + (int64_t)ad * HALF + 4 * j;
 #pragma unroll
@@ -352,10 +337,7 @@ __global__ void __launch_bounds__(256) compose_shared_il_rows_kernel(
       nxt = blocks[i + 1];
       cs_of(nxt, ncs, nsn);
     }
-    if (blk.src_token != src.src_token || blk.n_tokens != src.n_tokens || blk.request < 0 ||
-        blk.request >= batch || blk.dst_slot < 0 || (int64_t)blk.dst_slot + blk.n_tokens > cache_cap ||
-        blk.delta > max_abs_delta || blk.delta < -max_abs_delta)
-      continue;
+    if (!shared_block_ok(blk, src, batch, cache_cap, max_abs_delta)) continue;
     const int64_t dst_row0 = (((int64_t)l * batch + blk.request) * Hkv + h) * cache_cap + blk.dst_slot;
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
@@ -395,14 +377,12 @@ __global__ void __launch_bounds__(256) compose_tiles_kernel(
   constexpr int PASSES = (PIC_BLOCK_TOKENS + RPP - 1) / RPP;
 
   const int b = blockIdx.x / map_tiles, tile = blockIdx.x - b * map_tiles;
-  int ctx = ctx_len[b];
-  ctx = ctx < 0 ? 0 : (ctx > max_ctx ? max_ctx : ctx);
+  const int ctx = clamp_len(ctx_len[b], max_ctx);
   const int s0 = tile * PIC_BLOCK_TOKENS;
   if (s0 >= ctx) return;
   const int32_t src = tmap[((int64_t)b * map_tiles + tile) * 2];
   const int32_t dl = tmap[((int64_t)b * map_tiles + tile) * 2 + 1];
-  if (s0 + PIC_BLOCK_TOKENS <= ctx && src >= 0 && (int64_t)src + PIC_BLOCK_TOKENS <= pool_tokens &&
-      dl >= -max_abs_delta && dl <= max_abs_delta)
+  if (tile_run_ok(src, dl, s0, ctx, pool_tokens, max_abs_delta))
     return;   // a whole run: the prefill reads it from the pool
 
   const int h = blockIdx.y, l = blockIdx.z, Hkv = gridDim.y;
@@ -416,10 +396,8 @@ __global__ void __launch_bounds__(256) compose_tiles_kernel(
   for (int p = 0; p < PASSES; ++p) {
     const int slot = s0 + r0 + p * RPP;
     if (slot >= ctx) continue;
-    int32_t st = smap[(int64_t)b * map_cap + slot];
-    st = st < 0 ? 0 : (st >= pool_tokens ? (int32_t)(pool_tokens - 1) : st);
-    int32_t d = dmap[(int64_t)b * map_cap + slot];
-    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
+    const int32_t st = clamp_pool_token(smap[(int64_t)b * map_cap + slot], pool_tokens);
+    const int32_t d = clamp_delta(dmap[(int64_t)b * map_cap + slot], max_abs_delta);
     float cs[VEC], sn[VEC], x1[VEC], x2[VEC];
     load_cs<VEC, HALF>(ltable, d, c0, cs, sn);
     const int64_t sr = (pool0 + st) * HD, dr = (dst0 + slot) * HD;
@@ -449,8 +427,7 @@ __global__ void __launch_bounds__(256) rerotate_kernel(const T* k_in, T* k_out, 
        idx += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = idx / LPR;
     const int c0 = (int)(idx - row * LPR) * VEC;
-    int32_t d = delta[row / n_heads];
-    d = d > max_abs_delta ? max_abs_delta : (d < -max_abs_delta ? -max_abs_delta : d);
+    const int32_t d = clamp_delta(delta[row / n_heads], max_abs_delta);
     float cs[VEC], sn[VEC], x1[VEC], x2[VEC];
     load_cs<VEC, HALF>(table, d, c0, cs, sn);
     const int o1 = off1<VEC, HALF, IL>(c0), o2 = off2<VEC, HALF, IL>(c0);
