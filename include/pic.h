@@ -36,6 +36,9 @@
  *   - Device-side tables (gather blocks, context lengths) are read as given; kernels clamp
  *     every index they derive from them to the buffer sizes passed on the host, so a bad
  *     table gives wrong values, never an out-of-bounds access.
+ *   - Attention (3, 3a-3c, 4) on bf16 caches at head_dim 128 runs on the matrix-core kernels;
+ *     on float32 caches and on bf16 caches at head_dim 64 it runs on a row-wise kernel (one
+ *     workgroup per query row, float32 arithmetic) that needs no workspace and never splits.
  */
 #ifndef PIC_H
 #define PIC_H
@@ -284,7 +287,9 @@ pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q, c
      the context are treated as (-1, 0).
    The suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)), and with a tile map
    the non-run context tiles; a later pic_compose (or pic_compose_shared) fills the document
-   slots for decoding.  bf16 only.
+   slots for decoding.  bf16 only.  At head_dim 64 a tile map is accepted and not used: every
+   context key is turned on load (bit-identical to compose + prefill) and only the suffix rows
+   are stored.
      pool_k, pool_v, pool_tokens, table, max_abs_delta   as for pic_compose
      slot_src, slot_delta, map_cap   the map; map_cap >= max_ctx (entries are clamped to the
                                      pool and to max_abs_delta)
@@ -331,7 +336,9 @@ pic_status pic_frontier_prefill_attn(const pic_model* model, const void* q, cons
 /* ---- 4. decode (App. C.1: ordinary autoregressive decoding over the completed cache) ----
    For request b the new token sits at slot p = base_len[b] + step: k_new/v_new are written
    there, then its query attends over slots [0, p].  Split-K over the context: n_splits
-   chunks per (request, kv head) (0 picks a value), merged by log-sum-exp.
+   chunks per (request, kv head) (0 picks a value), merged by log-sum-exp; a kv head with
+   more than 16 query heads is served in groups of 16.  The row-wise path (float32, or bf16 at
+   head_dim 64) ignores n_splits.
      base_len [device, batch]  valid slots before the first decode step; clamped to
                                [0, max_base_len]; max_base_len + step + 1 <= cache_cap
      workspace                 pic_decode_workspace_bytes(...) bytes for the same batch,

@@ -17,7 +17,7 @@ LIB = os.path.join(PKG, "libpic.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["pic_api.cpp", "pic_plan.cpp", "rope_compose.hip", "attn_f32.hip", "prefill_bf16.hip", "decode_bf16.hip"]
+SOURCES = ["pic_api.cpp", "pic_plan.cpp", "rope_compose.hip", "attn_rows.hip", "prefill_bf16.hip", "decode_bf16.hip"]
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-fvisibility=hidden",

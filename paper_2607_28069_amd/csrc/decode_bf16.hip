@@ -8,8 +8,9 @@
 //  * a workgroup of 4 waves covers one context range of one (request, kv head); each wave
 //    streams its own quarter in 32-key tiles, with the next tile's loads in flight while the
 //    current one is used and no barrier inside the loop;
-//  * S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with the query heads along N (n_rep <= 16, unused
-//    columns zero): K goes straight from global memory into the A-operand layout (16 bytes per
+//  * S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with up to 16 query heads along N (unused columns
+//    zero); a kv head with more query heads is served by one workgroup per group of 16 heads,
+//    each streaming the context range: K goes straight from global memory into the A-operand layout (16 bytes per
 //    lane, 64 contiguous bytes per row per instruction);
 //  * O^T = V^T P^T with the same instruction: V moves global -> LDS with global_load_lds_dwordx4
 //    (row-major, chunk-swizzled) and its A operand comes from two transposing reads
@@ -68,6 +69,7 @@ struct DecodeArgs {
   float* ws_o;            // [L][B][Hq][S][D]   (n_splits > 1)
   float* ws_ml;           // [L][B][Hq][S][2]
   int32_t batch, cache_cap, n_q_heads, n_kv_heads, max_base, step, n_splits, chunk;
+  int32_t head_groups;    // groups of up to 16 query heads per kv head (ceil(n_rep / 16))
   float scale_log2;
   const float2* table;    // rope variant: [L or 1][max_abs_delta + 1][D/2] cos/sin rows
   int64_t table_stride;
@@ -134,11 +136,14 @@ decode_bf16_kernel(DecodeArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int split = blockIdx.x % a.n_splits;
-  const int bg = blockIdx.x / a.n_splits;
+  const int hgrp = blockIdx.x % a.head_groups;           // query heads 16 hgrp .. of kv head g
+  const int split = (blockIdx.x / a.head_groups) % a.n_splits;
+  const int bg = blockIdx.x / (a.head_groups * a.n_splits);
   const int b = bg / a.n_kv_heads, g = bg % a.n_kv_heads;
   const int l = blockIdx.y;
   const int n_rep = a.n_q_heads / a.n_kv_heads;
+  const int rep0 = 16 * hgrp;                             // first query head of this group
+  const int n_here = min(16, n_rep - rep0);               // query heads of this group
 
   const int32_t base = clamp_len(a.base_len[b], a.max_base);
   const int p = base + a.step;                       // the new token's slot
@@ -160,7 +165,7 @@ decode_bf16_kernel(DecodeArgs a) {
   // from the cache during this launch: the wave whose range holds it reads k_new / v_new.
   const float2* trow = kRope ? a.table + (int64_t)l * a.table_stride + (int64_t)min(p, a.max_abs_delta) * (kHD / 2)
                              : nullptr;   // rope variant: cos/sin of position p
-  if (p < a.cache_cap && p >= wc0 && p < wc1 && wave == 0 && lane < 32) {
+  if (hgrp == 0 && p < a.cache_cap && p >= wc0 && p < wc1 && wave == 0 && lane < 32) {
     const int c = lane & 15;
     u32x4* dst = reinterpret_cast<u32x4*>((lane < 16 ? a.cache_k : a.cache_v) + (bh_kv * a.cache_cap + p) * kHD);
     if (kRope && lane < 16) {   // the new key turned to p: lane c < 8 takes a chunk pair
@@ -192,8 +197,8 @@ decode_bf16_kernel(DecodeArgs a) {
   // Q^T operand: lane (n, g4) holds q[head g*n_rep + n][32 ks + 8 g4 .. +8)
   bf16x8_t qop[4];
   {
-    const bool ok = n < n_rep;
-    const int64_t qrow = ((int64_t)l * a.batch + b) * a.n_q_heads + g * n_rep + (ok ? n : 0);
+    const bool ok = n < n_here;
+    const int64_t qrow = ((int64_t)l * a.batch + b) * a.n_q_heads + g * n_rep + rep0 + (ok ? n : 0);
     const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + qrow * kHD);
     u32x4 qv[4];
 #pragma unroll
@@ -335,7 +340,7 @@ decode_bf16_kernel(DecodeArgs a) {
   __syncthreads();
   float* o_lds = reinterpret_cast<float*>(v_lds0);    // [4][16][128] fp32 = 32 KB
   float* ml_lds = reinterpret_cast<float*>(v_lds1);   // [4][16][2]
-  if (n < n_rep) {
+  if (n < n_here) {
 #pragma unroll
     for (int db = 0; db < 8; ++db)
       *reinterpret_cast<float4*>(o_lds + (wave * 16 + n) * kHD + 16 * db + 4 * g4) =
@@ -348,7 +353,7 @@ decode_bf16_kernel(DecodeArgs a) {
   __syncthreads();
   // thread -> (query n = tid / 16, head dims 8 (tid % 16) .. +8)
   const int mn = tid >> 4, md = 8 * (tid & 15);
-  if (mn < n_rep) {
+  if (mn < n_here) {
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, ml_lds[(w * 16 + mn) * 2]);
@@ -364,7 +369,7 @@ decode_bf16_kernel(DecodeArgs a) {
       o[0] += wt * x0.x; o[1] += wt * x0.y; o[2] += wt * x0.z; o[3] += wt * x0.w;
       o[4] += wt * x1.x; o[5] += wt * x1.y; o[6] += wt * x1.z; o[7] += wt * x1.w;
     }
-    const int64_t row = ((int64_t)l * a.batch + b) * a.n_q_heads + g * n_rep + mn;
+    const int64_t row = ((int64_t)l * a.batch + b) * a.n_q_heads + g * n_rep + rep0 + mn;
     if (a.n_splits == 1) {
       const float inv = 1.f / den;
       uint4 v;
@@ -464,7 +469,8 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   a.table = rope_table;
   a.table_stride = table_stride;
   a.max_abs_delta = max_abs_delta;
-  const dim3 grid(n_splits * s.batch * s.n_kv_heads, s.n_layers);
+  a.head_groups = decode_head_groups(s);
+  const dim3 grid(a.head_groups * n_splits * s.batch * s.n_kv_heads, s.n_layers);
   if (rope_table == nullptr)
     hipLaunchKernelGGL((decode_bf16_kernel<false, false>), grid, dim3(256), 0, stream, a);
   else if (interleaved)

@@ -106,11 +106,62 @@ pic::AttnShape shape_of(const pic_model* m, int32_t batch, int32_t cache_cap, fl
   return s;
 }
 
-pic_status check_attn_model(const pic_model* m) {
-  PIC_CHECK(check_model(m));
-  if (m->dtype == PIC_BF16 && m->head_dim != 128)
-    return fail(PIC_ERR_UNSUPPORTED, "bf16 attention is built for head_dim 128 only");
-  return PIC_OK;
+pic_status check_attn_model(const pic_model* m) { return check_model(m); }
+
+// bf16 caches at head_dim 128 run on the matrix-core kernels; float32 caches and bf16 caches
+// at head_dim 64 on the row-wise kernel.
+bool mfma_path(const pic_model* m) { return m->dtype == PIC_BF16 && m->head_dim == 128; }
+
+// Row-wise attention of n_q query rows per request at the positions `pos` gives them.
+// Options for bf16 rows: q_table (fused RoPE of the query), and a paged key source.
+struct RowOpts {
+  const void* q_table = nullptr;
+  int64_t table_stride = 0;
+  int32_t max_abs_delta = 0;
+  const void* pool_k = nullptr;
+  const void* pool_v = nullptr;
+  int64_t pool_tokens = 0;
+  const int32_t* smap = nullptr;
+  const int32_t* dmap = nullptr;
+  int32_t map_cap = 0;
+  const int32_t* ctx_len = nullptr;
+  int32_t max_ctx = 0;
+  const void* k_table = nullptr;
+};
+template <typename T>
+hipError_t launch_rows_as(const pic_model* m, const pic::AttnShape& s, const void* q, const void* ck,
+                          const void* cv, const pic::RowPos& pos, int32_t n_q, void* out, const RowOpts& o,
+                          hipStream_t st) {
+  pic::RowArgs<T> a;
+  a.s = s;
+  a.q = static_cast<const T*>(q);
+  a.cache_k = static_cast<const T*>(ck);
+  a.cache_v = static_cast<const T*>(cv);
+  a.pos = pos;
+  a.n_q = n_q;
+  a.out = static_cast<T*>(out);
+  a.q_table = static_cast<const float2*>(o.q_table);
+  a.k_table = static_cast<const float2*>(o.k_table);
+  a.table_stride = o.table_stride;
+  a.max_abs_delta = o.max_abs_delta;
+  a.interleaved = m->rope_pairing == PIC_ROPE_INTERLEAVED;
+  a.pool_k = static_cast<const T*>(o.pool_k);
+  a.pool_v = static_cast<const T*>(o.pool_v);
+  a.pool_tokens = o.pool_tokens;
+  a.smap = o.smap;
+  a.dmap = o.dmap;
+  a.map_cap = o.map_cap;
+  a.ctx_len = o.ctx_len;
+  a.max_ctx = o.max_ctx;
+  a.stream = st;
+  return pic::launch_attn_rows(a);
+}
+pic_status launch_rows(const pic_model* m, const pic::AttnShape& s, const void* q, const void* ck, const void* cv,
+                       const pic::RowPos& pos, int32_t n_q, void* out, hipStream_t st, const char* what,
+                       const RowOpts& o = RowOpts()) {
+  return hip_status(m->dtype == PIC_F32 ? launch_rows_as<float>(m, s, q, ck, cv, pos, n_q, out, o, st)
+                                        : launch_rows_as<pic::bf16_t>(m, s, q, ck, cv, pos, n_q, out, o, st),
+                    what);
 }
 
 }  // namespace
@@ -464,7 +515,7 @@ PIC_API pic_status pic_compose_shared(const pic_model* model, const void* pool_k
 PIC_API size_t pic_prefill_workspace_bytes(const pic_model* model, int32_t batch, int32_t n_suffix,
                                            int32_t max_ctx) {
   if (check_attn_model(model) != PIC_OK || batch < 0 || n_suffix < 0 || max_ctx < 0) return 0;
-  if (model->dtype == PIC_F32) return 0;
+  if (!mfma_path(model)) return 0;
   return pic::prefill_bf16_workspace(shape_of(model, batch, max_ctx + n_suffix, 0.f), n_suffix,
                                      max_ctx);
 }
@@ -502,8 +553,8 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
   const hipStream_t st = (hipStream_t)stream;
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   // a4: suffix K/V into slots [ctx, ctx + n_suffix) (App. C.1: inline KVs interleaved); the
-  // bf16 kernel does this itself
-  if (model->dtype == PIC_F32) {
+  // bf16 matrix-core kernel does this itself
+  if (!mfma_path(model)) {
     pic::RowPos pos;
     pos.base = ctx_len;
     pos.max_base = max_ctx;
@@ -511,11 +562,7 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
                                             model->n_kv_heads, k_suf, v_suf, cache_k, cache_v,
                                             batch, cache_cap, pos, n_suffix, st),
                          "suffix append launch"));
-    return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
-                                                static_cast<const float*>(cache_k),
-                                                static_cast<const float*>(cache_v), pos, n_suffix,
-                                                static_cast<float*>(out), st),
-                      "prefill attention launch");
+    return launch_rows(model, s, q, cache_k, cache_v, pos, n_suffix, out, st, "prefill attention launch");
   }
   return hip_status(pic::launch_prefill_bf16(s, static_cast<const pic::bf16_t*>(q),
                                              static_cast<const pic::bf16_t*>(k_suf),
@@ -569,6 +616,26 @@ PIC_API pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const vo
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+  if (!mfma_path(model)) {   // head_dim 64: keys turned as they are appended, queries in the kernel
+    const hipStream_t st = (hipStream_t)stream;
+    pic::RowPos pos;
+    pos.base = ctx_len;
+    pos.max_base = max_ctx;
+    PIC_CHECK(hip_status(pic::launch_append_rope(model->head_dim, model->rope_pairing == PIC_ROPE_INTERLEAVED,
+                                                 model->n_layers, model->n_kv_heads,
+                                                 static_cast<const pic::bf16_t*>(k_suf),
+                                                 static_cast<const pic::bf16_t*>(v_suf),
+                                                 static_cast<pic::bf16_t*>(cache_k),
+                                                 static_cast<pic::bf16_t*>(cache_v), batch, cache_cap, pos,
+                                                 n_suffix, static_cast<const float2*>(table), stride,
+                                                 max_abs_delta, st),
+                         "suffix append launch"));
+    RowOpts o;
+    o.q_table = table;
+    o.table_stride = stride;
+    o.max_abs_delta = max_abs_delta;
+    return launch_rows(model, s, q, cache_k, cache_v, pos, n_suffix, out, st, "fused-RoPE prefill launch", o);
+  }
   return hip_status(pic::launch_prefill_bf16_rope(
                         s, model->rope_pairing == PIC_ROPE_INTERLEAVED,
                         static_cast<const pic::bf16_t*>(q), static_cast<const pic::bf16_t*>(k_suf),
@@ -641,6 +708,29 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+  if (!mfma_path(model)) {   // head_dim 64: every context key through the slot map (tile map unused)
+    const hipStream_t st = (hipStream_t)stream;
+    pic::RowPos pos;
+    pos.base = ctx_len;
+    pos.max_base = max_ctx;
+    PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
+                                            model->n_kv_heads, k_suf, v_suf, cache_k, cache_v,
+                                            batch, cache_cap, pos, n_suffix, st),
+                         "suffix append launch"));
+    RowOpts o;
+    o.k_table = table;
+    o.table_stride = stride;
+    o.max_abs_delta = max_abs_delta;
+    o.pool_k = pool_k;
+    o.pool_v = pool_v;
+    o.pool_tokens = pool_tokens;
+    o.smap = slot_src;
+    o.dmap = slot_delta;
+    o.map_cap = map_cap > 0 ? map_cap : 1;
+    o.ctx_len = ctx_len;
+    o.max_ctx = max_ctx;
+    return launch_rows(model, s, q, cache_k, cache_v, pos, n_suffix, out, st, "paged prefill launch", o);
+  }
   return hip_status(pic::launch_prefill_bf16_paged(
                         s, model->rope_pairing == PIC_ROPE_INTERLEAVED,
                         static_cast<const pic::bf16_t*>(q), static_cast<const pic::bf16_t*>(k_suf),
@@ -657,7 +747,7 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
 PIC_API size_t pic_frontier_workspace_bytes(const pic_model* model, int32_t batch,
                                             int32_t n_inline, int32_t max_len) {
   if (check_attn_model(model) != PIC_OK || batch < 0 || n_inline < 0 || max_len < 0) return 0;
-  if (model->dtype == PIC_F32) return 0;
+  if (!mfma_path(model)) return 0;
   const int32_t max_ctx = max_len > n_inline ? max_len - n_inline : 0;
   return pic::prefill_bf16_workspace(shape_of(model, batch, max_len, 0.f), n_inline, max_ctx);
 }
@@ -705,12 +795,8 @@ PIC_API pic_status pic_frontier_prefill_attn(const pic_model* model, const void*
                                           model->n_kv_heads, k_inl, v_inl, cache_k, cache_v,
                                           batch, cache_cap, rp, n_inline, st),
                        "inline append launch"));
-  if (model->dtype == PIC_F32)
-    return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
-                                                static_cast<const float*>(cache_k),
-                                                static_cast<const float*>(cache_v), rp, n_inline,
-                                                static_cast<float*>(out), st),
-                      "frontier attention launch");
+  if (!mfma_path(model))
+    return launch_rows(model, s, q, cache_k, cache_v, rp, n_inline, out, st, "frontier attention launch");
   return hip_status(pic::launch_prefill_bf16_table(s, static_cast<const pic::bf16_t*>(q),
                                                    static_cast<const pic::bf16_t*>(cache_k),
                                                    static_cast<const pic::bf16_t*>(cache_v), rp,
@@ -726,14 +812,14 @@ PIC_API pic_status pic_frontier_prefill_attn(const pic_model* model, const void*
 
 PIC_API int32_t pic_decode_auto_splits(const pic_model* model, int32_t batch, int32_t max_len) {
   if (check_attn_model(model) != PIC_OK || batch <= 0 || max_len <= 0) return 1;
-  if (model->dtype == PIC_F32) return 1;
+  if (!mfma_path(model)) return 1;
   return pic::decode_bf16_auto_splits(shape_of(model, batch, max_len, 0.f), max_len);
 }
 
 PIC_API size_t pic_decode_workspace_bytes(const pic_model* model, int32_t batch, int32_t max_len,
                                           int32_t n_splits) {
   if (check_attn_model(model) != PIC_OK || batch < 0 || max_len < 0 || n_splits < 0) return 0;
-  if (model->dtype == PIC_F32) return 0;
+  if (!mfma_path(model)) return 0;
   if (n_splits == 0) n_splits = pic_decode_auto_splits(model, batch, max_len);
   return pic::decode_bf16_workspace(shape_of(model, batch, max_len, 0.f), max_len, n_splits);
 }
@@ -757,9 +843,6 @@ pic_status decode_impl(const pic_model* model, const void* q, const void* k_new,
   if (max_len > cache_cap)
     return fail(PIC_ERR_CAPACITY, "max_base_len + step + 1 = %lld exceeds cache_cap %d",
                 (long long)max_len, cache_cap);
-  const int n_rep = model->n_q_heads / model->n_kv_heads;
-  if (model->dtype == PIC_BF16 && n_rep > 16)
-    return fail(PIC_ERR_UNSUPPORTED, "bf16 decode supports up to 16 query heads per kv head");
   if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
   if ((int64_t)batch * model->n_q_heads > INT32_MAX)
     return fail(PIC_ERR_UNSUPPORTED, "too many query rows");
@@ -781,23 +864,34 @@ pic_status decode_impl(const pic_model* model, const void* q, const void* k_new,
   }
   const hipStream_t st = (hipStream_t)stream;
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
-  if (model->dtype == PIC_F32) {
+  if (!mfma_path(model)) {   // float32, or bf16 at head_dim 64: row-wise kernel, no splits
     pic::RowPos pos;
     pos.base = base_len;
     pos.max_base = max_base_len;
     pos.offset = step;
-    PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
-                                            model->n_kv_heads, k_new, v_new, cache_k, cache_v,
-                                            batch, cache_cap, pos, 1, st),
-                         "decode append launch"));
-    return hip_status(pic::launch_attn_rows_f32(s, static_cast<const float*>(q),
-                                                static_cast<const float*>(cache_k),
-                                                static_cast<const float*>(cache_v), pos, 1,
-                                                static_cast<float*>(out), st),
-                      "decode attention launch");
+    const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+    if (table)
+      PIC_CHECK(hip_status(pic::launch_append_rope(model->head_dim, model->rope_pairing == PIC_ROPE_INTERLEAVED,
+                                                   model->n_layers, model->n_kv_heads,
+                                                   static_cast<const pic::bf16_t*>(k_new),
+                                                   static_cast<const pic::bf16_t*>(v_new),
+                                                   static_cast<pic::bf16_t*>(cache_k),
+                                                   static_cast<pic::bf16_t*>(cache_v), batch, cache_cap, pos, 1,
+                                                   static_cast<const float2*>(table), stride, max_abs_delta, st),
+                           "decode append launch"));
+    else
+      PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
+                                              model->n_kv_heads, k_new, v_new, cache_k, cache_v,
+                                              batch, cache_cap, pos, 1, st),
+                           "decode append launch"));
+    RowOpts o;
+    o.q_table = table;
+    o.table_stride = stride;
+    o.max_abs_delta = max_abs_delta;
+    return launch_rows(model, s, q, cache_k, cache_v, pos, 1, out, st, "decode attention launch", o);
   }
   if (n_splits == 0) n_splits = pic::decode_bf16_auto_splits(s, (int32_t)max_len);
-  if ((int64_t)n_splits * batch * model->n_kv_heads > INT32_MAX)
+  if ((int64_t)n_splits * batch * model->n_kv_heads * ((model->n_q_heads / model->n_kv_heads + 15) / 16) > INT32_MAX)
     return fail(PIC_ERR_UNSUPPORTED, "too many splits");
   if (n_splits > max_len) n_splits = (int32_t)max_len;
   const size_t need = pic::decode_bf16_workspace(s, (int32_t)max_len, n_splits);

@@ -99,12 +99,46 @@ struct SplitPlan {
 };
 SplitPlan plan_prefill_splits(const AttnShape& s, int32_t n_suffix, int32_t max_ctx);
 
-// fp32 attention, one query row per workgroup.  Rows [L][B][n_q][Hq]: query token i of
-// request b sits at position pos(b, i) and sees slots [0, that position]; rows without a
-// position are left untouched.
-hipError_t launch_attn_rows_f32(const AttnShape& s, const float* q, const float* cache_k,
-                                const float* cache_v, const RowPos& pos, int32_t n_q, float* out,
-                                hipStream_t stream);
+// Row-wise attention (float32 caches; bf16 caches at head_dim 64), one query row per
+// workgroup.  Rows [L][B][n_q][Hq]: query token i of request b sits at position pos(b, i) and
+// sees slots [0, that position]; rows without a position are left untouched.  Options (bf16):
+// q_table turns each query to its position first (fused RoPE); pool_k non-NULL reads context
+// slots below clamp(ctx_len[b], max_ctx) from the pool through the slot map, keys turned by
+// the slot's shift with k_table (zero-copy composition).
+template <typename T>
+struct RowArgs {
+  AttnShape s;
+  const T* q = nullptr;
+  const T* cache_k = nullptr;
+  const T* cache_v = nullptr;
+  RowPos pos;
+  int32_t n_q = 0;
+  T* out = nullptr;
+  const float2* q_table = nullptr;   // [L or 1][max_abs_delta + 1][D/2], block l at l * table_stride
+  const float2* k_table = nullptr;
+  int64_t table_stride = 0;
+  int32_t max_abs_delta = 0;
+  bool interleaved = false;
+  const T* pool_k = nullptr;         // [L][Hkv][pool_tokens][D]
+  const T* pool_v = nullptr;
+  int64_t pool_tokens = 0;
+  const int32_t* smap = nullptr;     // [B][map_cap]
+  const int32_t* dmap = nullptr;
+  int32_t map_cap = 0;
+  const int32_t* ctx_len = nullptr;
+  int32_t max_ctx = 0;
+  hipStream_t stream = nullptr;
+};
+hipError_t launch_attn_rows(const RowArgs<float>& a);
+hipError_t launch_attn_rows(const RowArgs<bf16_t>& a);
+
+// launch_append for bf16 rows whose keys are turned to their slot's position on the way
+// (fused RoPE of request-time keys; the re-rotation kernel's arithmetic); values copied.
+hipError_t launch_append_rope(int head_dim, bool interleaved, int n_layers, int n_kv_heads,
+                              const bf16_t* k_new, const bf16_t* v_new, bf16_t* cache_k,
+                              bf16_t* cache_v, int32_t batch, int32_t cache_cap, const RowPos& pos,
+                              int32_t n_new, const float2* table, int64_t table_stride,
+                              int32_t max_abs_delta, hipStream_t stream);
 
 size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_ctx);
 // Also writes k_suf / v_suf into cache slots [ctx_len[b], ctx_len[b] + n_suffix).
@@ -163,6 +197,8 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
                                      void* workspace, size_t ws_bytes, hipStream_t stream);
 
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len);
+// Workgroups per (request, kv head, split) of the decode: one per group of up to 16 query heads.
+inline int32_t decode_head_groups(const AttnShape& s) { return (s.n_q_heads / s.n_kv_heads + 15) / 16; }
 // The decode scratch array (split-K partials of the allocation-free entry point): its size,
 // and the current device's copy of it (looked up on the first call on that device).
 size_t decode_scratch_bytes();

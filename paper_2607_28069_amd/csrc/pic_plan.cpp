@@ -46,11 +46,12 @@ size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_
 
 int32_t slot_map_tiles(int32_t map_cap) { return (int32_t)(((int64_t)map_cap + kPrefillKeys - 1) / kPrefillKeys); }
 
-// Decode workgroups per (request, kv head): enough 4-wave workgroups for one per compute unit
+// Decode workgroups per (request, kv head, group of 16 query heads): enough 4-wave workgroups
+// for one per compute unit
 // (256 per launch; measured faster than two per unit on split launches), each wave keeping at
 // least kDecodeMinWaveKeys keys.
 int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len) {
-  const int64_t pairs = (int64_t)s.batch * s.n_kv_heads * s.n_layers;
+  const int64_t pairs = (int64_t)s.batch * s.n_kv_heads * s.n_layers * decode_head_groups(s);
   int64_t splits = (256 + pairs - 1) / pairs;
   const int64_t per_split = (int64_t)kDecodeWaves * kDecodeMinWaveKeys;
   const int64_t max_splits = (max_len + per_split - 1) / per_split;

@@ -467,6 +467,49 @@ __global__ void __launch_bounds__(256) append_kernel(const T* __restrict__ k_new
   }
 }
 
+// append_kernel for bf16 rows whose keys are turned to their slot's position on the way, with
+// rerotate_kernel's arithmetic (table block of layer l at table + l * table_stride); one
+// (row, chunk pair) per thread, values copied as they are.
+template <int HD, bool IL>
+__global__ void __launch_bounds__(256) append_rope_kernel(const bf16_t* __restrict__ k_new,
+                                                          const bf16_t* __restrict__ v_new,
+                                                          bf16_t* __restrict__ cache_k, bf16_t* __restrict__ cache_v,
+                                                          int n_kv_heads, int32_t batch, int32_t cache_cap,
+                                                          RowPos pos, int32_t n_new, int64_t n_rows,
+                                                          const float2* __restrict__ table, int64_t table_stride,
+                                                          int32_t max_abs_delta) {
+  using V = Vec16<bf16_t>;
+  constexpr int VEC = V::N;
+  constexpr int HALF = HD / 2;
+  constexpr int LPR = HALF / VEC;
+  const int64_t n_items = n_rows * LPR;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n_items;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = idx / LPR;
+    const int c0 = (int)(idx - row * LPR) * VEC;
+    // row = ((l * B + b) * n_new + i) * Hkv + h
+    const int h = (int)(row % n_kv_heads);
+    const int64_t r1 = row / n_kv_heads;
+    const int i = (int)(r1 % n_new);
+    const int64_t lb = r1 / n_new;  // l * B + b
+    const int b = (int)(lb % batch);
+    const int l = (int)(lb / batch);
+    const int64_t slot = pos(b, i);
+    if (slot < 0 || slot >= cache_cap) continue;
+    float cs[VEC], sn[VEC], x1[VEC], x2[VEC];
+    load_cs<VEC, HALF>(table + l * table_stride, (int32_t)(slot < max_abs_delta ? slot : max_abs_delta), c0, cs, sn);
+    const int o1 = off1<VEC, HALF, IL>(c0), o2 = off2<VEC, HALF, IL>(c0);
+    V::load(k_new + row * HD + o1, x1);
+    V::load(k_new + row * HD + o2, x2);
+    rotate<VEC, IL>(x1, x2, cs, sn);
+    const int64_t dst = ((lb * n_kv_heads + h) * cache_cap + slot) * HD;
+    V::store(cache_k + dst + o1, x1);
+    V::store(cache_k + dst + o2, x2);
+    V::store_raw(cache_v + dst + o1, V::load_raw(v_new + row * HD + o1));
+    V::store_raw(cache_v + dst + o2, V::load_raw(v_new + row * HD + o2));
+  }
+}
+
 int grid_for(int64_t items, int threads) {
   int64_t g = (items + threads - 1) / threads;
   if (g < 1) g = 1;
@@ -593,6 +636,26 @@ hipError_t launch_append(pic_dtype dt, int head_dim, int n_layers, int n_kv_head
                        stream, (const T*)k_new, (const T*)v_new, (T*)cache_k, (T*)cache_v,
                        n_kv_heads, batch, cache_cap, pos, n_new, n_rows);
   });
+  return hipGetLastError();
+}
+
+hipError_t launch_append_rope(int head_dim, bool interleaved, int n_layers, int n_kv_heads,
+                              const bf16_t* k_new, const bf16_t* v_new, bf16_t* cache_k,
+                              bf16_t* cache_v, int32_t batch, int32_t cache_cap, const RowPos& pos,
+                              int32_t n_new, const float2* table, int64_t table_stride,
+                              int32_t max_abs_delta, hipStream_t stream) {
+  const int64_t n_rows = (int64_t)n_layers * batch * n_new * n_kv_heads;
+  if (n_rows == 0) return hipSuccess;
+  const dim3 grid(grid_for(n_rows * (head_dim / 16), 256));
+#define PIC_APPEND_ROPE(HDV, ILV)                                                                    \
+  hipLaunchKernelGGL((append_rope_kernel<HDV, ILV>), grid, dim3(256), 0, stream, k_new, v_new, cache_k, \
+                     cache_v, n_kv_heads, batch, cache_cap, pos, n_new, n_rows, table, table_stride,  \
+                     max_abs_delta)
+  if (head_dim == 64 && interleaved) PIC_APPEND_ROPE(64, true);
+  else if (head_dim == 64) PIC_APPEND_ROPE(64, false);
+  else if (interleaved) PIC_APPEND_ROPE(128, true);
+  else PIC_APPEND_ROPE(128, false);
+#undef PIC_APPEND_ROPE
   return hipGetLastError();
 }
 

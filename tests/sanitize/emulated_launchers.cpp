@@ -161,29 +161,65 @@ hipError_t launch_append(pic_dtype dt, int head_dim, int n_layers, int n_kv_head
   return hipSuccess;
 }
 
-hipError_t launch_attn_rows_f32(const AttnShape& s, const float* q, const float* cache_k, const float* cache_v,
-                                const RowPos& pos, int32_t n_q, float* out, hipStream_t) {
-  ++emu::launches;
-  const int HD = s.head_dim, Hq = s.n_q_heads, Hkv = s.n_kv_heads;
+namespace {
+template <typename T>
+hipError_t rows_walk(const RowArgs<T>& a) {
+  const AttnShape& s = a.s;
+  const int HD = s.head_dim, Hq = s.n_q_heads, Hkv = s.n_kv_heads, n_q = a.n_q;
   const int64_t rows = (int64_t)s.batch * n_q * Hq;
+  if (rows == 0 || s.n_layers == 0) return hipSuccess;
+  ++emu::launches;
   for (int l = 0; l < s.n_layers; ++l)
     for (int64_t row = 0; row < rows; ++row) {
       const int h = (int)(row % Hq), i = (int)((row / Hq) % n_q), b = (int)(row / ((int64_t)Hq * n_q));
       const int g = h / (Hq / Hkv);
-      const int64_t qpos = pos(b, i);
+      const int64_t qpos = a.pos(b, i);
       if (qpos < 0) continue;
       int64_t n_vis = qpos + 1;
       if (n_vis > s.cache_cap) n_vis = s.cache_cap;
       const int64_t qrow = (int64_t)l * s.batch * n_q * Hq + row;
-      emu::rd(q, qrow, HD);
+      emu::rd(a.q, qrow, HD);
+      if (a.q_table) rd_row(a.q_table + l * a.table_stride, std::min<int64_t>(qpos, a.max_abs_delta), (int64_t)HD / 2 * 8);
       const int64_t kv0 = (((int64_t)l * s.batch + b) * Hkv + g) * s.cache_cap;
+      const int32_t ctx = a.pool_k ? clamp_len(a.ctx_len[b], a.max_ctx) : 0;
       for (int64_t j = 0; j < n_vis; ++j) {
-        emu::rd(cache_k, kv0 + j, HD);
-        emu::rd(cache_v, kv0 + j, HD);
+        if (a.pool_k && j < ctx) {
+          const int32_t src = clamp_pool_token(a.smap[(int64_t)b * a.map_cap + j], a.pool_tokens);
+          const int32_t dl = clamp_delta(a.dmap[(int64_t)b * a.map_cap + j], a.max_abs_delta);
+          rd_row(a.k_table + l * a.table_stride, iabs(dl), (int64_t)HD / 2 * 8);
+          emu::rd(a.pool_k, ((int64_t)l * Hkv + g) * a.pool_tokens + src, HD);
+          emu::rd(a.pool_v, ((int64_t)l * Hkv + g) * a.pool_tokens + src, HD);
+        } else {
+          emu::rd(a.cache_k, kv0 + j, HD);
+          emu::rd(a.cache_v, kv0 + j, HD);
+        }
       }
-      emu::wr(out, qrow, HD);
+      emu::wr(a.out, qrow, HD);
     }
   return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_attn_rows(const RowArgs<float>& a) { return rows_walk(a); }
+hipError_t launch_attn_rows(const RowArgs<bf16_t>& a) { return rows_walk(a); }
+
+hipError_t launch_append_rope(int head_dim, bool, int n_layers, int n_kv_heads, const bf16_t* k_new,
+                              const bf16_t* v_new, bf16_t* cache_k, bf16_t* cache_v, int32_t batch,
+                              int32_t cache_cap, const RowPos& pos, int32_t n_new, const float2* table,
+                              int64_t table_stride, int32_t max_abs_delta, hipStream_t stream) {
+  const int64_t n_rows = (int64_t)n_layers * batch * n_new * n_kv_heads;
+  if (n_rows == 0) return hipSuccess;
+  for (int64_t row = 0; row < n_rows; ++row) {   // the table row of each placed key
+    const int64_t r1 = row / n_kv_heads;
+    const int i = (int)(r1 % n_new);
+    const int64_t lb = r1 / n_new;
+    const int b = (int)(lb % batch), l = (int)(lb / batch);
+    const int64_t slot = pos(b, i);
+    if (slot < 0 || slot >= cache_cap) continue;
+    rd_row(table + l * table_stride, std::min<int64_t>(slot, max_abs_delta), (int64_t)head_dim / 2 * 8);
+  }
+  return launch_append(PIC_BF16, head_dim, n_layers, n_kv_heads, k_new, v_new, cache_k, cache_v, batch, cache_cap,
+                       pos, n_new, stream);
 }
 
 // ---- bf16 prefill: one walk serves every mode of prefill_bf16_kernel ----
@@ -489,22 +525,24 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   int32_t chunk = (max_len + n_splits - 1) / n_splits;
   chunk = (chunk + kDecodeWaves * kTile - 1) / (kDecodeWaves * kTile) * (kDecodeWaves * kTile);
   const int n_rep = s.n_q_heads / s.n_kv_heads;
+  const int groups = decode_head_groups(s);
   for (int l = 0; l < s.n_layers; ++l)
-    for (int x = 0; x < n_splits * s.batch * s.n_kv_heads; ++x) {
-      const int split = x % n_splits, bg = x / n_splits;
+    for (int x = 0; x < groups * n_splits * s.batch * s.n_kv_heads; ++x) {
+      const int hgrp = x % groups, split = (x / groups) % n_splits, bg = x / (groups * n_splits);
+      const int rep0 = 16 * hgrp, n_here = std::min(16, n_rep - rep0);
       const int b = bg / s.n_kv_heads, g = bg % s.n_kv_heads;
       const int p = clamp_len(base_len[b], max_base) + step;
       const int n_vis = std::min(p + 1, s.cache_cap);
       const int wc0 = std::min(split * chunk, n_vis), wc1 = std::min(wc0 + chunk, n_vis);
       const int64_t bh_kv = ((int64_t)l * s.batch + b) * s.n_kv_heads + g;
-      if (p < s.cache_cap && p >= wc0 && p < wc1) {
+      if (hgrp == 0 && p < s.cache_cap && p >= wc0 && p < wc1) {
         rd_row(k_new, bh_kv, kRB);
         rd_row(v_new, bh_kv, kRB);
         wr_row(cache_k, bh_kv * s.cache_cap + p, kRB);
         wr_row(cache_v, bh_kv * s.cache_cap + p, kRB);
       }
       if (rope_table) rd_row(rope_table + l * table_stride, std::min(p, max_abs_delta), (int64_t)kAttnHeadDim / 2 * 8);
-      for (int n = 0; n < n_rep; ++n) rd_row(q, ((int64_t)l * s.batch + b) * s.n_q_heads + g * n_rep + n, kRB);
+      for (int n = 0; n < n_here; ++n) rd_row(q, ((int64_t)l * s.batch + b) * s.n_q_heads + g * n_rep + rep0 + n, kRB);
       const int sub = chunk / kDecodeWaves;
       for (int w = 0; w < kDecodeWaves; ++w) {
         const int c0 = std::min(wc0 + w * sub, wc1), c1 = std::min(c0 + sub, wc1);
@@ -520,8 +558,8 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
             }
           }
       }
-      for (int n = 0; n < n_rep; ++n) {
-        const int64_t row = ((int64_t)l * s.batch + b) * s.n_q_heads + g * n_rep + n;
+      for (int n = 0; n < n_here; ++n) {
+        const int64_t row = ((int64_t)l * s.batch + b) * s.n_q_heads + g * n_rep + rep0 + n;
         if (n_splits == 1) {
           wr_row(out, row, kRB);
         } else {

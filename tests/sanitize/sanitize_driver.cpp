@@ -248,8 +248,8 @@ void planted_short_cache() {
 void fuzz_attention() {
   for (int it = 0; it < 40; ++it) {
     const bool bf16 = rnd(0, 3) != 0;
-    const int D = bf16 ? 128 : (rnd(0, 1) ? 64 : 128);
-    const int Hkv = (int)rnd(1, 2), rep = bf16 ? (int)rnd(1, 7) : (int)rnd(1, 3);
+    const int D = rnd(0, 2) ? 128 : 64;
+    const int Hkv = (int)rnd(1, 2), rep = bf16 ? (rnd(0, 4) ? (int)rnd(1, 7) : (int)rnd(17, 40)) : (int)rnd(1, 3);
     pic_model m = model((int)rnd(1, 2), Hkv * rep, Hkv, D, bf16 ? PIC_BF16 : PIC_F32);
     const int L = m.n_layers;
     const int32_t batch = (int32_t)rnd(1, 3), n_suf = (int32_t)rnd(1, 70), max_ctx = (int32_t)rnd(0, bf16 ? 3000 : 300);
@@ -283,10 +283,10 @@ void fuzz_attention() {
       for (int b = 0; b < batch; ++b) base.as<int32_t>()[b] = garbage(dmax + 1);
       const int32_t splits = bf16 ? (int32_t)rnd(0, 9) : 0;
       Buf dws(pic_decode_workspace_bytes(&m, batch, dmax + step + 1, splits));
-      if (bf16 && rep <= 16)
+      if (bf16)
         EXPECT(pic_decode_attn(&m, dq.p, kn.p, vn.p, ck.p, cv.p, batch, cap, base.as<int32_t>(), step, dmax, 0.f,
                                splits, dout.p, dws.n ? dws.p : nullptr, dws.n, nullptr) == PIC_OK);
-      if (bf16 && rep <= 16)   // the allocation-free entry point: partials in the scratch array
+      if (bf16)   // the allocation-free entry point: partials in the scratch array
         EXPECT(pic_decode_attn_noalloc(&m, dq.p, kn.p, vn.p, ck.p, cv.p, batch, cap, base.as<int32_t>(), step, dmax,
                                        0.f, splits, dout.p, nullptr) == PIC_OK);
       if (!bf16)

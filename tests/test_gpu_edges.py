@@ -73,3 +73,41 @@ def test_calls_with_nothing_to_do_leave_outputs_untouched():
     pic.pic_compose(m, ck, cv, 16, ctx, 0, ctx, 16, ck, cv, 2, 16)                    # no blocks
     torch.cuda.synchronize()
     assert torch.all(out == 3.0) and torch.all(ck == 5.0) and torch.all(cv == 5.0)
+
+
+@pytest.mark.parametrize("n_q_heads,n_splits", [(40, 0), (40, 3), (64, 1)])
+def test_decode_more_than_16_query_heads_per_kv_head(n_q_heads, n_splits):
+    # 20 and 32 query heads per kv head: the decode serves them in groups of 16 (one workgroup
+    # per group, each streaming the context), with and without key splits; every head of every
+    # request against the oracle, and the no-workspace entry point bit-identical
+    w = dataclasses.replace(synth.get("c2"), name="wide_gqa", n_q_heads=n_q_heads, n_kv_heads=2, pool_docs=4,
+                            doc_len=300, docs_per_request=3, n_suffix=5, prefix_len=0, batch=3, decode_steps=2)
+    r = setup(w)
+    gpu_compose(r)
+    out = host(gpu_prefill(r))[0]
+    for b in range(w.batch):
+        ref, _, _ = oracle_prefill(r, b)
+        assert_attn_close(out[b], ref, "bf16")
+    ck0, cv0 = r.dev["cache_k"].clone(), r.dev["cache_v"].clone()
+    outs = [host(o)[0] for o in gpu_decode(r, 2, n_splits=n_splits)]
+    for b in range(w.batch):
+        _, K, V = oracle_prefill(r, b)
+        length = r.ctx[b] + w.n_suffix
+        for t in range(2):
+            ref, K, V = O.decode_step(K, V, length, r.inp["dq"][t][b], r.inp["dk"][t][b], r.inp["dv"][t][b])
+            length += 1
+            assert_attn_close(outs[t][b], ref, "bf16")
+    # the same two steps through pic_decode_attn_noalloc on the prefilled caches
+    ck, cv = ck0, cv0
+    base = torch.from_numpy((r.ctx + w.n_suffix).astype(np.int32)).to(DEV)
+    max_base = int((r.ctx + w.n_suffix).max())
+    for t in range(2):
+        q = to_dev(r.inp["dq"][t][None], torch.bfloat16)
+        k = to_dev(r.inp["dk"][t][None], torch.bfloat16)
+        v = to_dev(r.inp["dv"][t][None], torch.bfloat16)
+        o = torch.zeros((1, w.batch, w.n_q_heads, w.head_dim), dtype=torch.bfloat16, device=DEV)
+        pic.pic_decode_attn_noalloc(r.model, q, k, v, ck, cv, w.batch, r.cap, base, t, max_base, o,
+                                    n_splits=n_splits)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(o)[0], outs[t]), t
+    assert torch.equal(ck, r.dev["cache_k"]) and torch.equal(cv, r.dev["cache_v"])
