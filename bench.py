@@ -59,9 +59,10 @@ def parse(argv=None):
                         "its pool row) instead of grouping blocks that share a document run")
     p.add_argument("--no-extra", action="store_true",
                    help="skip the extra workload legs (profiling runs of one workload)")
-    p.add_argument("--extra", default="c5,c4,rerotate",
-                   help="extra legs after the headline: workloads (their own short step counts) and "
-                        "'rerotate' (standalone key re-rotation)")
+    p.add_argument("--extra", default="c5,c4,rerotate,copy",
+                   help="extra legs after the headline: workloads (their own short step counts), "
+                        "'rerotate' (standalone key re-rotation) and 'copy' (plain device copy and "
+                        "fill rates for reference)")
     p.add_argument("--copy-calib-gib", type=float, default=0.0,
                    help="also run a plain device copy of this size per step (counter calibration)")
     return p.parse_args(argv)
@@ -633,6 +634,34 @@ def rerotate_leg(dev, reps=10, warmup=3):
             "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
 
 
+def copy_leg(dev, gib=4, reps=10, warmup=3):
+    """Reference rates of plain streaming on this GPU, beside which the compose figures read: a
+    device-to-device copy of `gib` GiB (torch's copy kernel; bytes moved = read + write) and a
+    write-only fill of the same buffer.  Timed with HIP events on the launch stream."""
+    import torch
+
+    n = int(gib * (1 << 30)) // 2
+    src = torch.empty(n, dtype=torch.bfloat16, device=dev).normal_()
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {"bytes": 2 * n, "unit": "GB/s"}
+    for name, fn, moved in (("copy", lambda: dst.copy_(src), 4 * n), ("fill", lambda: dst.fill_(1.0), 2 * n)):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[f"{name}_ms"] = ms
+        out[f"{name}_gbps"] = moved / (ms * 1e-3) / 1e9
+    del src, dst
+    return out
+
+
 def _brief(name, fig):
     """The figures of one extra workload leg, flattened for the JSON line."""
     k = fig["kernels"]
@@ -724,6 +753,8 @@ def main():
     for name in extras:
         if name == "rerotate":
             legs["rerotate_keys"] = rerotate_leg(dev)
+        elif name == "copy":
+            legs["device_copy"] = copy_leg(dev)
         else:
             we = synth.get(name)
             if we.name == w.name:
@@ -740,7 +771,8 @@ def main():
         res["extra_workloads"] = legs
         for name, leg in legs.items():   # flat copies of the headline figures of each leg
             for key in ("ttft_ms_per_request", "ttft_ms_single_request", "prefill_tflops", "prefill_frac",
-                        "compose_ms", "compose_frac", "decode_gbps", "decode_frac", "achieved", "frac"):
+                        "compose_ms", "compose_frac", "decode_gbps", "decode_frac", "achieved", "frac",
+                        "copy_gbps", "fill_gbps"):
                 if leg.get(key) is not None:
                     res[f"{name}_{key}"] = leg[key]
     print(json.dumps(res), flush=True)

@@ -8,8 +8,8 @@ namespace pic {
 // Key-range splits of the prefill: enough workgroups to cover the 256 compute units in whole
 // rounds, each split keeping at least 8 key tiles.  Cost in units of one workgroup-tile
 // (~2 us): rounds * tiles per split, plus, for split runs, one tile (the combine launch; the
-// splits' own prologues run in parallel) and the fp32 partials each split writes and the
-// combine reads back (264 bytes per query row, twice, at ~4 TB/s).  Ties (within 3%) go to
+// splits' own prologues run in parallel) and the partials each split writes and the combine
+// reads back (bf16 output and fp32 (max, sum): 264 bytes per query row, twice, at ~4 TB/s).  Ties (within 3%) go to
 // fewer splits.
 SplitPlan plan_prefill_splits(const AttnShape& s, int32_t n_suffix, int32_t max_ctx) {
   SplitPlan p;
