@@ -204,6 +204,8 @@ class DeviceWorkload:
         self.mad = self.cap
         self.table = torch.empty(pic.pic_rope_table_bytes(self.model, self.mad) // 4, dtype=torch.float32,
                                  device=dev)
+        # floats per layer's table block with one table per layer (else every layer reads block 0)
+        self.table_block = (self.mad + 1) * (D // 2) * 2 if self.model.rope_tables > 1 else 0
         if w.rope_scaling == "llama3":
             pic.pic_rope_table_init_freq(self.model, pic.pic_rope_llama3_freq(D, w.rope_theta), self.mad,
                                          self.table)
@@ -274,15 +276,86 @@ class DeviceWorkload:
             pos_dev.view(-1)[: inl.size].copy_(tail, non_blocking=True)
         return nb, ng
 
-    def compose(self, blocks_dev, groups_dev, nb, ng, cache_k, cache_v, batch):
+    def compose(self, blocks_dev, groups_dev, nb, ng, cache_k, cache_v, batch, layers=None, stream=None):
+        """One compose launch over layers [l0, l1) (default: all): the pool, caches and (per-layer)
+        tables from layer l0 on, with the model restricted to those layers."""
         import paper_2607_28069_amd as pic
 
+        l0, l1 = layers if layers is not None else (0, self.L)
+        m = self.model if (l0, l1) == (0, self.L) else self.model.with_layers(l1 - l0)
+        tab = self.table[l0 * self.table_block:]
+        pk, pv, ck, cv = self.pool_k[l0:l1], self.pool_v[l0:l1], cache_k[l0:l1], cache_v[l0:l1]
         if self.shared_compose:
-            pic.pic_compose_shared(self.model, self.pool_k, self.pool_v, self.lay.pool_tokens, blocks_dev, nb,
-                                   groups_dev, ng, self.table, self.mad, cache_k, cache_v, batch, self.cap)
+            pic.pic_compose_shared(m, pk, pv, self.lay.pool_tokens, blocks_dev, nb, groups_dev, ng, tab, self.mad,
+                                   ck, cv, batch, self.cap, stream=stream)
         else:
-            pic.pic_compose(self.model, self.pool_k, self.pool_v, self.lay.pool_tokens, blocks_dev, nb,
-                            self.table, self.mad, cache_k, cache_v, batch, self.cap)
+            pic.pic_compose(m, pk, pv, self.lay.pool_tokens, blocks_dev, nb, tab, self.mad, ck, cv, batch, self.cap,
+                            stream=stream)
+
+    def plan_upload(self):
+        """Host plan of the batch and the asynchronous copy of its gather blocks: (n_blocks, n_groups)."""
+        import paper_2607_28069_amd as pic
+
+        lay = self.lay
+        if self.frontier:
+            blocks, _, inl, _ = pic.pic_plan_frontier(lay.items, lay.doc_offset, lay.doc_len,
+                                                      lay.doc_compile_pos, lay.pool_tokens)
+        else:
+            blocks, _ = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len,
+                                            lay.doc_compile_pos, lay.pool_tokens)
+        return self.upload(blocks, self.blocks_pinned, self.blocks_dev, self.groups_dev,
+                           inl if self.frontier else None, self.pos_dev if self.frontier else None)
+
+    def prefill_layer(self, l):
+        """Layer l's prefill call over the batch (the mode of this workload)."""
+        import paper_2607_28069_amd as pic
+
+        w, B, Ls, lay, block = self.w, self.w.batch, self.Ls, self.lay, self.table_block
+        if self.paged:
+            pic.pic_paged_prefill_attn(self.m1, self.pool_k[l], self.pool_v[l], lay.pool_tokens,
+                                       self.slot_src, self.slot_delta, self.slot_src.shape[1],
+                                       self.table[l * block:], self.mad, self.q[l],
+                                       self.k_suf[l], self.v_suf[l], self.cache_k[l], self.cache_v[l], B,
+                                       self.cap, self.ctx_dev, self.max_ctx, Ls, self.out[l], self.ws_pre,
+                                       tile_map=self.tile_map)
+        elif self.frontier:
+            pic.pic_frontier_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
+                                          self.cache_k[l], self.cache_v[l], B, self.cap,
+                                          self.pos_dev, self.n_valid_dev, Ls, self.max_len,
+                                          self.out[l], self.ws_pre)
+        elif self.fused_rope:
+            pic.pic_suffix_prefill_attn_rope(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
+                                             self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
+                                             self.max_ctx, Ls, self.table[l * block:], self.mad, self.out[l],
+                                             self.ws_pre)
+        else:
+            pic.pic_suffix_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
+                                        self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
+                                        self.max_ctx, Ls, self.out[l], self.ws_pre)
+
+    def ttft_overlapped(self, nb, ng, side, events, chunk):
+        """The TTFT launches with composition overlapped with prefill (composed-cache workloads):
+        layers are composed `chunk` at a time, the first chunk on the current stream and the
+        rest on `side`, and the prefill of layer l, on the current stream, waits only for its own
+        chunk, so later layers are composed while earlier ones are prefilled.  Same kernels,
+        inputs and results as the sequential order.  `events` holds L + 1 events."""
+        import torch
+
+        main, L, B = torch.cuda.current_stream(), self.L, self.w.batch
+        events[L].record(main)
+        side.wait_event(events[L])
+        for c0 in range(0, L, chunk):
+            s = main if c0 == 0 else side
+            self.compose(self.blocks_dev, self.groups_dev, nb, ng, self.cache_k, self.cache_v, B,
+                         layers=(c0, min(L, c0 + chunk)), stream=s)
+            events[c0].record(s)
+        for l in range(L if self.Ls else 0):
+            if l and l % chunk == 0:
+                main.wait_event(events[l])
+            self.prefill_layer(l)
+        if not self.Ls:   # nothing to prefill: join the side stream
+            for c0 in range(chunk, L, chunk):
+                main.wait_event(events[c0])
 
     def step(self, rec: dict | None = None, calib=None):
         """One pass of the path; with `rec`, appends timings (ms) to its lists."""
@@ -297,48 +370,20 @@ class DeviceWorkload:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         # -- TTFT region
-        lay = self.lay
-        if self.frontier:
-            blocks, _, inl, _ = pic.pic_plan_frontier(lay.items, lay.doc_offset, lay.doc_len,
-                                                      lay.doc_compile_pos, lay.pool_tokens)
-        else:
-            blocks, _ = pic.pic_plan_layout(lay.requests, lay.doc_offset, lay.doc_len,
-                                            lay.doc_compile_pos, lay.pool_tokens)
-        nb, ng = self.upload(blocks, self.blocks_pinned, self.blocks_dev, self.groups_dev,
-                             inl if self.frontier else None, self.pos_dev if self.frontier else None)
+        nb, ng = self.plan_upload()
         e0, e1 = ev(), ev()
         if not self.paged:
             e0.record(stream)
             self.compose(self.blocks_dev, self.groups_dev, nb, ng, self.cache_k, self.cache_v, B)
             e1.record(stream)
-        block = (self.mad + 1) * (w.head_dim // 2) * 2 if self.model.rope_tables > 1 else 0
+        block = self.table_block
         if self.paged:   # the token-level slot map, shared by every layer
             pic.pic_build_slot_map(self.blocks_dev, nb, B, self.slot_src.shape[1], self.slot_src,
                                    self.slot_delta, self.tile_map)
         p0, p1 = ev(), ev()
         p0.record(stream)
         for l in range(L if Ls else 0):
-            if self.paged:
-                pic.pic_paged_prefill_attn(self.m1, self.pool_k[l], self.pool_v[l], lay.pool_tokens,
-                                           self.slot_src, self.slot_delta, self.slot_src.shape[1],
-                                           self.table[l * block:], self.mad, self.q[l],
-                                           self.k_suf[l], self.v_suf[l], self.cache_k[l], self.cache_v[l], B,
-                                           self.cap, self.ctx_dev, self.max_ctx, Ls, self.out[l], self.ws_pre,
-                                           tile_map=self.tile_map)
-            elif self.frontier:
-                pic.pic_frontier_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
-                                              self.cache_k[l], self.cache_v[l], B, self.cap,
-                                              self.pos_dev, self.n_valid_dev, Ls, self.max_len,
-                                              self.out[l], self.ws_pre)
-            elif self.fused_rope:
-                pic.pic_suffix_prefill_attn_rope(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
-                                                 self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
-                                                 self.max_ctx, Ls, self.table[l * block:], self.mad, self.out[l],
-                                                 self.ws_pre)
-            else:
-                pic.pic_suffix_prefill_attn(self.m1, self.q[l], self.k_suf[l], self.v_suf[l],
-                                            self.cache_k[l], self.cache_v[l], B, self.cap, self.ctx_dev,
-                                            self.max_ctx, Ls, self.out[l], self.ws_pre)
+            self.prefill_layer(l)
         p1.record(stream)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
@@ -375,7 +420,34 @@ class DeviceWorkload:
                 rec["decode"].append(d0.elapsed_time(d1) / (L * self.n_dec))
 
 
-def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
+OVERLAP_CHUNK_BATCH = 1   # layers per compose launch when compose overlaps prefill: a batch
+OVERLAP_CHUNK_LONE = 4    # ... and a request served alone (fewer, longer launches)
+
+
+def overlapped_batch_ttft(wl, reps: int = 10, chunk: int = OVERLAP_CHUNK_BATCH):
+    """TTFT of the batch with composition overlapped with prefill (DeviceWorkload.ttft_overlapped),
+    host-timed like the steps' TTFT region: plan through the last prefill, between two device
+    synchronisations.  Returns the median ms per batch over `reps` runs after one untimed run,
+    or None where compose is not on the TTFT path (zero-copy) or nothing is prefilled."""
+    import torch
+
+    if wl.paged or not wl.Ls:
+        return None
+    side = torch.cuda.Stream()
+    events = [torch.cuda.Event() for _ in range(wl.L + 1)]
+    times = []
+    for r in range(reps + 1):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        nb, ng = wl.plan_upload()
+        wl.ttft_overlapped(nb, ng, side, events, chunk)
+        torch.cuda.current_stream().synchronize()
+        if r:
+            times.append((time.perf_counter() - t0) * 1e3)
+    return float(statistics.median(times))
+
+
+def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
     """TTFT (ms) of requests served alone, batch 1: the paper's per-request synchronized wall
     clock (App. C.2), where the batched figure divides a batch's time by its size.
 
@@ -384,9 +456,13 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
     untimed pass; the pool, suffix inputs and rotary table are those of the batched workload.
     A lone request's per-layer launches are short, so the launch sequence after the plan is
     also recorded once per request as a HIP graph and replayed (the plan and the copy of its
-    gather blocks stay in the timed region).  Returns the medians over all samples (eager,
-    graph replay): an occasional host stall of tens of milliseconds, seen on either path,
-    moves a 20-sample mean by several percent."""
+    gather blocks stay in the timed region).  Composed-cache workloads are also timed with
+    composition overlapped with prefill (chunks of OVERLAP_CHUNK_LONE layers composed on a
+    second stream, each layer's prefill waiting for its own chunk; `chunks` picks the schedules:
+    0 = sequential, n = overlapped in chunks of n layers).  Returns the medians over
+    all samples (eager, graph replay, overlapped eager, overlapped graph replay; the last two
+    None for zero-copy workloads): an occasional host stall of tens of milliseconds, seen on
+    either path, moves a 20-sample mean by several percent."""
     import numpy as np
     import torch
 
@@ -394,8 +470,10 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
 
     w, L, Ls, dev = wl.w, wl.L, wl.Ls, wl.dev
     if Ls == 0:
-        return None, None
+        return None, None, None, None
     lay, D, Hkv = wl.lay, w.head_dim, w.n_kv_heads
+    side = torch.cuda.Stream()
+    events = [torch.cuda.Event() for _ in range(L + 1)]
     cache_k = torch.zeros((L, 1, Hkv, wl.cap, D), dtype=wl.dt, device=dev)
     cache_v = torch.zeros_like(cache_k)
     if wl.frontier:
@@ -425,12 +503,23 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
         nb, ng = wl.upload(blocks, pinned, blocks_dev, groups_dev, inl if wl.frontier else None, pos_dev)
         return nb, ng, n_keys
 
-    def launches(views, ctx_i, nv_i, nb, ng, n_keys):   # compose (or slot map) + every layer's prefill
+    def launches(views, ctx_i, nv_i, nb, ng, n_keys, chunk=0):   # compose (or slot map) + every layer's prefill
+        main = torch.cuda.current_stream()   # the capture stream while a graph is recorded
         if wl.paged:
             pic.pic_build_slot_map(blocks_dev, nb, 1, slot_src.shape[1], slot_src, slot_delta, tile_map)
+        elif chunk:   # chunks of layers; all but the first on the side stream
+            events[L].record(main)
+            side.wait_event(events[L])
+            for c0 in range(0, L, chunk):
+                s = main if c0 == 0 else side
+                wl.compose(blocks_dev, groups_dev, nb, ng, cache_k, cache_v, 1, layers=(c0, min(L, c0 + chunk)),
+                           stream=s)
+                events[c0].record(s)
         else:
             wl.compose(blocks_dev, groups_dev, nb, ng, cache_k, cache_v, 1)
-        for q, k, v, ck, cv, out, pk, pv, tab in views:
+        for l, (q, k, v, ck, cv, out, pk, pv, tab) in enumerate(views):
+            if chunk and l and l % chunk == 0:
+                main.wait_event(events[l])
             if wl.paged:
                 pic.pic_paged_prefill_attn(wl.m1, pk, pv, lay.pool_tokens, slot_src, slot_delta,
                                            slot_src.shape[1], tab, wl.mad, q, k, v, ck, cv, 1, wl.cap,
@@ -444,7 +533,9 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
             else:
                 pic.pic_suffix_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, ctx_i, n_keys, Ls, out, ws)
 
-    eager, graphed = [], []
+    if chunks is None:
+        chunks = [0] if wl.paged else [0, OVERLAP_CHUNK_LONE]
+    eager, graphed = {c: [] for c in chunks}, {c: [] for c in chunks}
     stream = torch.cuda.current_stream()
     for i in range(min(n_requests, w.batch)):
         sl = slice(i, i + 1)
@@ -452,28 +543,32 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5):
         views = [(wl.q[l][sl], wl.k_suf[l][sl], wl.v_suf[l][sl], cache_k[l], cache_v[l], wl.out[l][sl],
                   wl.pool_k[l], wl.pool_v[l], wl.table[l * block:]) for l in range(L)]
         ctx_i, nv_i = wl.ctx_dev[sl], (wl.n_valid_dev[sl] if wl.frontier else None)
-        for rep in range(reps + 1):
+        for chunk in chunks:
+            for rep in range(reps + 1):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                launches(views, ctx_i, nv_i, *plan(i), chunk=chunk)
+                stream.synchronize()
+                if rep:
+                    eager[chunk].append((time.perf_counter() - t0) * 1e3)
+            planned = plan(i)
             torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            launches(views, ctx_i, nv_i, *plan(i))
-            stream.synchronize()
-            if rep:
-                eager.append((time.perf_counter() - t0) * 1e3)
-        planned = plan(i)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            launches(views, ctx_i, nv_i, *planned)
-        for rep in range(reps + 1):
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            assert plan(i) == planned
-            g.replay()
-            stream.synchronize()
-            if rep:
-                graphed.append((time.perf_counter() - t0) * 1e3)
-        del g
-    return float(statistics.median(eager)), float(statistics.median(graphed))
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                launches(views, ctx_i, nv_i, *planned, chunk=chunk)
+            for rep in range(reps + 1):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                assert plan(i) == planned
+                g.replay()
+                stream.synchronize()
+                if rep:
+                    graphed[chunk].append((time.perf_counter() - t0) * 1e3)
+            del g
+    med = lambda x: float(statistics.median(x)) if x else None
+    ov = next((c for c in chunks if c), None)
+    return (med(eager.get(0)), med(graphed.get(0)), med(eager[ov]) if ov else None,
+            med(graphed[ov]) if ov else None)
 
 
 # ------------------------------------------------------------------------------------------
@@ -550,7 +645,8 @@ def measure(w, dev, steps, warmup, n_dec, *, paged=False, fused_rope=False, per_
             wl.step(rec, calib)
         torch.cuda.synchronize()
         total_ms = (time.perf_counter() - t_start) * 1e3
-        single_ms = single_request_ttft(wl) if single else (None, None)
+        overlapped_ms = overlapped_batch_ttft(wl, reps=min(steps, 10))
+        single_ms = single_request_ttft(wl) if single else (None, None, None, None)
     finally:
         gc.enable()
 
@@ -589,7 +685,11 @@ def measure(w, dev, steps, warmup, n_dec, *, paged=False, fused_rope=False, per_
     roofline = {"kernel": dom_name, "bound": dom["bound"], "achieved": dom["achieved"], "peak": dom["peak"],
                 "unit": dom["unit"], "frac": dom["frac"], "traffic": traffic}
     fig = {"ttft_ms_batch": ttft_ms, "ttft_ms_per_request": ttft_ms / B,
+           "ttft_ms_batch_overlapped": overlapped_ms,
+           "ttft_ms_per_request_overlapped": overlapped_ms / B if overlapped_ms else None,
            "ttft_ms_single_request": single_ms[0], "ttft_ms_single_request_graph": single_ms[1],
+           "ttft_ms_single_request_overlapped": single_ms[2],
+           "ttft_ms_single_request_overlapped_graph": single_ms[3],
            "ms_per_step": total_ms / steps, "steps": steps, "warmup": warmup, "decode_tokens_per_step": n_dec,
            "context_tokens": ctx[0] if len(set(ctx)) == 1 else ctx, "batch": B, "layers": L,
            "kernels": kernels, "roofline": roofline}
@@ -666,8 +766,10 @@ def _brief(name, fig):
     """The figures of one extra workload leg, flattened for the JSON line."""
     k = fig["kernels"]
     out = {"workload": name, "ttft_ms_per_request": fig["ttft_ms_per_request"],
+           "ttft_ms_per_request_overlapped": fig["ttft_ms_per_request_overlapped"],
            "ttft_ms_single_request": fig["ttft_ms_single_request"],
            "ttft_ms_single_request_graph": fig["ttft_ms_single_request_graph"],
+           "ttft_ms_single_request_overlapped_graph": fig["ttft_ms_single_request_overlapped_graph"],
            "compose_ms": k["compose"]["ms_per_launch"], "compose_gbps": k["compose"]["achieved"],
            "compose_frac": k["compose"]["frac"],
            "compose_gbps_per_composed_row": k["compose"]["per_composed_row_gbps"],
@@ -733,8 +835,13 @@ def main():
                        "rope_local_global": w.local_global}
                       if (w.rope_pairing != "half" or w.rope_scaling or w.local_global) else {})},
         "ttft_ms_batch": fig["ttft_ms_batch"],
+        # the same TTFT with composition overlapped with prefill on a second stream
+        "ttft_ms_batch_overlapped": fig["ttft_ms_batch_overlapped"],
+        "ttft_ms_per_request_overlapped": fig["ttft_ms_per_request_overlapped"],
         "ttft_ms_single_request": fig["ttft_ms_single_request"],
         "ttft_ms_single_request_graph": fig["ttft_ms_single_request_graph"],
+        "ttft_ms_single_request_overlapped": fig["ttft_ms_single_request_overlapped"],
+        "ttft_ms_single_request_overlapped_graph": fig["ttft_ms_single_request_overlapped_graph"],
         "prefill_attn_tflops": kernels["suffix_prefill_attn"]["achieved"],
         # compose rate over the bytes the launch moves (distinct source runs read + all rows
         # written); the per-composed-row figure counts one pool read per composed row
@@ -770,7 +877,8 @@ def main():
     if legs:
         res["extra_workloads"] = legs
         for name, leg in legs.items():   # flat copies of the headline figures of each leg
-            for key in ("ttft_ms_per_request", "ttft_ms_single_request", "prefill_tflops", "prefill_frac",
+            for key in ("ttft_ms_per_request", "ttft_ms_per_request_overlapped", "ttft_ms_single_request",
+                        "ttft_ms_single_request_overlapped_graph", "prefill_tflops", "prefill_frac",
                         "compose_ms", "compose_frac", "decode_gbps", "decode_frac", "achieved", "frac",
                         "copy_gbps", "fill_gbps"):
                 if leg.get(key) is not None:
