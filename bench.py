@@ -63,6 +63,9 @@ def parse(argv=None):
                    help="extra legs after the headline: workloads (their own short step counts), "
                         "'rerotate' (standalone key re-rotation) and 'copy' (plain device copy and "
                         "fill rates for reference)")
+    p.add_argument("--no-overlap", action="store_true",
+                   help="skip the overlapped-schedule TTFT timing (profiling runs: it launches the "
+                        "prefill kernel again, sharing the GPU with compose)")
     p.add_argument("--copy-calib-gib", type=float, default=0.0,
                    help="also run a plain device copy of this size per step (counter calibration)")
     return p.parse_args(argv)
@@ -621,7 +624,7 @@ def cpu_baseline(w, budget_s):
 # ------------------------------------------------------------------------------------------
 
 def measure(w, dev, steps, warmup, n_dec, *, paged=False, fused_rope=False, per_block=False,
-            single=True, calib_gib=0.0, plain_path=True):
+            single=True, calib_gib=0.0, plain_path=True, overlap=True):
     """Runs `warmup` + `steps` bench steps of workload w and returns (workload, figures)."""
     import torch
 
@@ -645,7 +648,7 @@ def measure(w, dev, steps, warmup, n_dec, *, paged=False, fused_rope=False, per_
             wl.step(rec, calib)
         torch.cuda.synchronize()
         total_ms = (time.perf_counter() - t_start) * 1e3
-        overlapped_ms = overlapped_batch_ttft(wl, reps=min(steps, 10))
+        overlapped_ms = overlapped_batch_ttft(wl, reps=min(steps, 10)) if overlap else None
         single_ms = single_request_ttft(wl) if single else (None, None, None, None)
     finally:
         gc.enable()
@@ -804,7 +807,7 @@ def main():
     n_dec = args.decode_tokens if args.decode_tokens is not None else (w.decode_steps or 1)
     wl, fig = measure(w, dev, args.steps, args.warmup, n_dec, paged=args.paged, fused_rope=args.fused_rope,
                       per_block=args.per_block_compose, single=not args.no_single_request,
-                      calib_gib=args.copy_calib_gib,
+                      calib_gib=args.copy_calib_gib, overlap=not args.no_overlap,
                       plain_path=not (args.paged or args.fused_rope or args.per_block_compose))
     kernels = fig["kernels"]
     L, B, Ls = wl.L, w.batch, wl.Ls
