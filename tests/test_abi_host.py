@@ -306,6 +306,14 @@ def test_sizes(lib):
     assert pic.pic_decode_workspace_bytes(m, 64, 16640, 3) == 64 * 32 * 3 * 130 * 4
     assert pic.pic_decode_auto_splits(m, 1, 16640) > 1
     assert pic.pic_prefill_workspace_bytes(_model(dtype="f32", head_dim=64), 1, 16, 272) == 0
+    # bf16 prefill splits: per split and query row, the normalised output in bf16 (256 bytes)
+    # and the (max, sum) pair in fp32 (8 bytes); a lone 32-layer-Llama-shaped request splits
+    # (16 (m-tile, kv head) units), a batch of 16 does not
+    m32 = _model(n_layers=1, n_q_heads=32, n_kv_heads=8)
+    rows = 1 * 128 * 32
+    ws = pic.pic_prefill_workspace_bytes(m32, 1, 128, 10368)
+    assert ws > 0 and ws % (rows * 264) == 0 and 2 <= ws // (rows * 264) <= 32, ws
+    assert pic.pic_prefill_workspace_bytes(m32, 16, 128, 10368) == 0
 
 
 def test_plan_shared_groups_blocks_by_source():
