@@ -209,6 +209,10 @@ class DeviceWorkload:
                                  device=dev)
         # floats per layer's table block with one table per layer (else every layer reads block 0)
         self.table_block = (self.mad + 1) * (D // 2) * 2 if self.model.rope_tables > 1 else 0
+        # zero-copy prefill: the context tiles that are not whole pool runs are composed for all
+        # layers in one launch after the slot map, and the per-layer calls then take no slot map
+        # (the matrix-core path; the row path turns every key through the slot map)
+        self.tiles_ahead = w.dtype == "bf16" and w.head_dim == 128
         if w.rope_scaling == "llama3":
             pic.pic_rope_table_init_freq(self.model, pic.pic_rope_llama3_freq(D, w.rope_theta), self.mad,
                                          self.table)
@@ -255,17 +259,17 @@ class DeviceWorkload:
             blocks0, starts0 = pic.pic_plan_shared(blocks0)
         self.compose_moved = compose_moved_bytes(w, blocks0, starts0, L)
 
-    def upload(self, blocks, pinned, blocks_dev, groups_dev, inl=None, pos_dev=None):
+    def upload(self, blocks, pinned, blocks_dev, groups_dev, inl=None, pos_dev=None, grouped=True):
         """Asynchronous copy of one plan to the device: its gather blocks (grouped by source run
-        when composing with shared sources, with the group starts) and inline positions.
-        Returns (n_blocks, n_groups)."""
+        when composing with shared sources, with the group starts; `grouped` False: as planned,
+        for a slot map that needs no groups) and inline positions.  Returns (n_blocks, n_groups)."""
         import numpy as np
         import torch
 
         import paper_2607_28069_amd as pic
 
         nb, ng, at = len(blocks), 0, len(blocks) * 5
-        if self.shared_compose:
+        if self.shared_compose and grouped:
             blocks, starts = pic.pic_plan_shared(blocks)
             ng = len(starts) - 1
             pinned[at: at + ng + 1].copy_(torch.from_numpy(starts))
@@ -315,8 +319,10 @@ class DeviceWorkload:
 
         w, B, Ls, lay, block = self.w, self.w.batch, self.Ls, self.lay, self.table_block
         if self.paged:
+            ahead = self.tiles_ahead
             pic.pic_paged_prefill_attn(self.m1, self.pool_k[l], self.pool_v[l], lay.pool_tokens,
-                                       self.slot_src, self.slot_delta, self.slot_src.shape[1],
+                                       None if ahead else self.slot_src, None if ahead else self.slot_delta,
+                                       self.slot_src.shape[1],
                                        self.table[l * block:], self.mad, self.q[l],
                                        self.k_suf[l], self.v_suf[l], self.cache_k[l], self.cache_v[l], B,
                                        self.cap, self.ctx_dev, self.max_ctx, Ls, self.out[l], self.ws_pre,
@@ -383,6 +389,11 @@ class DeviceWorkload:
         if self.paged:   # the token-level slot map, shared by every layer
             pic.pic_build_slot_map(self.blocks_dev, nb, B, self.slot_src.shape[1], self.slot_src,
                                    self.slot_delta, self.tile_map)
+            if self.tiles_ahead:
+                pic.pic_compose_tiles(self.model, self.pool_k, self.pool_v, self.lay.pool_tokens, self.slot_src,
+                                      self.slot_delta, self.slot_src.shape[1], self.tile_map, self.table,
+                                      self.mad, self.ctx_dev, self.max_ctx, self.cache_k, self.cache_v, B,
+                                      self.cap)
         p0, p1 = ev(), ev()
         p0.record(stream)
         for l in range(L if Ls else 0):
@@ -425,6 +436,7 @@ class DeviceWorkload:
 
 OVERLAP_CHUNK_BATCH = 1   # layers per compose launch when compose overlaps prefill: a batch
 OVERLAP_CHUNK_LONE = 4    # ... and a request served alone (fewer, longer launches)
+ZERO_COPY = -1            # lone-request schedule: slot map + paged prefill, compose after the first token
 
 
 def overlapped_batch_ttft(wl, reps: int = 10, chunk: int = OVERLAP_CHUNK_BATCH):
@@ -450,7 +462,7 @@ def overlapped_batch_ttft(wl, reps: int = 10, chunk: int = OVERLAP_CHUNK_BATCH):
     return float(statistics.median(times))
 
 
-def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
+def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None) -> dict:
     """TTFT (ms) of requests served alone, batch 1: the paper's per-request synchronized wall
     clock (App. C.2), where the batched figure divides a batch's time by its size.
 
@@ -459,21 +471,26 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
     untimed pass; the pool, suffix inputs and rotary table are those of the batched workload.
     A lone request's per-layer launches are short, so the launch sequence after the plan is
     also recorded once per request as a HIP graph and replayed (the plan and the copy of its
-    gather blocks stay in the timed region).  Composed-cache workloads are also timed with
-    composition overlapped with prefill (chunks of OVERLAP_CHUNK_LONE layers composed on a
-    second stream, each layer's prefill waiting for its own chunk; `chunks` picks the schedules:
-    0 = sequential, n = overlapped in chunks of n layers).  Returns the medians over
-    all samples (eager, graph replay, overlapped eager, overlapped graph replay; the last two
-    None for zero-copy workloads): an occasional host stall of tens of milliseconds, seen on
-    either path, moves a 20-sample mean by several percent."""
-    import numpy as np
+    gather blocks stay in the timed region).  `chunks` picks the schedules, each timed eagerly
+    and replayed: 0 = the workload's own (compose, then every layer's prefill; zero-copy
+    workloads: slot map and paged prefill); n > 0 = composition overlapped with prefill, chunks
+    of n layers composed on a second stream, each layer's prefill waiting for its own chunk;
+    ZERO_COPY = slot map and paged prefill for a composed-cache workload (the cache for decoding
+    composed after the first token, outside the region).  Default: 0, and for plain suffix
+    workloads also OVERLAP_CHUNK_LONE and ZERO_COPY.  Returns {schedule: (eager, graph)} medians
+    over all samples: an occasional host stall of tens of milliseconds, seen on either path,
+    moves a 20-sample mean by several percent."""
     import torch
 
     import paper_2607_28069_amd as pic
 
     w, L, Ls, dev = wl.w, wl.L, wl.Ls, wl.dev
     if Ls == 0:
-        return None, None, None, None
+        return {}
+    plain = not (wl.paged or wl.frontier or wl.fused_rope)
+    if chunks is None:
+        chunks = [0, OVERLAP_CHUNK_LONE, ZERO_COPY] if plain else [0]
+    assert plain or chunks == [0], "overlapped and zero-copy schedules: plain suffix workloads only"
     lay, D, Hkv = wl.lay, w.head_dim, w.n_kv_heads
     side = torch.cuda.Stream()
     events = [torch.cuda.Event() for _ in range(L + 1)]
@@ -488,13 +505,14 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
     groups_dev = torch.empty_like(wl.groups_dev)
     pinned = torch.empty_like(wl.blocks_pinned)
     pos_dev = torch.empty((1, Ls), dtype=torch.int32, device=dev)
-    if wl.paged:
-        slot_src = torch.empty((1, wl.slot_src.shape[1]), dtype=torch.int32, device=dev)
+    if wl.paged or ZERO_COPY in chunks:
+        map_cap = max(wl.max_ctx, 1)
+        slot_src = torch.empty((1, map_cap), dtype=torch.int32, device=dev)
         slot_delta = torch.empty_like(slot_src)
-        tile_map = torch.empty((1,) + tuple(wl.tile_map.shape[1:]), dtype=torch.int32, device=dev)
+        tile_map = torch.empty((1, pic.pic_slot_map_tiles(map_cap), 2), dtype=torch.int32, device=dev)
     block = (wl.mad + 1) * (D // 2) * 2 if wl.model.rope_tables > 1 else 0
 
-    def plan(i):   # host plan + asynchronous copy of its blocks (and inline positions)
+    def plan(i, chunk=0):   # host plan + asynchronous copy of its blocks (and inline positions)
         if wl.frontier:
             blocks, total, inl, _ = pic.pic_plan_frontier([lay.items[i]], lay.doc_offset, lay.doc_len,
                                                           lay.doc_compile_pos, lay.pool_tokens)
@@ -503,14 +521,20 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
             blocks, ctx = pic.pic_plan_layout([lay.requests[i]], lay.doc_offset, lay.doc_len,
                                               lay.doc_compile_pos, lay.pool_tokens)
             n_keys = int(ctx[0])
-        nb, ng = wl.upload(blocks, pinned, blocks_dev, groups_dev, inl if wl.frontier else None, pos_dev)
+        nb, ng = wl.upload(blocks, pinned, blocks_dev, groups_dev, inl if wl.frontier else None, pos_dev,
+                           grouped=not (wl.paged or chunk == ZERO_COPY))
         return nb, ng, n_keys
 
     def launches(views, ctx_i, nv_i, nb, ng, n_keys, chunk=0):   # compose (or slot map) + every layer's prefill
         main = torch.cuda.current_stream()   # the capture stream while a graph is recorded
-        if wl.paged:
+        paged = wl.paged or chunk == ZERO_COPY
+        if paged:
             pic.pic_build_slot_map(blocks_dev, nb, 1, slot_src.shape[1], slot_src, slot_delta, tile_map)
-        elif chunk:   # chunks of layers; all but the first on the side stream
+            if wl.tiles_ahead:
+                pic.pic_compose_tiles(wl.model, wl.pool_k, wl.pool_v, lay.pool_tokens, slot_src, slot_delta,
+                                      slot_src.shape[1], tile_map, wl.table, wl.mad, ctx_i, n_keys, cache_k,
+                                      cache_v, 1, wl.cap)
+        elif chunk > 0:   # chunks of layers; all but the first on the side stream
             events[L].record(main)
             side.wait_event(events[L])
             for c0 in range(0, L, chunk):
@@ -521,12 +545,13 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
         else:
             wl.compose(blocks_dev, groups_dev, nb, ng, cache_k, cache_v, 1)
         for l, (q, k, v, ck, cv, out, pk, pv, tab) in enumerate(views):
-            if chunk and l and l % chunk == 0:
+            if chunk > 0 and l and l % chunk == 0:
                 main.wait_event(events[l])
-            if wl.paged:
-                pic.pic_paged_prefill_attn(wl.m1, pk, pv, lay.pool_tokens, slot_src, slot_delta,
-                                           slot_src.shape[1], tab, wl.mad, q, k, v, ck, cv, 1, wl.cap,
-                                           ctx_i, n_keys, Ls, out, ws, tile_map=tile_map)
+            if paged:
+                ahead = wl.tiles_ahead
+                pic.pic_paged_prefill_attn(wl.m1, pk, pv, lay.pool_tokens, None if ahead else slot_src,
+                                           None if ahead else slot_delta, slot_src.shape[1], tab, wl.mad, q, k,
+                                           v, ck, cv, 1, wl.cap, ctx_i, n_keys, Ls, out, ws, tile_map=tile_map)
             elif wl.frontier:
                 pic.pic_frontier_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, pos_dev, nv_i, Ls, n_keys,
                                               out, ws)
@@ -536,8 +561,6 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
             else:
                 pic.pic_suffix_prefill_attn(wl.m1, q, k, v, ck, cv, 1, wl.cap, ctx_i, n_keys, Ls, out, ws)
 
-    if chunks is None:
-        chunks = [0] if wl.paged else [0, OVERLAP_CHUNK_LONE]
     eager, graphed = {c: [] for c in chunks}, {c: [] for c in chunks}
     stream = torch.cuda.current_stream()
     for i in range(min(n_requests, w.batch)):
@@ -550,11 +573,11 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
             for rep in range(reps + 1):
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
-                launches(views, ctx_i, nv_i, *plan(i), chunk=chunk)
+                launches(views, ctx_i, nv_i, *plan(i, chunk), chunk=chunk)
                 stream.synchronize()
                 if rep:
                     eager[chunk].append((time.perf_counter() - t0) * 1e3)
-            planned = plan(i)
+            planned = plan(i, chunk)
             torch.cuda.synchronize()
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
@@ -562,16 +585,13 @@ def single_request_ttft(wl, n_requests: int = 4, reps: int = 5, chunks=None):
             for rep in range(reps + 1):
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
-                assert plan(i) == planned
+                assert plan(i, chunk) == planned
                 g.replay()
                 stream.synchronize()
                 if rep:
                     graphed[chunk].append((time.perf_counter() - t0) * 1e3)
             del g
-    med = lambda x: float(statistics.median(x)) if x else None
-    ov = next((c for c in chunks if c), None)
-    return (med(eager.get(0)), med(graphed.get(0)), med(eager[ov]) if ov else None,
-            med(graphed[ov]) if ov else None)
+    return {c: (float(statistics.median(eager[c])), float(statistics.median(graphed[c]))) for c in chunks}
 
 
 # ------------------------------------------------------------------------------------------
@@ -649,7 +669,7 @@ def measure(w, dev, steps, warmup, n_dec, *, paged=False, fused_rope=False, per_
         torch.cuda.synchronize()
         total_ms = (time.perf_counter() - t_start) * 1e3
         overlapped_ms = overlapped_batch_ttft(wl, reps=min(steps, 10)) if overlap else None
-        single_ms = single_request_ttft(wl) if single else (None, None, None, None)
+        single_ms = single_request_ttft(wl) if single else {}
     finally:
         gc.enable()
 
@@ -690,9 +710,12 @@ def measure(w, dev, steps, warmup, n_dec, *, paged=False, fused_rope=False, per_
     fig = {"ttft_ms_batch": ttft_ms, "ttft_ms_per_request": ttft_ms / B,
            "ttft_ms_batch_overlapped": overlapped_ms,
            "ttft_ms_per_request_overlapped": overlapped_ms / B if overlapped_ms else None,
-           "ttft_ms_single_request": single_ms[0], "ttft_ms_single_request_graph": single_ms[1],
-           "ttft_ms_single_request_overlapped": single_ms[2],
-           "ttft_ms_single_request_overlapped_graph": single_ms[3],
+           "ttft_ms_single_request": single_ms.get(0, (None, None))[0],
+           "ttft_ms_single_request_graph": single_ms.get(0, (None, None))[1],
+           "ttft_ms_single_request_overlapped": single_ms.get(OVERLAP_CHUNK_LONE, (None, None))[0],
+           "ttft_ms_single_request_overlapped_graph": single_ms.get(OVERLAP_CHUNK_LONE, (None, None))[1],
+           "ttft_ms_single_request_zero_copy": single_ms.get(ZERO_COPY, (None, None))[0],
+           "ttft_ms_single_request_zero_copy_graph": single_ms.get(ZERO_COPY, (None, None))[1],
            "ms_per_step": total_ms / steps, "steps": steps, "warmup": warmup, "decode_tokens_per_step": n_dec,
            "context_tokens": ctx[0] if len(set(ctx)) == 1 else ctx, "batch": B, "layers": L,
            "kernels": kernels, "roofline": roofline}
@@ -773,6 +796,11 @@ def _brief(name, fig):
            "ttft_ms_single_request": fig["ttft_ms_single_request"],
            "ttft_ms_single_request_graph": fig["ttft_ms_single_request_graph"],
            "ttft_ms_single_request_overlapped_graph": fig["ttft_ms_single_request_overlapped_graph"],
+        # a lone request's first token from the pool (slot map + paged prefill); its cache for
+        # decoding is composed afterwards, outside this region
+        "ttft_ms_single_request_zero_copy": fig["ttft_ms_single_request_zero_copy"],
+        "ttft_ms_single_request_zero_copy_graph": fig["ttft_ms_single_request_zero_copy_graph"],
+           "ttft_ms_single_request_zero_copy_graph": fig["ttft_ms_single_request_zero_copy_graph"],
            "compose_ms": k["compose"]["ms_per_launch"], "compose_gbps": k["compose"]["achieved"],
            "compose_frac": k["compose"]["frac"],
            "compose_gbps_per_composed_row": k["compose"]["per_composed_row_gbps"],
@@ -845,6 +873,10 @@ def main():
         "ttft_ms_single_request_graph": fig["ttft_ms_single_request_graph"],
         "ttft_ms_single_request_overlapped": fig["ttft_ms_single_request_overlapped"],
         "ttft_ms_single_request_overlapped_graph": fig["ttft_ms_single_request_overlapped_graph"],
+        # a lone request's first token from the pool (slot map + paged prefill); its cache for
+        # decoding is composed afterwards, outside this region
+        "ttft_ms_single_request_zero_copy": fig["ttft_ms_single_request_zero_copy"],
+        "ttft_ms_single_request_zero_copy_graph": fig["ttft_ms_single_request_zero_copy_graph"],
         "prefill_attn_tflops": kernels["suffix_prefill_attn"]["achieved"],
         # compose rate over the bytes the launch moves (distinct source runs read + all rows
         # written); the per-composed-row figure counts one pool read per composed row
@@ -881,7 +913,8 @@ def main():
         res["extra_workloads"] = legs
         for name, leg in legs.items():   # flat copies of the headline figures of each leg
             for key in ("ttft_ms_per_request", "ttft_ms_per_request_overlapped", "ttft_ms_single_request",
-                        "ttft_ms_single_request_overlapped_graph", "prefill_tflops", "prefill_frac",
+                        "ttft_ms_single_request_overlapped_graph", "ttft_ms_single_request_zero_copy_graph",
+                        "prefill_tflops", "prefill_frac",
                         "compose_ms", "compose_frac", "decode_gbps", "decode_frac", "achieved", "frac",
                         "copy_gbps", "fill_gbps"):
                 if leg.get(key) is not None:

@@ -290,14 +290,28 @@ pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q, c
    slots for decoding.  bf16 only.  At head_dim 64 a tile map is accepted and not used: every
    context key is turned on load (bit-identical to compose + prefill) and only the suffix rows
    are stored.
+   pic_compose_tiles composes, for every layer of `model` in one launch, the context tiles a
+   tile map does not mark as whole runs: the step each pic_paged_prefill_attn call with a tile
+   map otherwise takes for its own layer (same cache contents).  After it, the per-layer calls
+   may pass slot_src = slot_delta = NULL with the tile map: they then skip that step, reading
+   whole runs from the pool and every other tile from the cache (bf16 at head_dim 128 only;
+   results identical to passing the slot map).
      pool_k, pool_v, pool_tokens, table, max_abs_delta   as for pic_compose
      slot_src, slot_delta, map_cap   the map; map_cap >= max_ctx (entries are clamped to the
                                      pool and to max_abs_delta)
      q, k_suf, v_suf, cache_k, cache_v, batch, cache_cap, ctx_len, max_ctx, n_suffix, scale,
-     out, workspace   as for pic_suffix_prefill_attn (same workspace size) */
+     out, workspace   as for pic_suffix_prefill_attn (same workspace size)
+     pic_compose_tiles: the same pool, map, table, ctx_len, max_ctx (<= cache_cap) and caches,
+     all layers of the model */
 pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t batch,
                               int32_t map_cap, int32_t* slot_src, int32_t* slot_delta,
                               int32_t* tile_map, void* stream);
+pic_status pic_compose_tiles(const pic_model* model, const void* pool_k, const void* pool_v,
+                             int64_t pool_tokens, const int32_t* slot_src, const int32_t* slot_delta,
+                             int32_t map_cap, const int32_t* tile_map, const void* table,
+                             int32_t max_abs_delta, const int32_t* ctx_len, int32_t max_ctx,
+                             void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
+                             void* stream);
 pic_status pic_paged_prefill_attn(const pic_model* model, const void* pool_k, const void* pool_v,
                                   int64_t pool_tokens, const int32_t* slot_src,
                                   const int32_t* slot_delta, int32_t map_cap,

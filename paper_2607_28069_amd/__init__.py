@@ -27,7 +27,7 @@ EXPORTS = ("pic_plan_layout", "pic_plan_frontier", "pic_rope_table_bytes", "pic_
            "pic_rerotate_keys", "pic_compose", "pic_plan_shared", "pic_compose_shared",
            "pic_prefill_workspace_bytes",
            "pic_suffix_prefill_attn", "pic_suffix_prefill_attn_rope", "pic_build_slot_map",
-           "pic_paged_prefill_attn",
+           "pic_compose_tiles", "pic_paged_prefill_attn",
            "pic_frontier_workspace_bytes", "pic_frontier_prefill_attn",
            "pic_decode_workspace_bytes", "pic_decode_attn", "pic_decode_attn_rope", "pic_status_string",
            "pic_last_error",
@@ -98,6 +98,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "pic_suffix_prefill_attn_rope": (ctypes.c_int, [MP, P, P, P, P, P, I32, I32, P, I32, I32, P, I32, F, P, P,
                                                         SZ, P]),
         "pic_build_slot_map": (ctypes.c_int, [P, I32, I32, I32, P, P, P, P]),
+        "pic_compose_tiles": (ctypes.c_int, [MP, P, P, I64, P, P, I32, P, P, I32, P, I32, P, P, I32, I32, P]),
         "pic_paged_prefill_attn": (ctypes.c_int, [MP, P, P, I64, P, P, I32, P, P, I32, P, P, P, P, P, I32, I32,
                                                   P, I32, I32, F, P, P, SZ, P]),
         "pic_frontier_workspace_bytes": (SZ, [MP, I32, I32, I32]),
@@ -299,11 +300,23 @@ def pic_build_slot_map(blocks, n_blocks, batch, map_cap, slot_src, slot_delta, t
                                      _ptr(slot_delta), _ptr(tile_map), _stream(stream)))
 
 
+def pic_compose_tiles(model: Model, pool_k, pool_v, pool_tokens, slot_src, slot_delta, map_cap, tile_map, table,
+                      max_abs_delta, ctx_len, max_ctx, cache_k, cache_v, batch, cache_cap, stream=None):
+    """The context tiles the tile map does not mark as whole runs, composed into the caches for
+    every layer of `model` in one launch (then pic_paged_prefill_attn may take slot_src =
+    slot_delta = None with the tile map)."""
+    _check(load().pic_compose_tiles(ctypes.byref(model), _ptr(pool_k), _ptr(pool_v), int(pool_tokens),
+                                    _ptr(slot_src), _ptr(slot_delta), int(map_cap), _ptr(tile_map), _ptr(table),
+                                    int(max_abs_delta), _ptr(ctx_len), int(max_ctx), _ptr(cache_k), _ptr(cache_v),
+                                    int(batch), int(cache_cap), _stream(stream)))
+
+
 def pic_paged_prefill_attn(model: Model, pool_k, pool_v, pool_tokens, slot_src, slot_delta, map_cap, table,
                            max_abs_delta, q, k_suf, v_suf, cache_k, cache_v, batch, cache_cap, ctx_len, max_ctx,
                            n_suffix, out, workspace=None, scale=0.0, stream=None, tile_map=None):
     """tile_map None: keys turned one by one (bit-identical to compose + prefill); a tile map from
-    pic_build_slot_map: whole-run tiles turn the queries instead."""
+    pic_build_slot_map: whole-run tiles turn the queries instead (slot_src = slot_delta = None:
+    the other tiles were composed beforehand by pic_compose_tiles)."""
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().pic_paged_prefill_attn(ctypes.byref(model), _ptr(pool_k), _ptr(pool_v), int(pool_tokens),
                                          _ptr(slot_src), _ptr(slot_delta), int(map_cap), _ptr(tile_map),

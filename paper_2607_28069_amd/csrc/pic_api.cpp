@@ -659,6 +659,49 @@ PIC_API pic_status pic_build_slot_map(const pic_block* blocks, int32_t n_blocks,
                     "slot map launch");
 }
 
+PIC_API pic_status pic_compose_tiles(const pic_model* model, const void* pool_k, const void* pool_v,
+                                     int64_t pool_tokens, const int32_t* slot_src,
+                                     const int32_t* slot_delta, int32_t map_cap,
+                                     const int32_t* tile_map, const void* table,
+                                     int32_t max_abs_delta, const int32_t* ctx_len, int32_t max_ctx,
+                                     void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
+                                     void* stream) {
+  PIC_CHECK(check_attn_model(model));
+  if (!mfma_path(model))
+    return fail(PIC_ERR_UNSUPPORTED, "tile composition is built for bf16 caches at head_dim 128");
+  if (batch < 0 || cache_cap < 0 || max_ctx < 0 || pool_tokens < 0 || map_cap < 0)
+    return fail(PIC_ERR_INVALID_ARG, "negative size");
+  if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
+    return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
+  if (max_ctx > cache_cap)
+    return fail(PIC_ERR_CAPACITY, "max_ctx %d exceeds cache_cap %d", max_ctx, cache_cap);
+  if (map_cap < max_ctx)
+    return fail(PIC_ERR_CAPACITY, "map_cap %d is below max_ctx %d", map_cap, max_ctx);
+  if (max_ctx > 0 && pool_tokens == 0) return fail(PIC_ERR_RANGE, "empty pool");
+  if (model->n_layers > 65535) return fail(PIC_ERR_UNSUPPORTED, "more than 65535 layers");
+  PIC_CHECK(check_rows32(cache_cap, 0, pool_tokens));
+  if (batch == 0 || max_ctx == 0 || model->n_layers == 0) return ok();
+  PIC_CHECK(check_ptr(pool_k, "pool_k"));
+  PIC_CHECK(check_ptr(pool_v, "pool_v"));
+  PIC_CHECK(check_ptr(table, "table"));
+  PIC_CHECK(check_ptr(cache_k, "cache_k"));
+  PIC_CHECK(check_ptr(cache_v, "cache_v"));
+  if (!slot_src || !slot_delta) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL");
+  PIC_CHECK(check_ptr(tile_map, "tile_map"));
+  if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
+  const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
+  return hip_status(pic::launch_compose_tiles(model->rope_pairing == PIC_ROPE_INTERLEAVED, model->n_layers,
+                                              model->n_kv_heads, static_cast<const pic::bf16_t*>(pool_k),
+                                              static_cast<const pic::bf16_t*>(pool_v), pool_tokens, slot_src,
+                                              slot_delta, map_cap > 0 ? map_cap : 1, tile_map,
+                                              pic::slot_map_tiles(map_cap > 0 ? map_cap : 1), ctx_len,
+                                              max_ctx, static_cast<const float2*>(table), stride,
+                                              max_abs_delta, static_cast<pic::bf16_t*>(cache_k),
+                                              static_cast<pic::bf16_t*>(cache_v), batch, cache_cap,
+                                              (hipStream_t)stream),
+                    "tile compose launch");
+}
+
 PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* pool_k,
                                           const void* pool_v, int64_t pool_tokens,
                                           const int32_t* slot_src, const int32_t* slot_delta,
@@ -700,8 +743,12 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
   PIC_CHECK(check_ptr(cache_k, "cache_k"));
   PIC_CHECK(check_ptr(cache_v, "cache_v"));
   PIC_CHECK(check_ptr(out, "out"));
-  if (!slot_src || !slot_delta) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL");
   if (tile_map) PIC_CHECK(check_ptr(tile_map, "tile_map"));
+  if (!slot_src != !slot_delta) return fail(PIC_ERR_INVALID_ARG, "one of the slot maps is NULL");
+  // no slot map: the non-run tiles were composed beforehand (pic_compose_tiles), and the
+  // call reads whole runs from the pool and every other tile from the cache
+  if (!slot_src && !(tile_map && mfma_path(model)))
+    return fail(PIC_ERR_INVALID_ARG, "slot map is NULL (allowed only with a tile map at head_dim 128)");
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
   const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
   if (need > 0 && (workspace == nullptr || ws_bytes < need))

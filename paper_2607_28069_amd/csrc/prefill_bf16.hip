@@ -1089,6 +1089,7 @@ prefill_bf16_kernel(PrefillArgs a) {
 // select: its sums are not finite).  With n_valid (table mode), rows of tokens past
 // n_valid[b] are left untouched.
 constexpr int kCombineRowsPerWG = 16;
+constexpr int kCombineBatch = 16;
 __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __restrict__ ws_o,
                                                               const float2* __restrict__ ws_ml,
                                                               int32_t n_splits, int64_t rows_total,
@@ -1105,13 +1106,23 @@ __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __re
     if (i >= n_valid[b]) return;
   }
   const int d = 8 * (threadIdx.x & 15);
-  // one pass with a running reference max; the unrolled loop keeps several splits' loads in
-  // flight (their values do not depend on the running max)
+  // one pass with a running reference max, kCombineBatch splits at a time: all their loads
+  // are issued before the first is used (a split past n_splits reads as one that saw no key)
   float M = -INFINITY, den = 0.f, o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-  for (int s = 0; s < n_splits; ++s) {
-    const float2 ml = ws_ml[s * rows_total + row];
-    const uint4 x = *reinterpret_cast<const uint4*>(ws_o + (s * rows_total + row) * kHD + d);
+  for (int s0 = 0; s0 < n_splits; s0 += kCombineBatch) {
+    float2 mls[kCombineBatch];
+    uint4 xs[kCombineBatch];
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) {
+      const int64_t s = s0 + u;
+      mls[u] = s < n_splits ? ws_ml[s * rows_total + row] : make_float2(-INFINITY, 0.f);
+      xs[u] = s < n_splits ? *reinterpret_cast<const uint4*>(ws_o + (s * rows_total + row) * kHD + d)
+                           : uint4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+  for (int u = 0; u < kCombineBatch; ++u) {
+    const float2 ml = mls[u];
+    const uint4 x = xs[u];
     const bool seen = ml.x != -INFINITY;
     const float m_new = seen ? fmaxf(M, ml.x) : M;
     const float keep = seen ? __builtin_amdgcn_exp2f(M - m_new) : 1.f;   // 0 while M is -inf
@@ -1124,6 +1135,7 @@ __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __re
       o[2 * e] = o[2 * e] * keep + (seen ? w * __uint_as_float(xw[e] << 16) : 0.f);
       o[2 * e + 1] = o[2 * e + 1] * keep + (seen ? w * __uint_as_float(xw[e] & 0xFFFF0000u) : 0.f);
     }
+  }
   }
   const float inv = 1.f / den;
   uint4 v;
@@ -1161,31 +1173,32 @@ __global__ void __launch_bounds__(64) map_expand_kernel(const pic_block* __restr
   }
 }
 
-// grid over (request, 64-slot tile), 256 threads: a tile whose 64 slots map to pool tokens
-// src .. src + 63 with one shift is recorded as (src, shift), any other tile as (-1, 0).
+// One wave per (request, 64-slot tile), four per 256-thread workgroup, grid-stride: a tile
+// whose 64 slots map to pool tokens src .. src + 63 with one shift is recorded as (src, shift),
+// any other tile as (-1, 0).  Lane j reads slot k0 + j, so a tile's map entries load at once.
 __global__ void __launch_bounds__(256) map_tiles_kernel(const int32_t* __restrict__ smap,
                                                         const int32_t* __restrict__ dmap,
                                                         int64_t n_tiles, int32_t map_cap,
                                                         int32_t map_tiles, int32_t* tmap) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_tiles;
-       i += (int64_t)gridDim.x * blockDim.x) {
+  static_assert(kKeys == 64, "one lane per key of a tile");
+  const int lane = threadIdx.x & 63;
+  for (int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); i < n_tiles; i += (int64_t)gridDim.x * 4) {
     const int64_t b = i / map_tiles;
     const int32_t k0 = (int32_t)(i - b * map_tiles) * kKeys;
     int32_t src = -1, d = 0;
-    if (k0 + kKeys <= map_cap) {
-      const int32_t* sm = smap + b * map_cap + k0;
-      const int32_t* dm = dmap + b * map_cap + k0;
-      src = sm[0];
-      d = dm[0];
-      bool run = src >= 0;
-      for (int j = 1; j < kKeys && run; ++j) run = sm[j] == src + j && dm[j] == d;
-      if (!run) {
-        src = -1;
-        d = 0;
+    if (k0 + kKeys <= map_cap) {   // (uniform over the wave)
+      const int32_t sj = smap[b * map_cap + k0 + lane], dj = dmap[b * map_cap + k0 + lane];
+      const int32_t s0 = __shfl(sj, 0, 64), d0 = __shfl(dj, 0, 64);
+      const bool ok = s0 >= 0 && (int64_t)sj == (int64_t)s0 + lane && dj == d0;
+      if (__all(ok)) {
+        src = s0;
+        d = d0;
       }
     }
-    tmap[2 * i] = src;
-    tmap[2 * i + 1] = d;
+    if (lane == 0) {
+      tmap[2 * i] = src;
+      tmap[2 * i + 1] = d;
+    }
   }
 }
 
@@ -1314,7 +1327,7 @@ hipError_t launch_slot_map(const pic_block* blocks, int32_t n_blocks, int32_t ba
   if (tmap == nullptr) return hipSuccess;
   const int32_t mt = slot_map_tiles(map_cap);
   const int64_t n_tiles = (int64_t)batch * mt;
-  int64_t gt = (n_tiles + 255) / 256;
+  int64_t gt = (n_tiles + 3) / 4;   // four tiles (waves) per workgroup
   gt = gt < 1 ? 1 : (gt > 65536 ? 65536 : gt);
   hipLaunchKernelGGL(map_tiles_kernel, dim3((unsigned)gt), dim3(256), 0, stream, smap, dmap, n_tiles,
                      map_cap, mt, tmap);
@@ -1352,13 +1365,16 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
   a.max_ctx = max_ctx;
   if (tmap == nullptr)   // every tile read through the slot map, keys turned in LDS
     return launch(s, a, kModePaged, interleaved, n_suffix, max_ctx, workspace, ws_bytes, stream);
-  // with a tile map: the tiles that are not whole runs are composed into the cache first, then
-  // the prefill reads whole runs from the pool and everything else from the cache
-  const hipError_t e = launch_compose_tiles(interleaved, s.n_layers, s.n_kv_heads, pool_k, pool_v,
-                                            pool_tokens, smap, dmap, map_cap, tmap, a.map_tiles,
-                                            ctx_len, max_ctx, table, table_stride, max_abs_delta,
-                                            cache_k, cache_v, s.batch, s.cache_cap, stream);
-  if (e != hipSuccess) return e;
+  // with a tile map: the tiles that are not whole runs are composed into the cache first (here,
+  // or beforehand by the caller when no slot map is given), then the prefill reads whole runs
+  // from the pool and everything else from the cache
+  if (smap != nullptr) {
+    const hipError_t e = launch_compose_tiles(interleaved, s.n_layers, s.n_kv_heads, pool_k, pool_v,
+                                              pool_tokens, smap, dmap, map_cap, tmap, a.map_tiles,
+                                              ctx_len, max_ctx, table, table_stride, max_abs_delta,
+                                              cache_k, cache_v, s.batch, s.cache_cap, stream);
+    if (e != hipSuccess) return e;
+  }
   return launch(s, a, kModeRuns, interleaved, n_suffix, max_ctx, workspace, ws_bytes, stream);
 }
 

@@ -502,11 +502,13 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
   a.map_tiles = slot_map_tiles(map_cap);
   a.table = table; a.table_stride = table_stride; a.max_abs_delta = max_abs_delta;
   if (tile_map == nullptr) return prefill_walk(s, a, kModePaged, n_suffix, max_ctx, workspace, ws_bytes);
-  const hipError_t e = launch_compose_tiles(interleaved, s.n_layers, s.n_kv_heads, pool_k, pool_v, pool_tokens,
-                                            slot_src, slot_delta, map_cap, tile_map, a.map_tiles, ctx_len,
-                                            max_ctx, table, table_stride, max_abs_delta, cache_k, cache_v,
-                                            s.batch, s.cache_cap, stream);
-  if (e != hipSuccess) return e;
+  if (slot_src != nullptr) {   // no slot map: the tiles were composed beforehand
+    const hipError_t e = launch_compose_tiles(interleaved, s.n_layers, s.n_kv_heads, pool_k, pool_v, pool_tokens,
+                                              slot_src, slot_delta, map_cap, tile_map, a.map_tiles, ctx_len,
+                                              max_ctx, table, table_stride, max_abs_delta, cache_k, cache_v,
+                                              s.batch, s.cache_cap, stream);
+    if (e != hipSuccess) return e;
+  }
   return prefill_walk(s, a, kModeRuns, n_suffix, max_ctx, workspace, ws_bytes);
 }
 

@@ -323,6 +323,16 @@ void fuzz_attention() {
                                     with_map ? tm.as<int32_t>() : nullptr, table.p, mad, q.p, ks.p, vs.p, ck.p, cv.p,
                                     batch, cap, ctx.as<int32_t>(), max_ctx, n_suf, 0.f, out.p,
                                     ws.n ? ws.p : nullptr, ws.n, nullptr) == PIC_OK);
+    // the non-run tiles of every layer composed ahead, then the per-layer form without the slot
+    // map (head_dim 128 only: the row path turns every key through the slot map)
+    const bool mfma = m.head_dim == 128;
+    EXPECT(pic_compose_tiles(&m, pk.p, pv.p, pool_tokens, sm.as<int32_t>(), dm.as<int32_t>(), map_cap,
+                             tm.as<int32_t>(), table.p, mad, ctx.as<int32_t>(), max_ctx, ck.p, cv.p, batch, cap,
+                             nullptr) == (mfma ? PIC_OK : PIC_ERR_UNSUPPORTED));
+    EXPECT(pic_paged_prefill_attn(&m, pk.p, pv.p, pool_tokens, nullptr, nullptr, map_cap, tm.as<int32_t>(), table.p,
+                                  mad, q.p, ks.p, vs.p, ck.p, cv.p, batch, cap, ctx.as<int32_t>(), max_ctx, n_suf,
+                                  0.f, out.p, ws.n ? ws.p : nullptr, ws.n, nullptr) ==
+           (mfma ? PIC_OK : PIC_ERR_INVALID_ARG));
     // the slot map from garbage blocks
     const int32_t nb = (int32_t)rnd(0, 30);
     Buf blk(nb * sizeof(pic_block));
@@ -362,6 +372,15 @@ void argument_checks() {
   pic_model bad = model(1, 30, 8, 128, PIC_BF16);
   EXPECT(pic_compose(&bad, P, P, 100, reinterpret_cast<pic_block*>(P), 4, P, 10, P, P, 2, 100, nullptr) ==
          PIC_ERR_INVALID_ARG);
+  // tile composition: the tile map is required, and map_cap must cover max_ctx
+  EXPECT(pic_compose_tiles(&m, P, P, 100, I, I, 64, nullptr, P, 10, I, 64, P, P, 2, 100, nullptr) ==
+         PIC_ERR_INVALID_ARG);
+  EXPECT(pic_compose_tiles(&m, P, P, 100, I, I, 32, I, P, 10, I, 64, P, P, 2, 100, nullptr) == PIC_ERR_CAPACITY);
+  // the paged prefill without a slot map needs a tile map
+  EXPECT(pic_paged_prefill_attn(&m, P, P, 100, nullptr, nullptr, 64, nullptr, P, 10, P, P, P, P, P, 2, 200, I, 64,
+                                16, 0.f, P, P, 1 << 20, nullptr) == PIC_ERR_INVALID_ARG);
+  EXPECT(pic_paged_prefill_attn(&m, P, P, 100, I, nullptr, 64, I, P, 10, P, P, P, P, P, 2, 200, I, 64, 16, 0.f, P,
+                                P, 1 << 20, nullptr) == PIC_ERR_INVALID_ARG);
   EXPECT(pic::emu::launches == before);
 }
 

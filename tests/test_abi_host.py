@@ -420,6 +420,38 @@ def test_binding_refuses_host_and_strided_buffers(lib):
     assert pic._ptr(None) is None
 
 
+def test_compose_tiles_argument_checks(lib):
+    """pic_compose_tiles and the paged prefill without a slot map: refused before any launch."""
+    m = _model()
+    args = dict(pool_k=FAKE, pool_v=FAKE, pool_tokens=1000, slot_src=FAKE, slot_delta=FAKE, map_cap=600,
+                tile_map=FAKE, table=FAKE, max_abs_delta=100, ctx_len=FAKE, max_ctx=500, cache_k=FAKE,
+                cache_v=FAKE, batch=2, cache_cap=600)
+
+    def call(model, **kw):
+        a = dict(args, **kw)
+        return lib.pic_compose_tiles(ctypes.byref(model), *[a[k] for k in (
+            "pool_k", "pool_v", "pool_tokens", "slot_src", "slot_delta", "map_cap", "tile_map", "table",
+            "max_abs_delta", "ctx_len", "max_ctx", "cache_k", "cache_v", "batch", "cache_cap")], None)
+
+    assert call(m, tile_map=None) == -1
+    assert call(m, slot_src=None) == -1
+    assert call(m, ctx_len=None) == -1
+    assert call(m, map_cap=400) == -4                   # the map must cover max_ctx
+    assert call(m, max_ctx=700) == -4                   # longer than the cache
+    assert call(m, max_abs_delta=-1) == -6
+    assert call(_model(head_dim=64)) == -2              # built for head_dim 128
+    assert call(_model(dtype="f32")) == -2
+    assert call(m, batch=0) == 0                        # nothing to do, nothing launched
+    # the paged prefill: no slot map needs a tile map; one map alone is refused
+    common = [FAKE, FAKE, 1000]
+    tail = [FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 600, FAKE, 500, 64, ctypes.c_float(0.0), FAKE, None,
+            ctypes.c_size_t(0), None]
+    assert lib.pic_paged_prefill_attn(ctypes.byref(m), *common, None, None, 600, None, *tail) == -1
+    assert lib.pic_paged_prefill_attn(ctypes.byref(m), *common, FAKE, None, 600, FAKE, *tail) == -1
+    assert lib.pic_paged_prefill_attn(ctypes.byref(_model(head_dim=64)), *common, None, None, 600, FAKE,
+                                      *tail) == -1
+
+
 def test_noalloc_decode_argument_checks(lib):
     # The allocation-free decode checks like pic_decode_attn and refuses, before any launch or
     # scratch lookup, split partials larger than its per-GPU scratch array.

@@ -312,7 +312,7 @@ def test_llama8b_single_request_path():
     import paper_2607_28069_amd as pic
     assert pic.pic_prefill_workspace_bytes(wl.m1, 1, w.n_suffix, wl.max_ctx) > 0
     wl.out.zero_()
-    single_request_ttft(wl, n_requests=1, reps=1)
+    single_request_ttft(wl, n_requests=1, reps=1, chunks=[0])
     torch.cuda.synchronize()
     lay, r, Ls = wl.lay, 0, w.n_suffix
     m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]

@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import synth
-from bench import DeviceWorkload, single_request_ttft
+from bench import ZERO_COPY, DeviceWorkload, single_request_ttft
 from oracle import pic_oracle as O
 
 pytestmark = pytest.mark.gpu
@@ -87,3 +87,24 @@ def test_overlapped_lone_request_equals_sequential():
     from gpu_path import assert_attn_close
     assert_attn_close(got, ref_o, w.dtype)
     print(f"[overlap lone] layer {l} matches the oracle", flush=True)
+
+
+def test_zero_copy_lone_request_matches_oracle():
+    # the benchmark's zero-copy schedule for a request served alone (slot map + paged prefill,
+    # whole-run tiles read from the pool with the queries turned): every suffix token of two
+    # layers against the oracle, eager then graph replay (the last launch)
+    w = synth.get("c3")
+    wl = DeviceWorkload(w, DEV, n_dec=1, layers=2)
+    print(f"[zero-copy lone] {w.name} x {wl.L} layers", flush=True)
+    wl.out.zero_()
+    res = single_request_ttft(wl, n_requests=1, reps=1, chunks=[ZERO_COPY])
+    torch.cuda.synchronize()
+    assert set(res) == {ZERO_COPY}
+    from gpu_path import assert_attn_close
+    lay, r = wl.lay, 0
+    m = O.plan_layout([lay.requests[r]], lay.doc_offset, lay.doc_len, lay.doc_compile_pos)[0]
+    for l in range(wl.L):
+        K, V = O.compose_request(_host(wl.pool_k[l]), _host(wl.pool_v[l]), m, w.rope_theta, w.dtype)
+        ref_o, _, _ = O.suffix_prefill(K, V, _host(wl.q[l, r]), _host(wl.k_suf[l, r]), _host(wl.v_suf[l, r]))
+        assert_attn_close(_host(wl.out[l, r]), ref_o, w.dtype)
+        print(f"[zero-copy lone] layer {l} matches the oracle", flush=True)

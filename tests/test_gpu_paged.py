@@ -194,3 +194,53 @@ def test_paged_prefill_with_rotary_variants(pairing, runs, layout):
         assert any(tm[b, t, 0] >= 0 for b, t in ctx_tiles) and any(tm[b, t, 0] < 0 for b, t in ctx_tiles)
     print(f"[{pairing}, {layout}, {'tile map' if runs else 'per-key'}] two layers with their own "
           f"frequencies: paged == compose + prefill", flush=True)
+
+
+@pytest.mark.parametrize("pairing", ["half", "interleaved"])
+def test_tiles_composed_ahead_then_prefill_without_slot_map(pairing):
+    # pic_compose_tiles for both layers in one launch, then the paged prefill with the tile map
+    # and no slot map, against the paged prefill that composes its own tiles: identical caches
+    # and outputs (documents of 60..300 tokens, so both kinds of context tile occur; two layers
+    # with their own frequencies)
+    w = dataclasses.replace(synth.get("c2"), name="mixed", n_q_heads=28, n_kv_heads=4, pool_docs=5,
+                            doc_len=77, docs_per_request=4, n_suffix=37, prefix_len=13, batch=3,
+                            doc_len_jitter=(60, 300))
+    lay = S.pool_layout(w)
+    r = setup(w, requests=[[lay.prefix_entry, 3, 0, 4], [lay.prefix_entry], [2, 1, 0, 3, 4]], extra_cap=5)
+    d = gpu_compose(r)
+    D, L = w.head_dim, 2
+    m2 = pic.Model.of(L, w.n_q_heads, w.n_kv_heads, D, "bf16", w.rope_theta, pairing=pairing,
+                      per_layer_tables=True)
+    f = np.stack([pic.pic_rope_llama3_freq(D, 5e5), O.inv_freq(D, 1e4)])
+    table = torch.empty(pic.pic_rope_table_bytes(m2, d["mad"]) // 4, dtype=torch.float32, device=DEV)
+    pic.pic_rope_table_init_freq(m2, f, d["mad"], table)
+    pk = torch.cat([d["pool_k"], d["pool_k"].flip(-1)], 0).contiguous()
+    pv = torch.cat([d["pool_v"], d["pool_v"] * 2], 0).contiguous()
+    dt = tdtype(w)
+    q, ks, vs = (torch.cat([to_dev(r.inp[n][None], dt)] * 2, 0).contiguous() for n in ("q", "k_suf", "v_suf"))
+    max_ctx = int(r.ctx.max())
+    map_cap = max_ctx + 7
+    smap = torch.empty((w.batch, map_cap), dtype=torch.int32, device=DEV)
+    dmap = torch.empty_like(smap)
+    tmap = torch.empty((w.batch, pic.pic_slot_map_tiles(map_cap), 2), dtype=torch.int32, device=DEV)
+    pic.pic_build_slot_map(d["blocks"], d["blocks"].numel() // 5, w.batch, map_cap, smap, dmap, tmap)
+    tm = tmap.cpu().numpy()
+    assert (tm[..., 0] >= 0).any() and (tm[..., 0] < 0).any()
+    ws = torch.empty(max(pic.pic_prefill_workspace_bytes(m2, w.batch, w.n_suffix, max_ctx), 16),
+                     dtype=torch.uint8, device=DEV)
+    res = []
+    for ahead in (False, True):
+        shape = (L, w.batch, w.n_kv_heads, r.cap, D)
+        ck, cv = torch.zeros(shape, dtype=dt, device=DEV), torch.zeros(shape, dtype=dt, device=DEV)
+        out = torch.zeros((L, w.batch, w.n_suffix, w.n_q_heads, D), dtype=dt, device=DEV)
+        if ahead:
+            pic.pic_compose_tiles(m2, pk, pv, r.lay.pool_tokens, smap, dmap, map_cap, tmap, table, d["mad"],
+                                  d["ctx"], max_ctx, ck, cv, w.batch, r.cap)
+        pic.pic_paged_prefill_attn(m2, pk, pv, r.lay.pool_tokens, None if ahead else smap, None if ahead else dmap,
+                                   map_cap, table, d["mad"], q, ks, vs, ck, cv, w.batch, r.cap, d["ctx"], max_ctx,
+                                   w.n_suffix, out, ws, tile_map=tmap)
+        torch.cuda.synchronize()
+        res.append((out, ck, cv))
+    for a, b in zip(*res):
+        assert torch.equal(a, b), "composing the tiles ahead changed the result"
+    print(f"[{pairing}] tiles composed ahead for both layers: caches and outputs identical", flush=True)
