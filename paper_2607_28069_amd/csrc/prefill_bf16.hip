@@ -1088,8 +1088,10 @@ prefill_bf16_kernel(PrefillArgs a) {
 // between them (a split that saw no key of the row, reference max -inf, is dropped by a
 // select: its sums are not finite).  With n_valid (table mode), rows of tokens past
 // n_valid[b] are left untouched.
+// kBatch: splits whose loads are issued together (4, 8 or 16, the smallest that covers n_splits:
+// a larger batch holds more registers and lowers the occupancy that few splits need)
 constexpr int kCombineRowsPerWG = 16;
-constexpr int kCombineBatch = 16;
+template <int kCombineBatch>
 __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __restrict__ ws_o,
                                                               const float2* __restrict__ ws_ml,
                                                               int32_t n_splits, int64_t rows_total,
@@ -1246,10 +1248,17 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
     hipLaunchKernelGGL((prefill_bf16_kernel<kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
-  hipLaunchKernelGGL(prefill_combine_kernel,
-                     dim3((unsigned)((a.rows_total + kCombineRowsPerWG - 1) / kCombineRowsPerWG)), dim3(256), 0,
-                     stream, a.ws_o, a.ws_ml, p.n_splits, a.rows_total,
-                     mode == kModeTable ? a.n_valid : nullptr, n_q, s.n_q_heads, s.batch, a.out);
+  const dim3 cgrid((unsigned)((a.rows_total + kCombineRowsPerWG - 1) / kCombineRowsPerWG));
+  const int32_t* nv = mode == kModeTable ? a.n_valid : nullptr;
+  if (p.n_splits <= 4)
+    hipLaunchKernelGGL(prefill_combine_kernel<4>, cgrid, dim3(256), 0, stream, a.ws_o, a.ws_ml, p.n_splits,
+                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
+  else if (p.n_splits <= 8)
+    hipLaunchKernelGGL(prefill_combine_kernel<8>, cgrid, dim3(256), 0, stream, a.ws_o, a.ws_ml, p.n_splits,
+                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
+  else
+    hipLaunchKernelGGL(prefill_combine_kernel<16>, cgrid, dim3(256), 0, stream, a.ws_o, a.ws_ml, p.n_splits,
+                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
   return hipGetLastError();
 }
 
