@@ -5,7 +5,12 @@
 
 namespace pic {
 
-// Key-range splits of the prefill: enough workgroups to cover the 256 compute units in whole
+// Key-range splits of the prefill.  A launch whose (m-tile, request, kv head) units already
+// occupy half the 256 compute units is not split: under load the chip runs at its power limit,
+// where busy units speed up as others idle, so the last round's idle units cost little and the
+// partials and the combine cost more (measured: 224 units of the 32K Qwen workload 898 us
+// unsplit against 921 us in 8 key ranges; the frontier workload's 1152 units 900 against
+// 934 us in 2).  Smaller launches are split so that they cover the compute units in whole
 // rounds, each split keeping at least 8 key tiles.  Cost in units of one workgroup-tile
 // (~2 us): rounds * tiles per split, plus, for split runs, one tile (the combine launch; the
 // splits' own prologues run in parallel) and the partials each split writes and the combine
@@ -20,7 +25,7 @@ SplitPlan plan_prefill_splits(const AttnShape& s, int32_t n_suffix, int32_t max_
   const int tiles = (int)(((int64_t)max_ctx + n_suffix + kPrefillKeys - 1) / kPrefillKeys);
   int best = 1;
   double best_cost = 1e30;
-  for (int sp = 1; sp <= kPrefillMaxSplits; ++sp) {
+  for (int sp = 1; sp <= (base >= 128 ? 1 : kPrefillMaxSplits); ++sp) {
     const int tps = (tiles + sp - 1) / sp;
     if (sp > 1 && tps < 8) break;
     const int64_t rounds = (base * sp + 255) / 256;

@@ -82,13 +82,15 @@ def test_frontier_ragged_requests_and_split_keys():
     # largest): rows past a request's count stay untouched; the shape runs the key-range split
     # path (checked through the workspace the call asks for).
     w = synth.get("llama8b_frontier_1layer")
-    items = [[-40, 0, -10, 1, -20, 2, -64], [3, 4, -64], [-5, 5, -3, 6, -1], [7, 8, 9, -200]]
-    r = setup_frontier(w, items=items, n_inline_cap=200)
+    # (at most 100 inline tokens: 2 m-tiles x 4 requests x 8 kv heads = 64 units, so the
+    # launch is split over key ranges)
+    items = [[-40, 0, -10, 1, -20, 2, -30], [3, 4, -64], [-5, 5, -3, 6, -1], [7, 8, 9, -100]]
+    r = setup_frontier(w, items=items, n_inline_cap=100)
     m1 = r.model
-    assert pic.pic_frontier_workspace_bytes(m1, w.batch, 200, int(r.ctx.max())) > 0
+    assert pic.pic_frontier_workspace_bytes(m1, w.batch, 100, int(r.ctx.max())) > 0
     out, n_inl = gpu_frontier(r, sentinel=7.0)
     torch.cuda.synchronize()
-    assert list(n_inl) == [134, 64, 9, 200]
+    assert list(n_inl) == [100, 64, 9, 100]
     for _ in _check_cache_and_out(r, out, n_inl):
         pass
     o = host(out[0])
