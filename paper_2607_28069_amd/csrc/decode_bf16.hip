@@ -388,7 +388,10 @@ decode_bf16_kernel(DecodeArgs a) {
   }
 }
 
-// grid (B * Hq, L), 64 threads: merge the splits of one query head by log-sum-exp.
+// grid (B * Hq, L), 64 threads: merge the splits of one query head by log-sum-exp.  The loads
+// of kCombineBatch splits are issued together before any is used (one pass for the maximum,
+// one for the weighted sums); a split that saw no key (maximum -inf) adds nothing.
+constexpr int kCombineBatch = 8;
 __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restrict__ ws_o,
                                                             const float* __restrict__ ws_ml,
                                                             int32_t n_splits, int64_t rows_per_layer,
@@ -396,17 +399,32 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
   const int64_t row = (int64_t)blockIdx.y * rows_per_layer + blockIdx.x;
   const float* ml = ws_ml + row * n_splits * 2;
   float M = -INFINITY;
-  for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml[2 * s]);
+  for (int s0 = 0; s0 < n_splits; s0 += kCombineBatch) {
+    float mv[kCombineBatch];
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) mv[u] = s0 + u < n_splits ? ml[2 * (s0 + u)] : -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) M = fmaxf(M, mv[u]);
+  }
   float den = 0.f, o0 = 0.f, o1 = 0.f;
   const int d = 2 * threadIdx.x;
-  for (int s = 0; s < n_splits; ++s) {
-    const float ms = ml[2 * s];
-    if (ms == -INFINITY) continue;
-    const float w = __builtin_amdgcn_exp2f(ms - M);
-    den += w * ml[2 * s + 1];
-    const float2 o = *reinterpret_cast<const float2*>(ws_o + (row * n_splits + s) * kHD + d);
-    o0 += w * o.x;
-    o1 += w * o.y;
+  for (int s0 = 0; s0 < n_splits; s0 += kCombineBatch) {
+    float2 mlv[kCombineBatch], ov[kCombineBatch];
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) {
+      const int s = s0 + u;
+      mlv[u] = s < n_splits ? *reinterpret_cast<const float2*>(ml + 2 * s) : make_float2(-INFINITY, 0.f);
+      ov[u] = s < n_splits ? *reinterpret_cast<const float2*>(ws_o + (row * n_splits + s) * kHD + d)
+                           : make_float2(0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) {
+      if (mlv[u].x == -INFINITY) continue;
+      const float w = __builtin_amdgcn_exp2f(mlv[u].x - M);
+      den += w * mlv[u].y;
+      o0 += w * ov[u].x;
+      o1 += w * ov[u].y;
+    }
   }
   const float inv = 1.f / den;
   reinterpret_cast<uint32_t*>(out + row * kHD)[threadIdx.x] = pack_bf16x2(o0 * inv, o1 * inv);
