@@ -66,6 +66,10 @@ def parse(argv=None):
     p.add_argument("--no-overlap", action="store_true",
                    help="skip the overlapped-schedule TTFT timing (profiling runs: it launches the "
                         "prefill kernel again, sharing the GPU with compose)")
+    p.add_argument("--lone-only", default=None, metavar="SCHEDULES",
+                   help="only time one request served alone, with these comma-separated schedules "
+                        "(0: compose then prefill, n > 0: compose overlapped in chunks of n layers, "
+                        "-1: zero-copy), and print their medians (profiling runs of that path)")
     p.add_argument("--copy-calib-gib", type=float, default=0.0,
                    help="also run a plain device copy of this size per step (counter calibration)")
     return p.parse_args(argv)
@@ -833,6 +837,20 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     n_dec = args.decode_tokens if args.decode_tokens is not None else (w.decode_steps or 1)
+    if args.lone_only is not None:   # the lone-request path alone
+        chunks = [int(x) for x in args.lone_only.split(",") if x]
+        wl = DeviceWorkload(w, dev, 1, paged=args.paged, fused_rope=args.fused_rope,
+                            shared_compose=not args.per_block_compose)
+        torch.cuda.synchronize()
+        gc.collect()
+        gc.disable()
+        try:
+            res = single_request_ttft(wl, n_requests=1, reps=5, chunks=chunks)
+        finally:
+            gc.enable()
+        print(json.dumps({"workload": w.name, "unit": "ms", "lone_request_ttft":
+                          {str(c): {"eager": e, "graph": g} for c, (e, g) in res.items()}}), flush=True)
+        return
     wl, fig = measure(w, dev, args.steps, args.warmup, n_dec, paged=args.paged, fused_rope=args.fused_rope,
                       per_block=args.per_block_compose, single=not args.no_single_request,
                       calib_gib=args.copy_calib_gib, overlap=not args.no_overlap,
