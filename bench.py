@@ -321,7 +321,7 @@ class DeviceWorkload:
         """Layer l's prefill call over the batch (the mode of this workload)."""
         import paper_2607_28069_amd as pic
 
-        w, B, Ls, lay, block = self.w, self.w.batch, self.Ls, self.lay, self.table_block
+        B, Ls, lay, block = self.w.batch, self.Ls, self.lay, self.table_block
         if self.paged:
             ahead = self.tiles_ahead
             pic.pic_paged_prefill_attn(self.m1, self.pool_k[l], self.pool_v[l], lay.pool_tokens,
@@ -377,7 +377,7 @@ class DeviceWorkload:
 
         import paper_2607_28069_amd as pic
 
-        w, L, B, Ls = self.w, self.L, self.w.batch, self.Ls
+        L, B, Ls = self.L, self.w.batch, self.Ls
         stream = torch.cuda.current_stream()
         ev = lambda: torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
