@@ -183,7 +183,8 @@ pic_status pic_rope_llama3_freq(int32_t head_dim, double theta, double factor,
    with |delta| <= max_abs_delta (a larger entry is clamped to the table), table from
    pic_rope_table_init(_freq) for this model and max_abs_delta.  model->n_layers is ignored
    (fold layers into n_tokens); the first table block is used, so with per-layer tables
-   pass a pointer to layer l's block (l * (max_abs_delta + 1) * D/2 float pairs in). */
+   pass a pointer to layer l's block (l * (max_abs_delta + 1) * D/2 float pairs in).
+   n_tokens * n_heads above 2^48 rows fails with PIC_ERR_RANGE. */
 pic_status pic_rerotate_keys(const pic_model* model, const void* k_in, void* k_out,
                              int64_t n_tokens, int32_t n_heads, const int32_t* delta,
                              const void* table, int32_t max_abs_delta, void* stream);

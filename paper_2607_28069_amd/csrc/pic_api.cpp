@@ -75,6 +75,8 @@ pic_status check_model(const pic_model* m) {
 int32_t n_tables(const pic_model* m) { return m->rope_tables > 1 ? m->rope_tables : 1; }
 
 constexpr int32_t kMaxAbsDelta = 1 << 20;
+// Rows one re-rotation call may cover: their element offsets stay far inside int64.
+constexpr int64_t kMaxRerotateRows = int64_t(1) << 48;
 // The bf16 attention kernels address a cache stream (one layer, request and kv head), one
 // request's suffix rows and a pool head (one layer and kv head) with 32-bit byte offsets from
 // a buffer base: each must stay under 2^32 bytes (rows of 256 bytes).
@@ -401,6 +403,8 @@ PIC_API pic_status pic_rerotate_keys(const pic_model* model, const void* k_in, v
                                      const void* table, int32_t max_abs_delta, void* stream) {
   PIC_CHECK(check_model(model));
   if (n_tokens < 0 || n_heads <= 0) return fail(PIC_ERR_INVALID_ARG, "n_tokens < 0 or n_heads < 1");
+  if (n_tokens > kMaxRerotateRows / n_heads)
+    return fail(PIC_ERR_RANGE, "n_tokens * n_heads exceeds %lld rows", (long long)kMaxRerotateRows);
   if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
     return fail(PIC_ERR_RANGE, "max_abs_delta %d outside [0, %d]", max_abs_delta, kMaxAbsDelta);
   if (n_tokens == 0) return ok();

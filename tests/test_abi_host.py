@@ -289,6 +289,7 @@ def test_argument_checks_fail_before_any_launch(lib):
 
     assert lib.pic_rerotate_keys(ctypes.byref(m), FAKE, FAKE, 10, 8, None, FAKE, 10, None) == -1
     assert lib.pic_rerotate_keys(ctypes.byref(m), MIS, FAKE, 10, 8, FAKE, FAKE, 10, None) == -5
+    assert lib.pic_rerotate_keys(ctypes.byref(m), FAKE, FAKE, 1 << 62, 8, FAKE, FAKE, 10, None) == -6
     assert lib.pic_rope_table_init(ctypes.byref(m), 10, FAKE, 16, None) == -4
     assert lib.pic_rope_table_init(ctypes.byref(_model(rope_theta=0.5)), 10, FAKE, 1 << 20, None) == -1
 
