@@ -111,3 +111,51 @@ def test_decode_more_than_16_query_heads_per_kv_head(n_q_heads, n_splits):
         torch.cuda.synchronize()
         assert np.array_equal(host(o)[0], outs[t]), t
     assert torch.equal(ck, r.dev["cache_k"]) and torch.equal(cv, r.dev["cache_v"])
+
+
+def test_largest_cache_stream():
+    # One (request, kv head) cache stream of 2^24 - 1 rows of 256 bytes: the most the matrix-core
+    # prefill addresses with 32-bit byte offsets from a stream's base (larger caches fail with
+    # PIC_ERR_UNSUPPORTED).  The context fills every slot before the suffix and one decode step
+    # writes and reads the very last slot; sampled suffix tokens (all heads) and the decode step
+    # against the oracle, the stored suffix rows bit-exact.
+    w = dataclasses.replace(synth.get("c2"), name="largest_stream", n_q_heads=4, n_kv_heads=1, batch=1,
+                            n_suffix=16)
+    cap = (1 << 24) - 1
+    Ls, Hq, D = w.n_suffix, w.n_q_heads, w.head_dim
+    ctx = cap - 1 - Ls
+    m = pic.Model.of(1, Hq, 1, D, "bf16", w.rope_theta)
+    with pytest.raises(pic.PicError):
+        pic.pic_suffix_prefill_attn(m, *([torch.empty(16, dtype=torch.bfloat16, device=DEV)] * 5), 1, cap + 1,
+                                    torch.zeros(1, dtype=torch.int32, device=DEV), ctx, Ls,
+                                    torch.empty(16, dtype=torch.bfloat16, device=DEV))
+    bf = torch.bfloat16
+    gen = lambda name, shape: S.device_normal(w, name, shape, 0, DEV, bf)
+    ck, cv = gen("cache_k", (1, 1, 1, cap, D)), gen("cache_v", (1, 1, 1, cap, D))
+    q, ks, vs = gen("q", (1, 1, Ls, Hq, D)), gen("k_suf", (1, 1, Ls, 1, D)), gen("v_suf", (1, 1, Ls, 1, D))
+    dq, dk, dv = gen("dq", (1, 1, Hq, D)), gen("dk", (1, 1, 1, D)), gen("dv", (1, 1, 1, D))
+    # the oracle's keys and values: the generated context, then the suffix and decode inputs
+    K = host(ck[0, 0]).astype(np.float64)
+    V = host(cv[0, 0]).astype(np.float64)
+    K[0, ctx:ctx + Ls], V[0, ctx:ctx + Ls] = host(ks[0, 0, :, 0]), host(vs[0, 0, :, 0])
+    K[0, cap - 1], V[0, cap - 1] = host(dk[0, 0, 0]), host(dv[0, 0, 0])
+    print(f"[largest stream] cap={cap} ctx={ctx} Ls={Ls}", flush=True)
+
+    ctx_dev = torch.tensor([ctx], dtype=torch.int32, device=DEV)
+    out = torch.zeros((1, 1, Ls, Hq, D), dtype=bf, device=DEV)
+    ws = torch.empty(max(pic.pic_prefill_workspace_bytes(m, 1, Ls, ctx), 16), dtype=torch.uint8, device=DEV)
+    pic.pic_suffix_prefill_attn(m, q, ks, vs, ck, cv, 1, cap, ctx_dev, ctx, Ls, out, ws)
+    base = torch.tensor([ctx + Ls], dtype=torch.int32, device=DEV)
+    dout = torch.zeros((1, 1, Hq, D), dtype=bf, device=DEV)
+    dws = torch.empty(max(pic.pic_decode_workspace_bytes(m, 1, ctx + Ls + 1), 16), dtype=torch.uint8, device=DEV)
+    pic.pic_decode_attn(m, dq, dk, dv, ck, cv, 1, cap, base, 0, ctx + Ls, dout, dws)
+    torch.cuda.synchronize()
+    assert torch.equal(ck[0, 0, 0, ctx:ctx + Ls], ks[0, 0, :, 0]) and torch.equal(cv[0, 0, 0, ctx:ctx + Ls], vs[0, 0, :, 0])
+    assert torch.equal(ck[0, 0, 0, cap - 1], dk[0, 0, 0]) and torch.equal(cv[0, 0, 0, cap - 1], dv[0, 0, 0])
+
+    toks = np.array([0, Ls - 1])
+    qh = np.transpose(host(q)[0, 0][toks], (1, 0, 2))                       # [Hq][2][D]
+    ref = O.attention(qh, ctx + toks, K, V, np.arange(cap))
+    assert_attn_close(np.transpose(host(out)[0, 0][toks], (1, 0, 2)), ref, "bf16")
+    ref = O.attention(host(dq)[0, 0][:, None], [cap - 1], K, V, np.arange(cap))[:, 0]
+    assert_attn_close(host(dout)[0, 0], ref, "bf16")
