@@ -125,10 +125,11 @@ def test_largest_cache_stream():
     Ls, Hq, D = w.n_suffix, w.n_q_heads, w.head_dim
     ctx = cap - 1 - Ls
     m = pic.Model.of(1, Hq, 1, D, "bf16", w.rope_theta)
-    with pytest.raises(pic.PicError):
+    with pytest.raises(pic.PicError, match="exceeds") as err:
         pic.pic_suffix_prefill_attn(m, *([torch.empty(16, dtype=torch.bfloat16, device=DEV)] * 5), 1, cap + 1,
                                     torch.zeros(1, dtype=torch.int32, device=DEV), ctx, Ls,
                                     torch.empty(16, dtype=torch.bfloat16, device=DEV))
+    assert err.value.status == -2                      # PIC_ERR_UNSUPPORTED
     bf = torch.bfloat16
     gen = lambda name, shape: S.device_normal(w, name, shape, 0, DEV, bf)
     ck, cv = gen("cache_k", (1, 1, 1, cap, D)), gen("cache_v", (1, 1, 1, cap, D))

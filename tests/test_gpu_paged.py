@@ -23,8 +23,8 @@ import synth
 from oracle import pic_oracle as O
 from synth import inputs as S
 
-from gpu_path import (DEV, assert_attn_close, gpu_compose, gpu_prefill, host, oracle_prefill, setup,
-                      tdtype, to_dev)
+from gpu_path import (DEV, assert_attn_close, assert_keys_close, gpu_compose, gpu_prefill, host, oracle_prefill,
+                      setup, tdtype, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -244,3 +244,71 @@ def test_tiles_composed_ahead_then_prefill_without_slot_map(pairing):
     for a, b in zip(*res):
         assert torch.equal(a, b), "composing the tiles ahead changed the result"
     print(f"[{pairing}] tiles composed ahead for both layers: caches and outputs identical", flush=True)
+
+
+def test_paged_prefill_on_the_largest_pool_head():
+    # A pool head of 2^24 - 1 tokens: the most the paged prefill addresses with 32-bit byte
+    # offsets from a head's base (a larger pool fails with PIC_ERR_UNSUPPORTED).  The request
+    # places a 64-token entry from the bottom of the pool and a 1000-token entry ending at its
+    # last token, moved by 64 positions.  Per-key mode bit-identical to compose + prefill; whole-run
+    # mode (the tile map) and both against the oracle, which composes the same pool rows.
+    w = dataclasses.replace(synth.get("c2"), name="largest_pool", n_q_heads=4, n_kv_heads=1, batch=1, n_suffix=16)
+    T = (1 << 24) - 1
+    Ls, Hq, D = w.n_suffix, w.n_q_heads, w.head_dim
+    m = pic.Model.of(1, Hq, 1, D, "bf16", w.rope_theta)
+    bf = torch.bfloat16
+    gen = lambda name, shape: S.device_normal(w, name, shape, 0, DEV, bf)
+    pool_k, pool_v = gen("pool_k", (1, 1, T, D)), gen("pool_v", (1, 1, T, D))
+    q, ks, vs = gen("q", (1, 1, Ls, Hq, D)), gen("k_suf", (1, 1, Ls, 1, D)), gen("v_suf", (1, 1, Ls, 1, D))
+    offs, lens = [0, T - 1000], [64, 1000]
+    blocks, ctx_h = pic.pic_plan_layout([[0, 1]], offs, lens, [0, 0], T)
+    ctx = int(ctx_h[0])
+    assert ctx == 1064
+    cap = ctx + Ls
+    mad = cap
+    table = torch.empty(pic.pic_rope_table_bytes(m, mad) // 4, dtype=torch.float32, device=DEV)
+    pic.pic_rope_table_init(m, mad, table)
+    blk = torch.from_numpy(blocks.view(np.int32).reshape(-1).copy()).to(DEV)
+    ctx_dev = torch.tensor([ctx], dtype=torch.int32, device=DEV)
+    ws = torch.empty(max(pic.pic_prefill_workspace_bytes(m, 1, Ls, ctx), 16), dtype=torch.uint8, device=DEV)
+    with pytest.raises(pic.PicError, match="exceeds") as err:
+        pic.pic_paged_prefill_attn(m, pool_k, pool_v, T + 1, ctx_dev, ctx_dev, ctx, table, mad, q, ks, vs,
+                                   pool_k, pool_v, 1, cap, ctx_dev, ctx, Ls, q, ws)
+    assert err.value.status == -2                      # PIC_ERR_UNSUPPORTED
+
+    def caches():
+        return (torch.zeros((1, 1, 1, cap, D), dtype=bf, device=DEV), torch.zeros((1, 1, 1, cap, D), dtype=bf, device=DEV))
+
+    # compose + prefill
+    ck_m, cv_m = caches()
+    out_m = torch.zeros((1, 1, Ls, Hq, D), dtype=bf, device=DEV)
+    pic.pic_compose(m, pool_k, pool_v, T, blk, len(blocks), table, mad, ck_m, cv_m, 1, cap)
+    pic.pic_suffix_prefill_attn(m, q, ks, vs, ck_m, cv_m, 1, cap, ctx_dev, ctx, Ls, out_m, ws)
+    # paged, per key and with the tile map
+    smap = torch.zeros((1, ctx), dtype=torch.int32, device=DEV)
+    dmap = torch.zeros((1, ctx), dtype=torch.int32, device=DEV)
+    tmap = torch.zeros((1, pic.pic_slot_map_tiles(ctx), 2), dtype=torch.int32, device=DEV)
+    pic.pic_build_slot_map(blk, len(blocks), 1, ctx, smap, dmap, tmap)
+    outs = {}
+    for runs in (False, True):
+        ck, cv = caches()
+        o = torch.zeros((1, 1, Ls, Hq, D), dtype=bf, device=DEV)
+        pic.pic_paged_prefill_attn(m, pool_k, pool_v, T, smap, dmap, ctx, table, mad, q, ks, vs, ck, cv, 1, cap,
+                                   ctx_dev, ctx, Ls, o, ws, tile_map=tmap if runs else None)
+        torch.cuda.synchronize()
+        assert torch.equal(ck[..., ctx:, :], ck_m[..., ctx:, :]) and torch.equal(cv[..., ctx:, :], cv_m[..., ctx:, :])
+        outs[runs] = o
+    tm = tmap.cpu().numpy()
+    assert np.array_equal(tm[0, :16, 0], np.r_[0, T - 1000 + 64 * np.arange(15)]) and (tm[0, 16] == [-1, 0]).all()
+    assert torch.equal(outs[False], out_m), "per-key paged prefill differs from compose + prefill"
+
+    # the oracle, from the pool rows the request reads (bottom 64 and top 1000 tokens)
+    pk = np.concatenate([host(pool_k[0, :, :64]), host(pool_k[0, :, T - 1000:])], axis=1)
+    pv = np.concatenate([host(pool_v[0, :, :64]), host(pool_v[0, :, T - 1000:])], axis=1)
+    rmap = O.plan_layout([[0, 1]], [0, 64], lens, [0, 0])[0]
+    K, V = O.compose_request(pk, pv, rmap, w.rope_theta, "bf16")
+    assert_keys_close(host(ck_m[0, 0])[:, :ctx], K, "bf16")
+    assert np.array_equal(host(cv_m[0, 0])[:, :ctx], V)
+    ref, _, _ = O.suffix_prefill(K, V, host(q)[0, 0], host(ks)[0, 0], host(vs)[0, 0])
+    for runs in (False, True):
+        assert_attn_close(host(outs[runs])[0, 0], ref, "bf16")
