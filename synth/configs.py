@@ -10,7 +10,7 @@ arithmetic and is shared by the oracle-side tests and the GPU path.
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 
 
 @dataclass(frozen=True)
