@@ -92,7 +92,7 @@ def gpu_compose(r: Run, max_abs_delta=None, blocks=None):
     return d
 
 
-def gpu_prefill(r: Run):
+def gpu_prefill(r: Run, scale: float = 0.0):
     w, dt, d = r.w, tdtype(r.w), r.dev
     d["q"] = to_dev(r.inp["q"][None], dt)
     d["k_suf"] = to_dev(r.inp["k_suf"][None], dt)
@@ -101,11 +101,11 @@ def gpu_prefill(r: Run):
     nbytes = pic.pic_prefill_workspace_bytes(r.model, w.batch, w.n_suffix, int(r.ctx.max()))
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=DEV)
     pic.pic_suffix_prefill_attn(r.model, d["q"], d["k_suf"], d["v_suf"], d["cache_k"], d["cache_v"],
-                                w.batch, r.cap, d["ctx"], int(r.ctx.max()), w.n_suffix, d["out"], ws)
+                                w.batch, r.cap, d["ctx"], int(r.ctx.max()), w.n_suffix, d["out"], ws, scale=scale)
     return d["out"]
 
 
-def gpu_decode(r: Run, steps: int, n_splits: int = 0):
+def gpu_decode(r: Run, steps: int, n_splits: int = 0, scale: float = 0.0):
     """Decode steps after the prefilled suffix; returns list of [B][Hq][D] outputs."""
     w, dt, d = r.w, tdtype(r.w), r.dev
     base = r.ctx + w.n_suffix
@@ -120,7 +120,7 @@ def gpu_decode(r: Run, steps: int, n_splits: int = 0):
         v = to_dev(r.inp["dv"][t][None], dt)
         out = torch.zeros((1, w.batch, w.n_q_heads, w.head_dim), dtype=dt, device=DEV)
         pic.pic_decode_attn(r.model, q, k, v, d["cache_k"], d["cache_v"], w.batch, r.cap, d["base"], t,
-                            max_base, out, ws, n_splits=n_splits)
+                            max_base, out, ws, n_splits=n_splits, scale=scale)
         outs.append(out)
     return outs
 
@@ -129,9 +129,9 @@ def oracle_compose(r: Run, b: int):
     return O.compose_request(r.pool_k, r.inp["pool_v"], r.maps[b], r.w.rope_theta, r.w.dtype)
 
 
-def oracle_prefill(r: Run, b: int):
+def oracle_prefill(r: Run, b: int, scale: float | None = None):
     K, V = oracle_compose(r, b)
-    out, K2, V2 = O.suffix_prefill(K, V, r.inp["q"][b], r.inp["k_suf"][b], r.inp["v_suf"][b])
+    out, K2, V2 = O.suffix_prefill(K, V, r.inp["q"][b], r.inp["k_suf"][b], r.inp["v_suf"][b], scale)
     return out, K2, V2
 
 
@@ -162,7 +162,7 @@ def setup_frontier(w: Workload, items=None, n_inline_cap=None, mutate=None) -> R
     return r
 
 
-def gpu_frontier(r: Run, sentinel: float = 0.0):
+def gpu_frontier(r: Run, sentinel: float = 0.0, scale: float = 0.0):
     """Plan (C ABI), compose, frontier prefill; returns (out [1][B][n][Hq][D], n_inline)."""
     w, dt = r.w, tdtype(r.w)
     blocks, total, inl, n_inl = pic.pic_plan_frontier(r.lay.items, r.lay.doc_offset, r.lay.doc_len,
@@ -183,16 +183,16 @@ def gpu_frontier(r: Run, sentinel: float = 0.0):
     nbytes = pic.pic_frontier_workspace_bytes(r.model, w.batch, n, max_len)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=DEV)
     pic.pic_frontier_prefill_attn(r.model, d["q"], d["k_inl"], d["v_inl"], d["cache_k"], d["cache_v"],
-                                  w.batch, r.cap, d["pos"], d["n_valid"], n, max_len, d["out"], ws)
+                                  w.batch, r.cap, d["pos"], d["n_valid"], n, max_len, d["out"], ws, scale=scale)
     return d["out"], n_inl
 
 
-def oracle_frontier(r: Run, b: int):
+def oracle_frontier(r: Run, b: int, scale: float | None = None):
     """(out [n_b][Hq][D], K, V [Hkv][total][D]) of request b from the oracle."""
     f = r.fmaps[b]
     Kc, Vc = O.compose_request(r.pool_k, r.inp["pool_v"], f.cached, r.w.rope_theta, r.w.dtype)
     n = f.inline_pos.size
-    return O.frontier_prefill(Kc, Vc, f, r.inp["q"][b][:n], r.inp["k_suf"][b][:n], r.inp["v_suf"][b][:n])
+    return O.frontier_prefill(Kc, Vc, f, r.inp["q"][b][:n], r.inp["k_suf"][b][:n], r.inp["v_suf"][b][:n], scale)
 
 
 def bf16_ulp(x: np.ndarray) -> np.ndarray:

@@ -44,7 +44,7 @@ def _expected_tile_map(sm, dm, map_cap):
     return out
 
 
-def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, layers=1, runs=False):
+def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, layers=1, runs=False, scale=0.0):
     """Slot map + paged prefill of run r on fresh (zeroed) caches; returns (out, cache_k, cache_v).
     runs: also build the tile map and pass it (whole-run tiles turn the queries)."""
     w, d, dt = r.w, r.dev, tdtype(r.w)
@@ -65,7 +65,7 @@ def _paged(r, model=None, cache_k=None, cache_v=None, pool_k=None, pool_v=None, 
     pic.pic_paged_prefill_attn(m, d["pool_k"] if pool_k is None else pool_k,
                                d["pool_v"] if pool_v is None else pool_v, r.lay.pool_tokens, smap, dmap, map_cap,
                                d["table"], d["mad"], d["q"], d["k_suf"], d["v_suf"], ck, cv, w.batch, r.cap,
-                               d["ctx"], max_ctx, w.n_suffix, out, ws, tile_map=tmap)
+                               d["ctx"], max_ctx, w.n_suffix, out, ws, scale=scale, tile_map=tmap)
     # the map: pool token and shift of every composed slot, 0 / 0 past each context
     sm, dm = smap.cpu().numpy(), dmap.cpu().numpy()
     for b, mp in enumerate(r.maps):
