@@ -6,7 +6,7 @@ turn them inside the kernels.  They must equal, bit for bit, turning the same ro
 pic_rerotate_keys first and calling the plain kernels (outputs and cache), and match the oracle,
 which rotates with its own float64 R(p), within the attention tolerance.  Both pairings, one
 table for all layers and one table per layer, ragged contexts and a suffix that is not a
-multiple of the key tile.
+multiple of the key tile; the per-layer cases also pass a softmax scale other than 1/sqrt(D).
 """
 import numpy as np
 import pytest
@@ -51,6 +51,7 @@ def _bf16(shape):
 @pytest.mark.parametrize("pairing", ["half", "interleaved"])
 def test_fused_rope_prefill(pairing, per_layer):
     B, Ls = 3, 37
+    scale = 0.05 if per_layer else 0.0
     ctx = np.array([700, 2501, 1], np.int32)
     max_ctx, cap = int(ctx.max()), int(ctx.max()) + Ls + 3
     mad = max_ctx + Ls
@@ -68,7 +69,8 @@ def test_fused_rope_prefill(pairing, per_layer):
     # fused
     ck_a, cv_a = ck.clone(), cv.clone()
     out_a = torch.zeros((L, B, Ls, HQ, D), dtype=torch.bfloat16, device=DEV)
-    pic.pic_suffix_prefill_attn_rope(m, dq, dk, dv, ck_a, cv_a, B, cap, ctx_d, max_ctx, Ls, table, mad, out_a, ws)
+    pic.pic_suffix_prefill_attn_rope(m, dq, dk, dv, ck_a, cv_a, B, cap, ctx_d, max_ctx, Ls, table, mad, out_a, ws,
+                                     scale=scale)
     # turned first, then the plain kernel
     pos = (ctx[:, None] + np.arange(Ls)[None, :]).reshape(-1)          # [B * Ls]
     q_rot = torch.stack([_rerotate_rows(m1, dq[l].reshape(B * Ls, HQ, D), pos, table[l * block:], mad)
@@ -77,7 +79,7 @@ def test_fused_rope_prefill(pairing, per_layer):
                          for l in range(L)]).reshape(dk.shape)
     ck_b, cv_b = ck.clone(), cv.clone()
     out_b = torch.zeros_like(out_a)
-    pic.pic_suffix_prefill_attn(m, q_rot, k_rot, dv, ck_b, cv_b, B, cap, ctx_d, max_ctx, Ls, out_b, ws)
+    pic.pic_suffix_prefill_attn(m, q_rot, k_rot, dv, ck_b, cv_b, B, cap, ctx_d, max_ctx, Ls, out_b, ws, scale=scale)
     torch.cuda.synchronize()
     assert torch.equal(out_a, out_b), "fused-RoPE prefill differs from turn-then-prefill"
     assert torch.equal(ck_a, ck_b) and torch.equal(cv_a, cv_b), "caches differ"
@@ -92,7 +94,7 @@ def test_fused_rope_prefill(pairing, per_layer):
         kr = O.store(O.rope(np.transpose(k_raw[l, b], (1, 0, 2)), p, 0.0, pairing, freqs[l]), "bf16")
         Kf = np.concatenate([ckh[l, b][:, :n], kr], axis=1)
         Vf = np.concatenate([cvh[l, b][:, :n], np.transpose(v[l, b], (1, 0, 2))], axis=1)
-        ref = O.attention(qr, p, Kf, Vf, np.arange(n + Ls))
+        ref = O.attention(qr, p, Kf, Vf, np.arange(n + Ls), scale or None)
         assert_attn_close(np.transpose(got[l, b], (1, 0, 2)), ref, "bf16")
     print("fused == turned + plain (bitwise), oracle ok", flush=True)
 
@@ -101,6 +103,7 @@ def test_fused_rope_prefill(pairing, per_layer):
 @pytest.mark.parametrize("pairing", ["half", "interleaved"])
 def test_fused_rope_decode(pairing, per_layer):
     B, steps = 4, 2
+    scale = 0.05 if per_layer else 0.0
     base = np.array([5000, 37, 12000, 64], np.int32)
     max_base = int(base.max())
     cap, mad = max_base + steps + 5, max_base + steps
@@ -118,13 +121,13 @@ def test_fused_rope_decode(pairing, per_layer):
             dq, dk, dv = (to_dev(x, torch.bfloat16) for x in (q_raw, k_raw, v))
             out_a = torch.zeros((L, B, HQ, D), dtype=torch.bfloat16, device=DEV)
             pic.pic_decode_attn_rope(m, dq, dk, dv, ck_a, cv_a, B, cap, base_d, t, max_base, table, mad, out_a, ws,
-                                     n_splits=split)
+                                     n_splits=split, scale=scale)
             pos = base + t
             q_rot = torch.stack([_rerotate_rows(m1, dq[l], pos, table[l * block:], mad) for l in range(L)])
             k_rot = torch.stack([_rerotate_rows(m1, dk[l], pos, table[l * block:], mad) for l in range(L)])
             out_b = torch.zeros_like(out_a)
             pic.pic_decode_attn(m, q_rot, k_rot, dv, ck_b, cv_b, B, cap, base_d, t, max_base, out_b, ws,
-                                n_splits=split)
+                                n_splits=split, scale=scale)
             torch.cuda.synchronize()
             assert torch.equal(out_a, out_b), f"split {split} step {t}: fused-RoPE decode differs"
             assert torch.equal(ck_a, ck_b) and torch.equal(cv_a, cv_b), f"split {split} step {t}: caches differ"
@@ -137,6 +140,6 @@ def test_fused_rope_decode(pairing, per_layer):
                 kr = O.store(O.rope(k_raw[l, b][:, None, :], np.array([p]), 0.0, pairing, freqs[l]), "bf16")
                 assert_keys_close(ckh[l, b][:, p:p + 1], kr, "bf16")   # the stored key, turned
                 ref = O.attention(qr[:, None, :], np.array([p]), ckh[l, b][:, :p + 1], cvh[l, b][:, :p + 1],
-                                  np.arange(p + 1))[:, 0]
+                                  np.arange(p + 1), scale or None)[:, 0]
                 assert_attn_close(got[l, b], ref, "bf16")
         print(f"[{pairing}] split {split}: fused decode == turned + plain, oracle ok", flush=True)

@@ -107,7 +107,11 @@ def test_rerotate_keys_standalone():
         pic.pic_rerotate_keys(m, kin, kout, n, H, torch.from_numpy(delta).to(DEV), table, mad)
         ref = O.store(O.rerotate_keys(np.transpose(k, (1, 0, 2)), a, b, 5e5), dtype)
         assert_keys_close(np.transpose(host(kout), (1, 0, 2)), ref, dtype)
-        # delta 0 leaves keys bit-identical; in place is allowed
+        # in place gives the same keys as out of place
+        kin2 = kin.clone()
+        pic.pic_rerotate_keys(m, kin2, kin2, n, H, torch.from_numpy(delta).to(DEV), table, mad)
+        assert torch.equal(kin2, kout)
+        # delta 0 leaves keys bit-identical
         zero = torch.zeros(n, dtype=torch.int32, device=DEV)
         pic.pic_rerotate_keys(m, kin, kin, n, H, zero, table, mad)
         assert np.array_equal(host(kin).view(np.uint32), k.view(np.uint32))
