@@ -1,7 +1,9 @@
 """Degenerate and extreme cases on the GPU, against the oracle: a request that composes
 nothing (empty context: the suffix attends only to itself), a single-token suffix, a single
-suffix token with a one-token context, keys moved by the largest supported shift, and calls
-that have nothing to do (they launch nothing and leave outputs untouched)."""
+suffix token with a one-token context, keys moved by the largest supported shift, calls that
+have nothing to do (they launch nothing and leave outputs untouched), decode with more than 16
+query heads per kv head (plain, allocation-free and fused RoPE), and the largest cache stream the
+prefill addresses."""
 import dataclasses
 
 import numpy as np
@@ -160,3 +162,44 @@ def test_largest_cache_stream():
     assert_attn_close(np.transpose(host(out)[0, 0][toks], (1, 0, 2)), ref, "bf16")
     ref = O.attention(host(dq)[0, 0][:, None], [cap - 1], K, V, np.arange(cap))[:, 0]
     assert_attn_close(host(dout)[0, 0], ref, "bf16")
+
+
+@pytest.mark.parametrize("pairing", ["half", "interleaved"])
+def test_fused_rope_decode_more_than_16_query_heads_per_kv_head(pairing):
+    # 20 query heads per kv head (two head groups, each streaming the context; only the first
+    # stores the new token) with fused RoPE, split and unsplit: bit-identical to turning q and
+    # the new key with pic_rerotate_keys and calling the plain decode
+    Hq, Hkv, D, B, steps = 40, 2, 128, 3, 2
+    base = np.array([900, 33, 2100], np.int32)
+    max_base = int(base.max())
+    cap, mad = max_base + steps + 3, max_base + steps
+    m = pic.Model.of(1, Hq, Hkv, D, "bf16", 5e5, pairing=pairing)
+    table = torch.empty(pic.pic_rope_table_bytes(m, mad) // 4, dtype=torch.float32, device=DEV)
+    pic.pic_rope_table_init(m, mad, table)
+    rng = np.random.default_rng(5)
+    bf = lambda shape: to_dev(O.store(rng.standard_normal(shape), "bf16"), torch.bfloat16)
+    ck, cv = bf((1, B, Hkv, cap, D)), bf((1, B, Hkv, cap, D))
+    base_d = torch.from_numpy(base).to(DEV)
+
+    def turned(x, pos):
+        y = torch.empty_like(x)
+        pic.pic_rerotate_keys(m, x, y, x.shape[0], x.shape[1], torch.from_numpy(pos.astype(np.int32)).to(DEV),
+                              table, mad)
+        return y
+
+    for split in (0, 3):
+        ck_a, cv_a, ck_b, cv_b = ck.clone(), cv.clone(), ck.clone(), cv.clone()
+        ws = torch.zeros(max(pic.pic_decode_workspace_bytes(m, B, max_base + steps, split), 16), dtype=torch.uint8,
+                         device=DEV)
+        for t in range(steps):
+            q, k, v = bf((1, B, Hq, D)), bf((1, B, Hkv, D)), bf((1, B, Hkv, D))
+            out_a = torch.zeros((1, B, Hq, D), dtype=torch.bfloat16, device=DEV)
+            pic.pic_decode_attn_rope(m, q, k, v, ck_a, cv_a, B, cap, base_d, t, max_base, table, mad, out_a, ws,
+                                     n_splits=split)
+            out_b = torch.zeros_like(out_a)
+            pos = base + t
+            pic.pic_decode_attn(m, turned(q[0], pos)[None], turned(k[0], pos)[None], v, ck_b, cv_b, B, cap, base_d,
+                                t, max_base, out_b, ws, n_splits=split)
+            torch.cuda.synchronize()
+            assert torch.equal(out_a, out_b), (split, t)
+            assert torch.equal(ck_a, ck_b) and torch.equal(cv_a, cv_b), (split, t)
