@@ -203,3 +203,30 @@ def test_fused_rope_decode_more_than_16_query_heads_per_kv_head(pairing):
             torch.cuda.synchronize()
             assert torch.equal(out_a, out_b), (split, t)
             assert torch.equal(ck_a, ck_b) and torch.equal(cv_a, cv_b), (split, t)
+
+
+def test_empty_context_beside_a_long_one():
+    # one request composes nothing while the other composes 6 documents: the prefill launch is
+    # split over key ranges for the long request, so most of the empty request's ranges see no
+    # key at all (their partials carry a -inf maximum the combine must drop); decode likewise,
+    # split and unsplit
+    w = dataclasses.replace(synth.get("c2"), name="empty_and_long", pool_docs=6, doc_len=1000, docs_per_request=6,
+                            n_suffix=45, prefix_len=0, batch=2, decode_steps=2)
+    r = setup(w, requests=[[], [5, 0, 3, 1, 4, 2]])
+    assert list(r.ctx) == [0, 6000]
+    gpu_compose(r)
+    out = host(gpu_prefill(r))[0]
+    for b in range(w.batch):
+        ref, _, _ = oracle_prefill(r, b)
+        assert_attn_close(out[b], ref, "bf16")
+    ck0, cv0 = r.dev["cache_k"].clone(), r.dev["cache_v"].clone()
+    for n_splits in (0, 7):
+        r.dev["cache_k"], r.dev["cache_v"] = ck0.clone(), cv0.clone()
+        outs = [host(o)[0] for o in gpu_decode(r, 2, n_splits=n_splits)]
+        for b in range(w.batch):
+            _, K, V = oracle_prefill(r, b)
+            length = int(r.ctx[b]) + w.n_suffix
+            for t in range(2):
+                ref, K, V = O.decode_step(K, V, length, r.inp["dq"][t][b], r.inp["dk"][t][b], r.inp["dv"][t][b])
+                length += 1
+                assert_attn_close(outs[t][b], ref, "bf16")
