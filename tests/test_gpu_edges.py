@@ -230,3 +230,29 @@ def test_empty_context_beside_a_long_one():
                 ref, K, V = O.decode_step(K, V, length, r.inp["dq"][t][b], r.inp["dk"][t][b], r.inp["dv"][t][b])
                 length += 1
                 assert_attn_close(outs[t][b], ref, "bf16")
+
+
+@pytest.mark.parametrize("n_rep", [1, 2, 3, 5, 8])
+def test_query_heads_per_kv_head(n_rep):
+    # the matrix-core prefill packs the n_rep query heads of a kv head into its rows (row r is
+    # token r / n_rep, head r % n_rep, by a multiply-shift division) and decode puts them along
+    # N: plain multi-head attention (n_rep 1) and ratios that do not divide a 256-row tile,
+    # prefill split and unsplit, decode split and unsplit, every head against the oracle
+    for batch, n_suffix in ((2, 29), (32, 64)):
+        w = dataclasses.replace(synth.get("c2"), name=f"rep{n_rep}", n_q_heads=4 * n_rep, n_kv_heads=4, pool_docs=5,
+                                doc_len=300, docs_per_request=3, n_suffix=n_suffix, prefix_len=7, batch=batch,
+                                decode_steps=2)
+        r = setup(w)
+        gpu_compose(r)
+        out = host(gpu_prefill(r))[0]
+        for b in range(w.batch):
+            ref, _, _ = oracle_prefill(r, b)
+            assert_attn_close(out[b], ref, "bf16")
+        outs = [host(o)[0] for o in gpu_decode(r, 2, n_splits=3 if batch == 2 else 1)]
+        for b in range(w.batch):
+            _, K, V = oracle_prefill(r, b)
+            length = int(r.ctx[b]) + w.n_suffix
+            for t in range(2):
+                ref, K, V = O.decode_step(K, V, length, r.inp["dq"][t][b], r.inp["dk"][t][b], r.inp["dv"][t][b])
+                length += 1
+                assert_attn_close(outs[t][b], ref, "bf16")
