@@ -312,3 +312,24 @@ def test_paged_prefill_on_the_largest_pool_head():
     ref, _, _ = O.suffix_prefill(K, V, host(q)[0, 0], host(ks)[0, 0], host(vs)[0, 0])
     for runs in (False, True):
         assert_attn_close(host(outs[runs])[0, 0], ref, "bf16")
+
+
+@pytest.mark.parametrize("runs", [False, True], ids=["per-key", "whole-runs"])
+def test_paged_prefill_with_an_empty_context(runs):
+    # a request that composes nothing (every key of its suffix comes from k_suf) beside one that
+    # composes three documents: per-key mode bit-identical to compose + prefill, both modes
+    # against the oracle
+    w = dataclasses.replace(synth.get("c2"), name="paged_empty", pool_docs=3, doc_len=200, docs_per_request=3,
+                            n_suffix=40, prefix_len=0, batch=2)
+    r = setup(w, requests=[[], [2, 0, 1]])
+    assert list(r.ctx) == [0, 600]
+    gpu_compose(r)
+    out_m = gpu_prefill(r).clone()
+    out_p, ck_p, cv_p = _paged(r, runs=runs)
+    torch.cuda.synchronize()
+    _check_against_materialized(r, out_p, ck_p, cv_p, r.dev["cache_k"], r.dev["cache_v"], out_m, exact=not runs,
+                                tmap=_paged.tmap if runs else None)
+    got = host(out_p)[0]
+    for b in range(w.batch):
+        ref, _, _ = oracle_prefill(r, b)
+        assert_attn_close(got[b], ref, "bf16")
