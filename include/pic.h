@@ -36,9 +36,10 @@
  *   - Device-side tables (gather blocks, context lengths) are read as given; kernels clamp
  *     every index they derive from them to the buffer sizes passed on the host, so a bad
  *     table gives wrong values, never an out-of-bounds access.
- *   - Attention (3, 3a-3c, 4) on bf16 caches at head_dim 128 runs on the matrix-core kernels;
- *     on float32 caches and on bf16 caches at head_dim 64 it runs on a row-wise kernel (one
- *     workgroup per query row, float32 arithmetic) that needs no workspace and never splits.
+ *   - Attention on bf16 caches runs on the matrix-core kernels: prefill (3, 3a-3c) at
+ *     head_dim 128, decode (4) at head_dim 128 and 64.  Prefill at head_dim 64 and attention on
+ *     float32 caches run on a row-wise kernel (one workgroup per query row, float32
+ *     arithmetic) that needs no workspace and never splits.
  */
 #ifndef PIC_H
 #define PIC_H
@@ -352,8 +353,8 @@ pic_status pic_frontier_prefill_attn(const pic_model* model, const void* q, cons
    For request b the new token sits at slot p = base_len[b] + step: k_new/v_new are written
    there, then its query attends over slots [0, p].  Split-K over the context: n_splits
    chunks per (request, kv head) (0 picks a value), merged by log-sum-exp; a kv head with
-   more than 16 query heads is served in groups of 16.  The row-wise path (float32, or bf16 at
-   head_dim 64) ignores n_splits.
+   more than 16 query heads is served in groups of 16.  The row-wise path (float32 caches)
+   ignores n_splits.
      base_len [device, batch]  valid slots before the first decode step; clamped to
                                [0, max_base_len]; max_base_len + step + 1 <= cache_cap
      workspace                 pic_decode_workspace_bytes(...) bytes for the same batch,

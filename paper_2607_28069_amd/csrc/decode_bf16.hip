@@ -39,12 +39,21 @@ namespace {
 constexpr size_t kScratchBytes = PIC_DECODE_SCRATCH_BYTES;
 static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
-constexpr int kHD = 128;
 constexpr int kWaves = 4;
 constexpr int kTile = 32;                          // keys per wave tile
-constexpr int kRowBytes = kHD * 2;                 // 256
-constexpr int kVTileBytes = kTile * kRowBytes;     // 8 KB per wave per buffer
 constexpr int kMinWaveKeys = 64;
+// Sizes that follow the head dim HD (128 or 64): a row is HD/8 16-byte chunks; a lane's
+// operands hold HD/32 steps of 32 head dims; the output is HD/16 blocks of 16 head dims.
+template <int HD>
+struct Dims {
+  static_assert(HD == 128 || HD == 64, "head_dim 128 or 64");
+  static constexpr int kRowBytes = HD * 2;                  // 256 or 128
+  static constexpr int kVTileBytes = kTile * kRowBytes;     // per wave per buffer
+  static constexpr int kChunks = HD / 8;                    // 16-byte chunks per row
+  static constexpr int kSteps = HD / 32;                    // k steps of Q^T / K operands
+  static constexpr int kBlocks = HD / 16;                   // 16-dim output blocks
+  static constexpr int kRowsPerMove = 64 / kChunks;         // rows one 1 KB V move fills
+};
 static_assert(kWaves == kDecodeWaves && kMinWaveKeys == kDecodeMinWaveKeys, "host split planner tiling");
 constexpr int kNonTemporal = 2;                    // cache-policy bits of a streaming load
 
@@ -55,8 +64,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// V tile rows are 256 bytes; 16-byte chunk c of row `key` sits at slot c ^ v_swz(key).
-__device__ __forceinline__ int v_swz(int key) { return ((key & 3) << 1) | (((key >> 2) & 1) << 3); }
+// 16-byte chunk c of V row `key` sits at slot c ^ v_swz(key) of its row in LDS (256-byte rows:
+// 16 slots; 128-byte rows: 8 slots, so the XOR keeps to the low three bits).
+template <int HD>
+__device__ __forceinline__ int v_swz(int key) {
+  if constexpr (HD == 128) return ((key & 3) << 1) | (((key >> 2) & 1) << 3);
+  else return (key & 3) << 1;
+}
 
 struct DecodeArgs {
   const bf16_t* q;        // [L][B][Hq][D]
@@ -93,28 +107,29 @@ __device__ __forceinline__ u32x4 pack8(const float (&x)[8]) {
   return u32x4{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
                pack_bf16x2(x[6], x[7])};
 }
-// The 16 head dims 32 ks + 8 g4 .. + 8 (ks = 0..3) a lane holds of one row (the A / B operand
-// layout below), turned by row `trow` of the table: rotate-half pairs are chunks ks and ks + 2
-// (frequencies 32 ks + 8 g4 + j), interleaved pairs sit inside a chunk (16 ks + 4 g4 + m).
-template <bool kInterleaved>
-__device__ __forceinline__ void rot_operand(u32x4 (&c)[4], const float2* trow, int g4) {
+// The head dims 32 ks + 8 g4 .. + 8 (ks < HD/32) a lane holds of one row (the A / B operand
+// layout below), turned by row `trow` of the table: rotate-half pairs are chunks ks and
+// ks + HD/64 (frequencies 32 ks + 8 g4 + j), interleaved pairs sit inside a chunk (16 ks + 4 g4 + m).
+template <int HD, bool kInterleaved>
+__device__ __forceinline__ void rot_operand(u32x4 (&c)[Dims<HD>::kSteps], const float2* trow, int g4) {
+  constexpr int KS = Dims<HD>::kSteps;
   if constexpr (!kInterleaved) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < KS / 2; ++ks) {
       float x[8], y[8];
       unpack8(c[ks], x);
-      unpack8(c[ks + 2], y);
+      unpack8(c[ks + KS / 2], y);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const float2 cs = trow[32 * ks + 8 * g4 + j];
         rot_pair(x[j], y[j], cs.x, cs.y);
       }
       c[ks] = pack8(x);
-      c[ks + 2] = pack8(y);
+      c[ks + KS / 2] = pack8(y);
     }
   } else {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < KS; ++ks) {
       float x[8];
       unpack8(c[ks], x);
 #pragma unroll
@@ -128,9 +143,12 @@ __device__ __forceinline__ void rot_operand(u32x4 (&c)[4], const float2* trow, i
 }
 
 // grid (S * B * Hkv, L), 256 threads
-template <bool kRope, bool kInterleaved>
+template <int HD, bool kRope, bool kInterleaved>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 decode_bf16_kernel(DecodeArgs a) {
+  constexpr int kHD = HD, kRowBytes = Dims<HD>::kRowBytes, kVTileBytes = Dims<HD>::kVTileBytes;
+  constexpr int KC = Dims<HD>::kChunks, KS = Dims<HD>::kSteps, DB = Dims<HD>::kBlocks;
+  constexpr int RPM = Dims<HD>::kRowsPerMove;
   __shared__ __attribute__((aligned(16))) uint8_t v_lds0[kWaves * kVTileBytes];
   __shared__ __attribute__((aligned(16))) uint8_t v_lds1[kWaves * kVTileBytes];
 
@@ -165,13 +183,13 @@ decode_bf16_kernel(DecodeArgs a) {
   // from the cache during this launch: the wave whose range holds it reads k_new / v_new.
   const float2* trow = kRope ? a.table + (int64_t)l * a.table_stride + (int64_t)min(p, a.max_abs_delta) * (kHD / 2)
                              : nullptr;   // rope variant: cos/sin of position p
-  if (hgrp == 0 && p < a.cache_cap && p >= wc0 && p < wc1 && wave == 0 && lane < 32) {
-    const int c = lane & 15;
-    u32x4* dst = reinterpret_cast<u32x4*>((lane < 16 ? a.cache_k : a.cache_v) + (bh_kv * a.cache_cap + p) * kHD);
-    if (kRope && lane < 16) {   // the new key turned to p: lane c < 8 takes a chunk pair
-      if (c < 8) {
-        // rotate-half: chunks c, c + 8 (frequencies 8 c ..); interleaved: 2 c, 2 c + 1 (8 c ..)
-        const int ca = kInterleaved ? 2 * c : c, cb = kInterleaved ? 2 * c + 1 : c + 8;
+  if (hgrp == 0 && p < a.cache_cap && p >= wc0 && p < wc1 && wave == 0 && lane < 2 * KC) {
+    const int c = lane & (KC - 1);   // lanes [0, KC): K chunks, [KC, 2 KC): V chunks
+    u32x4* dst = reinterpret_cast<u32x4*>((lane < KC ? a.cache_k : a.cache_v) + (bh_kv * a.cache_cap + p) * kHD);
+    if (kRope && lane < KC) {   // the new key turned to p: lane c < KC/2 takes a chunk pair
+      if (c < KC / 2) {
+        // rotate-half: chunks c, c + KC/2 (frequencies 8 c ..); interleaved: 2 c, 2 c + 1 (8 c ..)
+        const int ca = kInterleaved ? 2 * c : c, cb = kInterleaved ? 2 * c + 1 : c + KC / 2;
         float x[8], y[8];
         unpack8(reinterpret_cast<const u32x4*>(Kn)[ca], x);
         unpack8(reinterpret_cast<const u32x4*>(Kn)[cb], y);
@@ -189,49 +207,50 @@ decode_bf16_kernel(DecodeArgs a) {
         dst[cb] = pack8(y);
       }
     } else {
-      dst[c] = reinterpret_cast<const u32x4*>(lane < 16 ? Kn : Vn)[c];
+      dst[c] = reinterpret_cast<const u32x4*>(lane < KC ? Kn : Vn)[c];
     }
   }
 
   const int n = lane & 15, g4 = lane >> 4;
   // Q^T operand: lane (n, g4) holds q[head g*n_rep + n][32 ks + 8 g4 .. +8)
-  bf16x8_t qop[4];
+  bf16x8_t qop[KS];
   {
     const bool ok = n < n_here;
     const int64_t qrow = ((int64_t)l * a.batch + b) * a.n_q_heads + g * n_rep + rep0 + (ok ? n : 0);
     const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + qrow * kHD);
-    u32x4 qv[4];
+    u32x4 qv[KS];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qv[ks] = ok ? qp[4 * ks + g4] : u32x4{0, 0, 0, 0};
-    if constexpr (kRope) rot_operand<kInterleaved>(qv, trow, g4);
+    for (int ks = 0; ks < KS; ++ks) qv[ks] = ok ? qp[4 * ks + g4] : u32x4{0, 0, 0, 0};
+    if constexpr (kRope) rot_operand<HD, kInterleaved>(qv, trow, g4);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) qop[ks] = as_bf16x8(qv[ks]);
+    for (int ks = 0; ks < KS; ++ks) qop[ks] = as_bf16x8(qv[ks]);
   }
 
   // K of one tile, straight into the A-operand layout: [mb][ks] = row k0 + 16 mb + n, head
   // dims 32 ks + 8 g4 .. +8.  Rows past the range are clamped (their scores are masked).
-  auto load_k = [&](int k0, u32x4 (&kr)[2][4]) {
+  auto load_k = [&](int k0, u32x4 (&kr)[2][KS]) {
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
       const int row = min(k0 + 16 * mb + n, c1 - 1);
       const bf16_t* src = row == p ? Kn : Kg + (int64_t)row * kHD;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+      for (int ks = 0; ks < KS; ++ks)
         kr[mb][ks] = *reinterpret_cast<const u32x4*>(src + 32 * ks + 8 * g4);
     }
   };
-  // V of one tile into this wave's LDS buffer: instruction i fills rows 4 i .. 4 i + 3, lane
-  // -> row 4 i + lane / 16, chunk slot lane % 16 (holding chunk slot ^ v_swz(row)).
-  const int ld_r = lane >> 4, ld_slot = lane & 15;
+  // V of one tile into this wave's LDS buffer: instruction i fills rows RPM i .. RPM i + RPM - 1
+  // (RPM = 64 / KC rows of KC chunks), lane -> row RPM i + lane / KC, chunk slot lane % KC
+  // (holding chunk slot ^ v_swz(row)).
+  const int ld_r = lane / KC, ld_slot = lane & (KC - 1);
   auto load_v = [&](int k0, uint8_t* buf) {
 #pragma unroll
-    for (int i = 0; i < kTile / 4; ++i) {
-      const int rl = 4 * i + ld_r;
+    for (int i = 0; i < kTile / RPM; ++i) {
+      const int rl = RPM * i + ld_r;
       const int row = min(k0 + rl, c1 - 1);
-      const int c = ld_slot ^ v_swz(rl);
+      const int c = ld_slot ^ v_swz<HD>(rl);
       const bf16_t* src = (row == p ? Vn : Vg + (int64_t)row * kHD) + 8 * c;
       __builtin_amdgcn_global_load_lds((const GLOBAL_AS void*)src,
-                                       (LDS_AS void*)(buf + wave * kVTileBytes + 4 * i * kRowBytes), 16, 0,
+                                       (LDS_AS void*)(buf + wave * kVTileBytes + RPM * i * kRowBytes), 16, 0,
                                        kNonTemporal);
     }
   };
@@ -241,25 +260,25 @@ decode_bf16_kernel(DecodeArgs a) {
   // Kept in registers: computed inline, the compiler makes these reads wait for the V loads in
   // flight into the other buffer.
   const int rr = (lane & 15) >> 2, qq = lane & 3;
-  int v_rd_off[8][2];
+  int v_rd_off[DB][2];
 #pragma unroll
-  for (int db = 0; db < 8; ++db)
+  for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       const int row = 16 * half + 4 * g4 + rr;
-      v_rd_off[db][half] = row * kRowBytes + (((2 * db + (qq >> 1)) ^ v_swz(row)) << 4) + 8 * (qq & 1);
+      v_rd_off[db][half] = row * kRowBytes + (((2 * db + (qq >> 1)) ^ v_swz<HD>(row)) << 4) + 8 * (qq & 1);
     }
   auto v_rd = [&](int db, int half) { return v_rd_off[db][half]; };
 
-  f32x4_t oacc[8];
+  f32x4_t oacc[DB];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) oacc[i] = f32x4_t{};
+  for (int i = 0; i < DB; ++i) oacc[i] = f32x4_t{};
   float m_run = -INFINITY, l_part = 0.f;
   const bf16x2_t ones = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);
 
   // One tile at k0; P = tile parity selects the (static) LDS buffers, so the compiler sees
   // that the loads in flight into one buffer do not alias reads from the other.
-  auto tile = [&](int k0, auto parity, u32x4 (&kcur)[2][4], u32x4 (&knext)[2][4]) {
+  auto tile = [&](int k0, auto parity, u32x4 (&kcur)[2][KS], u32x4 (&knext)[2][KS]) {
     constexpr int P = decltype(parity)::value;
     const uint8_t* vcur = P ? v_lds1 : v_lds0;
     uint8_t* vnext = P ? v_lds0 : v_lds1;
@@ -271,12 +290,12 @@ decode_bf16_kernel(DecodeArgs a) {
       if (p >= k0 && p < k0 + kTile) {
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
-          if (min(k0 + 16 * mb + n, c1 - 1) == p) rot_operand<kInterleaved>(kcur[mb], trow, g4);
+          if (min(k0 + 16 * mb + n, c1 - 1) == p) rot_operand<HD, kInterleaved>(kcur[mb], trow, g4);
       }
     }
     f32x4_t sacc[2] = {f32x4_t{}, f32x4_t{}};
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
         sacc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kcur[mb][ks]), qop[ks], sacc[mb], 0, 0, 0);
@@ -297,7 +316,7 @@ decode_bf16_kernel(DecodeArgs a) {
       m_run = m_new;
       l_part *= alpha;
 #pragma unroll
-      for (int db = 0; db < 8; ++db) oacc[db] *= alpha;
+      for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
     }
     uint32_t pw[4];
 #pragma unroll
@@ -314,7 +333,7 @@ decode_bf16_kernel(DecodeArgs a) {
     const bf16x8_t pop = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
     const uint8_t* vw = vcur + wave * kVTileBytes;
 #pragma unroll
-    for (int db = 0; db < 8; ++db) {
+    for (int db = 0; db < DB; ++db) {
       const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vw + v_rd(db, 0)));
       const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(vw + v_rd(db, 1)));
       const bf16x8_t vv = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -323,7 +342,7 @@ decode_bf16_kernel(DecodeArgs a) {
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the next tile is resident
   };
 
-  u32x4 k_a[2][4], k_b[2][4];
+  u32x4 k_a[2][KS], k_b[2][KS];
   if (c0 < c1) {
     load_k(c0, k_a);
     load_v(c0, v_lds0);
@@ -338,11 +357,11 @@ decode_bf16_kernel(DecodeArgs a) {
   float l_tot = l_part + __shfl_xor(l_part, 16, 64);
   l_tot += __shfl_xor(l_tot, 32, 64);
   __syncthreads();
-  float* o_lds = reinterpret_cast<float*>(v_lds0);    // [4][16][128] fp32 = 32 KB
+  float* o_lds = reinterpret_cast<float*>(v_lds0);    // [4][16][HD] fp32: all of v_lds0
   float* ml_lds = reinterpret_cast<float*>(v_lds1);   // [4][16][2]
   if (n < n_here) {
 #pragma unroll
-    for (int db = 0; db < 8; ++db)
+    for (int db = 0; db < DB; ++db)
       *reinterpret_cast<float4*>(o_lds + (wave * 16 + n) * kHD + 16 * db + 4 * g4) =
           make_float4(oacc[db][0], oacc[db][1], oacc[db][2], oacc[db][3]);
     if (g4 == 0) {
@@ -351,8 +370,8 @@ decode_bf16_kernel(DecodeArgs a) {
     }
   }
   __syncthreads();
-  // thread -> (query n = tid / 16, head dims 8 (tid % 16) .. +8)
-  const int mn = tid >> 4, md = 8 * (tid & 15);
+  // thread -> (query n = tid / KC, head dims 8 (tid % KC) .. +8)
+  const int mn = tid / KC, md = 8 * (tid & (KC - 1));
   if (mn < n_here) {
     float M = -INFINITY;
 #pragma unroll
@@ -388,10 +407,12 @@ decode_bf16_kernel(DecodeArgs a) {
   }
 }
 
-// grid (B * Hq, L), 64 threads: merge the splits of one query head by log-sum-exp.  The loads
-// of kCombineBatch splits are issued together before any is used (one pass for the maximum,
-// one for the weighted sums); a split that saw no key (maximum -inf) adds nothing.
+// grid (B * Hq, L), HD / 2 threads (two head dims each): merge the splits of one query head by
+// log-sum-exp.  The loads of kCombineBatch splits are issued together before any is used (one
+// pass for the maximum, one for the weighted sums); a split that saw no key (maximum -inf) adds
+// nothing.
 constexpr int kCombineBatch = 8;
+template <int HD>
 __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restrict__ ws_o,
                                                             const float* __restrict__ ws_ml,
                                                             int32_t n_splits, int64_t rows_per_layer,
@@ -414,7 +435,7 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
     for (int u = 0; u < kCombineBatch; ++u) {
       const int s = s0 + u;
       mlv[u] = s < n_splits ? *reinterpret_cast<const float2*>(ml + 2 * s) : make_float2(-INFINITY, 0.f);
-      ov[u] = s < n_splits ? *reinterpret_cast<const float2*>(ws_o + (row * n_splits + s) * kHD + d)
+      ov[u] = s < n_splits ? *reinterpret_cast<const float2*>(ws_o + (row * n_splits + s) * HD + d)
                            : make_float2(0.f, 0.f);
     }
 #pragma unroll
@@ -427,7 +448,23 @@ __global__ void __launch_bounds__(64) decode_combine_kernel(const float* __restr
     }
   }
   const float inv = 1.f / den;
-  reinterpret_cast<uint32_t*>(out + row * kHD)[threadIdx.x] = pack_bf16x2(o0 * inv, o1 * inv);
+  reinterpret_cast<uint32_t*>(out + row * HD)[threadIdx.x] = pack_bf16x2(o0 * inv, o1 * inv);
+}
+
+template <int HD>
+hipError_t launch_decode_hd(const DecodeArgs& a, dim3 grid, bool rope, bool interleaved, int32_t n_splits,
+                            const AttnShape& s, hipStream_t stream) {
+  if (!rope)
+    hipLaunchKernelGGL((decode_bf16_kernel<HD, false, false>), grid, dim3(256), 0, stream, a);
+  else if (interleaved)
+    hipLaunchKernelGGL((decode_bf16_kernel<HD, true, true>), grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_bf16_kernel<HD, true, false>), grid, dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || n_splits == 1) return e;
+  hipLaunchKernelGGL(decode_combine_kernel<HD>, dim3(s.batch * s.n_q_heads, s.n_layers), dim3(HD / 2), 0,
+                     stream, a.ws_o, a.ws_ml, n_splits, (int64_t)s.batch * s.n_q_heads, a.out);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -473,7 +510,7 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   a.out = out;
   const size_t rows = (size_t)s.n_layers * s.batch * s.n_q_heads * n_splits;
   a.ws_o = static_cast<float*>(workspace);
-  a.ws_ml = a.ws_o ? a.ws_o + rows * kHD : nullptr;
+  a.ws_ml = a.ws_o ? a.ws_o + rows * s.head_dim : nullptr;
   a.batch = s.batch;
   a.cache_cap = s.cache_cap;
   a.n_q_heads = s.n_q_heads;
@@ -489,17 +526,8 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   a.max_abs_delta = max_abs_delta;
   a.head_groups = decode_head_groups(s);
   const dim3 grid(a.head_groups * n_splits * s.batch * s.n_kv_heads, s.n_layers);
-  if (rope_table == nullptr)
-    hipLaunchKernelGGL((decode_bf16_kernel<false, false>), grid, dim3(256), 0, stream, a);
-  else if (interleaved)
-    hipLaunchKernelGGL((decode_bf16_kernel<true, true>), grid, dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL((decode_bf16_kernel<true, false>), grid, dim3(256), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || n_splits == 1) return e;
-  hipLaunchKernelGGL(decode_combine_kernel, dim3(s.batch * s.n_q_heads, s.n_layers), dim3(64), 0,
-                     stream, a.ws_o, a.ws_ml, n_splits, (int64_t)s.batch * s.n_q_heads, out);
-  return hipGetLastError();
+  if (s.head_dim == 64) return launch_decode_hd<64>(a, grid, rope_table != nullptr, interleaved, n_splits, s, stream);
+  return launch_decode_hd<128>(a, grid, rope_table != nullptr, interleaved, n_splits, s, stream);
 }
 
 }  // namespace pic

@@ -111,8 +111,10 @@ pic::AttnShape shape_of(const pic_model* m, int32_t batch, int32_t cache_cap, fl
 pic_status check_attn_model(const pic_model* m) { return check_model(m); }
 
 // bf16 caches at head_dim 128 run on the matrix-core kernels; float32 caches and bf16 caches
-// at head_dim 64 on the row-wise kernel.
+// at head_dim 64 on the row-wise kernel, except decode, whose matrix-core kernel serves bf16 at
+// both head dims.
 bool mfma_path(const pic_model* m) { return m->dtype == PIC_BF16 && m->head_dim == 128; }
+bool mfma_decode(const pic_model* m) { return m->dtype == PIC_BF16; }
 
 // Row-wise attention of n_q query rows per request at the positions `pos` gives them.
 // Options for bf16 rows: q_table (fused RoPE of the query), and a paged key source.
@@ -863,14 +865,14 @@ PIC_API pic_status pic_frontier_prefill_attn(const pic_model* model, const void*
 
 PIC_API int32_t pic_decode_auto_splits(const pic_model* model, int32_t batch, int32_t max_len) {
   if (check_attn_model(model) != PIC_OK || batch <= 0 || max_len <= 0) return 1;
-  if (!mfma_path(model)) return 1;
+  if (!mfma_decode(model)) return 1;
   return pic::decode_bf16_auto_splits(shape_of(model, batch, max_len, 0.f), max_len);
 }
 
 PIC_API size_t pic_decode_workspace_bytes(const pic_model* model, int32_t batch, int32_t max_len,
                                           int32_t n_splits) {
   if (check_attn_model(model) != PIC_OK || batch < 0 || max_len < 0 || n_splits < 0) return 0;
-  if (!mfma_path(model)) return 0;
+  if (!mfma_decode(model)) return 0;
   if (n_splits == 0) n_splits = pic_decode_auto_splits(model, batch, max_len);
   return pic::decode_bf16_workspace(shape_of(model, batch, max_len, 0.f), max_len, n_splits);
 }
@@ -915,7 +917,7 @@ pic_status decode_impl(const pic_model* model, const void* q, const void* k_new,
   }
   const hipStream_t st = (hipStream_t)stream;
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
-  if (!mfma_path(model)) {   // float32, or bf16 at head_dim 64: row-wise kernel, no splits
+  if (!mfma_decode(model)) {   // float32: row-wise kernel, no splits
     pic::RowPos pos;
     pos.base = base_len;
     pos.max_base = max_base_len;

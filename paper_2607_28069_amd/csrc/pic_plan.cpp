@@ -68,7 +68,7 @@ int32_t decode_bf16_auto_splits(const AttnShape& s, int32_t max_len) {
 size_t decode_bf16_workspace(const AttnShape& s, int32_t, int32_t n_splits) {
   if (n_splits <= 1) return 0;
   const size_t rows = (size_t)s.n_layers * s.batch * s.n_q_heads * n_splits;
-  return rows * (kAttnHeadDim + 2) * sizeof(float);
+  return rows * (s.head_dim + 2) * sizeof(float);
 }
 
 }  // namespace pic

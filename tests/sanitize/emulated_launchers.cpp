@@ -520,10 +520,11 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   if (s.batch == 0 || s.n_layers == 0) return hipSuccess;
   ++emu::launches;
   constexpr int kTile = 32;
+  const int64_t rb = (int64_t)s.head_dim * 2;   // bf16 row bytes (head_dim 128 or 64)
   const int32_t max_len = max_base + step + 1;
   const int64_t rows_all = (int64_t)s.n_layers * s.batch * s.n_q_heads * n_splits;
   float* ws_o = static_cast<float*>(workspace);
-  float* ws_ml = ws_o ? ws_o + rows_all * kAttnHeadDim : nullptr;
+  float* ws_ml = ws_o ? ws_o + rows_all * s.head_dim : nullptr;
   int32_t chunk = (max_len + n_splits - 1) / n_splits;
   chunk = (chunk + kDecodeWaves * kTile - 1) / (kDecodeWaves * kTile) * (kDecodeWaves * kTile);
   const int n_rep = s.n_q_heads / s.n_kv_heads;
@@ -538,13 +539,13 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
       const int wc0 = std::min(split * chunk, n_vis), wc1 = std::min(wc0 + chunk, n_vis);
       const int64_t bh_kv = ((int64_t)l * s.batch + b) * s.n_kv_heads + g;
       if (hgrp == 0 && p < s.cache_cap && p >= wc0 && p < wc1) {
-        rd_row(k_new, bh_kv, kRB);
-        rd_row(v_new, bh_kv, kRB);
-        wr_row(cache_k, bh_kv * s.cache_cap + p, kRB);
-        wr_row(cache_v, bh_kv * s.cache_cap + p, kRB);
+        rd_row(k_new, bh_kv, rb);
+        rd_row(v_new, bh_kv, rb);
+        wr_row(cache_k, bh_kv * s.cache_cap + p, rb);
+        wr_row(cache_v, bh_kv * s.cache_cap + p, rb);
       }
-      if (rope_table) rd_row(rope_table + l * table_stride, std::min(p, max_abs_delta), (int64_t)kAttnHeadDim / 2 * 8);
-      for (int n = 0; n < n_here; ++n) rd_row(q, ((int64_t)l * s.batch + b) * s.n_q_heads + g * n_rep + rep0 + n, kRB);
+      if (rope_table) rd_row(rope_table + l * table_stride, std::min(p, max_abs_delta), (int64_t)s.head_dim / 2 * 8);
+      for (int n = 0; n < n_here; ++n) rd_row(q, ((int64_t)l * s.batch + b) * s.n_q_heads + g * n_rep + rep0 + n, rb);
       const int sub = chunk / kDecodeWaves;
       for (int w = 0; w < kDecodeWaves; ++w) {
         const int c0 = std::min(wc0 + w * sub, wc1), c1 = std::min(c0 + sub, wc1);
@@ -552,21 +553,21 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
           for (int r = 0; r < kTile; ++r) {
             const int row = std::min(k0 + r, c1 - 1);
             if (row == p) {
-              rd_row(k_new, bh_kv, kRB);
-              rd_row(v_new, bh_kv, kRB);
+              rd_row(k_new, bh_kv, rb);
+              rd_row(v_new, bh_kv, rb);
             } else {
-              rd_row(cache_k, bh_kv * s.cache_cap + row, kRB);
-              rd_row(cache_v, bh_kv * s.cache_cap + row, kRB);
+              rd_row(cache_k, bh_kv * s.cache_cap + row, rb);
+              rd_row(cache_v, bh_kv * s.cache_cap + row, rb);
             }
           }
       }
       for (int n = 0; n < n_here; ++n) {
         const int64_t row = ((int64_t)l * s.batch + b) * s.n_q_heads + g * n_rep + rep0 + n;
         if (n_splits == 1) {
-          wr_row(out, row, kRB);
+          wr_row(out, row, rb);
         } else {
           const int64_t slot = row * n_splits + split;
-          emu::wr(ws_o, slot, kAttnHeadDim);
+          emu::wr(ws_o, slot, s.head_dim);
           emu::wr(ws_ml, slot, 2);
         }
       }
@@ -576,9 +577,9 @@ hipError_t launch_decode_bf16(const AttnShape& s, const bf16_t* q, const bf16_t*
   for (int64_t row = 0; row < (int64_t)s.n_layers * s.batch * s.n_q_heads; ++row) {
     for (int sp = 0; sp < n_splits; ++sp) {
       emu::rd(ws_ml, row * n_splits + sp, 2);
-      emu::rd(ws_o, row * n_splits + sp, kAttnHeadDim);
+      emu::rd(ws_o, row * n_splits + sp, s.head_dim);
     }
-    wr_row(out, row, kRB);
+    wr_row(out, row, rb);
   }
   return hipSuccess;
 }

@@ -1,7 +1,7 @@
-"""bf16 caches at head_dim 64 (the row-wise kernel; head_dim 128 runs on the matrix-core
-kernels) against the oracle: composition, suffix prefill and decode (with the no-workspace
-entry point), the general frontier layout, zero-copy (paged) prefill bit-identical to compose +
-prefill, and fused RoPE of request-time tokens bit-identical to turning them first.
+"""bf16 caches at head_dim 64 (prefill on the row-wise kernel, decode on the matrix-core kernel
+templated on the head dim) against the oracle: composition, suffix prefill and decode (with the
+no-workspace entry point), the general frontier layout, zero-copy (paged) prefill bit-identical to
+compose + prefill, and fused RoPE of request-time tokens bit-identical to turning them first.
 
 Tolerances as in test_gpu_parity: values bit-exact, bf16 keys within 1 bf16 ulp (+1e-5),
 attention within 2e-2 + 1e-2 |ref| with relative Frobenius error <= 1e-2.
@@ -148,9 +148,11 @@ def test_hd64_fused_rope(pairing):
     d_q, d_k, d_v = (to_dev(x, torch.bfloat16) for x in (q1, k1, v1))
     o_a, o_b = torch.zeros((L, B, HQ, D), dtype=torch.bfloat16, device=DEV), torch.zeros((L, B, HQ, D),
                                                                                         dtype=torch.bfloat16, device=DEV)
-    pic.pic_decode_attn_rope(m, d_q, d_k, d_v, ck_a, cv_a, B, cap, base, 0, int(max_ctx + Ls), table, mad, o_a)
+    dws = torch.empty(max(pic.pic_decode_workspace_bytes(m, B, int(max_ctx + Ls) + 1), 16), dtype=torch.uint8,
+                      device=DEV)
+    pic.pic_decode_attn_rope(m, d_q, d_k, d_v, ck_a, cv_a, B, cap, base, 0, int(max_ctx + Ls), table, mad, o_a, dws)
     dpos = ctx + Ls
     pic.pic_decode_attn(m, turned(d_q[:, :, None], HQ, dpos)[:, :, 0], turned(d_k[:, :, None], HKV, dpos)[:, :, 0],
-                        d_v, ck_b, cv_b, B, cap, base, 0, int(max_ctx + Ls), o_b)
+                        d_v, ck_b, cv_b, B, cap, base, 0, int(max_ctx + Ls), o_b, dws)
     torch.cuda.synchronize()
     assert torch.equal(o_a, o_b) and torch.equal(ck_a, ck_b)
