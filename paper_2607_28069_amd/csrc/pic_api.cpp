@@ -110,10 +110,12 @@ pic::AttnShape shape_of(const pic_model* m, int32_t batch, int32_t cache_cap, fl
 
 pic_status check_attn_model(const pic_model* m) { return check_model(m); }
 
-// bf16 caches at head_dim 128 run on the matrix-core kernels; float32 caches and bf16 caches
-// at head_dim 64 on the row-wise kernel, except decode, whose matrix-core kernel serves bf16 at
-// both head dims.
+// bf16 caches run on the matrix-core kernels: every prefill mode at head_dim 128 (mfma_path),
+// suffix and frontier prefill (mfma_prefill) and decode (mfma_decode) at head_dim 64 as well.
+// float32 caches, and the fused-RoPE and paged prefill of bf16 caches at head_dim 64, run on the
+// row-wise kernel.
 bool mfma_path(const pic_model* m) { return m->dtype == PIC_BF16 && m->head_dim == 128; }
+bool mfma_prefill(const pic_model* m) { return m->dtype == PIC_BF16; }
 bool mfma_decode(const pic_model* m) { return m->dtype == PIC_BF16; }
 
 // Row-wise attention of n_q query rows per request at the positions `pos` gives them.
@@ -521,7 +523,7 @@ PIC_API pic_status pic_compose_shared(const pic_model* model, const void* pool_k
 PIC_API size_t pic_prefill_workspace_bytes(const pic_model* model, int32_t batch, int32_t n_suffix,
                                            int32_t max_ctx) {
   if (check_attn_model(model) != PIC_OK || batch < 0 || n_suffix < 0 || max_ctx < 0) return 0;
-  if (!mfma_path(model)) return 0;
+  if (!mfma_prefill(model)) return 0;
   return pic::prefill_bf16_workspace(shape_of(model, batch, max_ctx + n_suffix, 0.f), n_suffix,
                                      max_ctx);
 }
@@ -560,7 +562,7 @@ PIC_API pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   // a4: suffix K/V into slots [ctx, ctx + n_suffix) (App. C.1: inline KVs interleaved); the
   // bf16 matrix-core kernel does this itself
-  if (!mfma_path(model)) {
+  if (!mfma_prefill(model)) {
     pic::RowPos pos;
     pos.base = ctx_len;
     pos.max_base = max_ctx;
@@ -617,7 +619,8 @@ PIC_API pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const vo
   PIC_CHECK(check_ptr(table, "table"));
   PIC_CHECK(check_ptr(out, "out"));
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
-  const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
+  // (head_dim 64: the row-wise kernel, which takes no workspace)
+  const size_t need = mfma_path(model) ? pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx) : 0;
   if (need > 0 && (workspace == nullptr || ws_bytes < need))
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
@@ -756,7 +759,8 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
   if (!slot_src && !(tile_map && mfma_path(model)))
     return fail(PIC_ERR_INVALID_ARG, "slot map is NULL (allowed only with a tile map at head_dim 128)");
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
-  const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
+  // (head_dim 64: the row-wise kernel, which takes no workspace)
+  const size_t need = mfma_path(model) ? pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx) : 0;
   if (need > 0 && (workspace == nullptr || ws_bytes < need))
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
@@ -800,7 +804,7 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
 PIC_API size_t pic_frontier_workspace_bytes(const pic_model* model, int32_t batch,
                                             int32_t n_inline, int32_t max_len) {
   if (check_attn_model(model) != PIC_OK || batch < 0 || n_inline < 0 || max_len < 0) return 0;
-  if (!mfma_path(model)) return 0;
+  if (!mfma_prefill(model)) return 0;
   const int32_t max_ctx = max_len > n_inline ? max_len - n_inline : 0;
   return pic::prefill_bf16_workspace(shape_of(model, batch, max_len, 0.f), n_inline, max_ctx);
 }
@@ -848,7 +852,7 @@ PIC_API pic_status pic_frontier_prefill_attn(const pic_model* model, const void*
                                           model->n_kv_heads, k_inl, v_inl, cache_k, cache_v,
                                           batch, cache_cap, rp, n_inline, st),
                        "inline append launch"));
-  if (!mfma_path(model))
+  if (!mfma_prefill(model))
     return launch_rows(model, s, q, cache_k, cache_v, rp, n_inline, out, st, "frontier attention launch");
   return hip_status(pic::launch_prefill_bf16_table(s, static_cast<const pic::bf16_t*>(q),
                                                    static_cast<const pic::bf16_t*>(cache_k),

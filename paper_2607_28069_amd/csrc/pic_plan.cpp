@@ -29,7 +29,7 @@ SplitPlan plan_prefill_splits(const AttnShape& s, int32_t n_suffix, int32_t max_
     const int tps = (tiles + sp - 1) / sp;
     if (sp > 1 && tps < 8) break;
     const int64_t rounds = (base * sp + 255) / 256;
-    const double partials = sp > 1 ? 1.0 + sp * rows * 2.0 * (kAttnHeadDim * 2 + 8) / 4e12 / 2e-6 : 0.0;
+    const double partials = sp > 1 ? 1.0 + sp * rows * 2.0 * (s.head_dim * 2 + 8) / 4e12 / 2e-6 : 0.0;
     const double cost = (double)rounds * tps + partials;
     if (cost < best_cost * 0.97) {
       best_cost = cost;
@@ -46,7 +46,7 @@ size_t prefill_bf16_workspace(const AttnShape& s, int32_t n_suffix, int32_t max_
   if (p.n_splits == 1) return 0;
   // per split and query row: the split's normalised output (bf16) and its (max, sum) pair
   const size_t rows = (size_t)s.n_layers * s.batch * n_suffix * s.n_q_heads;
-  return (size_t)p.n_splits * rows * (kAttnHeadDim * 2 + 2 * sizeof(float));
+  return (size_t)p.n_splits * rows * (s.head_dim * 2 + 2 * sizeof(float));
 }
 
 int32_t slot_map_tiles(int32_t map_cap) { return (int32_t)(((int64_t)map_cap + kPrefillKeys - 1) / kPrefillKeys); }

@@ -29,6 +29,10 @@
 //    hand (scheduling barriers): each LDS operand is read one product ahead of its use, and
 //    the PV products of a tile's last slice are issued after the tile barrier, covering the
 //    latency of the next tile's first reads.
+//  * Head dim D = 128 in every mode, or 64 in the suffix and table modes.  At 64 a row is 8
+//    chunks, one load instruction moves 8 rows, the score chains take 4 k steps and the output
+//    2 blocks of 32 dims; the tile body keeps its order, with one score product per two pairs
+//    of probabilities (the exponentials per flop double, so the vector unit limits it sooner).
 //  * Workgroups sharing a (request, kv head) key stream are mapped onto the same XCD (blocks
 //    are dealt round-robin over the 8 XCDs), so that stream is fetched into one L2.
 //  * The suffix's own keys/values are read straight from k_suf / v_suf; the workgroups of a
@@ -57,11 +61,19 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
 constexpr int kRowsPerWG = kWaves * kRowsPerWave;
 constexpr int kKeys = 64;                      // keys per tile
-constexpr int kHD = 128;
-constexpr int kRowBytes = kHD * 2;             // 256
-constexpr int kTileBytes = kKeys * kRowBytes;  // 16 KB
 constexpr int kNumXcd = 8;
-constexpr int kLoadSteps = kKeys / (4 * kWaves);   // 1 KB load instructions per wave per tile
+// Sizes that follow the head dim D (128; or 64 in the suffix and table modes).  A row is D / 8
+// 16-byte chunks, and one 1 KB load instruction of a wave moves 64 / (D / 8) rows of a tile.
+template <int HD>
+struct Dims {
+  static constexpr int kRowBytes = HD * 2;                   // 256 at D = 128
+  static constexpr int kTileBytes = kKeys * kRowBytes;       // 16 KB at D = 128
+  static constexpr int kChunks = HD / 8;                     // 16-byte chunks per row
+  static constexpr int kRowsPerLoad = 64 / kChunks;          // rows per 1 KB load instruction
+  static constexpr int kLoadSteps = kKeys / (kRowsPerLoad * kWaves);   // per wave and tile
+  static constexpr int kKSteps = HD / 16;                    // k steps of a score product
+  static constexpr int kDBlocks = HD / 32;                   // 32-dim blocks of the output
+};
 static_assert(kRowsPerWG == kPrefillRowsPerWG && kKeys == kPrefillKeys, "host split planner tiling");
 
 #define LDS_AS __attribute__((address_space(3)))
@@ -101,11 +113,25 @@ __device__ __forceinline__ int key_perm(int key) {
 // Byte offset of 16-byte chunk c of tile row `key`.  K is read 16 bytes per lane across 32
 // rows, V 8 bytes per lane across 4 rows by the transposing read; each has its own XOR
 // swizzle of the chunk index that keeps those reads free of bank conflicts (for 32 or 64
-// four-byte banks).
-__device__ __forceinline__ int k_swz(int key) { return key & 15; }
-__device__ __forceinline__ int v_swz(int key) { return ((key & 3) * 5) & 15; }
-__device__ __forceinline__ int k_off(int key, int c) { return key * kRowBytes + ((c ^ k_swz(key)) << 4); }
-__device__ __forceinline__ int v_off(int key, int c) { return key * kRowBytes + ((c ^ v_swz(key)) << 4); }
+// four-byte banks at D = 128).  At D = 64 a row is 128 bytes, half of the 64 banks' span, so
+// rows of the same parity share banks: K's swizzle takes key bits 1..3 (the 16 lanes of a
+// read phase, rows n .. n + 15 at one chunk, land on 16 distinct (parity, chunk) pairs), V's
+// moves rows 2 and 3 of each group of four to the other four-chunk half (the 4 rows x 4
+// chunks of a 32-lane phase cover all 64 banks once).
+template <int HD>
+__device__ __forceinline__ int k_swz(int key) {
+  if constexpr (HD == 128) return key & 15;
+  else return (key >> 1) & 7;
+}
+template <int HD>
+__device__ __forceinline__ int v_swz(int key) {
+  if constexpr (HD == 128) return ((key & 3) * 5) & 15;
+  else return (key & 2) << 1;
+}
+template <int HD>
+__device__ __forceinline__ int k_off(int key, int c) { return key * Dims<HD>::kRowBytes + ((c ^ k_swz<HD>(key)) << 4); }
+template <int HD>
+__device__ __forceinline__ int v_off(int key, int c) { return key * Dims<HD>::kRowBytes + ((c ^ v_swz<HD>(key)) << 4); }
 
 // Two ways to place the query tokens (n_suffix per request):
 //  * suffix: token i of request b at position ctx_len[b] + i, after the composed context;
@@ -190,11 +216,17 @@ __device__ __forceinline__ void rot_chunks(float (&x1)[8], float (&x2)[8], const
   }
 }
 
-template <int kMode, bool kInterleaved>
+template <int HD, int kMode, bool kInterleaved>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_bf16_kernel(PrefillArgs a) {
   constexpr bool kTable = kMode == kModeTable, kPaged = kMode == kModePaged, kRope = kMode == kModeRope;
   constexpr bool kRuns = kMode == kModeRuns, kPool = kPaged || kRuns;   // kPool: whole-run tiles from the pool
+  // (the modes that turn keys or queries work on 128-dim rows)
+  static_assert(HD == 128 || (HD == 64 && (kMode == kModeSuffix || kMode == kModeTable)), "head dim");
+  constexpr int kHD = HD;
+  constexpr int kRowBytes = Dims<HD>::kRowBytes, kTileBytes = Dims<HD>::kTileBytes;
+  constexpr int kChunks = Dims<HD>::kChunks, kRowsPerLoad = Dims<HD>::kRowsPerLoad;
+  constexpr int kLoadSteps = Dims<HD>::kLoadSteps, kKS = Dims<HD>::kKSteps, kDB = Dims<HD>::kDBlocks;
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
   // loads in flight into one buffer do not alias reads from another.  (The larger alignment
   // places them first, at the bottom of LDS, ahead of the paged mode's bigger areas.)
@@ -286,7 +318,8 @@ prefill_bf16_kernel(PrefillArgs a) {
     for (int o = 32; o > 0; o >>= 1) wm = max(wm, __shfl_xor(wm, o, 64));
     wave_max = __builtin_amdgcn_readfirstlane(wm);
   }
-  const int ld_row = 4 * wave + (lane >> 4), ld_slot = lane & 15;   // load row within a step
+  constexpr int kChunkShift = HD == 128 ? 4 : 3;   // log2(C)
+  const int ld_row = kRowsPerLoad * wave + (lane >> kChunkShift), ld_slot = lane & (kChunks - 1);   // load row within a step
   // this workgroup's key tiles: [t0, t0 + n_tiles) of the (pos_max_wg + 1) visible keys
   const int t0 = split * a.tiles_per_split;
   const int n_tiles = min((pos_max_wg + kKeys) / kKeys - t0, a.tiles_per_split);
@@ -359,23 +392,23 @@ prefill_bf16_kernel(PrefillArgs a) {
       }
     }
   } else if (!kTable) {
-    // item c: row i = c / 32, 16-byte chunk c % 16 of K (c % 32 < 16) or V; eight items per
-    // thread per pass, the loads issued before the stores
-    constexpr int kU = 8;
-    const int total = asm_i1 * 32;
-    for (int c0 = asm_i0 * 32 + tid; c0 < total; c0 += kU * kThreads) {
+    // item c: row i = c / (2 C), 16-byte chunk c % C of K (c % 2C < C) or V, C = D / 8 chunks
+    // per row; eight items per thread per pass, the loads issued before the stores
+    constexpr int kU = 8, kItemShift = HD == 128 ? 5 : 4;   // log2(2 C)
+    const int total = asm_i1 * 2 * kChunks;
+    for (int c0 = asm_i0 * 2 * kChunks + tid; c0 < total; c0 += kU * kThreads) {
       u32x4 w[kU];
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
-        const int c = c0 + u * kThreads, i = c >> 5, part = c & 31;
+        const int c = c0 + u * kThreads, i = c >> kItemShift, part = c & (2 * kChunks - 1);
         if (c < total)
-          w[u] = *reinterpret_cast<const u32x4*>((part < 16 ? Ks : Vs) + i * suf_stride + 8 * (part & 15));
+          w[u] = *reinterpret_cast<const u32x4*>((part < kChunks ? Ks : Vs) + i * suf_stride + 8 * (part & (kChunks - 1)));
       }
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
-        const int c = c0 + u * kThreads, i = c >> 5, part = c & 31;
+        const int c = c0 + u * kThreads, i = c >> kItemShift, part = c & (2 * kChunks - 1);
         if (c < total)
-          *reinterpret_cast<u32x4*>((part < 16 ? a.cache_k : a.cache_v) + (bh_kv + ctx + i) * kHD + 8 * (part & 15)) = w[u];
+          *reinterpret_cast<u32x4*>((part < kChunks ? a.cache_k : a.cache_v) + (bh_kv + ctx + i) * kHD + 8 * (part & (kChunks - 1))) = w[u];
       }
     }
   }
@@ -387,12 +420,12 @@ prefill_bf16_kernel(PrefillArgs a) {
     return;
   }
 
-  // ---- Q^T operand: lane (n, hh) holds q[row n][16 ks + 8 hh .. +8) for ks = 0..7
-  bf16x8_t qop[8];
+  // ---- Q^T operand: lane (n, hh) holds q[row n][16 ks + 8 hh .. +8) for ks = 0 .. D / 16 - 1
+  bf16x8_t qop[kKS];
   {
     const u32x4* qp = reinterpret_cast<const u32x4*>(a.q + qrow * kHD);
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0});
+    for (int ks = 0; ks < kKS; ++ks) qop[ks] = as_bf16x8(row_ok ? qp[2 * ks + hh] : u32x4{0, 0, 0, 0});
   }
   // rope mode: queries turned to their positions (called once the first tiles' loads are in
   // flight, so the table reads overlap them)
@@ -436,9 +469,9 @@ prefill_bf16_kernel(PrefillArgs a) {
   // slot.  The swizzles use key bits 0..3 (K) and 0..1 (V), which do not change with i, so
   // each lane's source offset within one step is a constant.  Rows past the last key (only in the last
   // tile) are clamped to it: their scores are masked, so they enter PV with probability 0.
-  const int k_goff = ld_row * kHD + 8 * (ld_slot ^ k_swz(ld_row));   // elements
-  const int v_goff = ld_row * kHD + 8 * (ld_slot ^ v_swz(ld_row));
-  const int v_gc = ld_slot ^ v_swz(ld_row), k_gc = ld_slot ^ k_swz(ld_row);
+  const int k_goff = ld_row * kHD + 8 * (ld_slot ^ k_swz<HD>(ld_row));   // elements
+  const int v_goff = ld_row * kHD + 8 * (ld_slot ^ v_swz<HD>(ld_row));
+  const int v_gc = ld_slot ^ v_swz<HD>(ld_row), k_gc = ld_slot ^ k_swz<HD>(ld_row);
   // paged mode: pool rows of this (layer, kv head), and the slot map of this request
   const bf16_t* PKg = kPool ? a.pool_k + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
   const bf16_t* PVg = kPool ? a.pool_v + ((int64_t)l * a.n_kv_heads + g) * a.pool_tokens * kHD : nullptr;
@@ -455,10 +488,10 @@ prefill_bf16_kernel(PrefillArgs a) {
   // (map entries are loaded raw and checked after the tile's loads have landed: a use right
   // after the load would make the wave wait for every load in flight, the tile's included)
   auto raw_src = [&](int t, int i) -> int32_t {   // ctx > 0
-    return smap[min(t * kKeys + 4 * kWaves * i + ld_row, ctx - 1)];
+    return smap[min(t * kKeys + kRowsPerLoad * kWaves * i + ld_row, ctx - 1)];
   };
   auto fin_src = [&](int t, int i, int32_t v) -> int32_t {
-    if (t * kKeys + 4 * kWaves * i + ld_row >= ctx) v = 0;
+    if (t * kKeys + kRowsPerLoad * kWaves * i + ld_row >= ctx) v = 0;
     return clamp_pool_token(v, a.pool_tokens);
   };
   auto map_src = [&](int t, int i) { return ctx > 0 ? fin_src(t, i, raw_src(t, i)) : 0; };
@@ -599,14 +632,14 @@ prefill_bf16_kernel(PrefillArgs a) {
     if (kPool && run >= 0) {   // a whole-run tile: pool rows run .. run + 63
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i)
-        dma16(is_v ? r_pv : r_pk, goff, (uint32_t)(run + 4 * kWaves * i) * kRowBytes,
-              dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes);
+        dma16(is_v ? r_pv : r_pk, goff, (uint32_t)(run + kRowsPerLoad * kWaves * i) * kRowBytes,
+              dst_tile + (kRowsPerLoad * kWaves * i + kRowsPerLoad * wave) * kRowBytes);
     } else if constexpr (kPaged) {
       const int32_t* rows = is_v ? src_v : src_k;
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
-        const int kk = min(t * kKeys + 4 * kWaves * i + ld_row, n_keys - 1);
-        uint8_t* dst = dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes;
+        const int kk = min(t * kKeys + kRowsPerLoad * kWaves * i + ld_row, n_keys - 1);
+        uint8_t* dst = dst_tile + (kRowsPerLoad * kWaves * i + kRowsPerLoad * wave) * kRowBytes;
         // (two separate moves: one move with a per-lane choice of base would need a loop
         // over the distinct bases)
         if (kk < ctx) dma16(is_v ? r_pv : r_pk, (uint32_t)rows[i] * kRowBytes + coff, 0, dst);
@@ -615,14 +648,14 @@ prefill_bf16_kernel(PrefillArgs a) {
     } else if ((t + 1) * kKeys <= ctx) {
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i)
-        dma16(rc, goff, (uint32_t)(t * kKeys + 4 * kWaves * i) * kRowBytes,
-              dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes);
+        dma16(rc, goff, (uint32_t)(t * kKeys + kRowsPerLoad * kWaves * i) * kRowBytes,
+              dst_tile + (kRowsPerLoad * kWaves * i + kRowsPerLoad * wave) * kRowBytes);
     } else {
       // a tile reaching the suffix: its keys come from k_suf / v_suf
 #pragma unroll
       for (int i = 0; i < kLoadSteps; ++i) {
-        const int kk = min(t * kKeys + 4 * kWaves * i + ld_row, n_keys - 1);
-        uint8_t* dst = dst_tile + (4 * kWaves * i + 4 * wave) * kRowBytes;
+        const int kk = min(t * kKeys + kRowsPerLoad * kWaves * i + ld_row, n_keys - 1);
+        uint8_t* dst = dst_tile + (kRowsPerLoad * kWaves * i + kRowsPerLoad * wave) * kRowBytes;
         if (kk < ctx) dma16(rc, (uint32_t)kk * kRowBytes + coff, 0, dst);
         if (kk >= ctx) dma16_other(rs, (uint32_t)((kk - ctx) * suf_stride) * 2u + coff, dst);
       }
@@ -633,8 +666,8 @@ prefill_bf16_kernel(PrefillArgs a) {
   // bf16.  Context rows only: suffix rows and clamped rows stay as loaded.
   auto rotate_own = [&](uint8_t* kt, int t, int32_t delta) {
     if (t * kKeys + rot_row >= ctx) return;
-    uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz(rot_row)) << 4);
-    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz(rot_row)) << 4);
+    uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz<HD>(rot_row)) << 4);
+    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz<HD>(rot_row)) << 4);
     const u32x4 w1 = *reinterpret_cast<const u32x4*>(p1);
     const u32x4 w2 = *reinterpret_cast<const u32x4*>(p2);
     float cs[8], sn[8];
@@ -689,8 +722,8 @@ prefill_bf16_kernel(PrefillArgs a) {
   auto rope_own = [&](uint8_t* kt, int t) {   // after rope_cs(t) has landed
     const int k = t * kKeys + rot_row;
     if (k < ctx || k >= n_keys) return;
-    uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz(rot_row)) << 4);
-    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz(rot_row)) << 4);
+    uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz<HD>(rot_row)) << 4);
+    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz<HD>(rot_row)) << 4);
     float x1[8], x2[8];
     unpack8(*reinterpret_cast<const u32x4*>(p1), x1);
     unpack8(*reinterpret_cast<const u32x4*>(p2), x2);
@@ -718,27 +751,27 @@ prefill_bf16_kernel(PrefillArgs a) {
 
   // ---- per-lane LDS read offsets, fixed for the whole loop (buffer, 32-row block and
   // 16-row slice steps are immediate offsets)
-  int k_rd[8];   // S^T A operand: row n, chunk 2 ks + hh
+  int k_rd[kKS];   // S^T A operand: row n, chunk 2 ks + hh
 #pragma unroll
-  for (int ks = 0; ks < 8; ++ks) k_rd[ks] = k_off(n, 2 * ks + hh);
+  for (int ks = 0; ks < kKS; ++ks) k_rd[ks] = k_off<HD>(n, 2 * ks + hh);
   // Transposing reads of V^T: 16-lane group G = lane / 16, lane j = lane % 16 = 4 rr + qq
   // points at row key_perm(16 s4 + 8 hh + 4 half + rr) = 16 s4 + 8 half + 4 hh + rr, head dims
   // 32 db + 16 (G & 1) + 4 qq .. +3; lane i of the group then receives head dim
   // 32 db + (lane & 31) of those 4 rows.
   const int tr_rr = (lane & 15) >> 2, tr_qq = lane & 3, tr_g1 = (lane >> 4) & 1;
-  int v_rd[4][2];
+  int v_rd[kDB][2];
 #pragma unroll
-  for (int db = 0; db < 4; ++db)
+  for (int db = 0; db < kDB; ++db)
 #pragma unroll
     for (int half = 0; half < 2; ++half)
-      v_rd[db][half] = v_off(8 * half + 4 * hh + tr_rr, 4 * db + 2 * tr_g1 + (tr_qq >> 1)) + 8 * (tr_qq & 1);
+      v_rd[db][half] = v_off<HD>(8 * half + 4 * hh + tr_rr, 4 * db + 2 * tr_g1 + (tr_qq >> 1)) + 8 * (tr_qq & 1);
 
   // ---- S^T = K Q^T for one tile: two independent 32-key accumulation chains
   auto scores = [&](const uint8_t* kt, f32x16_t (&s)[2]) {
     s[0] = f32x16_t{};
     s[1] = f32x16_t{};
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
+    for (int ks = 0; ks < kKS; ++ks)
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2) {
         const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + k_rd[ks] + 32 * kb2 * kRowBytes);
@@ -746,23 +779,23 @@ prefill_bf16_kernel(PrefillArgs a) {
       }
   };
 
-  f32x16_t oacc[4];
+  f32x16_t oacc[kDB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) oacc[i] = f32x16_t{};
+  for (int i = 0; i < kDB; ++i) oacc[i] = f32x16_t{};
   float m_run = -INFINITY, l_part = 0.f;
   // The PV products of a tile's last slice are issued after the tile barrier, at the start of
   // the next tile, while that tile's first LDS reads are in flight.  Pending: probabilities
   // pend_p and V^T operands pend_v (zero before the first tile: the products then add 0).
   bf16x8_t pend_p = as_bf16x8(u32x4{0, 0, 0, 0});
-  bf16x8_t pend_v[4];
+  bf16x8_t pend_v[kDB];
 #pragma unroll
-  for (int db = 0; db < 4; ++db) pend_v[db] = as_bf16x8(u32x4{0, 0, 0, 0});
+  for (int db = 0; db < kDB; ++db) pend_v[db] = as_bf16x8(u32x4{0, 0, 0, 0});
   // (not in paged mode, whose loop holds more state: there the slice is issued in its tile)
   constexpr bool kDefer = !kPaged;
   auto flush_pending = [&]() {
     if constexpr (!kDefer) return;
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
+    for (int db = 0; db < kDB; ++db)
       oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pend_v[db], pend_p, oacc[db], 0, 0, 0);
   };
 
@@ -806,7 +839,7 @@ prefill_bf16_kernel(PrefillArgs a) {
       m_run = m_new;
       l_part *= alpha;
 #pragma unroll
-      for (int db = 0; db < 4; ++db) oacc[db] *= alpha;
+      for (int db = 0; db < kDB; ++db) oacc[db] *= alpha;
     }
   };
 
@@ -958,14 +991,14 @@ prefill_bf16_kernel(PrefillArgs a) {
     auto vread = [&](int s4, int db, int half) {
       return __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS i16x4*)(v_cur + v_rd[db][half] + 16 * s4 * kRowBytes));
     };
-    u32x4 kq[8][2];
-    i16x4 vq[4][4][2];
+    u32x4 kq[kKS][2];
+    i16x4 vq[4][kDB][2];
     kq[0][0] = kread(0, 0);
     kq[0][1] = kread(0, 1);
     kq[1][0] = kread(1, 0);
     kq[1][1] = kread(1, 1);
 #pragma unroll
-    for (int db = 0; db < 4; ++db) {
+    for (int db = 0; db < kDB; ++db) {
       vq[0][db][0] = vread(0, db, 0);
       vq[0][db][1] = vread(0, db, 1);
     }
@@ -983,18 +1016,22 @@ prefill_bf16_kernel(PrefillArgs a) {
         pw[j] = pack_bf16x2(p0, p1);
         psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[j]), ones, psum, false);
         __builtin_amdgcn_sched_barrier(0);
-        // score product j of this slice: pair ks = 2 s4 + (j >> 1), block kb = j & 1
-        const int ks = 2 * s4 + (j >> 1), kb = j & 1;
-        if (kb == 0) snext[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kq[ks][0]), qop[ks], s4 == 0 && j == 0 ? f32x16_t{} : snext[0], 0, 0, 0);
-        else snext[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kq[ks][1]), qop[ks], s4 == 0 && j == 1 ? f32x16_t{} : snext[1], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (ks + 2 < 8) kq[ks + 2][kb] = kread(ks + 2, kb);
+        // score product pj of this slice (D = 128: one per pair of probabilities, pj = j;
+        // D = 64: one per two pairs): k step ks = (D / 64) s4 + (pj >> 1), block kb = pj & 1
+        constexpr int kJPer = 8 / kKS;   // probability pairs per score product
+        if (j % kJPer == 0) {
+          const int pj = j / kJPer, ks = (kKS / 4) * s4 + (pj >> 1), kb = pj & 1;
+          if (kb == 0) snext[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kq[ks][0]), qop[ks], ks == 0 ? f32x16_t{} : snext[0], 0, 0, 0);
+          else snext[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kq[ks][1]), qop[ks], ks == 0 ? f32x16_t{} : snext[1], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (ks + 2 < kKS) kq[ks + 2][kb] = kread(ks + 2, kb);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
       const bf16x8_t pop = as_bf16x8(u32x4{pw[0], pw[1], pw[2], pw[3]});
       if (s4 == 3 && kDefer) pend_p = pop;
 #pragma unroll
-      for (int db = 0; db < 4; ++db) {
+      for (int db = 0; db < kDB; ++db) {
         if (s4 + 1 < 4) {
           vq[s4 + 1][db][0] = vread(s4 + 1, db, 0);
           vq[s4 + 1][db][1] = vread(s4 + 1, db, 1);
@@ -1069,7 +1106,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   const float inv = 1.f / l_tot;
   bf16_t* op = a.n_splits == 1 ? a.out + orow * kHD : a.ws_o + (split * a.rows_total + orow) * kHD;
 #pragma unroll
-  for (int db = 0; db < 4; ++db)
+  for (int db = 0; db < kDB; ++db)
 #pragma unroll
     for (int qd = 0; qd < 4; ++qd) {
       const int d = 32 * db + 8 * qd + 4 * hh;
@@ -1083,15 +1120,15 @@ prefill_bf16_kernel(PrefillArgs a) {
 
 // Merge the key-range splits of each query row by log-sum-exp.  Split s left its output
 // normalised by its own row sum l_s (bf16) with its reference max m_s: the row is
-// sum_s w_s O_s / sum_s w_s with w_s = 2^(m_s - M) l_s, M any common reference.  grid (rows_total / 16), 256 threads:
-// 16 lanes per row, 8 head dims per lane; every split's loads are issued without a branch
+// sum_s w_s O_s / sum_s w_s with w_s = 2^(m_s - M) l_s, M any common reference.  grid (rows_total / 16),
+// 2 D threads: D / 8 lanes per row, 8 head dims per lane; every split's loads are issued without a branch
 // between them (a split that saw no key of the row, reference max -inf, is dropped by a
 // select: its sums are not finite).  With n_valid (table mode), rows of tokens past
 // n_valid[b] are left untouched.
 // kBatch: splits whose loads are issued together (4, 8 or 16, the smallest that covers n_splits:
 // a larger batch holds more registers and lowers the occupancy that few splits need)
 constexpr int kCombineRowsPerWG = 16;
-template <int kCombineBatch>
+template <int HD, int kCombineBatch>
 __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __restrict__ ws_o,
                                                               const float2* __restrict__ ws_ml,
                                                               int32_t n_splits, int64_t rows_total,
@@ -1099,7 +1136,8 @@ __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __re
                                                               int32_t n_q, int32_t n_q_heads,
                                                               int32_t batch,
                                                               bf16_t* __restrict__ out) {
-  const int64_t row = (int64_t)blockIdx.x * kCombineRowsPerWG + (threadIdx.x >> 4);
+  constexpr int kLanes = HD / 8;   // lanes per row
+  const int64_t row = (int64_t)blockIdx.x * kCombineRowsPerWG + threadIdx.x / kLanes;
   if (row >= rows_total) return;
   if (n_valid) {   // row = ((l * B + b) * n_q + i) * Hq + h
     const int64_t ti = row / n_q_heads;
@@ -1107,7 +1145,7 @@ __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __re
     const int b = (int)((ti / n_q) % batch);
     if (i >= n_valid[b]) return;
   }
-  const int d = 8 * (threadIdx.x & 15);
+  const int d = 8 * (threadIdx.x & (kLanes - 1));
   // one pass with a running reference max, kCombineBatch splits at a time: all their loads
   // are issued before the first is used (a split past n_splits reads as one that saw no key)
   float M = -INFINITY, den = 0.f, o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -1118,7 +1156,7 @@ __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __re
     for (int u = 0; u < kCombineBatch; ++u) {
       const int64_t s = s0 + u;
       mls[u] = s < n_splits ? ws_ml[s * rows_total + row] : make_float2(-INFINITY, 0.f);
-      xs[u] = s < n_splits ? *reinterpret_cast<const uint4*>(ws_o + (s * rows_total + row) * kHD + d)
+      xs[u] = s < n_splits ? *reinterpret_cast<const uint4*>(ws_o + (s * rows_total + row) * HD + d)
                            : uint4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
@@ -1145,7 +1183,7 @@ __global__ void __launch_bounds__(256) prefill_combine_kernel(const bf16_t* __re
   v.y = pack_bf16x2(o[2] * inv, o[3] * inv);
   v.z = pack_bf16x2(o[4] * inv, o[5] * inv);
   v.w = pack_bf16x2(o[6] * inv, o[7] * inv);
-  *reinterpret_cast<uint4*>(out + row * kHD + d) = v;
+  *reinterpret_cast<uint4*>(out + row * HD + d) = v;
 }
 
 }  // namespace
@@ -1204,6 +1242,53 @@ __global__ void __launch_bounds__(256) map_tiles_kernel(const int32_t* __restric
   }
 }
 
+template <int HD>
+hipError_t launch_hd(const AttnShape& s, const PrefillArgs& a, const SplitPlan& p, int mode, bool interleaved,
+                     int32_t n_q, hipStream_t stream) {
+  const int per_xcd = (a.n_wg + kNumXcd - 1) / kNumXcd;
+  const dim3 grid(per_xcd * kNumXcd, s.n_layers);
+  if constexpr (HD == 64) {   // suffix and table modes (the host dispatch sends only these)
+    if (mode == kModeTable)
+      hipLaunchKernelGGL((prefill_bf16_kernel<64, kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
+    else if (mode == kModeSuffix)
+      hipLaunchKernelGGL((prefill_bf16_kernel<64, kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
+    else
+      return hipErrorInvalidValue;
+  } else {
+    if (mode == kModeTable)
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
+    else if (mode == kModeRope && interleaved)
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRope, true>), grid, dim3(kThreads), 0, stream, a);
+    else if (mode == kModeRope)
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRope, false>), grid, dim3(kThreads), 0, stream, a);
+    else if (mode == kModePaged && interleaved)
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModePaged, true>), grid, dim3(kThreads), 0, stream, a);
+    else if (mode == kModeRuns && interleaved)
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRuns, true>), grid, dim3(kThreads), 0, stream, a);
+    else if (mode == kModeRuns)
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRuns, false>), grid, dim3(kThreads), 0, stream, a);
+    else if (mode == kModePaged)
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModePaged, false>), grid, dim3(kThreads), 0, stream, a);
+    else
+      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.n_splits == 1) return e;
+  const dim3 cgrid((unsigned)((a.rows_total + kCombineRowsPerWG - 1) / kCombineRowsPerWG));
+  const dim3 cblock(kCombineRowsPerWG * HD / 8);
+  const int32_t* nv = mode == kModeTable ? a.n_valid : nullptr;
+  if (p.n_splits <= 4)
+    hipLaunchKernelGGL((prefill_combine_kernel<HD, 4>), cgrid, cblock, 0, stream, a.ws_o, a.ws_ml, p.n_splits,
+                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
+  else if (p.n_splits <= 8)
+    hipLaunchKernelGGL((prefill_combine_kernel<HD, 8>), cgrid, cblock, 0, stream, a.ws_o, a.ws_ml, p.n_splits,
+                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
+  else
+    hipLaunchKernelGGL((prefill_combine_kernel<HD, 16>), cgrid, cblock, 0, stream, a.ws_o, a.ws_ml, p.n_splits,
+                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
+  return hipGetLastError();
+}
+
 hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved, int32_t n_q,
                   int32_t max_ctx, void* workspace, size_t ws_bytes, hipStream_t stream) {
   const int n_rep = s.n_q_heads / s.n_kv_heads;
@@ -1224,42 +1309,13 @@ hipError_t launch(const AttnShape& s, PrefillArgs a, int mode, bool interleaved,
   a.n_wg = p.m_tiles * p.n_splits * s.batch * s.n_kv_heads;
   a.rows_total = (int64_t)s.n_layers * s.batch * n_q * s.n_q_heads;
   a.ws_o = static_cast<bf16_t*>(workspace);
-  a.ws_ml = a.ws_o ? reinterpret_cast<float2*>(a.ws_o + (size_t)p.n_splits * a.rows_total * kHD) : nullptr;
+  a.ws_ml = a.ws_o ? reinterpret_cast<float2*>(a.ws_o + (size_t)p.n_splits * a.rows_total * s.head_dim) : nullptr;
   a.scale_log2 = s.scale_log2;
   if (p.n_splits > 1 && (workspace == nullptr || ws_bytes < prefill_bf16_workspace(s, n_q, max_ctx)))
     return hipErrorInvalidValue;
-  const int per_xcd = (a.n_wg + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(per_xcd * kNumXcd, s.n_layers);
-  if (mode == kModeTable)
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
-  else if (mode == kModeRope && interleaved)
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRope, true>), grid, dim3(kThreads), 0, stream, a);
-  else if (mode == kModeRope)
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRope, false>), grid, dim3(kThreads), 0, stream, a);
-  else if (mode == kModePaged && interleaved)
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModePaged, true>), grid, dim3(kThreads), 0, stream, a);
-  else if (mode == kModeRuns && interleaved)
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRuns, true>), grid, dim3(kThreads), 0, stream, a);
-  else if (mode == kModeRuns)
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModeRuns, false>), grid, dim3(kThreads), 0, stream, a);
-  else if (mode == kModePaged)
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModePaged, false>), grid, dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL((prefill_bf16_kernel<kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.n_splits == 1) return e;
-  const dim3 cgrid((unsigned)((a.rows_total + kCombineRowsPerWG - 1) / kCombineRowsPerWG));
-  const int32_t* nv = mode == kModeTable ? a.n_valid : nullptr;
-  if (p.n_splits <= 4)
-    hipLaunchKernelGGL(prefill_combine_kernel<4>, cgrid, dim3(256), 0, stream, a.ws_o, a.ws_ml, p.n_splits,
-                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
-  else if (p.n_splits <= 8)
-    hipLaunchKernelGGL(prefill_combine_kernel<8>, cgrid, dim3(256), 0, stream, a.ws_o, a.ws_ml, p.n_splits,
-                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
-  else
-    hipLaunchKernelGGL(prefill_combine_kernel<16>, cgrid, dim3(256), 0, stream, a.ws_o, a.ws_ml, p.n_splits,
-                       a.rows_total, nv, n_q, s.n_q_heads, s.batch, a.out);
-  return hipGetLastError();
+  if (s.head_dim == 64) return launch_hd<64>(s, a, p, mode, interleaved, n_q, stream);
+  if (s.head_dim == 128) return launch_hd<128>(s, a, p, mode, interleaved, n_q, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace

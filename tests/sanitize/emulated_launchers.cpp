@@ -258,8 +258,8 @@ hipError_t prefill_walk(const AttnShape& s, const PrefillEmu& a, int mode, int32
   const bool rope = mode == kModeRope, pool = paged || runs;
   const int64_t rows_total = (int64_t)s.n_layers * s.batch * n_q * s.n_q_heads;
   bf16_t* ws_o = static_cast<bf16_t*>(workspace);
-  float2* ws_ml = ws_o ? reinterpret_cast<float2*>(ws_o + (size_t)p.n_splits * rows_total * kAttnHeadDim) : nullptr;
-  const int64_t half = kAttnHeadDim / 2;
+  float2* ws_ml = ws_o ? reinterpret_cast<float2*>(ws_o + (size_t)p.n_splits * rows_total * s.head_dim) : nullptr;
+  const int64_t rb = (int64_t)s.head_dim * 2, half = s.head_dim / 2;   // bf16 row bytes (128 or 64 dims)
   const int n_wg = p.m_tiles * p.n_splits * s.batch * s.n_kv_heads;
   for (int l = 0; l < s.n_layers; ++l)
     for (int logical = 0; logical < n_wg; ++logical) {
@@ -301,11 +301,11 @@ hipError_t prefill_walk(const AttnShape& s, const PrefillEmu& a, int mode, int32
       const float2* ltab = a.table ? a.table + l * a.table_stride : nullptr;
       if (!table && mt == 0 && split == 0)   // cache assembly: the suffix rows into their slots
         for (int i = 0; i < n_q; ++i) {
-          rd_row(a.k_suf, suf0 + (int64_t)i * s.n_kv_heads, kRB);
-          rd_row(a.v_suf, suf0 + (int64_t)i * s.n_kv_heads, kRB);
+          rd_row(a.k_suf, suf0 + (int64_t)i * s.n_kv_heads, rb);
+          rd_row(a.v_suf, suf0 + (int64_t)i * s.n_kv_heads, rb);
           if (rope) rd_row(ltab, std::min(ctx + i, a.max_abs_delta), half * 8);
-          wr_row(a.cache_k, bh_kv + ctx + i, kRB);
-          wr_row(a.cache_v, bh_kv + ctx + i, kRB);
+          wr_row(a.cache_k, bh_kv + ctx + i, rb);
+          wr_row(a.cache_v, bh_kv + ctx + i, rb);
         }
       auto orow = [&](int j) { return (((int64_t)l * s.batch + b) * n_q + tok[j]) * s.n_q_heads + hq[j]; };
       if (n_tiles <= 0) {
@@ -315,7 +315,7 @@ hipError_t prefill_walk(const AttnShape& s, const PrefillEmu& a, int mode, int32
         continue;
       }
       for (int j = 0; j < kPrefillRowsPerWG; ++j) {
-        if (ok[j]) rd_row(a.q, orow(j), kRB);
+        if (ok[j]) rd_row(a.q, orow(j), rb);
         if (rope) rd_row(ltab, std::min(qpos[j], a.max_abs_delta), half * 8);
       }
       const int32_t* smap = paged ? a.smap + (int64_t)b * a.map_cap : nullptr;
@@ -336,13 +336,13 @@ hipError_t prefill_walk(const AttnShape& s, const PrefillEmu& a, int mode, int32
         const int64_t ph = ((int64_t)l * s.n_kv_heads + g) * a.pool_tokens;
         for (int r = 0; r < kPrefillKeys; ++r) {
           if (run >= 0) {
-            rd_row(a.pool_k, ph + run + r, kRB);
-            rd_row(a.pool_v, ph + run + r, kRB);
+            rd_row(a.pool_k, ph + run + r, rb);
+            rd_row(a.pool_v, ph + run + r, rb);
             continue;
           }
           if (!paged && (t + 1) * kPrefillKeys <= ctx) {
-            rd_row(a.cache_k, bh_kv + (int64_t)t * kPrefillKeys + r, kRB);
-            rd_row(a.cache_v, bh_kv + (int64_t)t * kPrefillKeys + r, kRB);
+            rd_row(a.cache_k, bh_kv + (int64_t)t * kPrefillKeys + r, rb);
+            rd_row(a.cache_v, bh_kv + (int64_t)t * kPrefillKeys + r, rb);
             continue;
           }
           const int kk = std::min(t * kPrefillKeys + r, n_keys - 1);
@@ -351,19 +351,19 @@ hipError_t prefill_walk(const AttnShape& s, const PrefillEmu& a, int mode, int32
             const int32_t st = smap[slot];
             const int32_t dl = dmap[slot];
             if (kk < ctx) {
-              rd_row(a.pool_k, ph + clamp_pool_token(st, a.pool_tokens), kRB);
-              rd_row(a.pool_v, ph + clamp_pool_token(st, a.pool_tokens), kRB);
+              rd_row(a.pool_k, ph + clamp_pool_token(st, a.pool_tokens), rb);
+              rd_row(a.pool_v, ph + clamp_pool_token(st, a.pool_tokens), rb);
               rd_row(ltab, iabs(clamp_delta(dl, a.max_abs_delta)), half * 8);
               continue;
             }
           } else if (kk < ctx) {
-            rd_row(a.cache_k, bh_kv + kk, kRB);
-            rd_row(a.cache_v, bh_kv + kk, kRB);
+            rd_row(a.cache_k, bh_kv + kk, rb);
+            rd_row(a.cache_v, bh_kv + kk, rb);
             continue;
           }
           if (kk >= ctx) {   // a suffix row, straight from k_suf / v_suf
-            rd_row(a.k_suf, suf0 + (int64_t)(kk - ctx) * s.n_kv_heads, kRB);
-            rd_row(a.v_suf, suf0 + (int64_t)(kk - ctx) * s.n_kv_heads, kRB);
+            rd_row(a.k_suf, suf0 + (int64_t)(kk - ctx) * s.n_kv_heads, rb);
+            rd_row(a.v_suf, suf0 + (int64_t)(kk - ctx) * s.n_kv_heads, rb);
             if (rope) rd_row(ltab, std::min(kk, a.max_abs_delta), half * 8);
           }
         }
@@ -371,9 +371,9 @@ hipError_t prefill_walk(const AttnShape& s, const PrefillEmu& a, int mode, int32
       for (int j = 0; j < kPrefillRowsPerWG; ++j) {
         if (!ok[j]) continue;
         if (p.n_splits == 1) {
-          wr_row(a.out, orow(j), kRB);
+          wr_row(a.out, orow(j), rb);
         } else {
-          wr_row(ws_o, split * rows_total + orow(j), kRB);
+          wr_row(ws_o, split * rows_total + orow(j), rb);
           wr_row(ws_ml, split * rows_total + orow(j), 8);
         }
       }
@@ -389,9 +389,9 @@ hipError_t prefill_walk(const AttnShape& s, const PrefillEmu& a, int mode, int32
     }
     for (int sp = 0; sp < p.n_splits; ++sp) {
       rd_row(ws_ml, sp * rows_total + row, 8);
-      rd_row(ws_o, sp * rows_total + row, kRB);
+      rd_row(ws_o, sp * rows_total + row, rb);
     }
-    wr_row(a.out, row, kRB);
+    wr_row(a.out, row, rb);
   }
   return hipSuccess;
 }
