@@ -36,11 +36,9 @@
  *   - Device-side tables (gather blocks, context lengths) are read as given; kernels clamp
  *     every index they derive from them to the buffer sizes passed on the host, so a bad
  *     table gives wrong values, never an out-of-bounds access.
- *   - Attention on bf16 caches runs on the matrix-core kernels: every prefill (3, 3a-3c) and
- *     decode (4) call at head_dim 128, and suffix prefill (3), frontier prefill (3b) and decode
- *     at head_dim 64.  Fused-RoPE (3a) and paged (3c) prefill at head_dim 64, and attention on
- *     float32 caches, run on a row-wise kernel (one workgroup per query row, float32
- *     arithmetic) that needs no workspace and never splits.
+ *   - Attention on bf16 caches runs on the matrix-core kernels (prefill 3, 3a-3c and decode 4,
+ *     head_dim 128 or 64).  Attention on float32 caches runs on a row-wise kernel (one
+ *     workgroup per query row, float32 arithmetic) that needs no workspace and never splits.
  */
 #ifndef PIC_H
 #define PIC_H
@@ -256,12 +254,9 @@ pic_status pic_suffix_prefill_attn(const pic_model* model, const void* q, const 
    per-layer tables, layer l's frequencies) as it loads them, in the float32 arithmetic and bf16
    rounding of pic_rerotate_keys, and stores the turned keys into the cache.  The result is
    bit-identical to turning q and k_suf with pic_rerotate_keys first and then calling
-   pic_suffix_prefill_attn (at head_dim 64, where this call runs on the row-wise kernel and
-   pic_suffix_prefill_attn on the matrix-core one, the cache is bit-identical and the output the
-   same to within bf16 attention rounding).  bf16 only.
+   pic_suffix_prefill_attn.  bf16 only.
      table, max_abs_delta   a pic_rope_table_init table with max_abs_delta >= max_ctx + n_suffix - 1
-   (other arguments and the workspace as for pic_suffix_prefill_attn; at head_dim 64 none is
-   needed) */
+   (other arguments and the workspace as for pic_suffix_prefill_attn) */
 pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q, const void* k_suf,
                                         const void* v_suf, void* cache_k, void* cache_v,
                                         int32_t batch, int32_t cache_cap, const int32_t* ctx_len,
@@ -293,16 +288,13 @@ pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q, c
      the context are treated as (-1, 0).
    The suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)), and with a tile map
    the non-run context tiles; a later pic_compose (or pic_compose_shared) fills the document
-   slots for decoding.  bf16 only.  At head_dim 64 the call runs on the row-wise kernel, takes
-   no workspace, and a tile map is accepted and not used: every context key is turned on load
-   with pic_compose's arithmetic and only the suffix rows are stored; outputs match compose +
-   prefill (the matrix-core kernel) to within bf16 attention rounding.
+   slots for decoding.  bf16 only.
    pic_compose_tiles composes, for every layer of `model` in one launch, the context tiles a
    tile map does not mark as whole runs: the step each pic_paged_prefill_attn call with a tile
    map otherwise takes for its own layer (same cache contents).  After it, the per-layer calls
    may pass slot_src = slot_delta = NULL with the tile map: they then skip that step, reading
-   whole runs from the pool and every other tile from the cache (bf16 at head_dim 128 only;
-   results identical to passing the slot map).
+   whole runs from the pool and every other tile from the cache (bf16 only; results identical
+   to passing the slot map).
      pool_k, pool_v, pool_tokens, table, max_abs_delta   as for pic_compose
      slot_src, slot_delta, map_cap   the map; map_cap >= max_ctx (entries are clamped to the
                                      pool and to max_abs_delta)

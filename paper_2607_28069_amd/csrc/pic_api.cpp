@@ -110,11 +110,8 @@ pic::AttnShape shape_of(const pic_model* m, int32_t batch, int32_t cache_cap, fl
 
 pic_status check_attn_model(const pic_model* m) { return check_model(m); }
 
-// bf16 caches run on the matrix-core kernels: every prefill mode at head_dim 128 (mfma_path),
-// suffix and frontier prefill (mfma_prefill) and decode (mfma_decode) at head_dim 64 as well.
-// float32 caches, and the fused-RoPE and paged prefill of bf16 caches at head_dim 64, run on the
-// row-wise kernel.
-bool mfma_path(const pic_model* m) { return m->dtype == PIC_BF16 && m->head_dim == 128; }
+// bf16 caches run on the matrix-core kernels (prefill in every mode and decode, head_dim 128 or
+// 64); float32 caches on the row-wise kernel.
 bool mfma_prefill(const pic_model* m) { return m->dtype == PIC_BF16; }
 bool mfma_decode(const pic_model* m) { return m->dtype == PIC_BF16; }
 
@@ -619,32 +616,11 @@ PIC_API pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const vo
   PIC_CHECK(check_ptr(table, "table"));
   PIC_CHECK(check_ptr(out, "out"));
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
-  // (head_dim 64: the row-wise kernel, which takes no workspace)
-  const size_t need = mfma_path(model) ? pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx) : 0;
+  const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
   if (need > 0 && (workspace == nullptr || ws_bytes < need))
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
-  if (!mfma_path(model)) {   // head_dim 64: keys turned as they are appended, queries in the kernel
-    const hipStream_t st = (hipStream_t)stream;
-    pic::RowPos pos;
-    pos.base = ctx_len;
-    pos.max_base = max_ctx;
-    PIC_CHECK(hip_status(pic::launch_append_rope(model->head_dim, model->rope_pairing == PIC_ROPE_INTERLEAVED,
-                                                 model->n_layers, model->n_kv_heads,
-                                                 static_cast<const pic::bf16_t*>(k_suf),
-                                                 static_cast<const pic::bf16_t*>(v_suf),
-                                                 static_cast<pic::bf16_t*>(cache_k),
-                                                 static_cast<pic::bf16_t*>(cache_v), batch, cache_cap, pos,
-                                                 n_suffix, static_cast<const float2*>(table), stride,
-                                                 max_abs_delta, st),
-                         "suffix append launch"));
-    RowOpts o;
-    o.q_table = table;
-    o.table_stride = stride;
-    o.max_abs_delta = max_abs_delta;
-    return launch_rows(model, s, q, cache_k, cache_v, pos, n_suffix, out, st, "fused-RoPE prefill launch", o);
-  }
   return hip_status(pic::launch_prefill_bf16_rope(
                         s, model->rope_pairing == PIC_ROPE_INTERLEAVED,
                         static_cast<const pic::bf16_t*>(q), static_cast<const pic::bf16_t*>(k_suf),
@@ -676,8 +652,7 @@ PIC_API pic_status pic_compose_tiles(const pic_model* model, const void* pool_k,
                                      void* cache_k, void* cache_v, int32_t batch, int32_t cache_cap,
                                      void* stream) {
   PIC_CHECK(check_attn_model(model));
-  if (!mfma_path(model))
-    return fail(PIC_ERR_UNSUPPORTED, "tile composition is built for bf16 caches at head_dim 128");
+  if (!mfma_prefill(model)) return fail(PIC_ERR_UNSUPPORTED, "tile composition is built for bf16 caches");
   if (batch < 0 || cache_cap < 0 || max_ctx < 0 || pool_tokens < 0 || map_cap < 0)
     return fail(PIC_ERR_INVALID_ARG, "negative size");
   if (max_abs_delta < 0 || max_abs_delta > kMaxAbsDelta)
@@ -699,7 +674,7 @@ PIC_API pic_status pic_compose_tiles(const pic_model* model, const void* pool_k,
   PIC_CHECK(check_ptr(tile_map, "tile_map"));
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
   const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
-  return hip_status(pic::launch_compose_tiles(model->rope_pairing == PIC_ROPE_INTERLEAVED, model->n_layers,
+  return hip_status(pic::launch_compose_tiles(model->rope_pairing == PIC_ROPE_INTERLEAVED, model->head_dim, model->n_layers,
                                               model->n_kv_heads, static_cast<const pic::bf16_t*>(pool_k),
                                               static_cast<const pic::bf16_t*>(pool_v), pool_tokens, slot_src,
                                               slot_delta, map_cap > 0 ? map_cap : 1, tile_map,
@@ -756,38 +731,13 @@ PIC_API pic_status pic_paged_prefill_attn(const pic_model* model, const void* po
   if (!slot_src != !slot_delta) return fail(PIC_ERR_INVALID_ARG, "one of the slot maps is NULL");
   // no slot map: the non-run tiles were composed beforehand (pic_compose_tiles), and the
   // call reads whole runs from the pool and every other tile from the cache
-  if (!slot_src && !(tile_map && mfma_path(model)))
-    return fail(PIC_ERR_INVALID_ARG, "slot map is NULL (allowed only with a tile map at head_dim 128)");
+  if (!slot_src && !tile_map) return fail(PIC_ERR_INVALID_ARG, "slot map is NULL (allowed only with a tile map)");
   if (!ctx_len) return fail(PIC_ERR_INVALID_ARG, "ctx_len is NULL");
-  // (head_dim 64: the row-wise kernel, which takes no workspace)
-  const size_t need = mfma_path(model) ? pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx) : 0;
+  const size_t need = pic_prefill_workspace_bytes(model, batch, n_suffix, max_ctx);
   if (need > 0 && (workspace == nullptr || ws_bytes < need))
     return fail(PIC_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   const pic::AttnShape s = shape_of(model, batch, cache_cap, scale);
   const int64_t stride = n_tables(model) > 1 ? (int64_t)(max_abs_delta + 1) * (model->head_dim / 2) : 0;
-  if (!mfma_path(model)) {   // head_dim 64: every context key through the slot map (tile map unused)
-    const hipStream_t st = (hipStream_t)stream;
-    pic::RowPos pos;
-    pos.base = ctx_len;
-    pos.max_base = max_ctx;
-    PIC_CHECK(hip_status(pic::launch_append(model->dtype, model->head_dim, model->n_layers,
-                                            model->n_kv_heads, k_suf, v_suf, cache_k, cache_v,
-                                            batch, cache_cap, pos, n_suffix, st),
-                         "suffix append launch"));
-    RowOpts o;
-    o.k_table = table;
-    o.table_stride = stride;
-    o.max_abs_delta = max_abs_delta;
-    o.pool_k = pool_k;
-    o.pool_v = pool_v;
-    o.pool_tokens = pool_tokens;
-    o.smap = slot_src;
-    o.dmap = slot_delta;
-    o.map_cap = map_cap > 0 ? map_cap : 1;
-    o.ctx_len = ctx_len;
-    o.max_ctx = max_ctx;
-    return launch_rows(model, s, q, cache_k, cache_v, pos, n_suffix, out, st, "paged prefill launch", o);
-  }
   return hip_status(pic::launch_prefill_bf16_paged(
                         s, model->rope_pairing == PIC_ROPE_INTERLEAVED,
                         static_cast<const pic::bf16_t*>(q), static_cast<const pic::bf16_t*>(k_suf),

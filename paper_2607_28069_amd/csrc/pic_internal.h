@@ -85,7 +85,6 @@ struct AttnShape {
 
 // Tiling the host planner (pic_plan.cpp) shares with the bf16 attention kernels (each kernel
 // file checks its own constants against these).
-constexpr int kAttnHeadDim = 128;          // head_dim of the bf16 attention kernels
 constexpr int kPrefillRowsPerWG = 256;     // query rows per prefill workgroup
 constexpr int kPrefillKeys = 64;           // keys per prefill tile
 constexpr int kPrefillMaxSplits = 32;      // most key-range splits the planner picks
@@ -171,8 +170,8 @@ hipError_t launch_prefill_bf16_rope(const AttnShape& s, bool interleaved, const 
 // src .. src + 63 under one shift, (-1, 0) for any other tile.
 int32_t slot_map_tiles(int32_t map_cap);
 // The context tiles of a paged prefill that are not whole pool runs (tile map), composed into
-// the cache from the slot map (bf16, head_dim 128; compose arithmetic).
-hipError_t launch_compose_tiles(bool interleaved, int n_layers, int n_kv_heads, const bf16_t* pool_k,
+// the cache from the slot map (bf16, head_dim 128 or 64; compose arithmetic).
+hipError_t launch_compose_tiles(bool interleaved, int head_dim, int n_layers, int n_kv_heads, const bf16_t* pool_k,
                                 const bf16_t* pool_v, int64_t pool_tokens, const int32_t* smap,
                                 const int32_t* dmap, int32_t map_cap, const int32_t* tmap,
                                 int32_t map_tiles, const int32_t* ctx_len, int32_t max_ctx,

@@ -221,12 +221,13 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
 prefill_bf16_kernel(PrefillArgs a) {
   constexpr bool kTable = kMode == kModeTable, kPaged = kMode == kModePaged, kRope = kMode == kModeRope;
   constexpr bool kRuns = kMode == kModeRuns, kPool = kPaged || kRuns;   // kPool: whole-run tiles from the pool
-  // (the modes that turn keys or queries work on 128-dim rows)
-  static_assert(HD == 128 || (HD == 64 && (kMode == kModeSuffix || kMode == kModeTable)), "head dim");
+  static_assert(HD == 128 || HD == 64, "head dim");
   constexpr int kHD = HD;
   constexpr int kRowBytes = Dims<HD>::kRowBytes, kTileBytes = Dims<HD>::kTileBytes;
   constexpr int kChunks = Dims<HD>::kChunks, kRowsPerLoad = Dims<HD>::kRowsPerLoad;
   constexpr int kLoadSteps = Dims<HD>::kLoadSteps, kKS = Dims<HD>::kKSteps, kDB = Dims<HD>::kDBlocks;
+  constexpr int kHalfChunks = kChunks / 2;   // rotate-half partner of chunk c: c + C / 2
+  constexpr int kQBytes = kKS * 1024;        // one wave's Q^T operand (paged mode keeps a copy)
   // Four distinct buffers (not one array indexed by parity) so the compiler can see that
   // loads in flight into one buffer do not alias reads from another.  (The larger alignment
   // places them first, at the bottom of LDS, ahead of the paged mode's bigger areas.)
@@ -237,7 +238,7 @@ prefill_bf16_kernel(PrefillArgs a) {
   // paged and rope modes: each wave's cos/sin of the key rows it turns (4 KB per wave)
   __shared__ __attribute__((aligned(16))) uint8_t cs_lds[(kPool || kRope) ? kWaves * 4096 : 16];
   // paged mode: each wave's unturned Q^T operand (8 KB per wave), the source of every turn
-  __shared__ __attribute__((aligned(16))) uint8_t q_lds[kPool ? kWaves * 8192 : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t q_lds[kPool ? kWaves * kQBytes : 16];
 
   // XCD-aware block order: hardware block w runs on XCD w % 8; give each XCD a contiguous
   // range of logical blocks so the m-tiles of one (request, kv head) share an L2.
@@ -339,37 +340,39 @@ prefill_bf16_kernel(PrefillArgs a) {
   const int asm_per = (a.n_suffix + asm_parts - 1) / asm_parts;
   const int asm_i0 = min(asm_part * asm_per, a.n_suffix), asm_i1 = min(asm_i0 + asm_per, a.n_suffix);
   if (kRope) {   // with the suffix keys turned to ctx + i
-    // item c: row i = c / 24; part < 8: K chunk pair part (rotate-half: chunks part, part + 8;
-    // interleaved: 2 part, 2 part + 1; both: frequencies 8 part .. 8 part + 7), part >= 8: V
-    // chunk part - 8.  Three items per thread per pass, all loads issued before any math.
+    // item c: row i = c / (3 C / 2), C = D / 8 chunks; part < C / 2: K chunk pair part
+    // (rotate-half: chunks part, part + C / 2; interleaved: 2 part, 2 part + 1; both:
+    // frequencies 8 part .. 8 part + 7), part >= C / 2: V chunk part - C / 2.  Three items per
+    // thread per pass, all loads issued before any math.
+    constexpr int kItems = 3 * kHalfChunks;   // per row
     const float2* trow0 = a.table + (int64_t)l * a.table_stride;
-    const int total = asm_i1 * 24;
-    for (int c0 = asm_i0 * 24 + tid; c0 < total; c0 += 3 * kThreads) {
+    const int total = asm_i1 * kItems;
+    for (int c0 = asm_i0 * kItems + tid; c0 < total; c0 += 3 * kThreads) {
       u32x4 w1[3], w2[3];
       float4 cs[3][4];
 #pragma unroll
       for (int u = 0; u < 3; ++u) {
         const int c = c0 + u * kThreads;
         if (c >= total) continue;
-        const int i = c / 24, part = c - 24 * i;
-        if (part < 8) {
-          const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : 64 + 8 * part;
+        const int i = c / kItems, part = c - kItems * i;
+        if (part < kHalfChunks) {
+          const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : kHD / 2 + 8 * part;
           w1[u] = *reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o1);
           w2[u] = *reinterpret_cast<const u32x4*>(Ks + i * suf_stride + o2);
           const float4* row = reinterpret_cast<const float4*>(trow0 + (int64_t)min(ctx + i, a.max_abs_delta) * (kHD / 2));
 #pragma unroll
           for (int j = 0; j < 4; ++j) cs[u][j] = row[4 * part + j];
         } else {
-          w1[u] = *reinterpret_cast<const u32x4*>(Vs + i * suf_stride + 8 * (part - 8));
+          w1[u] = *reinterpret_cast<const u32x4*>(Vs + i * suf_stride + 8 * (part - kHalfChunks));
         }
       }
 #pragma unroll
       for (int u = 0; u < 3; ++u) {
         const int c = c0 + u * kThreads;
         if (c >= total) continue;
-        const int i = c / 24, part = c - 24 * i;
-        if (part < 8) {
-          const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : 64 + 8 * part;
+        const int i = c / kItems, part = c - kItems * i;
+        if (part < kHalfChunks) {
+          const int o1 = kInterleaved ? 16 * part : 8 * part, o2 = kInterleaved ? 16 * part + 8 : kHD / 2 + 8 * part;
           float x1[8], x2[8];
           unpack8(w1[u], x1);
           unpack8(w2[u], x2);
@@ -387,7 +390,7 @@ prefill_bf16_kernel(PrefillArgs a) {
           *reinterpret_cast<u32x4*>(dst + o1) = pack8(x1);
           *reinterpret_cast<u32x4*>(dst + o2) = pack8(x2);
         } else {
-          *reinterpret_cast<u32x4*>(a.cache_v + (bh_kv + ctx + i) * kHD + 8 * (part - 8)) = w1[u];
+          *reinterpret_cast<u32x4*>(a.cache_v + (bh_kv + ctx + i) * kHD + 8 * (part - kHalfChunks)) = w1[u];
         }
       }
     }
@@ -432,20 +435,20 @@ prefill_bf16_kernel(PrefillArgs a) {
   auto rope_q = [&]() {
     const float2* trow = a.table + (int64_t)l * a.table_stride + (int64_t)min(qpos, a.max_abs_delta) * (kHD / 2);
     if constexpr (!kInterleaved) {
-      // pairs (d, d + 64): chunks ks and ks + 4, frequencies 16 ks + 8 hh .. + 7
+      // pairs (d, d + D / 2): operand steps ks and ks + D / 32, frequencies 16 ks + 8 hh .. + 7
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
+      for (int ks = 0; ks < kKS / 2; ++ks) {
         float x1[8], x2[8];
         unpack8(__builtin_bit_cast(u32x4, qop[ks]), x1);
-        unpack8(__builtin_bit_cast(u32x4, qop[ks + 4]), x2);
+        unpack8(__builtin_bit_cast(u32x4, qop[ks + kKS / 2]), x2);
         rot_chunks<false>(x1, x2, trow, 16 * ks + 8 * hh);
         qop[ks] = as_bf16x8(pack8(x1));
-        qop[ks + 4] = as_bf16x8(pack8(x2));
+        qop[ks + kKS / 2] = as_bf16x8(pack8(x2));
       }
     } else {
       // pairs (2i, 2i + 1) inside each chunk: dims 16 ks + 8 hh + 2m, frequency 8 ks + 4 hh + m
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
+      for (int ks = 0; ks < kKS; ++ks) {
         float x[8];
         unpack8(__builtin_bit_cast(u32x4, qop[ks]), x);
 #pragma unroll
@@ -459,8 +462,8 @@ prefill_bf16_kernel(PrefillArgs a) {
   };
   if constexpr (kPool) {   // keep the unturned operand (lane-private slots)
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-      *reinterpret_cast<u32x4*>(q_lds + wave * 8192 + (ks * 64 + lane) * 16) = __builtin_bit_cast(u32x4, qop[ks]);
+    for (int ks = 0; ks < kKS; ++ks)
+      *reinterpret_cast<u32x4*>(q_lds + wave * kQBytes + (ks * 64 + lane) * 16) = __builtin_bit_cast(u32x4, qop[ks]);
   }
 
   // ---- global -> LDS tile loads.  Instruction i of wave w writes 1 KB of LDS = tile rows
@@ -495,9 +498,13 @@ prefill_bf16_kernel(PrefillArgs a) {
     return clamp_pool_token(v, a.pool_tokens);
   };
   auto map_src = [&](int t, int i) { return ctx > 0 ? fin_src(t, i, raw_src(t, i)) : 0; };
-  // rotation item of this lane: row 32 i + 4 w + rr (i = lane / 32, rr = (lane / 8) % 4) of
-  // the wave's own load rows, 16-byte chunks c and c + 8 (c = lane % 8)
-  const int rot_row = 32 * (lane >> 5) + 4 * wave + ((lane >> 3) & 3), rot_c = lane & 7;
+  // rotation item of this lane: one of the wave's own load rows, 16-byte chunks c and c + C / 2.
+  // D = 128: row 32 i + 4 w + rr (i = lane / 32, rr = (lane / 8) % 4), c = lane % 8.  D = 64: row
+  // 8 w + (lane / 4) % 8, c = lane % 4; lanes 32 .. 63 repeat the items of lanes 0 .. 31 (rot_on
+  // false: they stage the same cos/sin and leave the rows to their twins).
+  const int rot_row = HD == 128 ? 32 * (lane >> 5) + 4 * wave + ((lane >> 3) & 3) : 8 * wave + ((lane >> 2) & 7);
+  const int rot_c = lane & (kHalfChunks - 1);
+  const bool rot_on = HD == 128 || lane < 32;
   // shift of this lane's rotation row of global tile t (0 past the context)
   auto raw_delta = [&](int t) -> int32_t { return dmap[min(t * kKeys + rot_row, ctx - 1)]; };   // ctx > 0
   auto fin_delta = [&](int t, int32_t d) -> int32_t {
@@ -515,9 +522,9 @@ prefill_bf16_kernel(PrefillArgs a) {
     cs_held = ad;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      // rotate-half: pairs 8c .. 8c + 7 (chunks c and c + 8); interleaved: pairs 4c .. 4c + 3
-      // (chunk c) and 32 + 4c .. 32 + 4c + 3 (chunk c + 8)
-      const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : 32 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
+      // rotate-half: pairs 8c .. 8c + 7 (chunks c and c + C / 2); interleaved: pairs 4c .. 4c + 3
+      // (chunk c) and D / 4 + 4c .. D / 4 + 4c + 3 (chunk c + C / 2)
+      const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : kHD / 4 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
       dma16(r_tab, (uint32_t)(ad * (kHD / 2) + f) * 8u, 0, cs_lds + wave * 4096 + j * 1024);
     }
   };
@@ -564,10 +571,10 @@ prefill_bf16_kernel(PrefillArgs a) {
   auto turn_q = [&](int32_t shift) {
     if (shift == q_shift) return;
     q_shift = shift;
-    const uint8_t* qs = q_lds + wave * 8192 + lane * 16;
+    const uint8_t* qs = q_lds + wave * kQBytes + lane * 16;
     if (shift == 0) {
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) qop[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(qs + ks * 1024));
+      for (int ks = 0; ks < kKS; ++ks) qop[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(qs + ks * 1024));
       return;
     }
     const float sg = shift < 0 ? -1.f : 1.f;   // sin(shift theta) = sg * sin(|shift| theta)
@@ -591,12 +598,12 @@ prefill_bf16_kernel(PrefillArgs a) {
       y = fmaf(v, c, -(u * sn));
     };
     if constexpr (!kInterleaved) {
-      // pairs (d, d + 64): chunks ks and ks + 4, frequencies 16 ks + 8 hh + j
+      // pairs (d, d + D / 2): operand steps ks and ks + D / 32, frequencies 16 ks + 8 hh + j
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
+      for (int ks = 0; ks < kKS / 2; ++ks) {
         float x[8], y[8];
         unpack(*reinterpret_cast<const u32x4*>(qs + ks * 1024), x);
-        unpack(*reinterpret_cast<const u32x4*>(qs + (ks + 4) * 1024), y);
+        unpack(*reinterpret_cast<const u32x4*>(qs + (ks + kKS / 2) * 1024), y);
 #pragma unroll
         for (int j4 = 0; j4 < 4; ++j4) {
           const float4 cs = row[8 * ks + 4 * hh + j4];
@@ -604,12 +611,12 @@ prefill_bf16_kernel(PrefillArgs a) {
           turn(x[2 * j4 + 1], y[2 * j4 + 1], cs.z, sg * cs.w);
         }
         qop[ks] = pack(x);
-        qop[ks + 4] = pack(y);
+        qop[ks + kKS / 2] = pack(y);
       }
     } else {
       // pairs (2i, 2i + 1) inside each chunk: frequencies 8 ks + 4 hh + m
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
+      for (int ks = 0; ks < kKS; ++ks) {
         float x[8];
         unpack(*reinterpret_cast<const u32x4*>(qs + ks * 1024), x);
 #pragma unroll
@@ -665,9 +672,9 @@ prefill_bf16_kernel(PrefillArgs a) {
   // by its shift, as the compose kernel does: fp32 x cos - y sin, x sin + y cos, rounded to
   // bf16.  Context rows only: suffix rows and clamped rows stay as loaded.
   auto rotate_own = [&](uint8_t* kt, int t, int32_t delta) {
-    if (t * kKeys + rot_row >= ctx) return;
+    if (t * kKeys + rot_row >= ctx || !rot_on) return;
     uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz<HD>(rot_row)) << 4);
-    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz<HD>(rot_row)) << 4);
+    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + kHalfChunks) ^ k_swz<HD>(rot_row)) << 4);
     const u32x4 w1 = *reinterpret_cast<const u32x4*>(p1);
     const u32x4 w2 = *reinterpret_cast<const u32x4*>(p2);
     float cs[8], sn[8];
@@ -694,7 +701,7 @@ prefill_bf16_kernel(PrefillArgs a) {
     };
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      if constexpr (kInterleaved) {   // pairs (2e, 2e + 1) of each chunk; chunk c+8 uses cs[4..7]
+      if constexpr (kInterleaved) {   // pairs (2e, 2e + 1) of each chunk; chunk c + C / 2 uses cs[4..7]
         float* x = k < 4 ? x1 : x2;
         turn(x[2 * (k & 3)], x[2 * (k & 3) + 1], cs[k], sn[k]);
       } else {
@@ -708,22 +715,22 @@ prefill_bf16_kernel(PrefillArgs a) {
   };
   auto wait_loads = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };   // vmcnt(0)
   // Rope mode: turn the suffix rows (keys ctx .. n_keys - 1) of K tile t, landed in `kt`, to
-  // their positions; this lane's item is chunks rot_c and rot_c + 8 of row rot_row.
+  // their positions; this lane's item is chunks rot_c and rot_c + C / 2 of row rot_row.
   auto rope_cs = [&](int t) {   // this lane's cos/sin for its suffix row of K tile t -> cos/sin area
     const int k = t * kKeys + rot_row;
     if (k < ctx || k >= n_keys) return;
     const uint32_t row = (uint32_t)min(k, a.max_abs_delta) * (kHD / 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {   // the frequency pairs the paged key turn uses (see load_cs)
-      const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : 32 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
+      const int f = kInterleaved ? (j < 2 ? 4 * rot_c + 2 * j : kHD / 4 + 4 * rot_c + 2 * (j - 2)) : 8 * rot_c + 2 * j;
       dma16(r_tab, (row + f) * 8u, 0, cs_lds + wave * 4096 + j * 1024);
     }
   };
   auto rope_own = [&](uint8_t* kt, int t) {   // after rope_cs(t) has landed
     const int k = t * kKeys + rot_row;
-    if (k < ctx || k >= n_keys) return;
+    if (k < ctx || k >= n_keys || !rot_on) return;
     uint8_t* p1 = kt + rot_row * kRowBytes + ((rot_c ^ k_swz<HD>(rot_row)) << 4);
-    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + 8) ^ k_swz<HD>(rot_row)) << 4);
+    uint8_t* p2 = kt + rot_row * kRowBytes + (((rot_c + kHalfChunks) ^ k_swz<HD>(rot_row)) << 4);
     float x1[8], x2[8];
     unpack8(*reinterpret_cast<const u32x4*>(p1), x1);
     unpack8(*reinterpret_cast<const u32x4*>(p2), x2);
@@ -738,10 +745,10 @@ prefill_bf16_kernel(PrefillArgs a) {
     }
 #pragma unroll
     for (int f = 0; f < 8; ++f) {
-      if constexpr (kInterleaved) {   // chunk c: pairs of frequencies 4 c ..; chunk c + 8: 32 + 4 c ..
+      if constexpr (kInterleaved) {   // chunk c: pairs of frequencies 4 c ..; chunk c + C / 2: D / 4 + 4 c ..
         float* x = f < 4 ? x1 : x2;
         rot_pair(x[2 * (f & 3)], x[2 * (f & 3) + 1], cs[f], sn[f]);
-      } else {                         // pairs (d, d + 64): frequencies 8 c ..
+      } else {                         // pairs (d, d + D / 2): frequencies 8 c ..
         rot_pair(x1[f], x2[f], cs[f], sn[f]);
       }
     }
@@ -1247,31 +1254,22 @@ hipError_t launch_hd(const AttnShape& s, const PrefillArgs& a, const SplitPlan& 
                      int32_t n_q, hipStream_t stream) {
   const int per_xcd = (a.n_wg + kNumXcd - 1) / kNumXcd;
   const dim3 grid(per_xcd * kNumXcd, s.n_layers);
-  if constexpr (HD == 64) {   // suffix and table modes (the host dispatch sends only these)
-    if (mode == kModeTable)
-      hipLaunchKernelGGL((prefill_bf16_kernel<64, kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
-    else if (mode == kModeSuffix)
-      hipLaunchKernelGGL((prefill_bf16_kernel<64, kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
-    else
-      return hipErrorInvalidValue;
-  } else {
-    if (mode == kModeTable)
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
-    else if (mode == kModeRope && interleaved)
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRope, true>), grid, dim3(kThreads), 0, stream, a);
-    else if (mode == kModeRope)
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRope, false>), grid, dim3(kThreads), 0, stream, a);
-    else if (mode == kModePaged && interleaved)
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModePaged, true>), grid, dim3(kThreads), 0, stream, a);
-    else if (mode == kModeRuns && interleaved)
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRuns, true>), grid, dim3(kThreads), 0, stream, a);
-    else if (mode == kModeRuns)
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeRuns, false>), grid, dim3(kThreads), 0, stream, a);
-    else if (mode == kModePaged)
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModePaged, false>), grid, dim3(kThreads), 0, stream, a);
-    else
-      hipLaunchKernelGGL((prefill_bf16_kernel<128, kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
-  }
+  if (mode == kModeTable)
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModeTable, false>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRope && interleaved)
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModeRope, true>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRope)
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModeRope, false>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModePaged && interleaved)
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModePaged, true>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRuns && interleaved)
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModeRuns, true>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModeRuns)
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModeRuns, false>), grid, dim3(kThreads), 0, stream, a);
+  else if (mode == kModePaged)
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModePaged, false>), grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((prefill_bf16_kernel<HD, kModeSuffix, false>), grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   const dim3 cgrid((unsigned)((a.rows_total + kCombineRowsPerWG - 1) / kCombineRowsPerWG));
@@ -1434,7 +1432,7 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
   // or beforehand by the caller when no slot map is given), then the prefill reads whole runs
   // from the pool and everything else from the cache
   if (smap != nullptr) {
-    const hipError_t e = launch_compose_tiles(interleaved, s.n_layers, s.n_kv_heads, pool_k, pool_v,
+    const hipError_t e = launch_compose_tiles(interleaved, s.head_dim, s.n_layers, s.n_kv_heads, pool_k, pool_v,
                                               pool_tokens, smap, dmap, map_cap, tmap, a.map_tiles,
                                               ctx_len, max_ctx, table, table_stride, max_abs_delta,
                                               cache_k, cache_v, s.batch, s.cache_cap, stream);

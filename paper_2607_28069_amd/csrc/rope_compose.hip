@@ -604,7 +604,7 @@ hipError_t launch_compose_shared(pic_dtype dt, int head_dim, bool interleaved, i
   return hipGetLastError();
 }
 
-hipError_t launch_compose_tiles(bool interleaved, int n_layers, int n_kv_heads, const bf16_t* pool_k,
+hipError_t launch_compose_tiles(bool interleaved, int head_dim, int n_layers, int n_kv_heads, const bf16_t* pool_k,
                                 const bf16_t* pool_v, int64_t pool_tokens, const int32_t* smap,
                                 const int32_t* dmap, int32_t map_cap, const int32_t* tmap,
                                 int32_t map_tiles, const int32_t* ctx_len, int32_t max_ctx,
@@ -613,14 +613,16 @@ hipError_t launch_compose_tiles(bool interleaved, int n_layers, int n_kv_heads, 
                                 hipStream_t stream) {
   if ((int64_t)batch * map_tiles == 0 || n_layers == 0) return hipSuccess;
   const dim3 grid((unsigned)((int64_t)batch * map_tiles), n_kv_heads, n_layers);
-  if (interleaved)
-    hipLaunchKernelGGL((compose_tiles_kernel<bf16_t, 128, true>), grid, dim3(256), 0, stream, pool_k, pool_v,
-                       pool_tokens, smap, dmap, map_cap, tmap, map_tiles, ctx_len, max_ctx, table,
-                       table_stride, max_abs_delta, cache_k, cache_v, batch, cache_cap);
-  else
-    hipLaunchKernelGGL((compose_tiles_kernel<bf16_t, 128, false>), grid, dim3(256), 0, stream, pool_k, pool_v,
-                       pool_tokens, smap, dmap, map_cap, tmap, map_tiles, ctx_len, max_ctx, table,
-                       table_stride, max_abs_delta, cache_k, cache_v, batch, cache_cap);
+#define PIC_COMPOSE_TILES(HD, IL)                                                                          \
+  hipLaunchKernelGGL((compose_tiles_kernel<bf16_t, HD, IL>), grid, dim3(256), 0, stream, pool_k, pool_v,    \
+                     pool_tokens, smap, dmap, map_cap, tmap, map_tiles, ctx_len, max_ctx, table,            \
+                     table_stride, max_abs_delta, cache_k, cache_v, batch, cache_cap)
+  if (head_dim == 64 && interleaved) PIC_COMPOSE_TILES(64, true);
+  else if (head_dim == 64) PIC_COMPOSE_TILES(64, false);
+  else if (head_dim == 128 && interleaved) PIC_COMPOSE_TILES(128, true);
+  else if (head_dim == 128) PIC_COMPOSE_TILES(128, false);
+  else return hipErrorInvalidValue;
+#undef PIC_COMPOSE_TILES
   return hipGetLastError();
 }
 

@@ -226,7 +226,6 @@ hipError_t launch_append_rope(int head_dim, bool, int n_layers, int n_kv_heads, 
 namespace {
 
 constexpr int kModeSuffix = 0, kModeTable = 1, kModePaged = 2, kModeRope = 3, kModeRuns = 4;
-constexpr int64_t kRB = kAttnHeadDim * 2;   // bf16 row bytes
 
 struct PrefillEmu {
   const bf16_t *q = nullptr, *k_suf = nullptr, *v_suf = nullptr;
@@ -429,12 +428,13 @@ hipError_t launch_prefill_bf16_table(const AttnShape& s, const bf16_t* q, const 
   return prefill_walk(s, a, kModeTable, n_q, max_ctx, workspace, ws_bytes);
 }
 
-hipError_t launch_compose_tiles(bool, int n_layers, int n_kv_heads, const bf16_t* pool_k, const bf16_t* pool_v,
+hipError_t launch_compose_tiles(bool, int head_dim, int n_layers, int n_kv_heads, const bf16_t* pool_k, const bf16_t* pool_v,
                                 int64_t pool_tokens, const int32_t* smap, const int32_t* dmap, int32_t map_cap,
                                 const int32_t* tmap, int32_t map_tiles, const int32_t* ctx_len, int32_t max_ctx,
                                 const float2* table, int64_t table_stride, int32_t max_abs_delta, bf16_t* cache_k,
                                 bf16_t* cache_v, int32_t batch, int32_t cache_cap, hipStream_t) {
   ++emu::launches;
+  const int64_t rb = (int64_t)head_dim * 2;   // bf16 row bytes
   for (int l = 0; l < n_layers; ++l)
     for (int h = 0; h < n_kv_heads; ++h)
       for (int64_t x = 0; x < (int64_t)batch * map_tiles; ++x) {
@@ -448,11 +448,11 @@ hipError_t launch_compose_tiles(bool, int n_layers, int n_kv_heads, const bf16_t
         for (int slot = s0; slot < std::min(s0 + PIC_BLOCK_TOKENS, ctx); ++slot) {
           const int32_t st = clamp_pool_token(smap[(int64_t)b * map_cap + slot], pool_tokens);
           const int32_t d = clamp_delta(dmap[(int64_t)b * map_cap + slot], max_abs_delta);
-          rd_row(table + l * table_stride, iabs(d), (int64_t)kAttnHeadDim / 2 * 8);
-          rd_row(pool_k, ((int64_t)l * n_kv_heads + h) * pool_tokens + st, kRB);
-          rd_row(pool_v, ((int64_t)l * n_kv_heads + h) * pool_tokens + st, kRB);
-          wr_row(cache_k, (((int64_t)l * batch + b) * n_kv_heads + h) * cache_cap + slot, kRB);
-          wr_row(cache_v, (((int64_t)l * batch + b) * n_kv_heads + h) * cache_cap + slot, kRB);
+          rd_row(table + l * table_stride, iabs(d), (int64_t)head_dim / 2 * 8);
+          rd_row(pool_k, ((int64_t)l * n_kv_heads + h) * pool_tokens + st, rb);
+          rd_row(pool_v, ((int64_t)l * n_kv_heads + h) * pool_tokens + st, rb);
+          wr_row(cache_k, (((int64_t)l * batch + b) * n_kv_heads + h) * cache_cap + slot, rb);
+          wr_row(cache_v, (((int64_t)l * batch + b) * n_kv_heads + h) * cache_cap + slot, rb);
         }
       }
   return hipSuccess;
@@ -503,7 +503,7 @@ hipError_t launch_prefill_bf16_paged(const AttnShape& s, bool interleaved, const
   a.table = table; a.table_stride = table_stride; a.max_abs_delta = max_abs_delta;
   if (tile_map == nullptr) return prefill_walk(s, a, kModePaged, n_suffix, max_ctx, workspace, ws_bytes);
   if (slot_src != nullptr) {   // no slot map: the tiles were composed beforehand
-    const hipError_t e = launch_compose_tiles(interleaved, s.n_layers, s.n_kv_heads, pool_k, pool_v, pool_tokens,
+    const hipError_t e = launch_compose_tiles(interleaved, s.head_dim, s.n_layers, s.n_kv_heads, pool_k, pool_v, pool_tokens,
                                               slot_src, slot_delta, map_cap, tile_map, a.map_tiles, ctx_len,
                                               max_ctx, table, table_stride, max_abs_delta, cache_k, cache_v,
                                               s.batch, s.cache_cap, stream);

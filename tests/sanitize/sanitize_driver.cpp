@@ -323,16 +323,13 @@ void fuzz_attention() {
                                     with_map ? tm.as<int32_t>() : nullptr, table.p, mad, q.p, ks.p, vs.p, ck.p, cv.p,
                                     batch, cap, ctx.as<int32_t>(), max_ctx, n_suf, 0.f, out.p,
                                     ws.n ? ws.p : nullptr, ws.n, nullptr) == PIC_OK);
-    // the non-run tiles of every layer composed ahead, then the per-layer form without the slot
-    // map (head_dim 128 only: the row path turns every key through the slot map)
-    const bool mfma = m.head_dim == 128;
+    // the non-run tiles of every layer composed ahead, then the per-layer form without the slot map
     EXPECT(pic_compose_tiles(&m, pk.p, pv.p, pool_tokens, sm.as<int32_t>(), dm.as<int32_t>(), map_cap,
                              tm.as<int32_t>(), table.p, mad, ctx.as<int32_t>(), max_ctx, ck.p, cv.p, batch, cap,
-                             nullptr) == (mfma ? PIC_OK : PIC_ERR_UNSUPPORTED));
+                             nullptr) == PIC_OK);
     EXPECT(pic_paged_prefill_attn(&m, pk.p, pv.p, pool_tokens, nullptr, nullptr, map_cap, tm.as<int32_t>(), table.p,
                                   mad, q.p, ks.p, vs.p, ck.p, cv.p, batch, cap, ctx.as<int32_t>(), max_ctx, n_suf,
-                                  0.f, out.p, ws.n ? ws.p : nullptr, ws.n, nullptr) ==
-           (mfma ? PIC_OK : PIC_ERR_INVALID_ARG));
+                                  0.f, out.p, ws.n ? ws.p : nullptr, ws.n, nullptr) == PIC_OK);
     // the slot map from garbage blocks
     const int32_t nb = (int32_t)rnd(0, 30);
     Buf blk(nb * sizeof(pic_block));

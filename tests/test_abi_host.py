@@ -440,8 +440,7 @@ def test_compose_tiles_argument_checks(lib):
     assert call(m, map_cap=400) == -4                   # the map must cover max_ctx
     assert call(m, max_ctx=700) == -4                   # longer than the cache
     assert call(m, max_abs_delta=-1) == -6
-    assert call(_model(head_dim=64)) == -2              # built for head_dim 128
-    assert call(_model(dtype="f32")) == -2
+    assert call(_model(dtype="f32")) == -2              # built for bf16 caches
     assert call(m, batch=0) == 0                        # nothing to do, nothing launched
     # the paged prefill: no slot map needs a tile map; one map alone is refused
     common = [FAKE, FAKE, 1000]
@@ -449,8 +448,12 @@ def test_compose_tiles_argument_checks(lib):
             ctypes.c_size_t(0), None]
     assert lib.pic_paged_prefill_attn(ctypes.byref(m), *common, None, None, 600, None, *tail) == -1
     assert lib.pic_paged_prefill_attn(ctypes.byref(m), *common, FAKE, None, 600, FAKE, *tail) == -1
+    # head_dim 64 takes the tile-map-only form too: the call gets past the slot-map check and stops
+    # at the missing ctx_len (nothing launched)
+    no_ctx = tail[:9] + [None] + tail[10:]
     assert lib.pic_paged_prefill_attn(ctypes.byref(_model(head_dim=64)), *common, None, None, 600, FAKE,
-                                      *tail) == -1
+                                      *no_ctx) == -1
+    assert b"ctx_len" in lib.pic_last_error()
 
 
 def test_noalloc_decode_argument_checks(lib):

@@ -137,18 +137,19 @@ def test_paged_prefill_equals_compose_then_prefill(name, runs):
 
 @pytest.mark.parametrize("runs", [False, True], ids=["per-key", "whole-runs"])
 @pytest.mark.parametrize("pairing", ["half", "interleaved"])
-@pytest.mark.parametrize("layout", ["c2", "mixed"])
+@pytest.mark.parametrize("layout", ["c2", "mixed", "mixed_hd64"])
 def test_paged_prefill_with_rotary_variants(pairing, runs, layout):
     # two layers with their own frequencies in one call; pool layer 1 differs from layer 0.
     # mixed: documents of 60..300 tokens, so with the tile map some context tiles are composed
-    # into the cache first (both pairings, per-layer tables) and the others read from the pool
+    # into the cache first (both pairings, per-layer tables) and the others read from the pool;
+    # mixed_hd64: the same at head_dim 64 (rotate-half partners 4 chunks apart)
     if layout == "c2":
         w = synth.get("c2")
         r = setup(w)
     else:
-        w = dataclasses.replace(synth.get("c2"), name="mixed", n_q_heads=28, n_kv_heads=4, pool_docs=5,
+        w = dataclasses.replace(synth.get("c2"), name=layout, n_q_heads=28, n_kv_heads=4, pool_docs=5,
                                 doc_len=77, docs_per_request=4, n_suffix=37, prefix_len=13, batch=3,
-                                doc_len_jitter=(60, 300))
+                                doc_len_jitter=(60, 300), head_dim=64 if layout == "mixed_hd64" else 128)
         lay = S.pool_layout(w)
         r = setup(w, requests=[[lay.prefix_entry, 3, 0, 4], [lay.prefix_entry], [2, 1, 0, 3, 4]], extra_cap=5)
     d = gpu_compose(r)
@@ -188,7 +189,7 @@ def test_paged_prefill_with_rotary_variants(pairing, runs, layout):
                                      freqs=fo[l])
             ref, _, _ = O.suffix_prefill(K, V, r.inp["q"][b], r.inp["k_suf"][b], r.inp["v_suf"][b])
             assert_attn_close(got[l, b], ref, "bf16")
-    if runs and layout == "mixed":   # both kinds of context tile occur: some were composed first
+    if runs and layout != "c2":   # both kinds of context tile occur: some were composed first
         tm = _paged.tmap
         ctx_tiles = [(b, t) for b in range(w.batch) for t in range((int(r.ctx[b]) + 63) // 64)]
         assert any(tm[b, t, 0] >= 0 for b, t in ctx_tiles) and any(tm[b, t, 0] < 0 for b, t in ctx_tiles)
@@ -196,15 +197,16 @@ def test_paged_prefill_with_rotary_variants(pairing, runs, layout):
           f"frequencies: paged == compose + prefill", flush=True)
 
 
+@pytest.mark.parametrize("head_dim", [128, 64])
 @pytest.mark.parametrize("pairing", ["half", "interleaved"])
-def test_tiles_composed_ahead_then_prefill_without_slot_map(pairing):
+def test_tiles_composed_ahead_then_prefill_without_slot_map(pairing, head_dim):
     # pic_compose_tiles for both layers in one launch, then the paged prefill with the tile map
     # and no slot map, against the paged prefill that composes its own tiles: identical caches
     # and outputs (documents of 60..300 tokens, so both kinds of context tile occur; two layers
     # with their own frequencies)
     w = dataclasses.replace(synth.get("c2"), name="mixed", n_q_heads=28, n_kv_heads=4, pool_docs=5,
                             doc_len=77, docs_per_request=4, n_suffix=37, prefix_len=13, batch=3,
-                            doc_len_jitter=(60, 300))
+                            doc_len_jitter=(60, 300), head_dim=head_dim)
     lay = S.pool_layout(w)
     r = setup(w, requests=[[lay.prefix_entry, 3, 0, 4], [lay.prefix_entry], [2, 1, 0, 3, 4]], extra_cap=5)
     d = gpu_compose(r)
@@ -243,7 +245,7 @@ def test_tiles_composed_ahead_then_prefill_without_slot_map(pairing):
         res.append((out, ck, cv))
     for a, b in zip(*res):
         assert torch.equal(a, b), "composing the tiles ahead changed the result"
-    print(f"[{pairing}] tiles composed ahead for both layers: caches and outputs identical", flush=True)
+    print(f"[{pairing}, D {head_dim}] tiles composed ahead for both layers: caches and outputs identical", flush=True)
 
 
 def test_paged_prefill_on_the_largest_pool_head():
