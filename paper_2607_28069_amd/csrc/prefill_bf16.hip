@@ -460,21 +460,6 @@ prefill_bf16_kernel(PrefillArgs a) {
       }
     }
   };
-  // The operand the score products take is q * scale * log2(e), rounded to bf16: scores then
-  // come out of the matrix core in log2 units, and a probability is exp2(score - reference)
-  // with no multiply per score.  (Rope mode scales the turned query; the paged and runs modes
-  // keep the scaled, unturned operand and turn that.)
-  auto scale_q = [&]() {
-#pragma unroll
-    for (int ks = 0; ks < kKS; ++ks) {
-      float x[8];
-      unpack8(__builtin_bit_cast(u32x4, qop[ks]), x);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] *= a.scale_log2;
-      qop[ks] = as_bf16x8(pack8(x));
-    }
-  };
-  if constexpr (!kRope) scale_q();
   if constexpr (kPool) {   // keep the unturned operand (lane-private slots)
 #pragma unroll
     for (int ks = 0; ks < kKS; ++ks)
@@ -832,19 +817,10 @@ prefill_bf16_kernel(PrefillArgs a) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
   };
 
-  // Scores of tile t are complete (log2 units): apply the frontier mask where the tile reaches
-  // past a query's position, then settle the reference the tile's probabilities take and
-  // leave the scores relative to it (the tile body takes p = exp2(score) as they stand).
-  //  * Fixed reference (fixed_ref, wave-uniform): while every row's largest score so far lies
-  //    in [-kFixedWindow, kFixedWindow] (or the row has seen no key yet), p = exp2(score)
-  //    against the reference 0, at most 2^64, and no probability a row keeps falls below
-  //    2^-62 of the row's largest.  m_run is then the row's largest score so far.
-  //  * Running reference: the first tile that leaves that window switches the wave to the row
-  //    maximum as reference (rescaling what has been accumulated), moved afterwards only when
-  //    a score exceeds it by more than 2^8 (p <= 256).
-  // Either way float32 sums and bf16 probabilities keep their relative precision.
-  constexpr float kFixedWindow = 64.f;
-  bool fixed_ref = true;
+  // Scores of tile t are complete: apply the frontier mask where the tile reaches past a
+  // query's position, and move the reference max if a score exceeds it by more than 2^8
+  // (rescaling what has been accumulated, for the whole wave at once).  Otherwise p <= 256,
+  // which float32 sums and bf16 probabilities hold without loss of relative precision.
   auto finish_scores = [&](int t, f32x16_t (&s)[2]) {   // t: global tile index
     const int k0 = t * kKeys;
     if (k0 + kKeys - 1 > pos_min_wg) {
@@ -861,32 +837,16 @@ prefill_bf16_kernel(PrefillArgs a) {
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kb2][e]);
-    const float m_tile = pair_max(mx);
-    const float m_all = fmaxf(m_run, m_tile);
-    bool rescale;
-    float alpha;
-    if (fixed_ref) {
-      rescale = __any(m_all > kFixedWindow || (m_all < -kFixedWindow && m_all != -INFINITY));
-      alpha = m_all == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(-m_all);   // reference 0 -> m_all
-      m_run = m_all;
-      if (rescale) fixed_ref = false;
-    } else {
-      rescale = __any(m_tile > m_run + 8.f);
-      alpha = __builtin_amdgcn_exp2f(m_run - m_all);
-      if (rescale) m_run = m_all;
-    }
-    if (rescale) {
-      flush_pending();   // the pending products belong to the old reference
+    const float m_tile = pair_max(mx) * a.scale_log2;
+    if (__any(m_tile > m_run + 8.f)) {
+      flush_pending();   // the pending products belong to the old reference max
       pend_p = as_bf16x8(u32x4{0, 0, 0, 0});
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
       l_part *= alpha;
 #pragma unroll
       for (int db = 0; db < kDB; ++db) oacc[db] *= alpha;
-    }
-    if (!fixed_ref) {
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[kb2][e] -= m_run;
     }
   };
 
@@ -963,7 +923,6 @@ prefill_bf16_kernel(PrefillArgs a) {
     if constexpr (kRope) {
       if ((t0 + 1) * kKeys > ctx) rope_cs(t0);
       rope_q();
-      scale_q();
     }
     wait_loads();
     if constexpr (kRope) {
@@ -1059,8 +1018,8 @@ prefill_bf16_kernel(PrefillArgs a) {
       uint32_t pw[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p0 = __builtin_amdgcn_exp2f(scur[kb2][8 * u + 2 * j]);
-        const float p1 = __builtin_amdgcn_exp2f(scur[kb2][8 * u + 2 * j + 1]);
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j], a.scale_log2, -m_run));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(scur[kb2][8 * u + 2 * j + 1], a.scale_log2, -m_run));
         pw[j] = pack_bf16x2(p0, p1);
         psum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[j]), ones, psum, false);
         __builtin_amdgcn_sched_barrier(0);
@@ -1163,10 +1122,7 @@ prefill_bf16_kernel(PrefillArgs a) {
       v.y = pack_bf16x2(oacc[db][4 * qd + 2] * inv, oacc[db][4 * qd + 3] * inv);
       *reinterpret_cast<uint2*>(op + d) = v;
     }
-  if (a.n_splits > 1 && hh == 0) {   // the reference the sums were taken against (-inf: no key seen)
-    const float m_ref = !fixed_ref || m_run == -INFINITY ? m_run : 0.f;
-    a.ws_ml[split * a.rows_total + orow] = make_float2(m_ref, l_tot);
-  }
+  if (a.n_splits > 1 && hh == 0) a.ws_ml[split * a.rows_total + orow] = make_float2(m_run, l_tot);
 }
 
 // Merge the key-range splits of each query row by log-sum-exp.  Split s left its output
