@@ -284,8 +284,11 @@ pic_status pic_suffix_prefill_attn_rope(const pic_model* model, const void* q, c
      context tile (document boundaries off the 64-slot grid, short documents, a partial last
      tile) is first composed into the cache from the slot map (pic_compose's arithmetic, a
      launch of its own on the same stream) and read from there.  Outputs then match compose +
-     prefill to within bf16 rounding, not bit for bit.  Entries outside the pool, the table or
-     the context are treated as (-1, 0).
+     prefill to within bf16 rounding, not bit for bit: the turned query's rounding moves a
+     score by about 2^-9 |q (*) k| scale, which stays inside the attention tolerance for
+     unit-scale q and k but reaches ~3 % of the output at scores near 90 nats (use tile_map
+     NULL where such scores occur).  Entries outside the pool, the table or the context are
+     treated as (-1, 0).
    The suffix K/V are stored (slots [ctx_len[b], ctx_len[b] + n_suffix)), and with a tile map
    the non-run context tiles; a later pic_compose (or pic_compose_shared) fills the document
    slots for decoding.  bf16 only.
