@@ -46,6 +46,11 @@ struct Vec16<float> {
   __device__ static void store(float* p, const float (&x)[4]) {
     *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
   }
+  __device__ static void load_nt(const float* p, float (&x)[4]) {
+    typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+    const u32x4_nt v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+    x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y); x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
+  }
   __device__ static uint4 load_raw(const float* p) { return *reinterpret_cast<const uint4*>(p); }
   __device__ static void widen(uint4 v, float (&x)[4]) {
     x[0] = __uint_as_float(v.x); x[1] = __uint_as_float(v.y); x[2] = __uint_as_float(v.z); x[3] = __uint_as_float(v.w);
@@ -73,6 +78,17 @@ struct Vec16<bf16_t> {
     const u32x4_nt v = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
                         pack_bf16x2(x[6], x[7])};
     __builtin_nontemporal_store(v, reinterpret_cast<u32x4_nt*>(p));
+  }
+  // Non-temporal: a row read once by a streaming launch (the in-place re-rotation)
+  __device__ static void load_nt(const bf16_t* p, float (&x)[8]) {
+    typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+    const u32x4_nt v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
   }
   __device__ static uint4 load_raw(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
   __device__ static void widen(uint4 v, float (&x)[8]) {
@@ -412,8 +428,12 @@ __global__ void __launch_bounds__(256) compose_tiles_kernel(
   }
 }
 
-// rows [n_tokens][n_heads][HD]; one (row, chunk) per thread, grid-stride.
-template <typename T, int HD, bool IL>
+// rows [n_tokens][n_heads][HD]; one (row, pair chunk) item per thread, LPR items per row, so a
+// wave's two 16-byte loads cover 64 / LPR whole rows.  The grid covers every item in one pass
+// for up to 2^31 items (a streaming launch runs fastest with one item per thread), with a
+// grid-stride loop beyond; rows are read and written non-temporally.  kWide: 64-bit item
+// indices (2^32 items or more), else 32-bit index arithmetic.
+template <typename T, int HD, bool IL, bool kWide>
 __global__ void __launch_bounds__(256) rerotate_kernel(const T* k_in, T* k_out, int64_t n_rows,
                                                        int32_t n_heads, const int32_t* __restrict__ delta,
                                                        const float2* __restrict__ table,
@@ -425,14 +445,22 @@ __global__ void __launch_bounds__(256) rerotate_kernel(const T* k_in, T* k_out, 
   const int64_t n_items = n_rows * LPR;
   for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n_items;
        idx += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t row = idx / LPR;
+    int64_t row, token;
+    if constexpr (kWide) {
+      row = idx / LPR;
+      token = row / n_heads;
+    } else {
+      const uint32_t r32 = (uint32_t)idx / LPR;
+      row = r32;
+      token = r32 / (uint32_t)n_heads;
+    }
     const int c0 = (int)(idx - row * LPR) * VEC;
-    const int32_t d = clamp_delta(delta[row / n_heads], max_abs_delta);
+    const int32_t d = clamp_delta(delta[token], max_abs_delta);
     float cs[VEC], sn[VEC], x1[VEC], x2[VEC];
-    load_cs<VEC, HALF>(table, d, c0, cs, sn);
     const int o1 = off1<VEC, HALF, IL>(c0), o2 = off2<VEC, HALF, IL>(c0);
-    V::load(k_in + row * HD + o1, x1);
-    V::load(k_in + row * HD + o2, x2);
+    V::load_nt(k_in + row * HD + o1, x1);
+    V::load_nt(k_in + row * HD + o2, x2);
+    load_cs<VEC, HALF>(table, d, c0, cs, sn);
     rotate<VEC, IL>(x1, x2, cs, sn);
     V::store(k_out + row * HD + o1, x1);
     V::store(k_out + row * HD + o2, x2);
@@ -543,12 +571,21 @@ hipError_t launch_rerotate(pic_dtype dt, int head_dim, bool interleaved, const v
   if (n_rows == 0) return hipSuccess;
   PIC_DISPATCH_TD(dt, head_dim, {
     constexpr int LPR = HD / 2 / (16 / (int)sizeof(T));
-    const dim3 grid(grid_for(n_rows * LPR, 256));
-    if (interleaved)
-      hipLaunchKernelGGL((rerotate_kernel<T, HD, true>), grid, dim3(256), 0, stream, (const T*)k_in,
+    const int64_t items = n_rows * LPR;
+    const int64_t blocks = (items + 255) / 256;
+    const dim3 grid((unsigned)(blocks < (1 << 23) ? blocks : (1 << 23)));   // one pass up to 2^31 items
+    const bool wide = items >= (int64_t(1) << 32);
+    if (interleaved && wide)
+      hipLaunchKernelGGL((rerotate_kernel<T, HD, true, true>), grid, dim3(256), 0, stream, (const T*)k_in,
+                         (T*)k_out, n_rows, n_heads, delta, table, max_abs_delta);
+    else if (interleaved)
+      hipLaunchKernelGGL((rerotate_kernel<T, HD, true, false>), grid, dim3(256), 0, stream, (const T*)k_in,
+                         (T*)k_out, n_rows, n_heads, delta, table, max_abs_delta);
+    else if (wide)
+      hipLaunchKernelGGL((rerotate_kernel<T, HD, false, true>), grid, dim3(256), 0, stream, (const T*)k_in,
                          (T*)k_out, n_rows, n_heads, delta, table, max_abs_delta);
     else
-      hipLaunchKernelGGL((rerotate_kernel<T, HD, false>), grid, dim3(256), 0, stream, (const T*)k_in,
+      hipLaunchKernelGGL((rerotate_kernel<T, HD, false, false>), grid, dim3(256), 0, stream, (const T*)k_in,
                          (T*)k_out, n_rows, n_heads, delta, table, max_abs_delta);
   });
   return hipGetLastError();
