@@ -33,7 +33,8 @@ METRIC = "composed-cache TTFT (ms/request); prefill attn TFLOP/s; rerotate+decod
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {"suffix_prefill_attn": "paper_2607_28069_amd/csrc/prefill_bf16.hip",
                   "compose": "paper_2607_28069_amd/csrc/rope_compose.hip",
-                  "decode_attn": "paper_2607_28069_amd/csrc/decode_bf16.hip"}
+                  "decode_attn": "paper_2607_28069_amd/csrc/decode_bf16.hip",
+                  "rerotate": "paper_2607_28069_amd/csrc/rope_compose.hip"}
 
 
 def parse(argv=None):
@@ -761,7 +762,8 @@ def rerotate_leg(dev, reps=10, warmup=3):
     return {"kernel": "rerotate_kernel", "tokens": n_tok, "heads": H, "head_dim": D, "dtype": "bf16",
             "ms_per_launch": ms, "per_launch": nbytes, "bound": "hbm",
             "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+            "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "traffic": lookup_traffic("rerotate_keys", "rerotate")}
 
 
 def copy_leg(dev, gib=4, reps=10, warmup=3):
